@@ -1,0 +1,320 @@
+"""CPU oracle for the GCN aggregation path -- TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, the GPU smoke check and the benchmark's CPU-baseline leg
+may import this package. The GPU library neither imports nor links it; the two
+share no code (only the seeded input generators in ``synth`` serve both).
+
+Python side of ``oracle.cpp`` (structure, normalization, fp64-accumulated
+aggregation, per-row uint8 quantization and fused halo dequantization; see
+the header there for the paper passages each function follows) plus the
+two-layer GCN training step in float64 numpy.
+
+Paper: SuperGCN (Chen et al., arXiv 2411.16025). Sections cited:
+  * 2.1  -- a GCN layer is AGGREGATE over neighbours then UPDATE (e.g. a
+            linear transform); GCN is the model family cited there.
+  * 2.4  -- integer quantization Z = min, S = (max - min)/(2^b - 1).
+  * 4    -- Index_add / SpMM aggregation, clustering and sorting of idx.
+  * 6.1  -- quantize, communicate, dequantize the boundary features.
+  * 6.3, Lemma 2 -- the layer written as A H W.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.cpp")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+SYMMETRIZE = 1
+ADD_SELF_LOOPS = 2
+
+
+def build(force: bool = True) -> str:
+    """Compile liboracle.so with g++ (OpenMP, no FMA contraction)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.check_call(
+            ["g++", "-O2", "-std=c++17", "-fopenmp", "-fPIC", "-shared", "-ffp-contract=off",
+             _SRC, "-o", tmp])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _L():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build(force=False)
+        lib = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        i64, u32 = ctypes.c_int64, ctypes.c_uint32
+        lib.orc_structure.argtypes = [i64, i64, i64, P, P, u32, ctypes.c_int, i64, P, P]
+        lib.orc_structure.restype = i64
+        lib.orc_rows_of.argtypes = [i64, i64, i64, P, P, u32, ctypes.c_int, i64, P, i64, P, P]
+        lib.orc_rows_of.restype = i64
+        lib.orc_row_degrees.argtypes = [i64, P, P, P]
+        lib.orc_normalize.argtypes = [i64, P, P, P, P]
+        lib.orc_normalize_listed.argtypes = [i64, P, P, P, P]
+        lib.orc_spmm.argtypes = [i64, P, P, P, P, i64, i64, P, P]
+        lib.orc_dequant.argtypes = [ctypes.c_uint8, ctypes.c_float, ctypes.c_float]
+        lib.orc_dequant.restype = ctypes.c_float
+        lib.orc_dequant_rows.argtypes = [i64, i64, P, i64, P, P, P, i64]
+        lib.orc_spmm_q8.argtypes = [i64, P, P, P, i64, P, i64, P, i64, P, P, i64, P, P]
+        lib.orc_quantize_rows.argtypes = [i64, i64, P, i64, P, i64, P, P]
+        lib.orc_num_threads.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def num_threads() -> int:
+    return _L().orc_num_threads()
+
+
+_ERR = {-1: "capacity", -2: "id out of range", -3: "symmetrize needs a square shape",
+        -4: "repeated selection"}
+
+
+def structure(n_rows, n_cols, src, dst, flags, transpose=False):
+    """Sorted, deduplicated (ptr int64, idx int32) of A or (transpose) A^T."""
+    src = _c(src, np.int32)
+    dst = _c(dst, np.int32)
+    cap = len(src) * (2 if flags & SYMMETRIZE else 1) + min(n_rows, n_cols)
+    n_major = n_cols if transpose else n_rows
+    ptr = np.empty(n_major + 1, np.int64)
+    idx = np.empty(max(cap, 1), np.int32)
+    nnz = _L().orc_structure(n_rows, n_cols, len(src), _p(src), _p(dst), flags, int(transpose),
+                             cap, _p(ptr), _p(idx))
+    if nnz < 0:
+        raise ValueError("oracle structure: " + _ERR[nnz])
+    return ptr, idx[:nnz].copy()
+
+
+def rows_of(n_rows, n_cols, src, dst, flags, sel, transpose=False):
+    """Structure of the listed (distinct) major ids only, from the edge list."""
+    src = _c(src, np.int32)
+    dst = _c(dst, np.int32)
+    sel = _c(sel, np.int32)
+    cap = len(src) * (2 if flags & SYMMETRIZE else 1) + len(sel)
+    ptr = np.empty(len(sel) + 1, np.int64)
+    idx = np.empty(max(cap, 1), np.int32)
+    tot = _L().orc_rows_of(n_rows, n_cols, len(src), _p(src), _p(dst), flags, int(transpose),
+                           len(sel), _p(sel), cap, _p(ptr), _p(idx))
+    if tot < 0:
+        raise ValueError("oracle rows_of: " + _ERR[tot])
+    return ptr, idx[:tot].copy()
+
+
+def row_degrees(ptr, idx):
+    """Entries per row whose column differs from the row id."""
+    ptr = _c(ptr, np.int64)
+    idx = _c(idx, np.int32)
+    deg = np.empty(len(ptr) - 1, np.int32)
+    _L().orc_row_degrees(len(ptr) - 1, _p(ptr), _p(idx), _p(deg))
+    return deg
+
+
+def normalize(ptr, idx, deg):
+    """val[k] = fp32(1 / sqrt((deg[r]+1)(deg[c]+1))) for entry k = (r, c)."""
+    ptr = _c(ptr, np.int64)
+    idx = _c(idx, np.int32)
+    deg = _c(deg, np.int32)
+    val = np.empty(len(idx), np.float32)
+    _L().orc_normalize(len(ptr) - 1, _p(ptr), _p(idx), _p(deg), _p(val))
+    return val
+
+
+def normalize_listed(ptr, deg_rows, deg_cols):
+    ptr = _c(ptr, np.int64)
+    deg_rows = _c(deg_rows, np.int32)
+    deg_cols = _c(deg_cols, np.int32)
+    val = np.empty(len(deg_cols), np.float32)
+    _L().orc_normalize_listed(len(ptr) - 1, _p(ptr), _p(deg_rows), _p(deg_cols), _p(val))
+    return val
+
+
+def spmm(ptr, idx, val, X):
+    """(Y, S): Y = A X accumulated in float64, S = sum of |terms| per element."""
+    ptr = _c(ptr, np.int64)
+    idx = _c(idx, np.int32)
+    val = _c(val, np.float32)
+    X = np.asarray(X, np.float32)
+    if X.strides[1] != 4:
+        X = np.ascontiguousarray(X)
+    assert X.ndim == 2
+    F = X.shape[1]
+    ldx = X.strides[0] // 4
+    n = len(ptr) - 1
+    Y = np.empty((n, F), np.float64)
+    S = np.empty((n, F), np.float64)
+    _L().orc_spmm(n, _p(ptr), _p(idx), _p(val), X.ctypes.data, ldx, F, _p(Y), _p(S))
+    return Y, S
+
+
+def dequant(q, scale, zero) -> np.float32:
+    return np.float32(_L().orc_dequant(int(q), float(scale), float(zero)))
+
+
+def dequant_rows(Q, zmin, scale):
+    Q = _c(Q, np.uint8)
+    n, F = Q.shape
+    out = np.empty((n, F), np.float32)
+    _L().orc_dequant_rows(n, F, _p(Q), F, _p(_c(zmin, np.float32)), _p(_c(scale, np.float32)),
+                          _p(out), F)
+    return out
+
+
+def spmm_q8(ptr, idx, val, n_local_cols, X_local, Q, zmin, scale):
+    """(Y, S) with columns >= n_local_cols dequantized from uint8 codes."""
+    ptr = _c(ptr, np.int64)
+    idx = _c(idx, np.int32)
+    val = _c(val, np.float32)
+    X_local = np.asarray(X_local, np.float32)
+    Q = np.asarray(Q, np.uint8)
+    if X_local.strides[1] != 4:
+        X_local = np.ascontiguousarray(X_local)
+    if Q.strides[1] != 1:
+        Q = np.ascontiguousarray(Q)
+    F = X_local.shape[1]
+    assert Q.shape[1] == F
+    n = len(ptr) - 1
+    Y = np.empty((n, F), np.float64)
+    S = np.empty((n, F), np.float64)
+    zmin = _c(zmin, np.float32)
+    scale = _c(scale, np.float32)
+    _L().orc_spmm_q8(n, _p(ptr), _p(idx), _p(val), n_local_cols, X_local.ctypes.data,
+                     X_local.strides[0] // 4, Q.ctypes.data, Q.strides[0], _p(zmin), _p(scale),
+                     F, _p(Y), _p(S))
+    return Y, S
+
+
+def quantize_rows(X):
+    """Per-row uint8 codes and (zmin, scale), round-to-nearest-even."""
+    X = np.asarray(X, np.float32)
+    if X.strides[1] != 4:
+        X = np.ascontiguousarray(X)
+    n, F = X.shape
+    Q = np.empty((n, F), np.uint8)
+    zmin = np.empty(n, np.float32)
+    scale = np.empty(n, np.float32)
+    _L().orc_quantize_rows(n, F, X.ctypes.data, X.strides[0] // 4, _p(Q), F, _p(zmin), _p(scale))
+    return Q, zmin, scale
+
+
+# ---------------------------------------------------------------------------
+# Whole-graph and sampled-row helpers.
+# ---------------------------------------------------------------------------
+
+class Graph:
+    """Oracle matrices of one workload: CSR (rows = dst) and CSC, both with
+    normalized values unless normalized=False (then every value is 1)."""
+
+    def __init__(self, n_rows, n_cols, src, dst, flags, deg=None, normalized=True):
+        self.n_rows, self.n_cols = n_rows, n_cols
+        self.csr_ptr, self.csr_idx = structure(n_rows, n_cols, src, dst, flags, False)
+        self.csc_ptr, self.csc_idx = structure(n_rows, n_cols, src, dst, flags, True)
+        if deg is None:
+            if n_rows != n_cols:
+                raise ValueError("a rectangular graph needs a supplied degree array")
+            deg = row_degrees(self.csr_ptr, self.csr_idx)
+        self.deg = np.asarray(deg, np.int32)
+        if normalized:
+            self.csr_val = normalize(self.csr_ptr, self.csr_idx, self.deg)
+            self.csc_val = normalize(self.csc_ptr, self.csc_idx, self.deg)
+        else:
+            self.csr_val = np.ones(len(self.csr_idx), np.float32)
+            self.csc_val = np.ones(len(self.csc_idx), np.float32)
+
+    @property
+    def nnz(self):
+        return len(self.csr_idx)
+
+    def fwd(self, X):
+        return spmm(self.csr_ptr, self.csr_idx, self.csr_val, X)
+
+    def bwd(self, G):
+        return spmm(self.csc_ptr, self.csc_idx, self.csc_val, G)
+
+
+def sampled(n_rows, n_cols, src, dst, flags, sel, transpose=False, deg=None):
+    """(ptr, idx, val) of the listed rows of A (or A^T), normalized.
+
+    deg: the supplied per-node degree array, or None to use the stored
+    non-self entry count of each node's row of A (square graphs)."""
+    sel = np.asarray(sel, np.int32)
+    ptr, idx = rows_of(n_rows, n_cols, src, dst, flags, sel, transpose)
+    if deg is not None:
+        deg = np.asarray(deg, np.int32)
+        deg_rows, deg_cols = deg[sel], deg[idx]
+    else:
+        nodes = np.unique(np.concatenate([sel, idx]))
+        nptr, nidx = rows_of(n_rows, n_cols, src, dst, flags, nodes, False)
+        owner = np.repeat(nodes, np.diff(nptr))
+        nd = np.bincount(np.searchsorted(nodes, owner[nidx != owner]),
+                         minlength=len(nodes)).astype(np.int32)
+        deg_rows = nd[np.searchsorted(nodes, sel)]
+        deg_cols = nd[np.searchsorted(nodes, idx)]
+    val = normalize_listed(ptr, deg_rows, deg_cols)
+    return ptr, idx, val
+
+
+# ---------------------------------------------------------------------------
+# Two-layer GCN training step (float64), Section 2.1: each layer aggregates
+# then applies a linear transform; the order A (X W) keeps the aggregation on
+# the narrower side. No bias, no dropout, no LayerNorm; ReLU between layers;
+# mean negative log-likelihood of log-softmax over all nodes.
+# ---------------------------------------------------------------------------
+
+def _agg64(ptr, idx, val, H):
+    """A H in float64 for float64 H (row order, double accumulation)."""
+    H = np.asarray(H, np.float64)
+    n = len(ptr) - 1
+    rows = np.repeat(np.arange(n), np.diff(ptr))
+    out = np.zeros((n, H.shape[1]), np.float64)
+    np.add.at(out, rows, val.astype(np.float64)[:, None] * H[idx])
+    return out
+
+
+def gcn_step(graph: Graph, X, W1, W2, labels):
+    """Loss and weight gradients of the 2-layer GCN, all in float64.
+
+    Returns dict(loss, dW1, dW2, Z1, A1, H1, Z2, logits)."""
+    X = np.asarray(X, np.float64)
+    W1 = np.asarray(W1, np.float64)
+    W2 = np.asarray(W2, np.float64)
+    y = np.asarray(labels)
+    n = X.shape[0]
+    fwd = lambda H: _agg64(graph.csr_ptr, graph.csr_idx, graph.csr_val, H)
+    bwd = lambda H: _agg64(graph.csc_ptr, graph.csc_idx, graph.csc_val, H)
+    Z1 = X @ W1
+    A1 = fwd(Z1)
+    H1 = np.maximum(A1, 0.0)
+    Z2 = H1 @ W2
+    logits = fwd(Z2)
+    m = logits.max(axis=1, keepdims=True)
+    lse = m[:, 0] + np.log(np.exp(logits - m).sum(axis=1))
+    loss = float(np.mean(lse - logits[np.arange(n), y]))
+    P = np.exp(logits - lse[:, None])
+    dlogits = P
+    dlogits[np.arange(n), y] -= 1.0
+    dlogits /= n
+    dZ2 = bwd(dlogits)
+    dW2 = H1.T @ dZ2
+    dH1 = dZ2 @ W2.T
+    dA1 = dH1 * (A1 > 0)
+    dZ1 = bwd(dA1)
+    dW1 = X.T @ dZ1
+    return dict(loss=loss, dW1=dW1, dW2=dW2, Z1=Z1, A1=A1, H1=H1, Z2=Z2, logits=logits)

@@ -1,0 +1,383 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle.
+
+Each test ties an oracle routine to something fixed independently of it:
+dense brute force built straight from the edge list, the eigenvector of the
+GCN propagation matrix, the adjoint identity, closed forms of small graphs,
+hand-derived golden matrices, nearest-code optimality of the quantizer, and
+finite differences of the training loss.
+"""
+
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+SYM, LOOPS = oracle.SYMMETRIZE, oracle.ADD_SELF_LOOPS
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------------------
+# Dense brute force: A~ straight from the edge list, no sorting involved.
+# ---------------------------------------------------------------------------
+
+def dense_adjacency(n_rows, n_cols, src, dst, flags):
+    A = np.zeros((n_rows, n_cols), np.float64)
+    A[dst, src] = 1.0
+    if flags & SYM:
+        A[src, dst] = 1.0
+    if flags & LOOPS:
+        m = min(n_rows, n_cols)
+        A[np.arange(m), np.arange(m)] = 1.0
+    return A
+
+
+def dense_ahat(A, deg):
+    d = np.asarray(deg, np.float64) + 1.0
+    n_rows = A.shape[0]
+    return A / np.sqrt(d[:n_rows, None] * d[None, : A.shape[1]])
+
+
+def csr_to_dense(ptr, idx, val, n_major, n_minor):
+    M = np.zeros((n_major, n_minor), np.float64)
+    rows = np.repeat(np.arange(n_major), np.diff(ptr))
+    M[rows, idx] = val
+    return M
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_dense_brute_force_symmetric(seed):
+    n = [7, 33, 64, 129, 200, 257, 400, 512][seed]
+    m = 3 * n + seed
+    src, dst = synth.er_edges(9000 + seed, n, m)
+    g = oracle.Graph(n, n, src, dst, SYM | LOOPS)
+    A = dense_adjacency(n, n, src, dst, SYM | LOOPS)
+    # structure: nonzero pattern of A~ equals the CSR and the CSC
+    pat = csr_to_dense(g.csr_ptr, g.csr_idx, np.ones(g.nnz), n, n)
+    assert np.array_equal(pat, A)
+    patc = csr_to_dense(g.csc_ptr, g.csc_idx, np.ones(len(g.csc_idx)), n, n)
+    assert np.array_equal(patc, A.T)
+    deg = A.sum(axis=1) - 1.0
+    assert np.array_equal(g.deg, deg.astype(np.int32))
+    Ah = dense_ahat(A, deg)
+    X = synth.uniform(3000 + seed, n, 5)
+    Y, S = g.fwd(X)
+    ref = Ah @ X.astype(np.float64)
+    # the oracle's only rounding beyond double is the fp32 val (<= 2^-24 rel)
+    assert np.all(np.abs(Y - ref) <= 2.0**-23 * S + 1e-300)
+    # val itself equals the dense normalized entry to fp32 rounding
+    dense_val = Ah[np.repeat(np.arange(n), np.diff(g.csr_ptr)), g.csr_idx]
+    assert np.array_equal(g.csr_val, dense_val.astype(np.float32))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_dense_brute_force_rectangular(seed):
+    # one worker's share: rows 0..n_r-1 are local, columns n_r.. are halo,
+    # normalization by a supplied global degree
+    n_r, n_c = [(10, 17), (64, 100), (130, 260), (300, 301)][seed]
+    m = 4 * n_r
+    src, dst = synth.er_edges(9100 + seed, n_c, m)
+    dst = dst % n_r
+    deg = (synth.splitmix64(9200 + seed, 0, n_c) % 50).astype(np.int32) + 3
+    g = oracle.Graph(n_r, n_c, src, dst, LOOPS, deg=deg)
+    A = dense_adjacency(n_r, n_c, src, dst, LOOPS)
+    assert np.array_equal(csr_to_dense(g.csr_ptr, g.csr_idx, np.ones(g.nnz), n_r, n_c), A)
+    assert np.array_equal(csr_to_dense(g.csc_ptr, g.csc_idx, np.ones(g.nnz), n_c, n_r), A.T)
+    Ah = dense_ahat(A, deg)
+    X = synth.uniform(3100 + seed, n_c, 9)
+    Y, S = g.fwd(X)
+    assert np.all(np.abs(Y - Ah @ X.astype(np.float64)) <= 2.0**-23 * S + 1e-300)
+    G = synth.uniform(4100 + seed, n_r, 9)
+    dX, S2 = g.bwd(G)
+    assert np.all(np.abs(dX - Ah.T @ G.astype(np.float64)) <= 2.0**-23 * S2 + 1e-300)
+
+
+def test_duplicates_and_drawn_self_loops_are_dropped():
+    src = np.array([0, 0, 1, 2, 2, 3, 3], np.int32)
+    dst = np.array([1, 1, 0, 2, 3, 2, 0], np.int32)
+    g = oracle.Graph(4, 4, src, dst, SYM | LOOPS)
+    # undirected edges {0,1}, {2,3}, {0,3} plus four self-loops
+    assert g.nnz == 3 * 2 + 4
+    assert list(g.deg) == [2, 1, 1, 2]
+
+
+def test_unnormalized_graph_is_index_add():
+    # Index_add (Section 4): rows of src added into dst, value 1 per entry
+    n = 50
+    src, dst = synth.er_edges(77, n, 300)
+    g = oracle.Graph(n, n, src, dst, 0, deg=np.zeros(n, np.int32), normalized=False)
+    X = synth.uniform(78, n, 3)
+    Y, _ = g.fwd(X)
+    ref = np.zeros((n, 3))
+    seen = set()
+    for s, d in zip(src, dst):
+        if (s, d) not in seen:
+            seen.add((s, d))
+            ref[d] += X[s]
+    assert np.array_equal(Y, ref)
+
+
+# ---------------------------------------------------------------------------
+# Invariants.
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("scale", [8, 11])
+def test_eigenvector_invariant(scale):
+    # A_hat sqrt(d~) = sqrt(d~) for symmetric binary A with one self-loop
+    n = 1 << scale
+    src, dst = synth.rmat_edges(500 + scale, n, 8 * n, perm_seed=600 + scale)
+    g = oracle.Graph(n, n, src, dst, SYM | LOOPS)
+    v = np.sqrt(g.deg.astype(np.float64) + 1.0)
+    x = v.astype(np.float32)[:, None]
+    Y, S = g.fwd(x)
+    # positive terms: error <= rounding of val (2^-24) and of x (2^-24)
+    assert np.all(np.abs(Y[:, 0] - v) <= 2.0**-22 * S[:, 0])
+
+
+def test_partition_row_sum_invariant():
+    # For any row set under degrees d~: (A_hat sqrt(d~))_i = nnz_i / sqrt(d~_i)
+    n_r, n_c = 300, 500
+    src, dst = synth.er_edges(31, n_c, 2000)
+    dst = dst % n_r
+    deg = (synth.splitmix64(32, 0, n_c) % 40).astype(np.int32) + 5
+    g = oracle.Graph(n_r, n_c, src, dst, LOOPS, deg=deg)
+    d = deg.astype(np.float64) + 1.0
+    Y, S = g.fwd(np.sqrt(d).astype(np.float32)[:, None])
+    expect = np.diff(g.csr_ptr) / np.sqrt(d[:n_r])
+    assert np.all(np.abs(Y[:, 0] - expect) <= 2.0**-22 * S[:, 0])
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_adjoint_identity(seed):
+    # <A x, g> = <x, A^T g>: ties the CSC path to the CSR path
+    n = 700
+    src, dst = synth.rmat_edges(40 + seed, n, 5000)  # directed, not symmetrized
+    g = oracle.Graph(n, n, src, dst, LOOPS)
+    assert not np.array_equal(g.csr_idx, g.csc_idx)
+    x = synth.uniform(50 + seed, n, 4)
+    gg = synth.uniform(60 + seed, n, 4)
+    Y, S = g.fwd(x)
+    dX, S2 = g.bwd(gg)
+    lhs = np.sum(Y * gg.astype(np.float64))
+    rhs = np.sum(x.astype(np.float64) * dX)
+    mag = np.sum(S * np.abs(gg)) + np.sum(np.abs(x) * S2)
+    assert abs(lhs - rhs) <= 1e-12 * mag
+
+
+# ---------------------------------------------------------------------------
+# Closed forms and hand-derived matrices.
+# ---------------------------------------------------------------------------
+
+def test_empty_graph_is_identity_bitwise():
+    n = 37
+    g = oracle.Graph(n, n, np.zeros(0, np.int32), np.zeros(0, np.int32), SYM | LOOPS)
+    assert np.all(g.csr_val == 1.0)
+    X = synth.uniform(5, n, 11)
+    Y, _ = g.fwd(X)
+    assert np.array_equal(Y.astype(np.float32), X)
+
+
+def test_cycle_closed_form():
+    n = 41
+    src = np.arange(n, dtype=np.int32)
+    dst = ((src + 1) % n).astype(np.int32)
+    g = oracle.Graph(n, n, src, dst, SYM | LOOPS)
+    X = synth.uniform(6, n, 3).astype(np.float64)
+    Y, S = g.fwd(X.astype(np.float32))
+    ref = (np.roll(X, 1, 0) + X + np.roll(X, -1, 0)) / 3.0
+    assert np.all(np.abs(Y - ref) <= 2.0**-23 * S)
+
+
+def test_complete_graph_closed_form():
+    n = 23
+    ii, jj = np.meshgrid(np.arange(n), np.arange(n))
+    g = oracle.Graph(n, n, ii.ravel().astype(np.int32), jj.ravel().astype(np.int32), SYM | LOOPS)
+    X = synth.uniform(7, n, 4).astype(np.float64)
+    Y, S = g.fwd(X.astype(np.float32))
+    assert np.all(np.abs(Y - X.mean(axis=0)[None, :]) <= 2.0**-23 * S)
+
+
+def test_star_closed_form():
+    k = 1000
+    src = np.arange(1, k + 1, dtype=np.int32)
+    dst = np.zeros(k, np.int32)
+    g = oracle.Graph(k + 1, k + 1, src, dst, SYM | LOOPS)
+    val = dict(zip(zip(np.repeat(np.arange(k + 1), np.diff(g.csr_ptr)), g.csr_idx), g.csr_val))
+    assert val[(0, 0)] == np.float32(1.0 / (k + 1))
+    assert val[(0, 5)] == np.float32(1.0 / math.sqrt(2 * (k + 1)))
+    assert val[(5, 0)] == val[(0, 5)]
+    assert val[(5, 5)] == np.float32(0.5)
+
+
+def _read_golden(name):
+    edges, entries = [], []
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            parts = line.split()
+            if parts[0] == "edges":
+                edges.append((int(parts[1]), int(parts[2])))
+            else:
+                entries.append((int(parts[0]), int(parts[1]), float(parts[2])))
+    return edges, entries
+
+
+@pytest.mark.parametrize("name", ["path3_ahat.txt", "star3_ahat.txt"])
+def test_golden_hand_derived(name):
+    edges, entries = _read_golden(name)
+    n = 1 + max(max(e) for e in edges)
+    src = np.array([e[0] for e in edges], np.int32)
+    dst = np.array([e[1] for e in edges], np.int32)
+    g = oracle.Graph(n, n, src, dst, SYM | LOOPS)
+    got = csr_to_dense(g.csr_ptr, g.csr_idx, g.csr_val.astype(np.float64), n, n)
+    want = np.zeros((n, n))
+    for r, c, v in entries:
+        want[r, c] = v
+    assert np.array_equal(got != 0, want != 0)
+    assert np.array_equal(got.astype(np.float32), want.astype(np.float32))
+
+
+# ---------------------------------------------------------------------------
+# Sampled rows agree with the whole-matrix route.
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("transpose", [False, True])
+def test_rows_of_matches_structure(transpose):
+    n = 3000
+    src, dst = synth.rmat_edges(90, n, 20000, perm_seed=91)
+    for flags in (SYM | LOOPS, LOOPS, 0):
+        ptr, idx = oracle.structure(n, n, src, dst, flags, transpose)
+        sel = np.unique(synth.splitmix64(92, 0, 300) % n).astype(np.int32)[::-1].copy()
+        sp, si = oracle.rows_of(n, n, src, dst, flags, sel, transpose)
+        for i, r in enumerate(sel):
+            assert np.array_equal(si[sp[i]:sp[i + 1]], idx[ptr[r]:ptr[r + 1]])
+
+
+def test_sampled_normalization_matches_graph():
+    n = 2048
+    src, dst = synth.rmat_edges(93, n, 16 * n, perm_seed=94)
+    g = oracle.Graph(n, n, src, dst, SYM | LOOPS)
+    sel = np.array([0, 5, 77, 1000, 2047], np.int32)
+    for transpose in (False, True):
+        ptr, idx, val = oracle.sampled(n, n, src, dst, SYM | LOOPS, sel, transpose)
+        gp = g.csc_ptr if transpose else g.csr_ptr
+        gi = g.csc_idx if transpose else g.csr_idx
+        gv = g.csc_val if transpose else g.csr_val
+        for i, r in enumerate(sel):
+            assert np.array_equal(idx[ptr[i]:ptr[i + 1]], gi[gp[r]:gp[r + 1]])
+            assert np.array_equal(val[ptr[i]:ptr[i + 1]], gv[gp[r]:gp[r + 1]])
+
+
+# ---------------------------------------------------------------------------
+# Quantization (Section 2.4) and the fused dequantize path.
+# ---------------------------------------------------------------------------
+
+def test_quantizer_nearest_code_and_roundtrip():
+    X = synth.normal(11, 400, 128)
+    X[3, :] = 0.25          # constant row: S = 0, every code 0, dequant = Z
+    X[4, :7] = [-3.0, 5.0, 1.0, 1.0, 2.0, -3.0, 5.0]
+    Q, Z, S = oracle.quantize_rows(X)
+    assert S[3] == 0 and np.all(Q[3] == 0)
+    D = oracle.dequant_rows(Q, Z, S)
+    assert np.all(D[3] == np.float32(0.25))
+    assert np.array_equal(Z, X.min(axis=1))
+    for i in range(X.shape[0]):
+        if S[i] == 0:
+            continue
+        assert Q[i, np.argmin(X[i])] == 0
+        assert Q[i, np.argmax(X[i])] == 255
+        # round trip within half a step (plus float rounding)
+        err = np.abs(X[i].astype(np.float64) - D[i])
+        assert np.all(err <= 0.5 * S[i] * (1 + 1e-5) + 4 * np.spacing(np.abs(X[i]).max()))
+        # the chosen code is the nearest of all 256 (brute force)
+        codes = np.arange(256, dtype=np.float64)
+        grid = codes[None, :] * np.float64(S[i]) + np.float64(Z[i])
+        best = np.abs(X[i].astype(np.float64)[:, None] - grid).min(axis=1)
+        chosen = np.abs(X[i].astype(np.float64) - (Q[i] * np.float64(S[i]) + Z[i]))
+        assert np.all(chosen <= best + 1e-6 * S[i])
+
+
+def test_dequant_single_rounding():
+    # dequant is fmaf(q, S, Z): q = 0 gives Z exactly; compare to exact double
+    assert oracle.dequant(0, 0.123, -7.5) == np.float32(-7.5)
+    rng = np.random.default_rng(0)
+    for _ in range(2000):
+        q = int(rng.integers(0, 256))
+        s = np.float32(rng.standard_normal() * 0.01)
+        z = np.float32(rng.standard_normal())
+        exact = q * np.float64(s) + np.float64(z)  # exact: 8-bit x 24-bit + 24-bit fits in 53
+        assert oracle.dequant(q, s, z) == np.float32(exact)
+
+
+def test_q8_permutation_graph_is_exact_dequant():
+    # one entry per row into a distinct halo column, value 1, no self-loops:
+    # Y = fmaf(1, deq, 0) = deq exactly
+    n_local, n_halo, F = 50, 64, 40
+    perm = synth.permutation(12, n_halo)
+    src = (n_local + perm).astype(np.int32)
+    dst = np.arange(n_halo, dtype=np.int32)
+    ptr, idx = oracle.structure(n_halo, n_local + n_halo, src, dst, 0)
+    val = np.ones(len(idx), np.float32)
+    Xl = synth.uniform(13, n_local, F)
+    Q = synth.random_bytes(14, n_halo, F)
+    Z = synth.uniform(15, n_halo, 1)[:, 0]
+    S = np.abs(synth.uniform(16, n_halo, 1)[:, 0]) * 0.01
+    Y, _ = oracle.spmm_q8(ptr, idx, val, n_local, Xl, Q, Z, S)
+    D = oracle.dequant_rows(Q, Z, S)
+    assert np.array_equal(Y.astype(np.float32), D[perm])
+
+
+def test_q8_matches_dequantized_then_plain():
+    n = 900
+    src, dst = synth.rmat_edges(17, n, 9000, perm_seed=18)
+    g = oracle.Graph(n, n, src, dst, SYM | LOOPS)
+    n_lc = 675
+    X = synth.normal(19, n, 24)
+    Q, Z, S = oracle.quantize_rows(X[n_lc:])
+    Xd = X.copy()
+    Xd[n_lc:] = oracle.dequant_rows(Q, Z, S)
+    Y1, S1 = oracle.spmm_q8(g.csr_ptr, g.csr_idx, g.csr_val, n_lc, X[:n_lc], Q, Z, S)
+    Y2, S2 = g.fwd(Xd)
+    assert np.array_equal(Y1, Y2) and np.array_equal(S1, S2)
+
+
+# ---------------------------------------------------------------------------
+# Two-layer GCN step: analytic gradients against finite differences.
+# ---------------------------------------------------------------------------
+
+def test_gcn_step_gradients_finite_difference():
+    n, fin, hid, ncls = 60, 7, 6, 5
+    src, dst = synth.rmat_edges(20, n, 240, perm_seed=21)
+    g = oracle.Graph(n, n, src, dst, SYM | LOOPS)
+    X = synth.normal(22, n, fin).astype(np.float64)
+    W1 = synth.glorot(23, fin, hid).astype(np.float64)
+    W2 = synth.glorot(24, hid, ncls).astype(np.float64)
+    y = synth.labels(25, n, ncls)
+    out = oracle.gcn_step(g, X, W1, W2, y)
+    eps = 1e-6
+    for W, dW, which in ((W1, out["dW1"], 0), (W2, out["dW2"], 1)):
+        for (i, j) in [(0, 0), (1, 2), (W.shape[0] - 1, W.shape[1] - 1), (3, 1)]:
+            Wp, Wm = W.copy(), W.copy()
+            Wp[i, j] += eps
+            Wm[i, j] -= eps
+            args_p = (Wp, W2) if which == 0 else (W1, Wp)
+            args_m = (Wm, W2) if which == 0 else (W1, Wm)
+            lp = oracle.gcn_step(g, X, *args_p, y)["loss"]
+            lm = oracle.gcn_step(g, X, *args_m, y)["loss"]
+            fd = (lp - lm) / (2 * eps)
+            assert abs(fd - dW[i, j]) <= 1e-6 * max(1.0, abs(fd))
+
+
+def test_gcn_step_initial_loss_near_log_classes():
+    n, ncls = 400, 47
+    src, dst = synth.rmat_edges(26, n, 3200, perm_seed=27)
+    g = oracle.Graph(n, n, src, dst, SYM | LOOPS)
+    X = synth.normal(28, n, 100)
+    out = oracle.gcn_step(g, X, synth.glorot(29, 100, 256), synth.glorot(30, 256, ncls),
+                          synth.labels(31, n, ncls))
+    assert abs(out["loss"] - math.log(ncls)) < 0.5
