@@ -1,0 +1,175 @@
+/* gcnagg.h -- C ABI of the GCN aggregation library for AMD Instinct MI355X
+ * (gfx950).
+ *
+ * The library computes the graph aggregation step of full-batch GCN training
+ * as described in SuperGCN (Chen et al., "Scaling Large-scale GNN Training
+ * to Thousands of Processors on CPU-based Supercomputers", arXiv 2411.16025):
+ *
+ *   forward   Y  = A_hat X            (Section 4: Index_add / SpMM)
+ *   backward  dX = A_hat^T G
+ *   with A_hat = D~^-1/2 (A + I) D~^-1/2, the GCN propagation matrix
+ *   (Section 2.1 cites GCN; Lemma 2 in Section 6.3 writes a layer as A H W),
+ *
+ * plus the consumer side of the paper's quantized boundary exchange
+ * (Section 6.1, step 3): halo feature rows arrive as 8-bit codes with a
+ * per-row zero point and scale (Section 2.4) and are dequantized inside the
+ * aggregation.
+ *
+ * Conventions shared by every call:
+ *  - Pointers are DEVICE pointers unless a parameter says "host".
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    Work is enqueued on it; a call returns before the work completes unless
+ *    stated otherwise. Inputs must stay valid until the stream reaches it.
+ *  - Matrices are row-major with an explicit leading dimension (elements
+ *    between consecutive rows), ld >= F.
+ *  - Edge (s -> d) means "row s of the input is added into row d of the
+ *    output": the stored entry has row d and column s (Section 4: rows of
+ *    src are added to dst at the positions idx names).
+ *  - Every call returns a gcn_status and never throws. On failure,
+ *    gcn_last_error() returns a message for the calling thread. Argument
+ *    errors are detected before any work is enqueued, so outputs are left
+ *    untouched.
+ *  - Calls that share a gcn_graph may run concurrently only if none of them
+ *    is gcn_normalize or gcn_graph_free.
+ */
+#ifndef GCNAGG_H
+#define GCNAGG_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct gcn_graph gcn_graph; /* opaque; owns its device arrays */
+
+typedef enum {
+  GCN_OK = 0,
+  GCN_EINVAL = 1, /* null pointer, non-positive size, ld < F, unknown dtype/flag, bad shape */
+  GCN_ERANGE = 2, /* vertex id out of range, n_local_cols > n_cols, sizes beyond int32 ids */
+  GCN_ENOMEM = 3, /* device allocation failed */
+  GCN_EHIP = 4,   /* a HIP runtime call failed */
+  GCN_ESTATE = 5  /* freed / corrupted handle, or call out of order */
+} gcn_status;
+
+/* gcn_build_csr flags */
+enum {
+  GCN_SYMMETRIZE = 1u,    /* also store the reverse of every edge (square graphs only) */
+  GCN_ADD_SELF_LOOPS = 2u /* drop drawn self pairs, then store one (i, i) per
+                             i < min(n_rows, n_cols) */
+};
+
+/* input element types of the aggregation calls; accumulation and output are fp32 */
+enum { GCN_DT_F32 = 0, GCN_DT_BF16 = 1 };
+
+/* gcn_aggregate_fwd_q8halo flags */
+enum { GCN_Q8_USE_CSC = 1u /* aggregate with A_hat^T instead of A_hat */ };
+
+/* Build the sparse structure of A (or A + I) from an edge list: the
+ * "clustering and sorting" step of Section 4 done on the device. Entries are
+ * sorted by (row, column) and deduplicated, so A is binary. The transpose is
+ * built as well (for symmetric graphs it is the same matrix and shares the
+ * arrays), so the backward pass reads A^T row by row without atomics. Rows
+ * are then binned by length for the aggregation kernels. Every stored value
+ * is 1.0 until gcn_normalize runs (an unnormalized graph aggregates like
+ * Index_add).
+ *
+ *  n_rows, n_cols  output rows / input rows of the operator, 1 .. 2^31-1.
+ *                  Columns >= n_rows of a rectangular graph are halo nodes.
+ *  n_edges         number of (src, dst) pairs, >= 0.
+ *  src, dst        int32 device arrays [n_edges]; src in [0, n_cols),
+ *                  dst in [0, n_rows) (checked on the device -> GCN_ERANGE).
+ *  flags           GCN_SYMMETRIZE (requires n_rows == n_cols) | GCN_ADD_SELF_LOOPS.
+ *  out             host pointer that receives the new handle.
+ * Synchronizes `stream` (the entry count and bin sizes are read back).
+ * Device memory: about 24 bytes per stored entry while building, 8 per
+ * entry afterwards (twice that for a non-symmetric graph). */
+gcn_status gcn_build_csr(int64_t n_rows, int64_t n_cols, int64_t n_edges, const int32_t* src,
+                         const int32_t* dst, uint32_t flags, void* stream, gcn_graph** out);
+
+/* Overwrite the stored values of A and A^T with the entries of
+ * A_hat = D~^-1/2 (A + I) D~^-1/2: entry (r, c) becomes
+ * (float)(1 / sqrt((double)(deg[r] + 1) * (double)(deg[c] + 1))), computed
+ * with IEEE double division and square root.
+ *  deg  NULL: deg[v] = number of stored entries of row v other than (v, v)
+ *       (square graphs only); otherwise an int32 device array indexed by
+ *       node id, [max(n_rows, n_cols)] entries, of caller-supplied degrees
+ *       without the self-loop (e.g. global degrees of a partition whose cut
+ *       edges live on other workers), each >= 0 (else GCN_EINVAL).
+ *  Synchronizes `stream` when deg is supplied (the degrees are checked). */
+gcn_status gcn_normalize(gcn_graph* g, const int32_t* deg, void* stream);
+
+/* Y[n_rows x F] = A_hat X. X is [n_cols x F] (ldx), fp32 or bf16 (dtype);
+ * Y is fp32 (ldy). Accumulation is fp32; each output element is summed in
+ * an order fixed by the graph alone, so repeated calls give identical bits. */
+gcn_status gcn_aggregate_fwd(const gcn_graph* g, const void* X, int64_t ldx, int dtype, float* Y,
+                             int64_t ldy, int64_t F, void* stream);
+
+/* dX[n_cols x F] = A_hat^T G, G is [n_rows x F]. Same rules as the forward. */
+gcn_status gcn_aggregate_bwd(const gcn_graph* g, const void* G, int64_t ldg, int dtype, float* dX,
+                             int64_t lddx, int64_t F, void* stream);
+
+/* Forward aggregation whose input rows >= n_local_cols are halo rows held as
+ * uint8 codes (Section 6.1 step 3; quantization of Section 2.4 with b = 8):
+ *   x[j, f] = X_local[j, f]                                   j <  n_local_cols
+ *   x[j, f] = fmaf((float)Q_halo[h, f], halo_scale[h], halo_min[h]),
+ *             h = j - n_local_cols                             j >= n_local_cols
+ *   Y = A_hat x   (or A_hat^T x with GCN_Q8_USE_CSC; then x has n_rows rows
+ *                  and Y has n_cols rows).
+ *  X_local     fp32 [n_local_cols x F] (ldx); may be NULL if n_local_cols == 0.
+ *  Q_halo      uint8 [n_in - n_local_cols x F] (ldq), n_in = rows of x.
+ *  halo_min, halo_scale   fp32 [n_in - n_local_cols] (zero point Z, scale S).
+ *  Y           fp32 output (ldy). */
+gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_local_cols, const float* X_local,
+                                    int64_t ldx, const uint8_t* Q_halo, int64_t ldq,
+                                    const float* halo_min, const float* halo_scale, float* Y,
+                                    int64_t ldy, int64_t F, uint32_t flags, void* stream);
+
+/* Per-row uint8 quantization (Section 2.4 with b = 8, the producer side of
+ * the quantized exchange): Z = min_f X[i, f], S = (max - min) / 255 in fp32,
+ * Q[i, f] = clamp(rint((X[i, f] - Z) / S), 0, 255) with IEEE fp32 division
+ * and round-half-even (the paper's implementation drops the stochastic
+ * rounding, Section 7.3); every code is 0 when S == 0.
+ *  X [n x F] fp32 (ldx) -> Q [n x F] uint8 (ldq), zmin[n], scale[n] fp32. */
+gcn_status gcn_quantize_rows_u8(int64_t n, int64_t F, const float* X, int64_t ldx, uint8_t* Q,
+                                int64_t ldq, float* zmin, float* scale, void* stream);
+
+/* ---- support calls ---------------------------------------------------- */
+
+/* Release every device array of the graph (after synchronizing the device
+ * work that uses it is the caller's job). NULL is ignored. */
+void gcn_graph_free(gcn_graph* g);
+
+/* Host outputs (any may be NULL): shape and stored-entry count. */
+gcn_status gcn_graph_info(const gcn_graph* g, int64_t* n_rows, int64_t* n_cols, int64_t* nnz);
+
+/* Copy the canonical arrays of A (which = 0) or A^T (which = 1) to HOST
+ * memory: ptr [n_major + 1] (int64), idx [nnz] (int32 columns, increasing
+ * within a row), val [nnz] (fp32). Any output may be NULL. Synchronizes. */
+gcn_status gcn_graph_export(const gcn_graph* g, int which, int64_t* ptr, int32_t* idx, float* val,
+                            void* stream);
+
+/* Row-length classes the aggregation kernels use, for A (which = 0) or A^T
+ * (which = 1). Writes up to `cap` records of 4 int64 each to host memory:
+ * {first_len, last_len, rows, entries}, last_len = -1 meaning unbounded.
+ * Returns the number of classes in *n_classes. */
+gcn_status gcn_graph_bins(const gcn_graph* g, int which, int64_t* records, int cap,
+                          int* n_classes);
+
+/* Per-kernel device timing. While enabled, every kernel launch of the
+ * library is bracketed by HIP events on its stream; gcn_profile_read
+ * synchronizes those events and returns, per kernel name, the number of
+ * launches and their summed duration in milliseconds (host arrays of `cap`
+ * entries; names are static strings). Disabling clears the records. */
+gcn_status gcn_profile_enable(int on);
+gcn_status gcn_profile_read(const char** names, int64_t* launches, double* total_ms, int cap,
+                            int* n_kernels);
+
+/* Message describing the last failure on the calling thread ("" if none). */
+const char* gcn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GCNAGG_H */

@@ -132,6 +132,9 @@ def normalize(ptr, idx, deg):
     ptr = _c(ptr, np.int64)
     idx = _c(idx, np.int32)
     deg = _c(deg, np.int32)
+    n_major = len(ptr) - 1
+    if len(idx) and (len(deg) < n_major or int(idx.max()) >= len(deg)):
+        raise ValueError("deg must cover every row and column id")
     val = np.empty(len(idx), np.float32)
     _L().orc_normalize(len(ptr) - 1, _p(ptr), _p(idx), _p(deg), _p(val))
     return val
@@ -231,6 +234,8 @@ class Graph:
                 raise ValueError("a rectangular graph needs a supplied degree array")
             deg = row_degrees(self.csr_ptr, self.csr_idx)
         self.deg = np.asarray(deg, np.int32)
+        if len(self.deg) < max(n_rows, n_cols):
+            raise ValueError("deg must cover every node id: max(n_rows, n_cols) entries")
         if normalized:
             self.csr_val = normalize(self.csr_ptr, self.csr_idx, self.deg)
             self.csc_val = normalize(self.csc_ptr, self.csc_idx, self.deg)

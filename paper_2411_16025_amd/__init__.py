@@ -1,0 +1,12 @@
+"""MI355X-native GCN aggregation (SuperGCN, arXiv 2411.16025, Sections 4 and 6).
+
+The work runs in libgcnagg.so (hand-written HIP for gfx950, C ABI declared in
+include/gcnagg.h); ``gcnagg`` is its argument-marshalling binding over torch
+device tensors.
+"""
+
+from .gcnagg import (  # noqa: F401
+    EXPORTS, GCN_ADD_SELF_LOOPS, GCN_DT_BF16, GCN_DT_F32, GCN_Q8_USE_CSC, GCN_SYMMETRIZE,
+    GcnError, Graph, LIB_PATH, gcn_aggregate_bwd, gcn_aggregate_fwd, gcn_aggregate_fwd_q8halo,
+    gcn_build_csr, gcn_graph_bins, gcn_graph_export, gcn_graph_info, gcn_normalize,
+    gcn_profile_enable, gcn_profile_read, gcn_quantize_rows_u8, lib)

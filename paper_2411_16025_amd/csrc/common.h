@@ -1,0 +1,143 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "../../include/gcnagg.h"
+
+namespace gcn {
+
+constexpr uint64_t kMagic = 0x47434E4147473031ULL;  // "GCNAGG01"
+constexpr uint64_t kFreed = 0xDEADDEADDEADDEADULL;
+
+// One stored entry of a sparse matrix: column id and value side by side, so
+// the aggregation loads both with one 8-byte access.
+struct __align__(8) Ent {
+  int32_t col;
+  float val;
+};
+
+// Row-length classes (the binning that balances work across wavefronts).
+// Class c holds rows whose length lies in [kClassLo[c], kClassHi[c]].
+// Classes 0..kNumShort-1 are the "short" classes processed one row per lane
+// group; class kMedium runs one wavefront per row; class kChunked runs one
+// workgroup per chunk of at most chunk_len entries.
+constexpr int kNumClasses = 9;
+constexpr int kClassEmpty = 0;
+constexpr int kFirstShort = 1;
+constexpr int kLastShort = 6;
+constexpr int kMedium = 7;
+constexpr int kChunked = 8;
+
+struct Plan {
+  int32_t* rows = nullptr;        // [n_major] row ids grouped by class, increasing within a class
+  int64_t class_off[kNumClasses + 1] = {};  // host copy of the class boundaries in `rows`
+  int64_t class_nnz[kNumClasses] = {};      // host: stored entries per class
+  int64_t medium_max = 256;                 // longest row of the medium class
+  int64_t chunk_len = 2048;                 // entries per chunk of a chunked row
+  // chunk table for rows of the chunked class
+  int64_t n_chunks = 0;
+  int32_t* chunk_row = nullptr;   // [n_chunks]
+  int64_t* chunk_beg = nullptr;   // [n_chunks] first entry
+  int32_t* chunk_part = nullptr;  // [n_chunks] partial-row slot, -1 = writes the output row
+  // rows split over more than one chunk ("giant" rows) and their partials
+  int64_t n_giant = 0;
+  int64_t n_parts = 0;
+  int32_t* giant_row = nullptr;       // [n_giant]
+  int32_t* giant_part_off = nullptr;  // [n_giant + 1] first partial slot of each giant row
+};
+
+struct Mat {
+  int64_t n_major = 0, n_minor = 0, nnz = 0;
+  int64_t* ptr = nullptr;  // [n_major + 1]
+  Ent* ent = nullptr;      // [nnz]
+  Plan plan;
+};
+
+}  // namespace gcn
+
+struct gcn_graph {
+  uint64_t magic;
+  int device;
+  int64_t n_rows, n_cols;
+  uint32_t flags;
+  bool csc_shared;  // symmetric graph: A^T is A, csc aliases csr
+  bool normalized;
+  gcn::Mat csr;     // rows = destination nodes
+  gcn::Mat csc;     // rows = source nodes (A^T)
+};
+
+namespace gcn {
+
+// ---- error reporting -------------------------------------------------------
+void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
+void clear_error();
+gcn_status hip_fail(hipError_t e, const char* what, const char* file, int line);
+
+#define GCN_HIP(call)                                                       \
+  do {                                                                      \
+    hipError_t e_ = (call);                                                 \
+    if (e_ != hipSuccess) return ::gcn::hip_fail(e_, #call, __FILE__, __LINE__); \
+  } while (0)
+
+#define GCN_CHECK(expr)                        \
+  do {                                         \
+    gcn_status s_ = (expr);                    \
+    if (s_ != GCN_OK) return s_;               \
+  } while (0)
+
+gcn_status dmalloc(void** p, size_t bytes, const char* what);
+template <class T>
+gcn_status dalloc(T** p, int64_t count, const char* what) {
+  return dmalloc(reinterpret_cast<void**>(p), (size_t)(count > 0 ? count : 1) * sizeof(T), what);
+}
+void dfree(void* p);
+// Stream-ordered temporaries (hipMallocAsync / hipFreeAsync on `stream`).
+gcn_status tmalloc(void** p, size_t bytes, hipStream_t stream, const char* what);
+template <class T>
+gcn_status talloc(T** p, int64_t count, hipStream_t stream, const char* what) {
+  return tmalloc(reinterpret_cast<void**>(p), (size_t)(count > 0 ? count : 1) * sizeof(T), stream,
+                 what);
+}
+void tfree(void* p, hipStream_t stream);
+
+gcn_status check_graph(const gcn_graph* g);
+
+// ---- per-kernel profiling (see gcn_profile_enable) --------------------------
+bool profiling();
+struct ProfScope {
+  const char* name;
+  hipStream_t stream;
+  hipEvent_t start = nullptr;
+  ProfScope(const char* n, hipStream_t s);
+  ~ProfScope();
+};
+
+// ---- device primitives (sort.hip) -------------------------------------------
+// Stable LSD radix sort of n 64-bit keys on bits [0, bits); keys end up in
+// *keys (buffers may be swapped; both must hold n keys).
+gcn_status radix_sort_u64(uint64_t** keys, uint64_t** alt, int64_t n, int bits,
+                          hipStream_t stream);
+// Stable partition pass: sort by bits [lo_bit, lo_bit + 8) only.
+gcn_status radix_pass_u64(const uint64_t* in, uint64_t* out, int64_t n, int shift,
+                          hipStream_t stream);
+// Exclusive scan of int64 values; out[n] receives the total. in == out allowed.
+gcn_status scan_i64(const int64_t* in, int64_t* out, int64_t n, hipStream_t stream);
+
+// ---- plan building (build.hip) ----------------------------------------------
+gcn_status build_plan(Mat& m, hipStream_t stream);
+void free_mat(Mat& m, bool arrays);
+
+inline int bits_for(uint64_t max_value) {
+  int b = 0;
+  while (b < 64 && (max_value >> b) != 0) ++b;
+  return b;
+}
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace gcn

@@ -1,0 +1,288 @@
+"""Python binding of libgcnagg.so (argument marshalling only).
+
+Every function has the name of the C entry point it wraps (include/gcnagg.h)
+and passes device pointers of torch tensors plus the current torch stream.
+All computation runs in the library's HIP kernels; there is no fallback: if
+the library is missing or the call fails, an exception is raised.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgcnagg.so")
+
+GCN_SYMMETRIZE = 1
+GCN_ADD_SELF_LOOPS = 2
+GCN_DT_F32 = 0
+GCN_DT_BF16 = 1
+GCN_Q8_USE_CSC = 1
+
+STATUS = {0: "GCN_OK", 1: "GCN_EINVAL", 2: "GCN_ERANGE", 3: "GCN_ENOMEM", 4: "GCN_EHIP",
+          5: "GCN_ESTATE"}
+
+# every symbol include/gcnagg.h declares
+EXPORTS = ("gcn_build_csr", "gcn_normalize", "gcn_aggregate_fwd", "gcn_aggregate_bwd",
+           "gcn_aggregate_fwd_q8halo", "gcn_quantize_rows_u8", "gcn_graph_free",
+           "gcn_graph_info", "gcn_graph_export", "gcn_graph_bins", "gcn_profile_enable",
+           "gcn_profile_read", "gcn_last_error")
+
+
+class GcnError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__("%s: %s" % (STATUS.get(status, str(status)), message))
+        self.status = status
+        self.message = message
+
+
+_lib = None
+
+
+def lib():
+    """Load libgcnagg.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libgcnagg.so is not built (%s); run __graft_entry__.build()"
+                               % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        P, i64, u32, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint32, ctypes.c_int
+        L.gcn_build_csr.argtypes = [i64, i64, i64, P, P, u32, P, ctypes.POINTER(P)]
+        L.gcn_normalize.argtypes = [P, P, P]
+        L.gcn_aggregate_fwd.argtypes = [P, P, i64, i32, P, i64, i64, P]
+        L.gcn_aggregate_bwd.argtypes = [P, P, i64, i32, P, i64, i64, P]
+        L.gcn_aggregate_fwd_q8halo.argtypes = [P, i64, P, i64, P, i64, P, P, P, i64, i64, u32, P]
+        L.gcn_quantize_rows_u8.argtypes = [i64, i64, P, i64, P, i64, P, P, P]
+        L.gcn_graph_free.argtypes = [P]
+        L.gcn_graph_free.restype = None
+        L.gcn_graph_info.argtypes = [P, P, P, P]
+        L.gcn_graph_export.argtypes = [P, i32, P, P, P, P]
+        L.gcn_graph_bins.argtypes = [P, i32, P, i32, P]
+        L.gcn_profile_enable.argtypes = [i32]
+        L.gcn_profile_read.argtypes = [P, P, P, i32, P]
+        L.gcn_last_error.argtypes = []
+        L.gcn_last_error.restype = ctypes.c_char_p
+        for name in EXPORTS:
+            if name not in ("gcn_graph_free", "gcn_last_error"):
+                getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != 0:
+        raise GcnError(status, lib().gcn_last_error().decode())
+
+
+def _stream(stream):
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _dev(t, dtype=None, name="tensor"):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError("%s must be a CUDA (HIP) torch tensor" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must have dtype %s (got %s)" % (name, dtype, t.dtype))
+    return t
+
+
+def _rowmajor(t, name):
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("%s must be a 2-D row-major tensor (unit column stride)" % name)
+    return t.stride(0)
+
+
+class Graph:
+    """Owner of a gcn_graph handle."""
+
+    def __init__(self, handle: int):
+        self._h = ctypes.c_void_p(handle)
+        self.n_rows, self.n_cols, self.nnz = gcn_graph_info(self)
+
+    @property
+    def handle(self):
+        if not self._h:
+            raise GcnError(5, "graph already freed")
+        return self._h
+
+    def free(self):
+        if self._h:
+            lib().gcn_graph_free(self._h)
+            self._h = ctypes.c_void_p(0)
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def gcn_build_csr(n_rows: int, n_cols: int, src: torch.Tensor, dst: torch.Tensor, flags: int,
+                  stream=None) -> Graph:
+    _dev(src, torch.int32, "src")
+    _dev(dst, torch.int32, "dst")
+    if src.numel() != dst.numel() or not src.is_contiguous() or not dst.is_contiguous():
+        raise ValueError("src and dst must be contiguous and of equal length")
+    out = ctypes.c_void_p(0)
+    _check(lib().gcn_build_csr(n_rows, n_cols, src.numel(), src.data_ptr(), dst.data_ptr(), flags,
+                               _stream(stream), ctypes.byref(out)))
+    return Graph(out.value)
+
+
+def gcn_normalize(g: Graph, deg: torch.Tensor | None = None, stream=None):
+    if deg is not None:
+        _dev(deg, torch.int32, "deg")
+        if not deg.is_contiguous() or deg.numel() != max(g.n_rows, g.n_cols):
+            raise ValueError("deg must be contiguous with max(n_rows, n_cols) entries")
+    _check(lib().gcn_normalize(g.handle, deg.data_ptr() if deg is not None else None,
+                               _stream(stream)))
+
+
+def _dtype_code(t):
+    if t.dtype == torch.float32:
+        return GCN_DT_F32
+    if t.dtype == torch.bfloat16:
+        return GCN_DT_BF16
+    raise TypeError("input must be float32 or bfloat16")
+
+
+def gcn_aggregate_fwd(g: Graph, X: torch.Tensor, Y: torch.Tensor | None = None, stream=None):
+    """Y = A_hat X (allocates Y if not given)."""
+    _dev(X, None, "X")
+    ldx = _rowmajor(X, "X")
+    if X.shape[0] != g.n_cols:
+        raise ValueError("X must have n_cols = %d rows" % g.n_cols)
+    F = X.shape[1]
+    if Y is None:
+        Y = torch.empty((g.n_rows, F), dtype=torch.float32, device=X.device)
+    _dev(Y, torch.float32, "Y")
+    ldy = _rowmajor(Y, "Y")
+    if tuple(Y.shape) != (g.n_rows, F):
+        raise ValueError("Y must be n_rows x F")
+    _check(lib().gcn_aggregate_fwd(g.handle, X.data_ptr(), ldx, _dtype_code(X), Y.data_ptr(), ldy,
+                                   F, _stream(stream)))
+    return Y
+
+
+def gcn_aggregate_bwd(g: Graph, G: torch.Tensor, dX: torch.Tensor | None = None, stream=None):
+    """dX = A_hat^T G (allocates dX if not given)."""
+    _dev(G, None, "G")
+    ldg = _rowmajor(G, "G")
+    if G.shape[0] != g.n_rows:
+        raise ValueError("G must have n_rows = %d rows" % g.n_rows)
+    F = G.shape[1]
+    if dX is None:
+        dX = torch.empty((g.n_cols, F), dtype=torch.float32, device=G.device)
+    _dev(dX, torch.float32, "dX")
+    lddx = _rowmajor(dX, "dX")
+    if tuple(dX.shape) != (g.n_cols, F):
+        raise ValueError("dX must be n_cols x F")
+    _check(lib().gcn_aggregate_bwd(g.handle, G.data_ptr(), ldg, _dtype_code(G), dX.data_ptr(),
+                                   lddx, F, _stream(stream)))
+    return dX
+
+
+def gcn_aggregate_fwd_q8halo(g: Graph, n_local_cols: int, X_local, Q_halo, halo_min, halo_scale,
+                             Y: torch.Tensor | None = None, use_csc: bool = False, F=None,
+                             stream=None):
+    """Y = A_hat [X_local; fmaf(Q, S, Z)] (or A_hat^T with use_csc)."""
+    n_in, n_out = (g.n_rows, g.n_cols) if use_csc else (g.n_cols, g.n_rows)
+    ldx = ldq = 0
+    if X_local is not None:
+        _dev(X_local, torch.float32, "X_local")
+        ldx = _rowmajor(X_local, "X_local")
+        F = X_local.shape[1] if F is None else F
+        if X_local.shape[0] < n_local_cols:
+            raise ValueError("X_local has fewer than n_local_cols rows")
+    if Q_halo is not None:
+        _dev(Q_halo, torch.uint8, "Q_halo")
+        ldq = _rowmajor(Q_halo, "Q_halo")
+        F = Q_halo.shape[1] if F is None else F
+        n_h = n_in - n_local_cols
+        if Q_halo.shape[0] < n_h:
+            raise ValueError("Q_halo has fewer than %d rows" % n_h)
+        for t, nm in ((halo_min, "halo_min"), (halo_scale, "halo_scale")):
+            _dev(t, torch.float32, nm)
+            if t.numel() < n_h or not t.is_contiguous():
+                raise ValueError("%s needs %d contiguous entries" % (nm, n_h))
+    if F is None:
+        raise ValueError("F is unknown")
+    if Y is None:
+        dev = (X_local if X_local is not None else Q_halo).device
+        Y = torch.empty((n_out, F), dtype=torch.float32, device=dev)
+    _dev(Y, torch.float32, "Y")
+    ldy = _rowmajor(Y, "Y")
+    if tuple(Y.shape) != (n_out, F):
+        raise ValueError("Y must be %d x %d" % (n_out, F))
+    ptr = lambda t: t.data_ptr() if t is not None else None
+    _check(lib().gcn_aggregate_fwd_q8halo(
+        g.handle, n_local_cols, ptr(X_local), ldx, ptr(Q_halo), ldq, ptr(halo_min),
+        ptr(halo_scale), Y.data_ptr(), ldy, F, GCN_Q8_USE_CSC if use_csc else 0, _stream(stream)))
+    return Y
+
+
+def gcn_quantize_rows_u8(X: torch.Tensor, Q=None, zmin=None, scale=None, stream=None):
+    """Per-row uint8 codes and (zmin, scale) of an fp32 matrix."""
+    _dev(X, torch.float32, "X")
+    ldx = _rowmajor(X, "X")
+    n, F = X.shape
+    if Q is None:
+        Q = torch.empty((n, F), dtype=torch.uint8, device=X.device)
+    if zmin is None:
+        zmin = torch.empty(n, dtype=torch.float32, device=X.device)
+    if scale is None:
+        scale = torch.empty(n, dtype=torch.float32, device=X.device)
+    ldq = _rowmajor(Q, "Q")
+    _check(lib().gcn_quantize_rows_u8(n, F, X.data_ptr(), ldx, Q.data_ptr(), ldq, zmin.data_ptr(),
+                                      scale.data_ptr(), _stream(stream)))
+    return Q, zmin, scale
+
+
+def gcn_graph_info(g: Graph):
+    a, b, c = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().gcn_graph_info(g._h, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)))
+    return a.value, b.value, c.value
+
+
+def gcn_graph_export(g: Graph, which: int = 0, stream=None):
+    """Host copies (ptr int64, idx int32, val float32) of A (0) or A^T (1)."""
+    n_major = g.n_rows if which == 0 else g.n_cols
+    ptr = np.empty(n_major + 1, np.int64)
+    idx = np.empty(max(g.nnz, 1), np.int32)
+    val = np.empty(max(g.nnz, 1), np.float32)
+    _check(lib().gcn_graph_export(g.handle, which, ptr.ctypes.data, idx.ctypes.data,
+                                  val.ctypes.data, _stream(stream)))
+    return ptr, idx[:g.nnz], val[:g.nnz]
+
+
+def gcn_graph_bins(g: Graph, which: int = 0):
+    """List of dicts {first_len, last_len, rows, entries} per row-length class."""
+    rec = np.zeros((16, 4), np.int64)
+    n = ctypes.c_int(0)
+    _check(lib().gcn_graph_bins(g.handle, which, rec.ctypes.data, 16, ctypes.byref(n)))
+    return [dict(first_len=int(a), last_len=int(b), rows=int(c), entries=int(d))
+            for a, b, c, d in rec[:n.value]]
+
+
+def gcn_profile_enable(on: bool = True):
+    _check(lib().gcn_profile_enable(1 if on else 0))
+
+
+def gcn_profile_read():
+    """{kernel name: (launches, total ms)} of the launches since enabling."""
+    cap = 64
+    names = (ctypes.c_char_p * cap)()
+    launches = np.zeros(cap, np.int64)
+    ms = np.zeros(cap, np.float64)
+    n = ctypes.c_int(0)
+    _check(lib().gcn_profile_read(ctypes.cast(names, ctypes.c_void_p), launches.ctypes.data, ms.ctypes.data, cap,
+                                  ctypes.byref(n)))
+    return {names[i].decode(): (int(launches[i]), float(ms[i])) for i in range(min(n.value, cap))}
