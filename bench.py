@@ -1,0 +1,319 @@
+#!/usr/bin/env python
+"""Benchmark of the GCN aggregation hot path on one MI355X.
+
+One step = one forward aggregation Y = A_hat x and one backward aggregation
+dX = A_hat^T g over the same graph, where the last quarter of the node ids
+are halo rows held as uint8 codes with a per-row (min, scale) that the
+kernels dequantize on read (fused dequantize + aggregate). The default
+workload is the RMAT graph of scale 24 (16,777,216 nodes, 32 draws per
+node, quadrant probabilities .57/.19/.19/.05, relabelled by a seeded
+permutation, symmetrized, deduplicated, one self-loop per node), F = 128,
+fp32 inputs drawn from N(0, 1).
+
+Reported: modeled HBM bytes per second (CSR bytes + gathered-row bytes +
+output bytes, the minimum traffic of the algorithm) for the whole step,
+its fraction of the 8 TB/s HBM peak, edge-features per second, the
+dominant kernel's roofline figures from per-launch HIP events, and the CPU
+oracle timed on a bounded row sample of the same workload.
+
+The graph build (sort, deduplication, transpose, binning) and the
+normalization run once per graph; they are timed separately and are not
+part of a step.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "aggregation GB/s (% of HBM peak) + edge-features/s, fwd Â·X and bwd Âᵀ·G"
+HBM_PEAK_GBS = 8000.0
+AGG_SOURCE = os.path.join(ROOT, "paper_2411_16025_amd", "csrc", "aggregate.hip")
+COUNTERS = os.path.join(ROOT, "profiles", "agg_counters_rmat24_q8.txt")
+
+# kernel name -> row-length classes whose rows it processes
+KERNEL_CLASSES = {"agg_zero_rows": [0], "agg_short": [1, 2, 3, 4, 5, 6], "agg_medium": [7],
+                  "agg_chunk": [8]}
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="rmat24_q8",
+                    choices=["rmat24_q8", "rmat20", "er4096", "product", "partition"])
+    ap.add_argument("--cpu-target-s", type=float, default=12.0,
+                    help="approximate seconds of oracle work for the CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-steps", type=int, default=2,
+                    help="extra steps with per-kernel HIP event timing")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="first run one plain device copy of this size (a known-size kernel "
+                         "for scaling hardware byte counters)")
+    return ap.parse_args()
+
+
+def model_bytes(rows, entries, halo_entries, F, halo=True):
+    """Minimum traffic: row pointer (8 B/row), column + value (8 B/entry),
+    gathered rows (4F B for fp32, F + 8 B for a uint8 row with its min and
+    scale), output rows (4F B)."""
+    local = entries - halo_entries
+    return 8 * rows + 8 * entries + 4 * F * local + (F + 8) * halo_entries + 4 * F * rows
+
+
+def file_sha256(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def read_counters(kernel):
+    """HBM bytes per dispatch from the committed rocprofv3 PMC summary, only
+    if it was taken on the current aggregation source."""
+    if not os.path.exists(COUNTERS):
+        return None
+    kv = {}
+    for line in open(COUNTERS):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_sha256") != file_sha256(AGG_SOURCE) or kv.get("kernel") != kernel:
+        return None
+    try:
+        return float(kv["fetch_bytes_per_dispatch"]) + float(kv["write_bytes_per_dispatch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the aggregation path is built and timed on a "
+              "single MI355X (multi-GPU sharding is a design note, not part of this build); "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_2411_16025_amd as G
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    G.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    if args.calibrate_copy_mib > 0:
+        a = torch.empty(args.calibrate_copy_mib << 18, dtype=torch.float32, device=dev).fill_(1.0)
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+        log("copy calibration: %d MiB" % args.calibrate_copy_mib)
+
+    t0 = time.time()
+    w = {"rmat24_q8": synth.rmat24_q8, "rmat20": synth.rmat20, "er4096": synth.er_4096,
+         "product": synth.product_like, "partition": synth.partition_111m}[args.workload]()
+    k_seed = {"rmat24_q8": 5, "rmat20": 2, "er4096": 1, "product": 3, "partition": 4}[args.workload]
+    log("generated %s: %d edges in %.1f s" % (w.name, len(w.src), time.time() - t0))
+    F = w.F
+    q8 = w.n_local_cols is not None
+
+    # ---- build (once per graph; not part of a step) ----
+    src_d = torch.from_numpy(w.src).to(dev)
+    dst_d = torch.from_numpy(w.dst).to(dev)
+    torch.cuda.synchronize()
+    tb = time.time()
+    g = G.gcn_build_csr(w.n_rows, w.n_cols, src_d, dst_d, w.flags)
+    torch.cuda.synchronize()
+    build_ms = (time.time() - tb) * 1e3
+    del src_d, dst_d
+    deg_d = torch.from_numpy(w.deg).to(dev) if w.deg is not None else None
+    torch.cuda.synchronize()
+    tn = time.time()
+    G.gcn_normalize(g, deg_d)
+    torch.cuda.synchronize()
+    norm_ms = (time.time() - tn) * 1e3
+    log("built graph: nnz=%d build %.1f ms normalize %.1f ms" % (g.nnz, build_ms, norm_ms))
+
+    # ---- inputs (host generation, then HBM resident) ----
+    tx = time.time()
+    gen = synth.normal if q8 else synth.uniform
+    X_h = gen(3000 + k_seed, w.n_cols, F)
+    X = torch.from_numpy(X_h).to(dev)
+    G_h = gen(4000 + k_seed, w.n_rows, F)
+    Gd = torch.from_numpy(G_h).to(dev)
+    del G_h
+    if args.no_cpu_baseline:
+        X_h = None
+    nlc = w.n_local_cols
+    if q8:
+        QX, ZX, SX = G.gcn_quantize_rows_u8(X[nlc:])
+        QG, ZG, SG = G.gcn_quantize_rows_u8(Gd[nlc:])
+        X_loc, G_loc = X[:nlc], Gd[:nlc]
+    Y = torch.empty((w.n_rows, F), dtype=torch.float32, device=dev)
+    dX = torch.empty((w.n_cols, F), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    log("inputs ready in %.1f s" % (time.time() - tx))
+
+    if q8:
+        def fwd():
+            G.gcn_aggregate_fwd_q8halo(g, nlc, X_loc, QX, ZX, SX, Y=Y)
+
+        def bwd():
+            G.gcn_aggregate_fwd_q8halo(g, nlc, G_loc, QG, ZG, SG, Y=dX, use_csc=True)
+    else:
+        def fwd():
+            G.gcn_aggregate_fwd(g, X, Y=Y)
+
+        def bwd():
+            G.gcn_aggregate_bwd(g, Gd, dX=dX)
+
+    def step():
+        fwd()
+        bwd()
+
+    # ---- timed region ----
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ts = time.time()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    step_ms = (time.time() - ts) * 1e3 / args.steps
+    log("timed %d steps: %.3f ms/step" % (args.steps, step_ms))
+
+    # fwd / bwd split, HIP events on the stream the library launches on
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    fwd_ms = bwd_ms = 0.0
+    for _ in range(args.steps):
+        ev[0].record()
+        fwd()
+        ev[1].record()
+        bwd()
+        ev[2].record()
+        ev[2].synchronize()
+        fwd_ms += ev[0].elapsed_time(ev[1]) / args.steps
+        bwd_ms += ev[1].elapsed_time(ev[2]) / args.steps
+
+    # per-kernel durations (events around every launch, separate from the timed region)
+    G.gcn_profile_enable(True)
+    for _ in range(args.profile_steps):
+        step()
+    torch.cuda.synchronize()
+    prof = G.gcn_profile_read()
+    G.gcn_profile_enable(False)
+
+    # ---- traffic model ----
+    bins_f = G.gcn_graph_bins(g, 0, halo_from=nlc if q8 else -1)
+    bins_b = G.gcn_graph_bins(g, 1, halo_from=nlc if q8 else -1)
+
+    def pass_bytes(bins):
+        rows = sum(b["rows"] for b in bins)
+        ents = sum(b["entries"] for b in bins)
+        halo = sum(b["halo_entries"] for b in bins)
+        return model_bytes(rows, ents, halo, F) + 8, ents, halo
+
+    Bf, nnz_f, halo_f = pass_bytes(bins_f)
+    Bb, nnz_b, _ = pass_bytes(bins_b)
+    value = (Bf + Bb) / (step_ms * 1e-3) / 1e9
+    ef_per_s = (nnz_f + nnz_b) * F / (step_ms * 1e-3)
+
+    # dominant kernel and its roofline figures
+    agg = {k: v for k, v in prof.items() if k in KERNEL_CLASSES}
+    roofline = None
+    if agg:
+        dom = max(agg, key=lambda k: agg[k][1])
+        launches, tot_ms = agg[dom]
+        per_launch_bytes = 0.5 * sum(
+            model_bytes(b["rows"], b["entries"], b["halo_entries"], F)
+            for bins in (bins_f, bins_b) for c, b in enumerate(bins) if c in KERNEL_CLASSES[dom])
+        avg_ms = tot_ms / launches
+        achieved = per_launch_bytes / (avg_ms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": read_counters(dom),
+                    "bytes_per_launch": int(per_launch_bytes), "avg_launch_ms": round(avg_ms, 4)}
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name, "n_rows": w.n_rows, "n_cols": w.n_cols, "nnz": g.nnz,
+                   "F": F, "halo_rows": (w.n_cols - nlc) if q8 else 0,
+                   "halo_storage": "u8 + fp32 (min, scale) per row" if q8 else None,
+                   "step": "fwd A_hat x + bwd A_hat^T g" + (" with fused uint8 halo dequant" if q8 else "")},
+        "hbm_frac": round(value / HBM_PEAK_GBS, 4),
+        "edge_features_per_s": float("%.4g" % ef_per_s),
+        "fwd_ms": round(fwd_ms, 4), "bwd_ms": round(bwd_ms, 4),
+        "modeled_bytes_per_step": int(Bf + Bb),
+        "build_ms": round(build_ms, 1), "normalize_ms": round(norm_ms, 1),
+        "kernels_ms_per_step": {k: round(v[1] / max(args.profile_steps, 1), 4)
+                                for k, v in prof.items()},
+        "row_classes": [[b["first_len"], b["last_len"], b["rows"], b["entries"]] for b in bins_f],
+        "roofline": roofline,
+    }
+
+    # ---- CPU baseline: the oracle on a bounded sample of the same workload ----
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, X_h, nlc, F, args.cpu_target_s)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w, X_h, nlc, F, target_s):
+    import oracle
+    import synth
+
+    order = synth.permutation(778, w.n_rows)  # rows in a seeded random order
+    q8 = nlc is not None
+    if q8:
+        Q, Z, S = oracle.quantize_rows(X_h[nlc:])
+
+    def run(n_sel):
+        sel = np.sort(order[:n_sel]).astype(np.int32)
+        ptr, idx = oracle.rows_of(w.n_rows, w.n_cols, w.src, w.dst, w.flags, sel)
+        val = np.ones(len(idx), np.float32)  # unit weights: the cost does not depend on them
+        t = time.time()
+        if q8:
+            oracle.spmm_q8(ptr, idx, val, nlc, X_h[:nlc], Q, Z, S)
+        else:
+            oracle.spmm(ptr, idx, val, X_h)
+        dt = time.time() - t
+        halo = int(np.sum(idx >= nlc)) if q8 else 0
+        return dt, len(sel), len(idx), halo
+
+    n = min(w.n_rows, max(64, w.n_rows // 400))
+    dt, rows, ents, halo = run(n)
+    for _ in range(4):  # grow the sample until it is about target_s of oracle work
+        if dt >= 0.6 * target_s or n >= w.n_rows:
+            break
+        n = int(min(w.n_rows, n * min(8.0, target_s / max(dt, 1e-3))))
+        dt, rows, ents, halo = run(n)
+    B = model_bytes(rows, ents, halo, F)
+    return {"value": round(B / dt / 1e9, 3), "unit": "GB/s", "cores": oracle.num_threads(),
+            "kind": "oracle", "edge_features_per_s": float("%.4g" % (ents * F / dt)),
+            "seconds": round(dt, 2),
+            "sample": "forward aggregation (fp64 accumulation%s) over %d uniformly sampled rows "
+                      "(%d entries) of %s, unit weights; structure of the sampled rows built by "
+                      "the oracle from the edge list beforehand (untimed)"
+                      % (", uint8 halo dequantized" if q8 else "", rows, ents, w.name)}
+
+
+if __name__ == "__main__":
+    main()

@@ -150,11 +150,13 @@ gcn_status gcn_graph_export(const gcn_graph* g, int which, int64_t* ptr, int32_t
                             void* stream);
 
 /* Row-length classes the aggregation kernels use, for A (which = 0) or A^T
- * (which = 1). Writes up to `cap` records of 4 int64 each to host memory:
- * {first_len, last_len, rows, entries}, last_len = -1 meaning unbounded.
- * Returns the number of classes in *n_classes. */
-gcn_status gcn_graph_bins(const gcn_graph* g, int which, int64_t* records, int cap,
-                          int* n_classes);
+ * (which = 1). Writes up to `cap` records of 5 int64 each to host memory:
+ * {first_len, last_len, rows, entries, entries with column >= halo_from},
+ * last_len = -1 meaning unbounded (pass halo_from = -1 to skip the last
+ * count, which is then 0). Returns the number of classes in *n_classes.
+ * Synchronizes `stream` when halo_from >= 0. */
+gcn_status gcn_graph_bins(const gcn_graph* g, int which, int64_t halo_from, int64_t* records,
+                          int cap, int* n_classes, void* stream);
 
 /* Per-kernel device timing. While enabled, every kernel launch of the
  * library is bracketed by HIP events on its stream; gcn_profile_read

@@ -194,6 +194,31 @@ __global__ void k_chunks(const int32_t* __restrict__ rows, int64_t n, const int6
   if (i == n - 1) giant_part_off[n_giant] = (int32_t)part_off[n];
 }
 
+// per-class count of entries whose column is >= halo_from
+__global__ void k_class_halo(const int64_t* __restrict__ ptr, const Ent* __restrict__ ent,
+                             int64_t n_major, int64_t medium_max, int64_t halo_from,
+                             unsigned long long* __restrict__ counts) {
+  __shared__ unsigned long long cnt[kNumClasses];
+  if (threadIdx.x < kNumClasses) cnt[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r < n_major) {
+    int64_t lo = ptr[r], hi = ptr[r + 1];
+    const int64_t end = hi;
+    const int c = row_class(hi - lo, medium_max);
+    while (lo < hi) {  // first column >= halo_from
+      const int64_t mid = (lo + hi) >> 1;
+      if ((int64_t)ent[mid].col < halo_from)
+        lo = mid + 1;
+      else
+        hi = mid;
+    }
+    if (end > lo) atomicAdd(&cnt[c], (unsigned long long)(end - lo));
+  }
+  __syncthreads();
+  if (threadIdx.x < kNumClasses && cnt[threadIdx.x]) atomicAdd(&counts[threadIdx.x], cnt[threadIdx.x]);
+}
+
 // ---- normalization -------------------------------------------------------------
 
 // deg[v] = stored entries of row v other than (v, v)
@@ -706,22 +731,38 @@ extern "C" gcn_status gcn_graph_export(const gcn_graph* g, int which, int64_t* p
   return GCN_OK;
 }
 
-extern "C" gcn_status gcn_graph_bins(const gcn_graph* g, int which, int64_t* records, int cap,
-                                     int* n_classes) {
+extern "C" gcn_status gcn_graph_bins(const gcn_graph* g, int which, int64_t halo_from,
+                                     int64_t* records, int cap, int* n_classes, void* stream_) {
   clear_error();
   GCN_CHECK(check_graph(g));
   if (which != 0 && which != 1) {
     set_error("which must be 0 (A) or 1 (A^T)");
     return GCN_EINVAL;
   }
-  const Plan& p = (which ? g->csc : g->csr).plan;
+  const Mat& m = which ? g->csc : g->csr;
+  const Plan& p = m.plan;
+  unsigned long long halo[kNumClasses] = {};
+  if (halo_from >= 0 && m.n_major > 0) {
+    hipStream_t stream = (hipStream_t)stream_;
+    unsigned long long* d = nullptr;
+    GCN_CHECK(talloc(&d, kNumClasses, stream, "halo counts"));
+    GCN_HIP(hipMemsetAsync(d, 0, sizeof(halo), stream));
+    hipLaunchKernelGGL(k_class_halo, dim3(grid_for(m.n_major)), dim3(kThreads), 0, stream,
+                       (const int64_t*)m.ptr, (const Ent*)m.ent, m.n_major, p.medium_max, halo_from,
+                       d);
+    GCN_HIP(hipGetLastError());
+    GCN_HIP(hipMemcpyAsync(halo, d, sizeof(halo), hipMemcpyDeviceToHost, stream));
+    tfree(d, stream);
+    GCN_HIP(hipStreamSynchronize(stream));
+  }
   static const int64_t lo[kNumClasses] = {0, 1, 2, 3, 5, 9, 17, 33, -1};
   static const int64_t hi[kNumClasses] = {0, 1, 2, 4, 8, 16, 32, -1, -1};
   for (int c = 0; c < kNumClasses && c < cap && records; ++c) {
-    records[4 * c + 0] = c == kChunked ? p.medium_max + 1 : lo[c];
-    records[4 * c + 1] = c == kMedium ? p.medium_max : hi[c];
-    records[4 * c + 2] = p.class_off[c + 1] - p.class_off[c];
-    records[4 * c + 3] = p.class_nnz[c];
+    records[5 * c + 0] = c == kChunked ? p.medium_max + 1 : lo[c];
+    records[5 * c + 1] = c == kMedium ? p.medium_max : hi[c];
+    records[5 * c + 2] = p.class_off[c + 1] - p.class_off[c];
+    records[5 * c + 3] = p.class_nnz[c];
+    records[5 * c + 4] = (int64_t)halo[c];
   }
   if (n_classes) *n_classes = kNumClasses;
   return GCN_OK;

@@ -61,7 +61,7 @@ def lib():
         L.gcn_graph_free.restype = None
         L.gcn_graph_info.argtypes = [P, P, P, P]
         L.gcn_graph_export.argtypes = [P, i32, P, P, P, P]
-        L.gcn_graph_bins.argtypes = [P, i32, P, i32, P]
+        L.gcn_graph_bins.argtypes = [P, i32, i64, P, i32, P, P]
         L.gcn_profile_enable.argtypes = [i32]
         L.gcn_profile_read.argtypes = [P, P, P, i32, P]
         L.gcn_last_error.argtypes = []
@@ -263,13 +263,14 @@ def gcn_graph_export(g: Graph, which: int = 0, stream=None):
     return ptr, idx[:g.nnz], val[:g.nnz]
 
 
-def gcn_graph_bins(g: Graph, which: int = 0):
-    """List of dicts {first_len, last_len, rows, entries} per row-length class."""
-    rec = np.zeros((16, 4), np.int64)
+def gcn_graph_bins(g: Graph, which: int = 0, halo_from: int = -1, stream=None):
+    """Per row-length class: dict(first_len, last_len, rows, entries, halo_entries)."""
+    rec = np.zeros((16, 5), np.int64)
     n = ctypes.c_int(0)
-    _check(lib().gcn_graph_bins(g.handle, which, rec.ctypes.data, 16, ctypes.byref(n)))
-    return [dict(first_len=int(a), last_len=int(b), rows=int(c), entries=int(d))
-            for a, b, c, d in rec[:n.value]]
+    _check(lib().gcn_graph_bins(g.handle, which, halo_from, rec.ctypes.data, 16, ctypes.byref(n),
+                                _stream(stream)))
+    return [dict(first_len=int(a), last_len=int(b), rows=int(c), entries=int(d),
+                 halo_entries=int(e)) for a, b, c, d, e in rec[:n.value]]
 
 
 def gcn_profile_enable(on: bool = True):
