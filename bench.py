@@ -56,7 +56,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="rmat24_q8",
-                    choices=["rmat24_q8", "rmat20", "er4096", "product", "partition"])
+                    choices=["rmat24_q8", "rmat24", "rmat20", "er4096", "product", "partition"])
     ap.add_argument("--cpu-target-s", type=float, default=12.0,
                     help="approximate seconds of oracle work for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -126,9 +126,9 @@ def main():
         log("copy calibration: %d MiB" % args.calibrate_copy_mib)
 
     t0 = time.time()
-    w = {"rmat24_q8": synth.rmat24_q8, "rmat20": synth.rmat20, "er4096": synth.er_4096,
+    w = {"rmat24_q8": synth.rmat24_q8, "rmat24": synth.rmat24, "rmat20": synth.rmat20, "er4096": synth.er_4096,
          "product": synth.product_like, "partition": synth.partition_111m}[args.workload]()
-    k_seed = {"rmat24_q8": 5, "rmat20": 2, "er4096": 1, "product": 3, "partition": 4}[args.workload]
+    k_seed = {"rmat24_q8": 5, "rmat24": 5, "rmat20": 2, "er4096": 1, "product": 3, "partition": 4}[args.workload]
     log("generated %s: %d edges in %.1f s" % (w.name, len(w.src), time.time() - t0))
     F = w.F
     q8 = w.n_local_cols is not None

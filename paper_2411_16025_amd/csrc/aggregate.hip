@@ -43,25 +43,37 @@ constexpr int kWavesPerBlock = kBlock / 64;
 
 // ---- gather policies ----------------------------------------------------------
 
+// Every policy splits a gather into fetch (issue the loads of features
+// [f0, f0 + VEC) of input row j into raw registers, f0 < F) and decode (turn
+// the raw registers into fp32 values). A loop issues the fetches of a whole
+// group of entries before it decodes any of them, so no load waits on the
+// arithmetic of another.
+
 template <int VEC>
 struct SrcF32 {
   const float* __restrict__ x;
   int64_t ld;
   int F;
-  // features [f0, f0 + VEC) of input row j (f0 < F)
-  __device__ inline void load(int32_t j, int f0, float* out) const {
+  struct Raw {
+    float v[VEC];
+  };
+  __device__ inline void fetch(int32_t j, int f0, Raw& r) const {
     const float* p = x + (int64_t)j * ld + f0;
     if constexpr (VEC == 4) {
       if (f0 + 4 <= F) {
         const f4 v = *reinterpret_cast<const f4*>(p);
-        out[0] = v.x; out[1] = v.y; out[2] = v.z; out[3] = v.w;
+        r.v[0] = v.x; r.v[1] = v.y; r.v[2] = v.z; r.v[3] = v.w;
       } else {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) out[v] = (f0 + v < F) ? p[v] : 0.f;
+        for (int v = 0; v < 4; ++v) r.v[v] = (f0 + v < F) ? p[v] : 0.f;
       }
     } else {
-      out[0] = p[0];
+      r.v[0] = p[0];
     }
+  }
+  __device__ inline void decode(const Raw& r, int32_t, float* out) const {
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) out[v] = r.v[v];
   }
 };
 
@@ -72,25 +84,33 @@ struct SrcBF16 {
   const uint16_t* __restrict__ x;
   int64_t ld;
   int F;
-  __device__ inline void load(int32_t j, int f0, float* out) const {
+  struct Raw {
+    uint16_t v[VEC];
+  };
+  __device__ inline void fetch(int32_t j, int f0, Raw& r) const {
     const uint16_t* p = x + (int64_t)j * ld + f0;
     if constexpr (VEC == 4) {
       if (f0 + 4 <= F) {
         const us4 v = *reinterpret_cast<const us4*>(p);
-        out[0] = bf16_to_f32(v.x); out[1] = bf16_to_f32(v.y);
-        out[2] = bf16_to_f32(v.z); out[3] = bf16_to_f32(v.w);
+        r.v[0] = v.x; r.v[1] = v.y; r.v[2] = v.z; r.v[3] = v.w;
       } else {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) out[v] = (f0 + v < F) ? bf16_to_f32(p[v]) : 0.f;
+        for (int v = 0; v < 4; ++v) r.v[v] = (f0 + v < F) ? p[v] : (uint16_t)0;
       }
     } else {
-      out[0] = bf16_to_f32(p[0]);
+      r.v[0] = p[0];
     }
+  }
+  __device__ inline void decode(const Raw& r, int32_t, float* out) const {
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) out[v] = bf16_to_f32(r.v[v]);
   }
 };
 
 // Input rows j < n_local are fp32; rows j >= n_local are uint8 codes with a
-// per-row zero point and scale: x = fmaf(q, S, Z), exactly one rounding.
+// per-row zero point and scale: x = fmaf(q, S, Z), exactly one rounding. A
+// halo row's raw registers hold the packed codes, Z and S in the slots a
+// local row uses for its features, so both kinds cost the same registers.
 template <int VEC>
 struct SrcQ8 {
   const float* __restrict__ x;
@@ -101,27 +121,45 @@ struct SrcQ8 {
   const float* __restrict__ zmin;
   const float* __restrict__ scale;
   int F;
-  __device__ inline void load(int32_t j, int f0, float* out) const {
+  struct Raw {
+    float v[VEC < 3 ? 3 : VEC];  // local: features; halo: {codes, Z, S}
+  };
+  __device__ inline void fetch(int32_t j, int f0, Raw& r) const {
     if ((int64_t)j < n_local) {
-      SrcF32<VEC>{x, ldx, F}.load(j, f0, out);
+      typename SrcF32<VEC>::Raw fr;
+      SrcF32<VEC>{x, ldx, F}.fetch(j, f0, fr);
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) r.v[v] = fr.v[v];
       return;
     }
     const int64_t h = (int64_t)j - n_local;
     const uint8_t* p = q + h * ldq + f0;
-    const float z = zmin[h], s = scale[h];
+    r.v[1] = zmin[h];
+    r.v[2] = scale[h];
+    uint32_t c;
     if constexpr (VEC == 4) {
       if (f0 + 4 <= F) {
-        const uint32_t w = *reinterpret_cast<const uint32_t*>(p);
-        out[0] = __builtin_fmaf((float)(w & 255u), s, z);
-        out[1] = __builtin_fmaf((float)((w >> 8) & 255u), s, z);
-        out[2] = __builtin_fmaf((float)((w >> 16) & 255u), s, z);
-        out[3] = __builtin_fmaf((float)(w >> 24), s, z);
+        c = *reinterpret_cast<const uint32_t*>(p);
       } else {
+        c = 0;
 #pragma unroll
-        for (int v = 0; v < 4; ++v) out[v] = (f0 + v < F) ? __builtin_fmaf((float)p[v], s, z) : 0.f;
+        for (int v = 0; v < 4; ++v)
+          if (f0 + v < F) c |= (uint32_t)p[v] << (8 * v);
       }
     } else {
-      out[0] = __builtin_fmaf((float)p[0], s, z);
+      c = p[0];
+    }
+    r.v[0] = __uint_as_float(c);
+  }
+  __device__ inline void decode(const Raw& r, int32_t j, float* out) const {
+    if ((int64_t)j >= n_local) {
+      const uint32_t c = __float_as_uint(r.v[0]);
+#pragma unroll
+      for (int v = 0; v < VEC; ++v)
+        out[v] = __builtin_fmaf((float)((c >> (8 * v)) & 255u), r.v[2], r.v[1]);
+    } else {
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) out[v] = r.v[v];
     }
   }
 };
@@ -144,34 +182,83 @@ __device__ inline void store_row(float* __restrict__ y, int f0, int F, const flo
   }
 }
 
-// acc += sum over k = first, first + stride, ... < end of val[k] * x[col[k]],
-// in increasing k; U gathers are issued before they are consumed.
-template <int VEC, int U, class Src>
-__device__ inline void accumulate(const Ent* __restrict__ ent, int64_t first, int64_t end,
-                                  int64_t stride, const Src& src, int f0, bool active,
-                                  float* acc) {
-  for (int64_t k = first; k < end; k += (int64_t)U * stride) {
-    float w[U];
-    float xv[U][VEC];
+// Gathers in flight per lane in the entry loops.
+#ifndef GCN_AGG_UNROLL
+#define GCN_AGG_UNROLL 4
+#endif
+// Unroll factor of the loop over gather groups inside a 64-entry block (1
+// keeps the register count, and so the occupancy, of one group).
+#ifndef GCN_GROUP_UNROLL
+#define GCN_GROUP_UNROLL 1
+#endif
+// Waves per SIMD the entry-loop kernels must fit (caps their registers).
+#ifndef GCN_MIN_WAVES
+#define GCN_MIN_WAVES 8
+#endif
+#define GCN_PRAGMA(x) _Pragma(#x)
+#define GCN_UNROLL_N(n) GCN_PRAGMA(unroll n)
+
+// One (column, value) pair, loaded without keeping it in the caches: the
+// entry stream is read once per pass, so L2 and the Infinity Cache are left
+// to the gathered feature rows, which hub columns reuse.
+__device__ inline Ent load_ent(const Ent* p) {
+  const uint64_t raw = __builtin_nontemporal_load(reinterpret_cast<const uint64_t*>(p));
+  Ent e;
+  e.col = (int32_t)(uint32_t)raw;
+  e.val = __uint_as_float((uint32_t)(raw >> 32));
+  return e;
+}
+
+// One wavefront adds val[k] * x[col[k]] for the entries k of [beg, end) in
+// 64-entry blocks starting at beg + 64 * (first + j * stride), j = 0, 1, ...
+// The 64 lanes load a block's (column, value) pairs with one coalesced
+// access, and the next block's load is issued before this block's gathers;
+// slot s takes block positions s, s + E, s + 2E, ... through lane shuffles,
+// with U row gathers in flight per lane. A slot's terms are added in
+// increasing entry order.
+template <int VEC, int G, int U, class Src>
+__device__ inline void accumulate_blocks(const Ent* __restrict__ ent, int64_t beg, int64_t end,
+                                         int64_t first, int64_t stride, const Src& src, int f0,
+                                         bool active, float* acc) {
+  constexpr int E = 64 / G;
+  constexpr int UU = U < G ? U : G;
+  const int lane = threadIdx.x & 63;
+  const int slot = lane / G;
+  int64_t base = beg + first * 64;
+  const int64_t step = stride * 64;
+  Ent cur = {0, 0.f};
+  if (base + lane < end) cur = load_ent(ent + base + lane);
+  while (base < end) {
+    const int64_t nbase = base + step;
+    Ent nxt = {0, 0.f};
+    const int n = (int)((end - base) < 64 ? (end - base) : 64);
+    GCN_UNROLL_N(GCN_GROUP_UNROLL)
+    for (int p0 = 0; p0 < G; p0 += UU) {
+      if (p0 * E >= n) break;
+      float w[UU];
+      int32_t col[UU];
+      typename Src::Raw raw[UU];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int64_t ku = k + (int64_t)u * stride;
-      w[u] = 0.f;
+      for (int u = 0; u < UU; ++u) {
+        const int pos = (p0 + u) * E + slot;
+        col[u] = __shfl(cur.col, pos, 64);
+        w[u] = __shfl(cur.val, pos, 64);
+        if (pos < n && active) src.fetch(col[u], f0, raw[u]);
+      }
+      // the next block's pairs travel with the first group's gathers
+      if (p0 == 0 && nbase + lane < end) nxt = load_ent(ent + nbase + lane);
 #pragma unroll
-      for (int v = 0; v < VEC; ++v) xv[u][v] = 0.f;
-      if (ku < end) {
-        const Ent e = ent[ku];
-        w[u] = e.val;
-        if (active) src.load(e.col, f0, xv[u]);
+      for (int u = 0; u < UU; ++u) {
+        if ((p0 + u) * E + slot < n && active) {
+          float xv[VEC];
+          src.decode(raw[u], col[u], xv);
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) acc[v] = __builtin_fmaf(w[u], xv[v], acc[v]);
+        }
       }
     }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (k + (int64_t)u * stride < end) {
-#pragma unroll
-        for (int v = 0; v < VEC; ++v) acc[v] = __builtin_fmaf(w[u], xv[u][v], acc[v]);
-      }
-    }
+    cur = nxt;
+    base = nbase;
   }
 }
 
@@ -189,6 +276,7 @@ __device__ inline void reduce_slots(float* acc) {
 struct ShortArgs {
   int64_t row_off[kLastShort - kFirstShort + 2];   // rows of short class c start at row_off[c-1]
   int64_t wave_off[kLastShort - kFirstShort + 2];  // first wavefront of each short class
+  int32_t len_hi[kLastShort - kFirstShort + 1];    // longest row of each short class
 };
 
 // ---- kernels ---------------------------------------------------------------------
@@ -210,31 +298,70 @@ __global__ __launch_bounds__(kBlock) void k_zero_rows(const int32_t* __restrict_
 }
 
 // Rows with 1..32 entries: one row per slot, E rows per wavefront, the rows
-// of one wavefront from one length class.
+// of one wavefront from one length class. The G lanes of a slot load the
+// row's (column, value) pairs with one coalesced access and share them by
+// lane shuffles; the loop bound is the class's longest row, so every lane
+// of the wavefront runs the same iterations.
 template <int VEC, int G, class Src>
-__global__ __launch_bounds__(kBlock) void k_short(const int64_t* __restrict__ ptr,
+__global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* __restrict__ ptr,
                                                   const Ent* __restrict__ ent,
                                                   const int32_t* __restrict__ rows, ShortArgs sa,
                                                   Src src, float* __restrict__ y, int64_t ldy,
                                                   int F) {
   constexpr int E = 64 / G;
   constexpr int NS = kLastShort - kFirstShort + 1;
+  constexpr int U = 4;
   const int lane = threadIdx.x & 63;
+  const int slot = lane / G, gl = lane % G;
   const int64_t wave = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+  if (wave >= sa.wave_off[NS]) return;  // whole wavefront leaves together
   int c = 0;
 #pragma unroll
   for (int k = 1; k < NS; ++k)
     if (wave >= sa.wave_off[k]) c = k;
-  const int64_t i = sa.row_off[c] + (wave - sa.wave_off[c]) * E + lane / G;
-  const int f0 = (int)blockIdx.y * G * VEC + (lane % G) * VEC;
-  if (wave >= sa.wave_off[NS] || i >= sa.row_off[c + 1] || f0 >= F) return;
-  const int32_t r = rows[i];
-  const int64_t b = ptr[r], e = ptr[r + 1];
+  const int64_t i = sa.row_off[c] + (wave - sa.wave_off[c]) * E + slot;
+  const int f0 = (int)blockIdx.y * G * VEC + gl * VEC;
+  const bool has_row = i < sa.row_off[c + 1];
+  const bool active = has_row && f0 < F;
+  int32_t r = 0;
+  int64_t b = 0;
+  int len = 0;
+  if (has_row) {
+    r = rows[i];
+    b = ptr[r];
+    len = (int)(ptr[r + 1] - b);
+  }
   float acc[VEC];
 #pragma unroll
   for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
-  accumulate<VEC, 4>(ent, b, e, 1, src, f0, true, acc);
-  store_row<VEC>(y + (int64_t)r * ldy, f0, F, acc);
+  const int hi = sa.len_hi[c];
+  for (int p0 = 0; p0 < hi; p0 += G) {
+    Ent me = {0, 0.f};
+    if (p0 + gl < len) me = load_ent(ent + b + p0 + gl);
+    const int np = (hi - p0) < G ? (hi - p0) : G;
+    for (int p = 0; p < np; p += U) {
+      float w[U];
+      int32_t col[U];
+      typename Src::Raw raw[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int pos = (p + u) < G ? (p + u) : (G - 1);
+        col[u] = __shfl(me.col, slot * G + pos, 64);
+        w[u] = __shfl(me.val, slot * G + pos, 64);
+        if (p + u < np && p0 + p + u < len && active) src.fetch(col[u], f0, raw[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (p + u < np && p0 + p + u < len && active) {
+          float xv[VEC];
+          src.decode(raw[u], col[u], xv);
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) acc[v] = __builtin_fmaf(w[u], xv[v], acc[v]);
+        }
+      }
+    }
+  }
+  if (active) store_row<VEC>(y + (int64_t)r * ldy, f0, F, acc);
 }
 
 // Rows with 33..medium_max entries: one wavefront per row.
@@ -244,7 +371,6 @@ __global__ __launch_bounds__(kBlock) void k_medium(const int64_t* __restrict__ p
                                                    const int32_t* __restrict__ rows, int64_t n,
                                                    Src src, float* __restrict__ y, int64_t ldy,
                                                    int F) {
-  constexpr int E = 64 / G;
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
   if (i >= n) return;  // whole wavefront leaves together
@@ -256,38 +382,37 @@ __global__ __launch_bounds__(kBlock) void k_medium(const int64_t* __restrict__ p
   float acc[VEC];
 #pragma unroll
   for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
-  accumulate<VEC, 4>(ent, b + slot, e, E, src, f0, active, acc);
+  accumulate_blocks<VEC, G, GCN_AGG_UNROLL>(ent, b, e, 0, 1, src, f0, active, acc);
   reduce_slots<VEC, G>(acc);
   if (slot == 0 && active) store_row<VEC>(y + (int64_t)r * ldy, f0, F, acc);
 }
 
-// One workgroup per chunk of a long row. The 4*E slots of the workgroup
-// interleave the chunk's entries; wavefront sums meet in LDS and are added in
-// wavefront order. Single-chunk rows write Y, others a partial row.
+// One workgroup per chunk of a long row. Wavefront w of the workgroup takes
+// the chunk's 64-entry blocks w, w + 4, w + 8, ...; wavefront sums meet in
+// LDS and are added in wavefront order. Single-chunk rows write Y, others a
+// partial row.
 template <int VEC, int G, class Src>
-__global__ __launch_bounds__(kBlock) void k_chunk(const int64_t* __restrict__ ptr,
-                                                  const Ent* __restrict__ ent,
+__global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_chunk(const Ent* __restrict__ ent,
                                                   const int32_t* __restrict__ chunk_row,
                                                   const int64_t* __restrict__ chunk_beg,
-                                                  const int32_t* __restrict__ chunk_part,
-                                                  int64_t chunk_len, Src src,
+                                                  const int64_t* __restrict__ chunk_end,
+                                                  const int32_t* __restrict__ chunk_part, Src src,
                                                   float* __restrict__ y, int64_t ldy,
                                                   float* __restrict__ parts, int64_t ldp, int F) {
-  constexpr int E = 64 / G;
   __shared__ float red[kWavesPerBlock][G * VEC];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int slot = lane / G, gl = lane % G;
   const int64_t c = blockIdx.x;
   const int32_t r = chunk_row[c];
   const int64_t beg = chunk_beg[c];
-  const int64_t end = std::min(beg + chunk_len, ptr[r + 1]);
+  const int64_t end = chunk_end[c];
   const int f0 = (int)blockIdx.y * G * VEC + gl * VEC;
   const bool active = f0 < F;
   float acc[VEC];
 #pragma unroll
   for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
-  accumulate<VEC, 4>(ent, beg + wave * E + slot, end, (int64_t)kWavesPerBlock * E, src, f0,
-                     active, acc);
+  accumulate_blocks<VEC, G, GCN_AGG_UNROLL>(ent, beg, end, wave, kWavesPerBlock, src, f0, active,
+                                            acc);
   reduce_slots<VEC, G>(acc);
   if (slot == 0) {
 #pragma unroll
@@ -377,7 +502,10 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
   for (int c = kFirstShort; c <= kLastShort + 1; ++c) {
     sa.row_off[c - kFirstShort] = p.class_off[c];
     sa.wave_off[c - kFirstShort] = waves;
-    if (c <= kLastShort) waves += ceil_div(p.class_off[c + 1] - p.class_off[c], E);
+    if (c <= kLastShort) {
+      waves += ceil_div(p.class_off[c + 1] - p.class_off[c], E);
+      sa.len_hi[c - kFirstShort] = kClassHi[c];
+    }
   }
   if (waves > 0) {
     ProfScope ps("agg_short", stream);
@@ -403,9 +531,9 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
     {
       ProfScope ps("agg_chunk", stream);
       hipLaunchKernelGGL((k_chunk<VEC, G, Src>), dim3((unsigned)p.n_chunks, tiles), dim3(kBlock), 0,
-                         stream, (const int64_t*)m.ptr, (const Ent*)m.ent,
-                         (const int32_t*)p.chunk_row, (const int64_t*)p.chunk_beg,
-                         (const int32_t*)p.chunk_part, p.chunk_len, src, y, ldy, parts, ldp, F);
+                         stream, (const Ent*)m.ent, (const int32_t*)p.chunk_row,
+                         (const int64_t*)p.chunk_beg, (const int64_t*)p.chunk_end,
+                         (const int32_t*)p.chunk_part, src, y, ldy, parts, ldp, F);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) {
         tfree(parts, stream);

@@ -173,7 +173,8 @@ __global__ void k_chunks(const int32_t* __restrict__ rows, int64_t n, const int6
                          int64_t chunk_len, const int64_t* __restrict__ chunk_off,
                          const int64_t* __restrict__ part_off, const int64_t* __restrict__ giant_idx,
                          int32_t* __restrict__ chunk_row, int64_t* __restrict__ chunk_beg,
-                         int32_t* __restrict__ chunk_part, int32_t* __restrict__ giant_row,
+                         int64_t* __restrict__ chunk_end, int32_t* __restrict__ chunk_part,
+                         int32_t* __restrict__ giant_row,
                          int32_t* __restrict__ giant_part_off, int64_t n_giant) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
@@ -184,6 +185,7 @@ __global__ void k_chunks(const int32_t* __restrict__ rows, int64_t n, const int6
   for (int64_t k = 0; k < nc; ++k) {
     chunk_row[c0 + k] = r;
     chunk_beg[c0 + k] = b + k * chunk_len;
+    chunk_end[c0 + k] = b + ((k + 1) * chunk_len < len ? (k + 1) * chunk_len : len);
     chunk_part[c0 + k] = nc > 1 ? (int32_t)(part_off[i] + k) : -1;
   }
   if (nc > 1) {
@@ -450,12 +452,13 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
   }
   GCN_CHECK(dalloc(&p.chunk_row, p.n_chunks, "chunk rows"));
   GCN_CHECK(dalloc(&p.chunk_beg, p.n_chunks, "chunk starts"));
+  GCN_CHECK(dalloc(&p.chunk_end, p.n_chunks, "chunk ends"));
   GCN_CHECK(dalloc(&p.chunk_part, p.n_chunks, "chunk partial slots"));
   GCN_CHECK(dalloc(&p.giant_row, p.n_giant, "giant rows"));
   GCN_CHECK(dalloc(&p.giant_part_off, p.n_giant + 1, "giant partial offsets"));
   hipLaunchKernelGGL(k_chunks, dim3(grid_for(nc_rows)), dim3(kThreads), 0, stream, crow, nc_rows,
                      m.ptr, p.chunk_len, (const int64_t*)chunk_off, (const int64_t*)part_off,
-                     (const int64_t*)giant_idx, p.chunk_row, p.chunk_beg, p.chunk_part,
+                     (const int64_t*)giant_idx, p.chunk_row, p.chunk_beg, p.chunk_end, p.chunk_part,
                      p.giant_row, p.giant_part_off, p.n_giant);
   GCN_HIP(hipGetLastError());
   tfree(scratch, stream);
@@ -470,6 +473,7 @@ void free_mat(Mat& m, bool arrays) {
   dfree(p.rows);
   dfree(p.chunk_row);
   dfree(p.chunk_beg);
+  dfree(p.chunk_end);
   dfree(p.chunk_part);
   dfree(p.giant_row);
   dfree(p.giant_part_off);

@@ -32,6 +32,8 @@ constexpr int kFirstShort = 1;
 constexpr int kLastShort = 6;
 constexpr int kMedium = 7;
 constexpr int kChunked = 8;
+// longest row of each class up to the short ones
+constexpr int kClassHi[kLastShort + 1] = {0, 1, 2, 4, 8, 16, 32};
 
 struct Plan {
   int32_t* rows = nullptr;        // [n_major] row ids grouped by class, increasing within a class
@@ -43,6 +45,7 @@ struct Plan {
   int64_t n_chunks = 0;
   int32_t* chunk_row = nullptr;   // [n_chunks]
   int64_t* chunk_beg = nullptr;   // [n_chunks] first entry
+  int64_t* chunk_end = nullptr;   // [n_chunks] one past the last entry
   int32_t* chunk_part = nullptr;  // [n_chunks] partial-row slot, -1 = writes the output row
   // rows split over more than one chunk ("giant" rows) and their partials
   int64_t n_giant = 0;

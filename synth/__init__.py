@@ -201,6 +201,11 @@ def rmat24_q8() -> Workload:
     return rmat(24, 32, 128, 5, name="rmat24_ef32_f128_q8halo", halo_fraction=0.25)
 
 
+def rmat24() -> Workload:
+    """RMAT scale 24, edge factor 32, F = 128, every input row fp32."""
+    return rmat(24, 32, 128, 5)
+
+
 def product_like(n: int = 2_449_029, draws: int = 65_700_000, k: int = 3) -> Workload:
     """Product-graph-shaped RMAT: n nodes by rejection from the next power of
     two, permuted, symmetrized, +I. The default draw count targets about
