@@ -112,27 +112,34 @@ gcn_status gcn_aggregate_bwd(const gcn_graph* g, const void* G, int64_t ldg, int
 /* Forward aggregation whose input rows >= n_local_cols are halo rows held as
  * uint8 codes (Section 6.1 step 3; quantization of Section 2.4 with b = 8):
  *   x[j, f] = X_local[j, f]                                   j <  n_local_cols
- *   x[j, f] = fmaf((float)Q_halo[h, f], halo_scale[h], halo_min[h]),
+ *   x[j, f] = fmaf((float)Q_halo[h, f], halo_scale[h * ldp], halo_min[h * ldp]),
  *             h = j - n_local_cols                             j >= n_local_cols
  *   Y = A_hat x   (or A_hat^T x with GCN_Q8_USE_CSC; then x has n_rows rows
  *                  and Y has n_cols rows).
  *  X_local     fp32 [n_local_cols x F] (ldx); may be NULL if n_local_cols == 0.
  *  Q_halo      uint8 [n_in - n_local_cols x F] (ldq), n_in = rows of x.
- *  halo_min, halo_scale   fp32 [n_in - n_local_cols] (zero point Z, scale S).
+ *  halo_min, halo_scale   fp32 zero point Z and scale S of halo row h at
+ *              element h * ldp (ldp >= 1). ldp = 1: two plain arrays;
+ *              ldp = 2 with halo_scale == halo_min + 1: (Z, S) pairs side by
+ *              side (8-byte aligned), read with one 8-byte load per gather.
  *  Y           fp32 output (ldy). */
 gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_local_cols, const float* X_local,
                                     int64_t ldx, const uint8_t* Q_halo, int64_t ldq,
-                                    const float* halo_min, const float* halo_scale, float* Y,
-                                    int64_t ldy, int64_t F, uint32_t flags, void* stream);
+                                    const float* halo_min, const float* halo_scale, int64_t ldp,
+                                    float* Y, int64_t ldy, int64_t F, uint32_t flags,
+                                    void* stream);
 
 /* Per-row uint8 quantization (Section 2.4 with b = 8, the producer side of
  * the quantized exchange): Z = min_f X[i, f], S = (max - min) / 255 in fp32,
  * Q[i, f] = clamp(rint((X[i, f] - Z) / S), 0, 255) with IEEE fp32 division
  * and round-half-even (the paper's implementation drops the stochastic
  * rounding, Section 7.3); every code is 0 when S == 0.
- *  X [n x F] fp32 (ldx) -> Q [n x F] uint8 (ldq), zmin[n], scale[n] fp32. */
+ *  X [n x F] fp32 (ldx) -> Q [n x F] uint8 (ldq); zmin[i * ldp] and
+ *  scale[i * ldp] fp32 (ldp >= 1; ldp = 2 with scale = zmin + 1 writes the
+ *  (Z, S) pairs that gcn_aggregate_fwd_q8halo reads with one load). */
 gcn_status gcn_quantize_rows_u8(int64_t n, int64_t F, const float* X, int64_t ldx, uint8_t* Q,
-                                int64_t ldq, float* zmin, float* scale, void* stream);
+                                int64_t ldq, float* zmin, float* scale, int64_t ldp,
+                                void* stream);
 
 /* ---- support calls ---------------------------------------------------- */
 

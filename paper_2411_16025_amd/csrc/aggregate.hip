@@ -36,6 +36,7 @@ namespace gcn {
 namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef float f2 __attribute__((ext_vector_type(2)));
 typedef uint16_t us4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBlock = 256;
@@ -120,6 +121,8 @@ struct SrcQ8 {
   int64_t ldq;
   const float* __restrict__ zmin;
   const float* __restrict__ scale;
+  int64_t ldp;
+  bool paired;  // (Z, S) side by side: one 8-byte load
   int F;
   struct Raw {
     float v[VEC < 3 ? 3 : VEC];  // local: features; halo: {codes, Z, S}
@@ -134,8 +137,14 @@ struct SrcQ8 {
     }
     const int64_t h = (int64_t)j - n_local;
     const uint8_t* p = q + h * ldq + f0;
-    r.v[1] = zmin[h];
-    r.v[2] = scale[h];
+    if (paired) {
+      const f2 zs = *reinterpret_cast<const f2*>(zmin + 2 * h);
+      r.v[1] = zs.x;
+      r.v[2] = zs.y;
+    } else {
+      r.v[1] = zmin[h * ldp];
+      r.v[2] = scale[h * ldp];
+    }
     uint32_t c;
     if constexpr (VEC == 4) {
       if (f0 + 4 <= F) {
@@ -651,8 +660,8 @@ extern "C" gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_loc
                                                const float* X_local, int64_t ldx,
                                                const uint8_t* Q_halo, int64_t ldq,
                                                const float* halo_min, const float* halo_scale,
-                                               float* Y, int64_t ldy, int64_t F, uint32_t flags,
-                                               void* stream) {
+                                               int64_t ldp, float* Y, int64_t ldy, int64_t F,
+                                               uint32_t flags, void* stream) {
   clear_error();
   GCN_CHECK(check_common(g, F));
   if (flags & ~(uint32_t)GCN_Q8_USE_CSC) {
@@ -673,10 +682,12 @@ extern "C" gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_loc
     set_error("X_local must be non-NULL with ldx >= F when n_local_cols > 0");
     return GCN_EINVAL;
   }
-  if (n_local_cols < n_in && (!Q_halo || !halo_min || !halo_scale || ldq < F)) {
-    set_error("Q_halo, halo_min, halo_scale must be non-NULL with ldq >= F when halo rows exist");
+  if (n_local_cols < n_in && (!Q_halo || !halo_min || !halo_scale || ldq < F || ldp < 1)) {
+    set_error("Q_halo, halo_min, halo_scale must be non-NULL with ldq >= F and ldp >= 1 when "
+              "halo rows exist");
     return GCN_EINVAL;
   }
+  const bool paired = ldp == 2 && halo_scale == halo_min + 1 && aligned(halo_min, 8);
   const int Fi = (int)F;
   const bool vec4 = aligned(Y, 16) && ldy % 4 == 0 && (n_local_cols == 0 ||
                     (aligned(X_local, 16) && ldx % 4 == 0)) &&
@@ -689,6 +700,8 @@ extern "C" gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_loc
     t.ldq = ldq;
     t.zmin = halo_min;
     t.scale = halo_scale;
+    t.ldp = ldp;
+    t.paired = paired;
     t.F = Fi;
     return t;
   });

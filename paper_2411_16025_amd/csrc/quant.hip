@@ -16,7 +16,7 @@ __global__ __launch_bounds__(kBlock) void k_quantize_rows(int64_t n, int F,
                                                           const float* __restrict__ x, int64_t ldx,
                                                           uint8_t* __restrict__ q, int64_t ldq,
                                                           float* __restrict__ zmin,
-                                                          float* __restrict__ scale) {
+                                                          float* __restrict__ scale, int64_t ldp) {
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
   if (i >= n) return;
@@ -33,8 +33,8 @@ __global__ __launch_bounds__(kBlock) void k_quantize_rows(int64_t n, int F,
   }
   const float s = (mx - mn) / 255.0f;
   if (lane == 0) {
-    zmin[i] = mn;
-    scale[i] = s;
+    zmin[i * ldp] = mn;
+    scale[i * ldp] = s;
   }
   uint8_t* qr = q + i * ldq;
   for (int f = lane; f < F; f += 64) {
@@ -52,22 +52,22 @@ using namespace gcn;
 
 extern "C" gcn_status gcn_quantize_rows_u8(int64_t n, int64_t F, const float* X, int64_t ldx,
                                            uint8_t* Q, int64_t ldq, float* zmin, float* scale,
-                                           void* stream) {
+                                           int64_t ldp, void* stream) {
   clear_error();
   if (n < 0 || F <= 0 || F >= (1ll << 31)) {
     set_error("need n >= 0 and F in [1, 2^31)");
     return GCN_EINVAL;
   }
   if (n == 0) return GCN_OK;
-  if (!X || !Q || !zmin || !scale || ldx < F || ldq < F) {
-    set_error("X, Q, zmin, scale must be non-NULL with ldx, ldq >= F");
+  if (!X || !Q || !zmin || !scale || ldx < F || ldq < F || ldp < 1) {
+    set_error("X, Q, zmin, scale must be non-NULL with ldx, ldq >= F and ldp >= 1");
     return GCN_EINVAL;
   }
   hipStream_t s = (hipStream_t)stream;
   ProfScope ps("quantize_rows_u8", s);
   const int64_t blocks = ceil_div(n, kBlock / 64);
   hipLaunchKernelGGL(k_quantize_rows, dim3((unsigned)blocks), dim3(kBlock), 0, s, n, (int)F, X, ldx,
-                     Q, ldq, zmin, scale);
+                     Q, ldq, zmin, scale, ldp);
   GCN_HIP(hipGetLastError());
   return GCN_OK;
 }

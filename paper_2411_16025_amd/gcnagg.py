@@ -55,8 +55,9 @@ def lib():
         L.gcn_normalize.argtypes = [P, P, P]
         L.gcn_aggregate_fwd.argtypes = [P, P, i64, i32, P, i64, i64, P]
         L.gcn_aggregate_bwd.argtypes = [P, P, i64, i32, P, i64, i64, P]
-        L.gcn_aggregate_fwd_q8halo.argtypes = [P, i64, P, i64, P, i64, P, P, P, i64, i64, u32, P]
-        L.gcn_quantize_rows_u8.argtypes = [i64, i64, P, i64, P, i64, P, P, P]
+        L.gcn_aggregate_fwd_q8halo.argtypes = [P, i64, P, i64, P, i64, P, P, i64, P, i64, i64, u32,
+                                               P]
+        L.gcn_quantize_rows_u8.argtypes = [i64, i64, P, i64, P, i64, P, P, i64, P]
         L.gcn_graph_free.argtypes = [P]
         L.gcn_graph_free.restype = None
         L.gcn_graph_info.argtypes = [P, P, P, P]
@@ -193,9 +194,13 @@ def gcn_aggregate_bwd(g: Graph, G: torch.Tensor, dX: torch.Tensor | None = None,
 def gcn_aggregate_fwd_q8halo(g: Graph, n_local_cols: int, X_local, Q_halo, halo_min, halo_scale,
                              Y: torch.Tensor | None = None, use_csc: bool = False, F=None,
                              stream=None):
-    """Y = A_hat [X_local; fmaf(Q, S, Z)] (or A_hat^T with use_csc)."""
+    """Y = A_hat [X_local; fmaf(Q, S, Z)] (or A_hat^T with use_csc).
+
+    halo_min / halo_scale are 1-D tensors with a common stride ldp; the
+    columns of an [n_halo, 2] tensor give the paired (Z, S) layout."""
     n_in, n_out = (g.n_rows, g.n_cols) if use_csc else (g.n_cols, g.n_rows)
     ldx = ldq = 0
+    ldp = 1
     if X_local is not None:
         _dev(X_local, torch.float32, "X_local")
         ldx = _rowmajor(X_local, "X_local")
@@ -211,8 +216,11 @@ def gcn_aggregate_fwd_q8halo(g: Graph, n_local_cols: int, X_local, Q_halo, halo_
             raise ValueError("Q_halo has fewer than %d rows" % n_h)
         for t, nm in ((halo_min, "halo_min"), (halo_scale, "halo_scale")):
             _dev(t, torch.float32, nm)
-            if t.numel() < n_h or not t.is_contiguous():
-                raise ValueError("%s needs %d contiguous entries" % (nm, n_h))
+            if t.dim() != 1 or t.numel() < n_h:
+                raise ValueError("%s must be 1-D with at least %d entries" % (nm, n_h))
+        ldp = halo_min.stride(0)
+        if halo_scale.stride(0) != ldp or ldp < 1:
+            raise ValueError("halo_min and halo_scale need the same positive stride")
     if F is None:
         raise ValueError("F is unknown")
     if Y is None:
@@ -225,24 +233,35 @@ def gcn_aggregate_fwd_q8halo(g: Graph, n_local_cols: int, X_local, Q_halo, halo_
     ptr = lambda t: t.data_ptr() if t is not None else None
     _check(lib().gcn_aggregate_fwd_q8halo(
         g.handle, n_local_cols, ptr(X_local), ldx, ptr(Q_halo), ldq, ptr(halo_min),
-        ptr(halo_scale), Y.data_ptr(), ldy, F, GCN_Q8_USE_CSC if use_csc else 0, _stream(stream)))
+        ptr(halo_scale), ldp, Y.data_ptr(), ldy, F, GCN_Q8_USE_CSC if use_csc else 0,
+        _stream(stream)))
     return Y
 
 
-def gcn_quantize_rows_u8(X: torch.Tensor, Q=None, zmin=None, scale=None, stream=None):
-    """Per-row uint8 codes and (zmin, scale) of an fp32 matrix."""
+def gcn_quantize_rows_u8(X: torch.Tensor, Q=None, zmin=None, scale=None, paired=False,
+                         stream=None):
+    """Per-row uint8 codes and (zmin, scale) of an fp32 matrix.
+
+    paired=True stores (Z, S) side by side in an [n, 2] tensor and returns
+    its two columns (stride 2)."""
     _dev(X, torch.float32, "X")
     ldx = _rowmajor(X, "X")
     n, F = X.shape
     if Q is None:
         Q = torch.empty((n, F), dtype=torch.uint8, device=X.device)
+    if zmin is None and scale is None and paired:
+        zs = torch.empty((n, 2), dtype=torch.float32, device=X.device)
+        zmin, scale = zs[:, 0], zs[:, 1]
     if zmin is None:
         zmin = torch.empty(n, dtype=torch.float32, device=X.device)
     if scale is None:
         scale = torch.empty(n, dtype=torch.float32, device=X.device)
+    ldp = zmin.stride(0)
+    if scale.stride(0) != ldp:
+        raise ValueError("zmin and scale need the same stride")
     ldq = _rowmajor(Q, "Q")
     _check(lib().gcn_quantize_rows_u8(n, F, X.data_ptr(), ldx, Q.data_ptr(), ldq, zmin.data_ptr(),
-                                      scale.data_ptr(), _stream(stream)))
+                                      scale.data_ptr(), ldp, _stream(stream)))
     return Q, zmin, scale
 
 

@@ -64,7 +64,7 @@ def test_calls_reject_null_and_corrupt_handles(L):
     assert L.gcn_normalize(None, None, None) == 1
     assert L.gcn_aggregate_fwd(None, None, 0, 0, None, 0, 4, None) == 1
     assert L.gcn_aggregate_bwd(None, None, 0, 0, None, 0, 4, None) == 1
-    assert L.gcn_aggregate_fwd_q8halo(None, 0, None, 0, None, 0, None, None, None, 0, 4, 0,
+    assert L.gcn_aggregate_fwd_q8halo(None, 0, None, 0, None, 0, None, None, 1, None, 0, 4, 0,
                                       None) == 1
     # a block of memory that is not a graph handle is reported as ESTATE
     junk = (ctypes.c_uint64 * 64)()
@@ -76,10 +76,11 @@ def test_calls_reject_null_and_corrupt_handles(L):
 
 def test_quantize_rejects_bad_arguments(L):
     fake = ctypes.c_void_p(0x1000)
-    assert L.gcn_quantize_rows_u8(4, 0, fake, 4, fake, 4, fake, fake, None) == 1
-    assert L.gcn_quantize_rows_u8(4, 8, fake, 4, fake, 8, fake, fake, None) == 1  # ldx < F
-    assert L.gcn_quantize_rows_u8(4, 8, None, 8, fake, 8, fake, fake, None) == 1
-    assert L.gcn_quantize_rows_u8(0, 8, None, 8, None, 8, None, None, None) == 0  # nothing to do
+    assert L.gcn_quantize_rows_u8(4, 0, fake, 4, fake, 4, fake, fake, 1, None) == 1
+    assert L.gcn_quantize_rows_u8(4, 8, fake, 4, fake, 8, fake, fake, 1, None) == 1  # ldx < F
+    assert L.gcn_quantize_rows_u8(4, 8, None, 8, fake, 8, fake, fake, 1, None) == 1
+    assert L.gcn_quantize_rows_u8(4, 8, fake, 8, fake, 8, fake, fake, 0, None) == 1  # ldp < 1
+    assert L.gcn_quantize_rows_u8(0, 8, None, 8, None, 8, None, None, 1, None) == 0  # no rows
 
 
 def test_last_error_is_per_thread(L):

@@ -345,6 +345,35 @@ def test_q8_halo_fwd_and_bwd(G, F):
                                      SG), what="q8 bwd")
 
 
+def test_q8_paired_params_and_quantizer(G):
+    # (Z, S) side by side (ldp = 2), written by the GPU quantizer and read by
+    # the fused kernel; codes and params must equal the oracle's bit for bit
+    import torch
+    note("q8 paired params")
+    n = 1 << 13
+    src, dst = synth.rmat_edges(98, n, 12 * n, perm_seed=99)
+    og = oracle.Graph(n, n, src, dst, SYM | LOOPS)
+    g = gpu_graph(G, n, n, src, dst, SYM | LOOPS)
+    nlc, F = n - n // 4, 128
+    X = synth.normal(100, n, F)
+    Q, Z, S = oracle.quantize_rows(X[nlc:])
+    Xd = dev(X)
+    q, z, s = G.gcn_quantize_rows_u8(Xd[nlc:], paired=True)
+    assert z.stride(0) == 2 and s.data_ptr() == z.data_ptr() + 4
+    assert np.array_equal(host(q), Q)
+    assert np.array_equal(host(z).view(np.uint32), Z.view(np.uint32))
+    assert np.array_equal(host(s).view(np.uint32), S.view(np.uint32))
+    Y = host(G.gcn_aggregate_fwd_q8halo(g, nlc, Xd[:nlc], q, z, s))
+    assert_close(Y, *oracle.spmm_q8(og.csr_ptr, og.csr_idx, og.csr_val, nlc, X[:nlc], Q, Z, S),
+                 what="q8 paired")
+    # a general stride (ldp = 3) reads the same values
+    zs3 = torch.zeros((n - nlc, 3), dtype=torch.float32, device="cuda:0")
+    zs3[:, 0] = dev(Z)
+    zs3[:, 1] = dev(S)
+    Y3 = host(G.gcn_aggregate_fwd_q8halo(g, nlc, Xd[:nlc], q, zs3[:, 0], zs3[:, 1]))
+    assert np.array_equal(Y3.view(np.uint32), Y.view(np.uint32))
+
+
 def test_q8_rectangular_csc(G):
     # non-symmetric rectangular graph: the CSC path with halo rows of G
     note("q8 rectangular csc")
