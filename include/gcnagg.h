@@ -141,6 +141,53 @@ gcn_status gcn_quantize_rows_u8(int64_t n, int64_t F, const float* X, int64_t ld
                                 int64_t ldq, float* zmin, float* scale, int64_t ldp,
                                 void* stream);
 
+/* ---- the dense side of a layer: UPDATE of Section 2.1 ------------------ */
+
+/* GEMM operations */
+enum { GCN_GEMM_NN = 0, GCN_GEMM_NT = 1, GCN_GEMM_TN = 2 };
+
+/* fp32 GEMM on the matrix cores, row-major operands:
+ *   GCN_GEMM_NN  C[M x N] = A[M x K] B[K x N]
+ *   GCN_GEMM_NT  C[M x N] = A[M x K] B[N x K]^T
+ *   GCN_GEMM_TN  C[M x N] = A[K x M]^T B[K x N]   (K may be millions: split
+ *                into fixed chunks whose partial products are added in chunk
+ *                order, so results repeat bit for bit; needs M * N < 2^31)
+ * lda, ldb, ldc are the row strides of the stored matrices. fp32 inputs and
+ * fp32 accumulation. */
+gcn_status gcn_gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                        const float* B, int64_t ldb, float* C, int64_t ldc, void* stream);
+
+/* H[i, f] = max(H[i, f], 0) in place, H [n x F] (ld). */
+gcn_status gcn_relu(int64_t n, int64_t F, float* H, int64_t ld, void* stream);
+
+/* dH[i, f] = 0 where H[i, f] <= 0 (H is the ReLU output), in place. */
+gcn_status gcn_relu_bwd(int64_t n, int64_t F, const float* H, int64_t ldh, float* dH, int64_t ld,
+                        void* stream);
+
+/* Softmax cross-entropy over n rows of C <= 64 logits: *loss (device double)
+ * = mean_i (logsumexp(z_i) - z_i[y_i]), dlogits = (softmax(z) - onehot(y)) / n.
+ * labels (int32 [n]) must lie in [0, C). Row losses are added in a fixed order
+ * in double. */
+gcn_status gcn_softmax_xent(int64_t n, int64_t C, const float* logits, int64_t ld,
+                            const int32_t* labels, float* dlogits, int64_t ldd, double* loss,
+                            void* stream);
+
+/* One training step of a 2-layer GCN on a square graph (Section 2.1: each
+ * layer aggregates, then applies a linear transform), in the order
+ *   Z1 = X W1, H1 = relu(A_hat Z1), Z2 = H1 W2, logits = A_hat Z2,
+ *   loss = mean softmax cross-entropy, then the exact backward:
+ *   dZ2 = A_hat^T dlogits, dW2 = H1^T dZ2, dH1 = dZ2 W2^T masked by H1 > 0,
+ *   dZ1 = A_hat^T dH1, dW1 = X^T dZ1.
+ *  X [n x f_in] (ldx), W1 [f_in x hidden], W2 [hidden x n_classes] (dense,
+ *  row-major), labels int32 [n] in [0, n_classes), n_classes <= 64.
+ *  Outputs: dW1, dW2 (same shapes as W1, W2), *loss (device double).
+ * No bias, dropout or normalization layer. Intermediates are allocated
+ * stream-ordered for the duration of the call. */
+gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t ldx, int64_t f_in,
+                         const float* W1, int64_t hidden, const float* W2, int64_t n_classes,
+                         const int32_t* labels, float* dW1, float* dW2, double* loss,
+                         void* stream);
+
 /* ---- support calls ---------------------------------------------------- */
 
 /* Release every device array of the graph (after synchronizing the device

@@ -62,6 +62,7 @@ def _L():
         lib.orc_normalize.argtypes = [i64, P, P, P, P]
         lib.orc_normalize_listed.argtypes = [i64, P, P, P, P]
         lib.orc_spmm.argtypes = [i64, P, P, P, P, i64, i64, P, P]
+        lib.orc_spmm_f64.argtypes = [i64, P, P, P, P, i64, i64, P]
         lib.orc_dequant.argtypes = [ctypes.c_uint8, ctypes.c_float, ctypes.c_float]
         lib.orc_dequant.restype = ctypes.c_float
         lib.orc_dequant_rows.argtypes = [i64, i64, P, i64, P, P, P, i64]
@@ -285,18 +286,22 @@ def sampled(n_rows, n_cols, src, dst, flags, sel, transpose=False, deg=None):
 
 def _agg64(ptr, idx, val, H):
     """A H in float64 for float64 H (row order, double accumulation)."""
-    H = np.asarray(H, np.float64)
+    H = np.ascontiguousarray(H, np.float64)
+    ptr = _c(ptr, np.int64)
+    idx = _c(idx, np.int32)
+    val = _c(val, np.float32)
     n = len(ptr) - 1
-    rows = np.repeat(np.arange(n), np.diff(ptr))
-    out = np.zeros((n, H.shape[1]), np.float64)
-    np.add.at(out, rows, val.astype(np.float64)[:, None] * H[idx])
+    out = np.empty((n, H.shape[1]), np.float64)
+    _L().orc_spmm_f64(n, _p(ptr), _p(idx), _p(val), H.ctypes.data, H.shape[1], H.shape[1],
+                      _p(out))
     return out
 
 
 def gcn_step(graph: Graph, X, W1, W2, labels):
     """Loss and weight gradients of the 2-layer GCN, all in float64.
 
-    Returns dict(loss, dW1, dW2, Z1, A1, H1, Z2, logits)."""
+    Returns dict(loss, dW1, dW2) and the intermediates Z1, A1, H1, Z2, logits,
+    dlogits, dZ2, dH1 (before the ReLU mask), dZ1."""
     X = np.asarray(X, np.float64)
     W1 = np.asarray(W1, np.float64)
     W2 = np.asarray(W2, np.float64)
@@ -312,8 +317,7 @@ def gcn_step(graph: Graph, X, W1, W2, labels):
     m = logits.max(axis=1, keepdims=True)
     lse = m[:, 0] + np.log(np.exp(logits - m).sum(axis=1))
     loss = float(np.mean(lse - logits[np.arange(n), y]))
-    P = np.exp(logits - lse[:, None])
-    dlogits = P
+    dlogits = np.exp(logits - lse[:, None])
     dlogits[np.arange(n), y] -= 1.0
     dlogits /= n
     dZ2 = bwd(dlogits)
@@ -322,4 +326,5 @@ def gcn_step(graph: Graph, X, W1, W2, labels):
     dA1 = dH1 * (A1 > 0)
     dZ1 = bwd(dA1)
     dW1 = X.T @ dZ1
-    return dict(loss=loss, dW1=dW1, dW2=dW2, Z1=Z1, A1=A1, H1=H1, Z2=Z2, logits=logits)
+    return dict(loss=loss, dW1=dW1, dW2=dW2, Z1=Z1, A1=A1, H1=H1, Z2=Z2, logits=logits,
+                dlogits=dlogits, dZ2=dZ2, dH1=dH1, dZ1=dZ1)

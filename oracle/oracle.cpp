@@ -220,6 +220,22 @@ void orc_spmm(int64_t n_major, const int64_t* ptr, const int32_t* idx, const flo
     }
 }
 
+// Y = A H for a float64 H (the training step keeps every intermediate in
+// double): Y[r, f] = sum_k val[k] * H[idx[k], f] in stored order.
+void orc_spmm_f64(int64_t n_major, const int64_t* ptr, const int32_t* idx, const float* val,
+                  const double* H, int64_t ldh, int64_t F, double* Y) {
+#pragma omp parallel for schedule(dynamic, 256)
+  for (int64_t r = 0; r < n_major; ++r) {
+    double* y = Y + r * F;
+    for (int64_t f = 0; f < F; ++f) y[f] = 0.0;
+    for (int64_t k = ptr[r]; k < ptr[r + 1]; ++k) {
+      const double w = (double)val[k];
+      const double* h = H + (int64_t)idx[k] * ldh;
+      for (int64_t f = 0; f < F; ++f) y[f] += w * h[f];
+    }
+  }
+}
+
 // Dequantized value of one code: fmaf(q, S, Z), a single rounding.
 float orc_dequant(uint8_t q, float scale, float zero) { return std::fmaf((float)q, scale, zero); }
 

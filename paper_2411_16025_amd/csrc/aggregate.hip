@@ -638,6 +638,18 @@ gcn_status aggregate(const gcn_graph* g, const Mat& m, const void* X, int64_t ld
 
 }  // namespace
 
+gcn_status aggregate_f32(const Mat& m, const float* X, int64_t ldx, float* Y, int64_t ldy,
+                         int64_t F, hipStream_t stream) {
+  const int Fi = (int)F;
+  const bool vec4 = aligned(Y, 16) && ldy % 4 == 0 && aligned(X, 16) && ldx % 4 == 0;
+  return dispatch<SrcF32>(m, vec4, Fi, Y, ldy, stream, [&](auto t) {
+    t.x = X;
+    t.ld = ldx;
+    t.F = Fi;
+    return t;
+  });
+}
+
 }  // namespace gcn
 
 using namespace gcn;

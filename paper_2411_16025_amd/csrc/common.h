@@ -131,6 +131,18 @@ gcn_status radix_pass_u64(const uint64_t* in, uint64_t* out, int64_t n, int shif
 // Exclusive scan of int64 values; out[n] receives the total. in == out allowed.
 gcn_status scan_i64(const int64_t* in, int64_t* out, int64_t n, hipStream_t stream);
 
+// ---- aggregation and dense operations (aggregate.hip, dense.hip) -------------
+// Y = M X for fp32 X (M is a graph's CSR or CSC).
+gcn_status aggregate_f32(const Mat& m, const float* X, int64_t ldx, float* Y, int64_t ldy,
+                         int64_t F, hipStream_t stream);
+gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                    const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream);
+gcn_status relu_fwd(int64_t n, int64_t F, float* H, int64_t ld, hipStream_t stream);
+gcn_status relu_bwd(int64_t n, int64_t F, const float* H, int64_t ldh, float* dH, int64_t ld,
+                    hipStream_t stream);
+gcn_status softmax_xent(int64_t n, int C, const float* z, int64_t ldz, const int32_t* y,
+                        float* dz, int64_t ldd, double* loss, hipStream_t stream);
+
 // ---- plan building (build.hip) ----------------------------------------------
 gcn_status build_plan(Mat& m, hipStream_t stream);
 void free_mat(Mat& m, bool arrays);

@@ -1,0 +1,370 @@
+// Dense side of a GCN layer (the UPDATE of SuperGCN, arXiv 2411.16025,
+// Section 2.1: after aggregation, a linear transform): fp32 GEMMs on the
+// gfx950 matrix cores, ReLU, and softmax cross-entropy.
+//
+// GEMM shapes of full-batch GCN training are tall and skinny: the node count
+// is in the millions, feature and class counts are at most a few hundred.
+//  * C = A op(B) with M = nodes (NN, NT): one 256-thread workgroup computes a
+//    64 x 64 tile of C over all of K, staging 32-deep slices of A and B in
+//    LDS; each wavefront owns 16 rows and issues v_mfma_f32_16x16x4_f32 on
+//    four 16 x 16 blocks.
+//  * C = A^T B with K = nodes (the weight gradients): K is split into fixed
+//    chunks; every chunk writes a partial C tile and a second kernel adds the
+//    partials in chunk order, so the result is the same on every run.
+//
+// v_mfma_f32_16x16x4_f32 operand layout (lane l of the wavefront): a holds
+// A[l % 16][k0 + l / 16], b holds B[k0 + l / 16][l % 16], and result element
+// i holds C[4 * (l / 16) + i][l % 16].
+
+#include <algorithm>
+
+#include "common.h"
+
+namespace gcn {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kTile = 64;  // C tile is kTile x kTile
+constexpr int kKc = 32;    // K slice staged in LDS
+constexpr int kPad = 1;    // LDS row padding against bank conflicts
+constexpr int64_t kSplitRows = 8192;  // K chunk of the A^T B kernel
+
+enum Op { kNN = 0, kNT = 1 };
+
+// C[M x N] = A[M x K] * B[K x N] (NN) or A[M x K] * B[N x K]^T (NT).
+template <int OP>
+__global__ __launch_bounds__(kThreads) void k_gemm_tall(int64_t M, int64_t N, int64_t K,
+                                                        const float* __restrict__ A, int64_t lda,
+                                                        const float* __restrict__ B, int64_t ldb,
+                                                        float* __restrict__ C, int64_t ldc) {
+  __shared__ float As[kTile][kKc + kPad];  // As[m][k]
+  __shared__ float Bs[kKc][kTile + kPad];  // Bs[k][n]
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int64_t m0 = (int64_t)blockIdx.x * kTile;
+  const int64_t n0 = (int64_t)blockIdx.y * kTile;
+  f4 acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+  for (int64_t k0 = 0; k0 < K; k0 += kKc) {
+    // A slice: 64 rows x 32 k, 8 consecutive k per thread
+    {
+      const int r = t >> 2, c = (t & 3) * 8;
+      const int64_t gm = m0 + r;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int64_t gk = k0 + c + e;
+        As[r][c + e] = (gm < M && gk < K) ? A[gm * lda + gk] : 0.f;
+      }
+    }
+    if (OP == kNN) {  // B slice: 32 k x 64 n, 8 consecutive n per thread
+      const int r = t >> 3, c = (t & 7) * 8;
+      const int64_t gk = k0 + r;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int64_t gn = n0 + c + e;
+        Bs[r][c + e] = (gk < K && gn < N) ? B[gk * ldb + gn] : 0.f;
+      }
+    } else {  // B stored N x K: rows n, 8 consecutive k per thread, transposed into Bs
+      const int r = t >> 2, c = (t & 3) * 8;
+      const int64_t gn = n0 + r;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int64_t gk = k0 + c + e;
+        Bs[c + e][r] = (gn < N && gk < K) ? B[gn * ldb + gk] : 0.f;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < kKc; kk += 4) {
+      const float a = As[16 * w + (lane & 15)][kk + (lane >> 4)];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float b = Bs[kk + (lane >> 4)][16 * j + (lane & 15)];
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[j], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t gn = n0 + 16 * j + (lane & 15);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t gm = m0 + 16 * w + 4 * (lane >> 4) + i;
+      if (gm < M && gn < N) C[gm * ldc + gn] = acc[j][i];
+    }
+  }
+}
+
+// Partial C tiles of C = A^T B over rows [chunk * split, ...) of A and B.
+// A is [K x M], B is [K x N]; part holds [n_chunks][M][N].
+__global__ __launch_bounds__(kThreads) void k_gemm_tn_partial(int64_t M, int64_t N, int64_t K,
+                                                              int64_t split,
+                                                              const float* __restrict__ A,
+                                                              int64_t lda,
+                                                              const float* __restrict__ B,
+                                                              int64_t ldb,
+                                                              float* __restrict__ part) {
+  __shared__ float As[kKc][kTile + kPad];  // As[k][m]
+  __shared__ float Bs[kKc][kTile + kPad];  // Bs[k][n]
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int64_t m0 = (int64_t)blockIdx.x * kTile;
+  const int64_t n0 = (int64_t)blockIdx.y * kTile;
+  const int64_t chunk = blockIdx.z;
+  const int64_t kb = chunk * split;
+  const int64_t ke = std::min(K, kb + split);
+  f4 acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+  for (int64_t k0 = kb; k0 < ke; k0 += kKc) {
+    const int r = t >> 3, c = (t & 7) * 8;
+    const int64_t gk = k0 + r;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int64_t gm = m0 + c + e, gn = n0 + c + e;
+      As[r][c + e] = (gk < ke && gm < M) ? A[gk * lda + gm] : 0.f;
+      Bs[r][c + e] = (gk < ke && gn < N) ? B[gk * ldb + gn] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < kKc; kk += 4) {
+      const float a = As[kk + (lane >> 4)][16 * w + (lane & 15)];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float b = Bs[kk + (lane >> 4)][16 * j + (lane & 15)];
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[j], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+  float* out = part + chunk * M * N;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t gn = n0 + 16 * j + (lane & 15);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t gm = m0 + 16 * w + 4 * (lane >> 4) + i;
+      if (gm < M && gn < N) out[gm * N + gn] = acc[j][i];
+    }
+  }
+}
+
+// C[m][n] = sum over chunks, in chunk order, of part[chunk][m][n].
+__global__ __launch_bounds__(kThreads) void k_sum_partials(int64_t M, int64_t N, int64_t n_chunks,
+                                                           const float* __restrict__ part,
+                                                           float* __restrict__ C, int64_t ldc) {
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (e >= M * N) return;
+  float s = 0.f;
+  for (int64_t c = 0; c < n_chunks; ++c) s += part[c * M * N + e];
+  C[(e / N) * ldc + (e % N)] = s;
+}
+
+// one wavefront per row
+__global__ __launch_bounds__(kThreads) void k_relu(int64_t n, int64_t F, float* __restrict__ h,
+                                                   int64_t ld) {
+  const int64_t i = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  if (i >= n) return;
+  float* row = h + i * ld;
+  for (int64_t f = threadIdx.x & 63; f < F; f += 64) row[f] = fmaxf(row[f], 0.f);
+}
+
+// dh[i, f] = 0 where h[i, f] <= 0 (h = relu(a), so h > 0 exactly where a > 0)
+__global__ __launch_bounds__(kThreads) void k_relu_bwd(int64_t n, int64_t F,
+                                                       const float* __restrict__ h, int64_t ldh,
+                                                       float* __restrict__ dh, int64_t ld) {
+  const int64_t i = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  if (i >= n) return;
+  for (int64_t f = threadIdx.x & 63; f < F; f += 64)
+    if (!(h[i * ldh + f] > 0.f)) dh[i * ld + f] = 0.f;
+}
+
+// One wavefront per row (C <= 64 classes, lane = class): log-softmax with the
+// row maximum subtracted, per-row loss lse - z[y] accumulated in double per
+// workgroup in a fixed order, and dz = (softmax - onehot(y)) / n.
+__global__ __launch_bounds__(kThreads) void k_softmax_xent(int64_t n, int C,
+                                                           const float* __restrict__ z, int64_t ldz,
+                                                           const int32_t* __restrict__ y,
+                                                           float* __restrict__ dz, int64_t ldd,
+                                                           double* __restrict__ block_loss) {
+  __shared__ double wl[kThreads / 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t i = (int64_t)blockIdx.x * (kThreads / 64) + w;
+  double row_loss = 0.0;
+  if (i < n) {
+    const float v = lane < C ? z[i * ldz + lane] : -INFINITY;
+    float m = v;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+    const float ex = lane < C ? expf(v - m) : 0.f;
+    float s = ex;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+    const int32_t yi = y[i];  // labels lie in [0, C)
+    const float zy = __shfl(v, yi, 64);
+    const float lse = m + logf(s);
+    row_loss = (double)(lse - zy);
+    if (lane < C) dz[i * ldd + lane] = (ex / s - (lane == yi ? 1.f : 0.f)) / (float)n;
+  }
+  if (lane == 0) wl[w] = row_loss;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double s = 0.0;
+    for (int k = 0; k < kThreads / 64; ++k) s += wl[k];
+    block_loss[blockIdx.x] = s;
+  }
+}
+
+// loss = (sum of block losses in block order) / n, one thread
+__global__ void k_loss_total(int64_t nb, int64_t n, const double* __restrict__ block_loss,
+                             double* __restrict__ loss) {
+  if (blockIdx.x != 0 || threadIdx.x != 0) return;
+  double s = 0.0;
+  for (int64_t b = 0; b < nb; ++b) s += block_loss[b];
+  *loss = s / (double)n;
+}
+
+}  // namespace
+
+gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                    const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream) {
+  if (M == 0 || N == 0) return GCN_OK;
+  if (op == GCN_GEMM_TN) {
+    // chunk length: kSplitRows, grown so the chunk count fits the grid's z range
+    const int64_t split = std::max<int64_t>(kSplitRows, ceil_div(ceil_div(K, 65535), kKc) * kKc);
+    const int64_t n_chunks = std::max<int64_t>(1, ceil_div(K, split));
+    float* part = nullptr;
+    GCN_CHECK(talloc(&part, n_chunks * M * N, stream, "GEMM partials"));
+    {
+      ProfScope ps("gemm_tn_partial", stream);
+      hipLaunchKernelGGL(k_gemm_tn_partial, dim3((unsigned)ceil_div(M, kTile),
+                                                 (unsigned)ceil_div(N, kTile), (unsigned)n_chunks),
+                         dim3(kThreads), 0, stream, M, N, K, split, A, lda, B, ldb, part);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) {
+        tfree(part, stream);
+        return hip_fail(e, "k_gemm_tn_partial", __FILE__, __LINE__);
+      }
+    }
+    {
+      ProfScope ps("gemm_sum_partials", stream);
+      hipLaunchKernelGGL(k_sum_partials, dim3((unsigned)ceil_div(M * N, kThreads)), dim3(kThreads),
+                         0, stream, M, N, n_chunks, (const float*)part, C, ldc);
+      hipError_t e = hipGetLastError();
+      tfree(part, stream);
+      if (e != hipSuccess) return hip_fail(e, "k_sum_partials", __FILE__, __LINE__);
+    }
+    return GCN_OK;
+  }
+  const dim3 grid((unsigned)ceil_div(M, kTile), (unsigned)ceil_div(N, kTile));
+  ProfScope ps(op == GCN_GEMM_NN ? "gemm_nn" : "gemm_nt", stream);
+  if (op == GCN_GEMM_NN)
+    hipLaunchKernelGGL(k_gemm_tall<kNN>, grid, dim3(kThreads), 0, stream, M, N, K, A, lda, B, ldb,
+                       C, ldc);
+  else
+    hipLaunchKernelGGL(k_gemm_tall<kNT>, grid, dim3(kThreads), 0, stream, M, N, K, A, lda, B, ldb,
+                       C, ldc);
+  GCN_HIP(hipGetLastError());
+  return GCN_OK;
+}
+
+gcn_status relu_fwd(int64_t n, int64_t F, float* H, int64_t ld, hipStream_t stream) {
+  if (n * F == 0) return GCN_OK;
+  ProfScope ps("relu", stream);
+  hipLaunchKernelGGL(k_relu, dim3((unsigned)ceil_div(n, kThreads / 64)), dim3(kThreads), 0, stream,
+                     n, F, H, ld);
+  GCN_HIP(hipGetLastError());
+  return GCN_OK;
+}
+
+gcn_status relu_bwd(int64_t n, int64_t F, const float* H, int64_t ldh, float* dH, int64_t ld,
+                    hipStream_t stream) {
+  if (n * F == 0) return GCN_OK;
+  ProfScope ps("relu_bwd", stream);
+  hipLaunchKernelGGL(k_relu_bwd, dim3((unsigned)ceil_div(n, kThreads / 64)), dim3(kThreads), 0,
+                     stream, n, F, H, ldh, dH, ld);
+  GCN_HIP(hipGetLastError());
+  return GCN_OK;
+}
+
+gcn_status softmax_xent(int64_t n, int C, const float* z, int64_t ldz, const int32_t* y,
+                        float* dz, int64_t ldd, double* loss, hipStream_t stream) {
+  const int64_t nb = std::max<int64_t>(1, ceil_div(n, kThreads / 64));
+  double* bl = nullptr;
+  GCN_CHECK(talloc(&bl, nb, stream, "block losses"));
+  {
+    ProfScope ps("softmax_xent", stream);
+    hipLaunchKernelGGL(k_softmax_xent, dim3((unsigned)nb), dim3(kThreads), 0, stream, n, C, z, ldz,
+                       y, dz, ldd, bl);
+  }
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL(k_loss_total, dim3(1), dim3(64), 0, stream, nb, n, (const double*)bl, loss);
+    e = hipGetLastError();
+  }
+  tfree(bl, stream);
+  if (e != hipSuccess) return hip_fail(e, "softmax_xent", __FILE__, __LINE__);
+  return GCN_OK;
+}
+
+}  // namespace gcn
+
+using namespace gcn;
+
+extern "C" gcn_status gcn_gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A,
+                                   int64_t lda, const float* B, int64_t ldb, float* C, int64_t ldc,
+                                   void* stream) {
+  clear_error();
+  if (op != GCN_GEMM_NN && op != GCN_GEMM_NT && op != GCN_GEMM_TN) {
+    set_error("unknown GEMM op %d", op);
+    return GCN_EINVAL;
+  }
+  if (M < 0 || N < 0 || K < 0 || (M > 0 && N > 0 && (!A || !B || !C)) || ldc < N) {
+    set_error("invalid GEMM sizes or pointers");
+    return GCN_EINVAL;
+  }
+  const int64_t a_cols = op == GCN_GEMM_TN ? M : K;
+  const int64_t b_cols = op == GCN_GEMM_NT ? K : N;
+  if (lda < a_cols || ldb < b_cols) {
+    set_error("leading dimensions too small (lda=%lld ldb=%lld)", (long long)lda, (long long)ldb);
+    return GCN_EINVAL;
+  }
+  if (op == GCN_GEMM_TN && (M * N >= (1ll << 31))) {
+    set_error("A^T B output too large");
+    return GCN_ERANGE;
+  }
+  return gemm_f32(op, M, N, K, A, lda, B, ldb, C, ldc, (hipStream_t)stream);
+}
+
+extern "C" gcn_status gcn_relu(int64_t n, int64_t F, float* H, int64_t ld, void* stream) {
+  clear_error();
+  if (n < 0 || F < 0 || (n * F > 0 && !H) || ld < F) {
+    set_error("invalid ReLU arguments");
+    return GCN_EINVAL;
+  }
+  return relu_fwd(n, F, H, ld, (hipStream_t)stream);
+}
+
+extern "C" gcn_status gcn_relu_bwd(int64_t n, int64_t F, const float* H, int64_t ldh, float* dH,
+                                   int64_t ld, void* stream) {
+  clear_error();
+  if (n < 0 || F < 0 || (n * F > 0 && (!H || !dH)) || ldh < F || ld < F) {
+    set_error("invalid ReLU backward arguments");
+    return GCN_EINVAL;
+  }
+  return relu_bwd(n, F, H, ldh, dH, ld, (hipStream_t)stream);
+}
+
+extern "C" gcn_status gcn_softmax_xent(int64_t n, int64_t C, const float* logits, int64_t ld,
+                                       const int32_t* labels, float* dlogits, int64_t ldd,
+                                       double* loss, void* stream) {
+  clear_error();
+  if (n <= 0 || C <= 0 || C > 64 || !logits || !labels || !dlogits || !loss || ld < C ||
+      ldd < C) {
+    set_error("invalid softmax cross-entropy arguments (1 <= C <= 64)");
+    return GCN_EINVAL;
+  }
+  return softmax_xent(n, (int)C, logits, ld, labels, dlogits, ldd, loss, (hipStream_t)stream);
+}

@@ -1,0 +1,62 @@
+// One training step of a 2-layer GCN built from the library's kernels:
+// aggregation (Section 4 of SuperGCN, arXiv 2411.16025) interleaved with the
+// dense UPDATE of each layer (Section 2.1). Everything runs on the caller's
+// stream without host synchronization.
+
+#include "common.h"
+
+using namespace gcn;
+
+extern "C" gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t ldx, int64_t f_in,
+                                    const float* W1, int64_t hidden, const float* W2,
+                                    int64_t n_classes, const int32_t* labels, float* dW1,
+                                    float* dW2, double* loss, void* stream_) {
+  clear_error();
+  GCN_CHECK(check_graph(g));
+  if (g->n_rows != g->n_cols) {
+    set_error("the GCN step needs a square graph");
+    return GCN_EINVAL;
+  }
+  if (!X || !W1 || !W2 || !labels || !dW1 || !dW2 || !loss || f_in <= 0 || hidden <= 0 ||
+      n_classes <= 0 || n_classes > 64 || ldx < f_in) {
+    set_error("invalid GCN step arguments (1 <= n_classes <= 64)");
+    return GCN_EINVAL;
+  }
+  hipStream_t s = (hipStream_t)stream_;
+  const int64_t n = g->n_rows;
+  const int64_t ldh = (hidden + 3) & ~int64_t(3);
+  const int64_t ldc = (n_classes + 3) & ~int64_t(3);
+  float *z1 = nullptr, *h1 = nullptr, *z2 = nullptr, *lg = nullptr, *dl = nullptr, *dz2 = nullptr;
+  gcn_status st = talloc(&z1, n * ldh, s, "Z1");
+  if (st == GCN_OK) st = talloc(&h1, n * ldh, s, "H1");
+  if (st == GCN_OK) st = talloc(&z2, n * ldc, s, "Z2");
+  if (st == GCN_OK) st = talloc(&lg, n * ldc, s, "logits");
+  if (st == GCN_OK) st = talloc(&dl, n * ldc, s, "dlogits");
+  if (st == GCN_OK) st = talloc(&dz2, n * ldc, s, "dZ2");
+  // forward
+  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NN, n, hidden, f_in, X, ldx, W1, hidden, z1, ldh, s);
+  if (st == GCN_OK) st = aggregate_f32(g->csr, z1, ldh, h1, ldh, hidden, s);
+  if (st == GCN_OK) st = relu_fwd(n, hidden, h1, ldh, s);
+  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NN, n, n_classes, hidden, h1, ldh, W2, n_classes, z2,
+                                  ldc, s);
+  if (st == GCN_OK) st = aggregate_f32(g->csr, z2, ldc, lg, ldc, n_classes, s);
+  if (st == GCN_OK) st = softmax_xent(n, (int)n_classes, lg, ldc, labels, dl, ldc, loss, s);
+  // backward
+  if (st == GCN_OK) st = aggregate_f32(g->csc, dl, ldc, dz2, ldc, n_classes, s);
+  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_TN, hidden, n_classes, n, h1, ldh, dz2, ldc, dW2,
+                                  n_classes, s);
+  float* dh1 = z1;  // Z1 is dead after the first aggregation
+  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NT, n, hidden, n_classes, dz2, ldc, W2, n_classes, dh1,
+                                  ldh, s);
+  if (st == GCN_OK) st = relu_bwd(n, hidden, h1, ldh, dh1, ldh, s);
+  float* dz1 = h1;  // H1 is dead once the ReLU mask is applied
+  if (st == GCN_OK) st = aggregate_f32(g->csc, dh1, ldh, dz1, ldh, hidden, s);
+  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_TN, f_in, hidden, n, X, ldx, dz1, ldh, dW1, hidden, s);
+  tfree(dz2, s);
+  tfree(dl, s);
+  tfree(lg, s);
+  tfree(z2, s);
+  tfree(h1, s);
+  tfree(z1, s);
+  return st;
+}

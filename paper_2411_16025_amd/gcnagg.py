@@ -26,8 +26,11 @@ STATUS = {0: "GCN_OK", 1: "GCN_EINVAL", 2: "GCN_ERANGE", 3: "GCN_ENOMEM", 4: "GC
           5: "GCN_ESTATE"}
 
 # every symbol include/gcnagg.h declares
+GCN_GEMM_NN, GCN_GEMM_NT, GCN_GEMM_TN = 0, 1, 2
+
 EXPORTS = ("gcn_build_csr", "gcn_normalize", "gcn_aggregate_fwd", "gcn_aggregate_bwd",
-           "gcn_aggregate_fwd_q8halo", "gcn_quantize_rows_u8", "gcn_graph_free",
+           "gcn_aggregate_fwd_q8halo", "gcn_quantize_rows_u8", "gcn_gemm_f32", "gcn_relu",
+           "gcn_relu_bwd", "gcn_softmax_xent", "gcn_gcn2_step", "gcn_graph_free",
            "gcn_graph_info", "gcn_graph_export", "gcn_graph_bins", "gcn_profile_enable",
            "gcn_profile_read", "gcn_last_error")
 
@@ -58,6 +61,11 @@ def lib():
         L.gcn_aggregate_fwd_q8halo.argtypes = [P, i64, P, i64, P, i64, P, P, i64, P, i64, i64, u32,
                                                P]
         L.gcn_quantize_rows_u8.argtypes = [i64, i64, P, i64, P, i64, P, P, i64, P]
+        L.gcn_gemm_f32.argtypes = [i32, i64, i64, i64, P, i64, P, i64, P, i64, P]
+        L.gcn_relu.argtypes = [i64, i64, P, i64, P]
+        L.gcn_relu_bwd.argtypes = [i64, i64, P, i64, P, i64, P]
+        L.gcn_softmax_xent.argtypes = [i64, i64, P, i64, P, P, i64, P, P]
+        L.gcn_gcn2_step.argtypes = [P, P, i64, i64, P, i64, P, i64, P, P, P, P, P]
         L.gcn_graph_free.argtypes = [P]
         L.gcn_graph_free.restype = None
         L.gcn_graph_info.argtypes = [P, P, P, P]
@@ -263,6 +271,89 @@ def gcn_quantize_rows_u8(X: torch.Tensor, Q=None, zmin=None, scale=None, paired=
     _check(lib().gcn_quantize_rows_u8(n, F, X.data_ptr(), ldx, Q.data_ptr(), ldq, zmin.data_ptr(),
                                       scale.data_ptr(), ldp, _stream(stream)))
     return Q, zmin, scale
+
+
+def gcn_gemm_f32(op: int, A: torch.Tensor, B: torch.Tensor, C: torch.Tensor | None = None,
+                 stream=None):
+    """C = A B (NN), A B^T (NT) or A^T B (TN) on the matrix cores, fp32."""
+    for t, nm in ((A, "A"), (B, "B")):
+        _dev(t, torch.float32, nm)
+    lda, ldb = _rowmajor(A, "A"), _rowmajor(B, "B")
+    if op == GCN_GEMM_NN:
+        (M, K), (K2, N) = A.shape, B.shape
+    elif op == GCN_GEMM_NT:
+        (M, K), (N, K2) = A.shape, B.shape
+    elif op == GCN_GEMM_TN:
+        (K, M), (K2, N) = A.shape, B.shape
+    else:
+        raise ValueError("unknown op")
+    if K != K2:
+        raise ValueError("inner dimensions differ")
+    if C is None:
+        C = torch.empty((M, N), dtype=torch.float32, device=A.device)
+    _dev(C, torch.float32, "C")
+    ldc = _rowmajor(C, "C")
+    if tuple(C.shape) != (M, N):
+        raise ValueError("C must be %d x %d" % (M, N))
+    _check(lib().gcn_gemm_f32(op, M, N, K, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc,
+                              _stream(stream)))
+    return C
+
+
+def gcn_relu(H: torch.Tensor, stream=None):
+    """H = max(H, 0) in place."""
+    _dev(H, torch.float32, "H")
+    ld = _rowmajor(H, "H")
+    _check(lib().gcn_relu(H.shape[0], H.shape[1], H.data_ptr(), ld, _stream(stream)))
+    return H
+
+
+def gcn_relu_bwd(H: torch.Tensor, dH: torch.Tensor, stream=None):
+    """dH *= (H > 0) in place."""
+    _dev(H, torch.float32, "H")
+    _dev(dH, torch.float32, "dH")
+    if H.shape != dH.shape:
+        raise ValueError("H and dH shapes differ")
+    _check(lib().gcn_relu_bwd(H.shape[0], H.shape[1], H.data_ptr(), _rowmajor(H, "H"),
+                              dH.data_ptr(), _rowmajor(dH, "dH"), _stream(stream)))
+    return dH
+
+
+def gcn_softmax_xent(logits: torch.Tensor, labels: torch.Tensor, stream=None):
+    """(loss device double scalar, dlogits) of the mean softmax cross-entropy."""
+    _dev(logits, torch.float32, "logits")
+    _dev(labels, torch.int32, "labels")
+    n, C = logits.shape
+    if labels.numel() != n or not labels.is_contiguous():
+        raise ValueError("labels must be contiguous with one entry per row")
+    d = torch.empty_like(logits)
+    loss = torch.empty((), dtype=torch.float64, device=logits.device)
+    _check(lib().gcn_softmax_xent(n, C, logits.data_ptr(), _rowmajor(logits, "logits"),
+                                  labels.data_ptr(), d.data_ptr(), _rowmajor(d, "dlogits"),
+                                  loss.data_ptr(), _stream(stream)))
+    return loss, d
+
+
+def gcn_gcn2_step(g: Graph, X: torch.Tensor, W1: torch.Tensor, W2: torch.Tensor,
+                  labels: torch.Tensor, stream=None):
+    """(loss, dW1, dW2) of one training step of the 2-layer GCN."""
+    _dev(X, torch.float32, "X")
+    for t, nm in ((W1, "W1"), (W2, "W2")):
+        _dev(t, torch.float32, nm)
+        if not t.is_contiguous():
+            raise ValueError("%s must be contiguous" % nm)
+    _dev(labels, torch.int32, "labels")
+    f_in, hidden = W1.shape
+    hidden2, n_classes = W2.shape
+    if hidden2 != hidden or X.shape != (g.n_rows, f_in) or labels.numel() != g.n_rows:
+        raise ValueError("shape mismatch")
+    dW1 = torch.empty_like(W1)
+    dW2 = torch.empty_like(W2)
+    loss = torch.empty((), dtype=torch.float64, device=X.device)
+    _check(lib().gcn_gcn2_step(g.handle, X.data_ptr(), _rowmajor(X, "X"), f_in, W1.data_ptr(),
+                               hidden, W2.data_ptr(), n_classes, labels.data_ptr(),
+                               dW1.data_ptr(), dW2.data_ptr(), loss.data_ptr(), _stream(stream)))
+    return loss, dW1, dW2
 
 
 def gcn_graph_info(g: Graph):

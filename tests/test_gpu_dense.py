@@ -1,0 +1,154 @@
+"""GPU parity of the dense side of a layer and of the 2-layer GCN step.
+
+GEMMs are compared with float64 products of the same fp32 inputs, within
+1e-5 of the sum of |terms| per element (fp32 accumulation); the TN product is
+also checked for identical bits across runs. Softmax cross-entropy against
+its float64 definition. The whole step against the oracle's float64 step on a small graph and on the
+product-shaped graph: the loss within 1e-5 relative, dW1 and dW2 within
+1e-5 of the sum of |products| of their last GEMM.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import assert_close, dev, host, note
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def G():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2411_16025_amd as pkg
+    pkg.lib()
+    return pkg
+
+
+SHAPES = [(1, 1, 1), (64, 64, 32), (1000, 47, 256), (777, 256, 100), (130, 100, 5),
+          (4099, 33, 47)]
+
+
+@pytest.mark.parametrize("M,N,K", SHAPES)
+def test_gemm_nn_nt(G, M, N, K):
+    note("gemm nn/nt %dx%dx%d" % (M, N, K))
+    A = synth.uniform(201, M, K)
+    B = synth.uniform(202, K, N)
+    ref = A.astype(np.float64) @ B.astype(np.float64)
+    S = np.abs(A).astype(np.float64) @ np.abs(B).astype(np.float64)
+    C = host(G.gcn_gemm_f32(G.GCN_GEMM_NN, dev(A), dev(B)))
+    assert_close(C, ref, S, what="NN")
+    Bt = np.ascontiguousarray(B.T)
+    C2 = host(G.gcn_gemm_f32(G.GCN_GEMM_NT, dev(A), dev(Bt)))
+    assert_close(C2, ref, S, what="NT")
+
+
+@pytest.mark.parametrize("K,M,N", [(5, 3, 2), (8192, 100, 256), (20000, 256, 47),
+                                   (100003, 64, 64), (33, 1, 300)])
+def test_gemm_tn_split_k(G, K, M, N):
+    import torch
+    note("gemm tn %dx%dx%d" % (K, M, N))
+    A = synth.uniform(203, K, M)
+    B = synth.uniform(204, K, N)
+    ref = A.T.astype(np.float64) @ B.astype(np.float64)
+    S = np.abs(A).T.astype(np.float64) @ np.abs(B).astype(np.float64)
+    Ad, Bd = dev(A), dev(B)
+    C = G.gcn_gemm_f32(G.GCN_GEMM_TN, Ad, Bd)
+    assert_close(host(C), ref, S, what="TN")
+    C2 = G.gcn_gemm_f32(G.GCN_GEMM_TN, Ad, Bd)
+    assert torch.equal(C.view(torch.int32), C2.view(torch.int32))
+
+
+def test_gemm_strided_operands(G):
+    import torch
+    note("gemm strided")
+    A = synth.uniform(205, 300, 40, ld=44)
+    B = synth.uniform(206, 40, 20, ld=23)
+    Cfull = torch.full((300, 25), 3.0, device="cuda:0")
+    G.gcn_gemm_f32(G.GCN_GEMM_NN, dev(A)[:, :40], dev(B)[:, :20], C=Cfull[:, :20])
+    ref = A[:, :40].astype(np.float64) @ B[:, :20].astype(np.float64)
+    S = np.abs(A[:, :40]).astype(np.float64) @ np.abs(B[:, :20]).astype(np.float64)
+    Ch = host(Cfull)
+    assert_close(Ch[:, :20], ref, S, what="strided")
+    assert np.all(Ch[:, 20:] == 3.0)
+
+
+def test_relu_and_backward(G):
+    note("relu")
+    H = synth.uniform(207, 1000, 70)
+    dH = synth.uniform(208, 1000, 70)
+    Hd = dev(H)
+    G.gcn_relu(Hd)
+    assert np.array_equal(host(Hd), np.maximum(H, 0))
+    dHd = dev(dH)
+    G.gcn_relu_bwd(Hd, dHd)
+    assert np.array_equal(host(dHd), np.where(H > 0, dH, 0).astype(np.float32))
+
+
+@pytest.mark.parametrize("n,C", [(1, 1), (5000, 47), (333, 64), (100, 2)])
+def test_softmax_xent(G, n, C):
+    note("softmax xent n=%d C=%d" % (n, C))
+    z = synth.normal(209, n, C) * 3
+    y = synth.labels(210, n, C)
+    loss, d = G.gcn_softmax_xent(dev(z), dev(y))
+    z64 = z.astype(np.float64)
+    m = z64.max(axis=1, keepdims=True)
+    lse = m[:, 0] + np.log(np.exp(z64 - m).sum(axis=1))
+    ref = np.mean(lse - z64[np.arange(n), y])
+    assert abs(float(loss) - ref) <= 1e-6 * max(1.0, abs(ref))
+    P = np.exp(z64 - lse[:, None])
+    P[np.arange(n), y] -= 1.0
+    P /= n
+    assert np.allclose(host(d), P, rtol=1e-5, atol=1e-7 / n)
+
+
+def _step_check(G, w, f_in, hidden, n_classes, seed):
+    import torch
+    g = G.gcn_build_csr(w.n_rows, w.n_cols, dev(w.src), dev(w.dst), w.flags)
+    G.gcn_normalize(g)
+    X = synth.normal(3000 + seed, w.n_rows, f_in)
+    W1 = synth.glorot(5000 + seed, f_in, hidden)
+    W2 = synth.glorot(5100 + seed, hidden, n_classes)
+    y = synth.labels(5200 + seed, w.n_rows, n_classes)
+    loss, dW1, dW2 = G.gcn_gcn2_step(g, dev(X), dev(W1), dev(W2), dev(y))
+    torch.cuda.synchronize()
+    og = oracle.Graph(w.n_rows, w.n_cols, w.src, w.dst, w.flags)
+    ref = oracle.gcn_step(og, X, W1, W2, y)
+    assert abs(float(loss) - ref["loss"]) <= 1e-5 * abs(ref["loss"]), (float(loss), ref["loss"])
+    # Each weight-gradient element sums n products of mixed sign; its fp32
+    # error scales with the magnitude of every product that can enter it:
+    # |X|^T (A_hat^T |dH1|) with dH1 before the ReLU mask (an activation within
+    # rounding of 0 may fall on either side), and |H1|^T (A_hat^T |dlogits|).
+    S_dz1 = oracle._agg64(og.csc_ptr, og.csc_idx, og.csc_val, np.abs(ref["dH1"]))
+    S_dz2 = oracle._agg64(og.csc_ptr, og.csc_idx, og.csc_val, np.abs(ref["dlogits"]))
+    S1 = np.abs(X).astype(np.float64).T @ S_dz1
+    S2 = np.abs(ref["H1"]).T @ S_dz2
+    assert_close(host(dW1), ref["dW1"], S1, what="dW1")
+    assert_close(host(dW2), ref["dW2"], S2, what="dW2")
+    # repeated steps give identical bits
+    loss2, dW1b, dW2b = G.gcn_gcn2_step(g, dev(X), dev(W1), dev(W2), dev(y))
+    assert float(loss2) == float(loss)
+    assert torch.equal(dW1b.view(torch.int32), dW1.view(torch.int32))
+    assert torch.equal(dW2b.view(torch.int32), dW2.view(torch.int32))
+    return float(loss)
+
+
+def test_gcn_step_small(G):
+    note("gcn step small")
+    n = 3000
+    src, dst = synth.rmat_edges(211, n, 12 * n, perm_seed=212)
+    w = synth.Workload("rmat3000", n, n, src, dst, synth.SYMMETRIZE | synth.ADD_SELF_LOOPS, 100)
+    _step_check(G, w, 100, 256, 47, 11)
+
+
+def test_gcn_step_product_like(G):
+    import gc
+    import torch
+    note("gcn step product-like full size")
+    w = synth.product_like()
+    loss = _step_check(G, w, 100, 256, 47, 3)
+    assert abs(loss - np.log(47)) < 0.5
+    gc.collect()
+    torch.cuda.empty_cache()

@@ -381,3 +381,16 @@ def test_gcn_step_initial_loss_near_log_classes():
     out = oracle.gcn_step(g, X, synth.glorot(29, 100, 256), synth.glorot(30, 256, ncls),
                           synth.labels(31, n, ncls))
     assert abs(out["loss"] - math.log(ncls)) < 0.5
+
+
+def test_double_input_aggregation_matches_dense():
+    # the float64-input aggregation of the training step against dense A_hat H
+    n = 150
+    src, dst = synth.er_edges(33, n, 600)
+    g = oracle.Graph(n, n, src, dst, SYM | LOOPS)
+    A = dense_adjacency(n, n, src, dst, SYM | LOOPS)
+    Ah = csr_to_dense(g.csr_ptr, g.csr_idx, g.csr_val.astype(np.float64), n, n)
+    assert np.array_equal(Ah != 0, A != 0)
+    H = np.random.default_rng(3).standard_normal((n, 7))
+    got = oracle._agg64(g.csr_ptr, g.csr_idx, g.csr_val, H)
+    assert np.allclose(got, Ah @ H, rtol=1e-13, atol=1e-13)
