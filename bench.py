@@ -56,7 +56,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="rmat24_q8",
-                    choices=["rmat24_q8", "rmat24", "rmat20", "er4096", "product", "partition"])
+                    choices=["rmat24_q8", "rmat24", "rmat20", "er4096", "product", "partition",
+                             "gcn_step"])
     ap.add_argument("--cpu-target-s", type=float, default=12.0,
                     help="approximate seconds of oracle work for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -99,6 +100,74 @@ def read_counters(kernel):
         return None
 
 
+FP32_MFMA_PEAK_TFLOPS = 157.3
+
+
+def run_gcn_step(args):
+    """One training step of the 2-layer GCN (F_in 100, hidden 256, 47 classes)
+    on the product-shaped graph: four aggregations, five GEMMs, ReLU and
+    softmax cross-entropy, all in the library."""
+    import torch
+    import synth
+    import paper_2411_16025_amd as G
+
+    dev = torch.device("cuda:0")
+    w = synth.product_like()
+    g = G.gcn_build_csr(w.n_rows, w.n_cols, torch.from_numpy(w.src).to(dev),
+                        torch.from_numpy(w.dst).to(dev), w.flags)
+    G.gcn_normalize(g)
+    n, f_in, hidden, ncls = w.n_rows, 100, 256, 47
+    X = torch.from_numpy(synth.normal(3003, n, f_in)).to(dev)
+    W1 = torch.from_numpy(synth.glorot(5003, f_in, hidden)).to(dev)
+    W2 = torch.from_numpy(synth.glorot(5103, hidden, ncls)).to(dev)
+    y = torch.from_numpy(synth.labels(5203, n, ncls)).to(dev)
+    step = lambda: G.gcn_gcn2_step(g, X, W1, W2, y)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ts = time.time()
+    for _ in range(args.steps):
+        out = step()
+    torch.cuda.synchronize()
+    step_ms = (time.time() - ts) * 1e3 / args.steps
+    G.gcn_profile_enable(True)
+    for _ in range(max(1, args.profile_steps)):
+        step()
+    torch.cuda.synchronize()
+    prof = G.gcn_profile_read()
+    G.gcn_profile_enable(False)
+    ps = max(1, args.profile_steps)
+    gemm_flop = 2 * n * (f_in * hidden * 2 + hidden * ncls * 3)
+    gemm_ms = sum(v[1] for k, v in prof.items() if k.startswith("gemm")) / ps
+    agg_ms = sum(v[1] for k, v in prof.items() if k.startswith("agg")) / ps
+    bins = G.gcn_graph_bins(g, 0)
+    rows = sum(b["rows"] for b in bins)
+    ents = sum(b["entries"] for b in bins)
+    agg_bytes = 2 * (model_bytes(rows, ents, 0, hidden) + model_bytes(rows, ents, 0, ncls))
+    out_json = {
+        "metric": "2-layer GCN training step (fwd + bwd), product-shaped graph",
+        "value": round(step_ms, 3), "unit": "ms", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(step_ms, 3), "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name, "nodes": n, "nnz": g.nnz, "f_in": f_in, "hidden": hidden,
+                   "classes": ncls},
+        "loss": float(out[0]),
+        "aggregation_ms_per_step": round(agg_ms, 3),
+        "aggregation_modeled_GBps": round(agg_bytes / (agg_ms * 1e-3) / 1e9, 1),
+        "gemm_ms_per_step": round(gemm_ms, 3),
+        "gemm_TFLOPs": round(gemm_flop / (gemm_ms * 1e-3) / 1e12, 2),
+        "gemm_frac_of_fp32_mfma_peak": round(gemm_flop / (gemm_ms * 1e-3) / 1e12
+                                             / FP32_MFMA_PEAK_TFLOPS, 4),
+        "kernels_ms_per_step": {k: round(v[1] / ps, 4) for k, v in prof.items()},
+        "roofline": {"bound": "hbm", "kernel": "aggregation (4 passes)",
+                     "achieved": round(agg_bytes / (agg_ms * 1e-3) / 1e9, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(agg_bytes / (agg_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": None},
+    }
+    print(json.dumps(out_json), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -106,6 +175,9 @@ def main():
               "single MI355X (multi-GPU sharding is a design note, not part of this build); "
               "run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.workload == "gcn_step":
+        run_gcn_step(args)
+        return
 
     import torch
     import synth

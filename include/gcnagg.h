@@ -31,6 +31,10 @@
  *    untouched.
  *  - Calls that share a gcn_graph may run concurrently only if none of them
  *    is gcn_normalize or gcn_graph_free.
+ *  - Temporaries are allocated stream-ordered from the device's default
+ *    memory pool; on first use the library sets that pool's release
+ *    threshold to keep freed blocks for reuse (they stay reserved for the
+ *    process).
  */
 #ifndef GCNAGG_H
 #define GCNAGG_H

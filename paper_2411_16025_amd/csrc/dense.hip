@@ -217,13 +217,22 @@ __global__ __launch_bounds__(kThreads) void k_softmax_xent(int64_t n, int C,
   }
 }
 
-// loss = (sum of block losses in block order) / n, one thread
-__global__ void k_loss_total(int64_t nb, int64_t n, const double* __restrict__ block_loss,
-                             double* __restrict__ loss) {
-  if (blockIdx.x != 0 || threadIdx.x != 0) return;
+// loss = (sum of the block losses) / n by one workgroup in a fixed order:
+// thread t adds blocks t, t + 256, ... in turn, then a fixed tree combines
+// the 256 sums.
+__global__ __launch_bounds__(kThreads) void k_loss_total(int64_t nb, int64_t n,
+                                                         const double* __restrict__ block_loss,
+                                                         double* __restrict__ loss) {
+  __shared__ double part[kThreads];
   double s = 0.0;
-  for (int64_t b = 0; b < nb; ++b) s += block_loss[b];
-  *loss = s / (double)n;
+  for (int64_t b = threadIdx.x; b < nb; b += kThreads) s += block_loss[b];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  for (int off = kThreads / 2; off > 0; off >>= 1) {
+    if ((int)threadIdx.x < off) part[threadIdx.x] += part[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *loss = part[0] / (double)n;
 }
 
 }  // namespace
@@ -301,7 +310,9 @@ gcn_status softmax_xent(int64_t n, int C, const float* z, int64_t ldz, const int
   }
   hipError_t e = hipGetLastError();
   if (e == hipSuccess) {
-    hipLaunchKernelGGL(k_loss_total, dim3(1), dim3(64), 0, stream, nb, n, (const double*)bl, loss);
+    ProfScope ps("loss_total", stream);
+    hipLaunchKernelGGL(k_loss_total, dim3(1), dim3(kThreads), 0, stream, nb, n, (const double*)bl,
+                       loss);
     e = hipGetLastError();
   }
   tfree(bl, stream);

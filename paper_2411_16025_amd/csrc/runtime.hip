@@ -63,8 +63,32 @@ void dfree(void* p) {
   if (p) (void)hipFree(p);
 }
 
+// Stream-ordered temporaries come from the device's default memory pool. By
+// default the pool hands freed blocks back to the driver at every
+// synchronization, which makes each call pay for mapping its temporaries
+// again; once per device the pool is told to keep them instead.
+namespace {
+std::mutex g_pool_mu;
+uint64_t g_pool_done = 0;  // bit d set once device d's pool is configured
+
+void keep_pool_memory() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return;
+  std::lock_guard<std::mutex> lk(g_pool_mu);
+  if (g_pool_done & (1ull << dev)) return;
+  hipMemPool_t pool;
+  if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+    uint64_t keep = UINT64_MAX;
+    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+  }
+  (void)hipGetLastError();
+  g_pool_done |= 1ull << dev;
+}
+}  // namespace
+
 gcn_status tmalloc(void** p, size_t bytes, hipStream_t stream, const char* what) {
   *p = nullptr;
+  keep_pool_memory();
   hipError_t e = hipMallocAsync(p, bytes, stream);
   if (e != hipSuccess) {
     *p = nullptr;
