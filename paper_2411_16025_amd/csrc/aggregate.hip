@@ -175,8 +175,14 @@ struct SrcQ8 {
 
 // ---- helpers -------------------------------------------------------------------
 
+// Store a finished output row tile; relu clamps it at 0 (the activation of a
+// layer fused into the aggregation that produces it).
 template <int VEC>
-__device__ inline void store_row(float* __restrict__ y, int f0, int F, const float* acc) {
+__device__ inline void store_row(float* __restrict__ y, int f0, int F, const float* acc_in,
+                                 bool relu = false) {
+  float acc[VEC];
+#pragma unroll
+  for (int v = 0; v < VEC; ++v) acc[v] = relu ? fmaxf(acc_in[v], 0.f) : acc_in[v];
   if constexpr (VEC == 4) {
     if (f0 + 4 <= F) {
       f4 v = {acc[0], acc[1], acc[2], acc[3]};
@@ -316,7 +322,7 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* 
                                                   const Ent* __restrict__ ent,
                                                   const int32_t* __restrict__ rows, ShortArgs sa,
                                                   Src src, float* __restrict__ y, int64_t ldy,
-                                                  int F) {
+                                                  int F, bool relu) {
   constexpr int E = 64 / G;
   constexpr int NS = kLastShort - kFirstShort + 1;
   constexpr int U = 4;
@@ -370,7 +376,7 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* 
       }
     }
   }
-  if (active) store_row<VEC>(y + (int64_t)r * ldy, f0, F, acc);
+  if (active) store_row<VEC>(y + (int64_t)r * ldy, f0, F, acc, relu);
 }
 
 // Rows with 33..medium_max entries: one wavefront per row.
@@ -379,7 +385,7 @@ __global__ __launch_bounds__(kBlock) void k_medium(const int64_t* __restrict__ p
                                                    const Ent* __restrict__ ent,
                                                    const int32_t* __restrict__ rows, int64_t n,
                                                    Src src, float* __restrict__ y, int64_t ldy,
-                                                   int F) {
+                                                   int F, bool relu) {
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
   if (i >= n) return;  // whole wavefront leaves together
@@ -393,7 +399,7 @@ __global__ __launch_bounds__(kBlock) void k_medium(const int64_t* __restrict__ p
   for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
   accumulate_blocks<VEC, G, GCN_AGG_UNROLL>(ent, b, e, 0, 1, src, f0, active, acc);
   reduce_slots<VEC, G>(acc);
-  if (slot == 0 && active) store_row<VEC>(y + (int64_t)r * ldy, f0, F, acc);
+  if (slot == 0 && active) store_row<VEC>(y + (int64_t)r * ldy, f0, F, acc, relu);
 }
 
 // One workgroup per chunk of a long row. Wavefront w of the workgroup takes
@@ -407,7 +413,8 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_chunk(const Ent* __re
                                                   const int64_t* __restrict__ chunk_end,
                                                   const int32_t* __restrict__ chunk_part, Src src,
                                                   float* __restrict__ y, int64_t ldy,
-                                                  float* __restrict__ parts, int64_t ldp, int F) {
+                                                  float* __restrict__ parts, int64_t ldp, int F,
+                                                  bool relu) {
   __shared__ float red[kWavesPerBlock][G * VEC];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int slot = lane / G, gl = lane % G;
@@ -438,7 +445,7 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_chunk(const Ent* __re
     }
     const int32_t part = chunk_part[c];
     if (part < 0)
-      store_row<VEC>(y + (int64_t)r * ldy, f0, F, acc);
+      store_row<VEC>(y + (int64_t)r * ldy, f0, F, acc, relu);
     else
       store_row<VEC>(parts + (int64_t)part * ldp, f0, F, acc);
   }
@@ -452,7 +459,7 @@ __global__ __launch_bounds__(kBlock) void k_reduce_parts(const int32_t* __restri
                                                          int64_t n_giant,
                                                          const float* __restrict__ parts,
                                                          int64_t ldp, float* __restrict__ y,
-                                                         int64_t ldy, int F) {
+                                                         int64_t ldy, int F, bool relu) {
   constexpr int E = 64 / G;
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
@@ -481,7 +488,7 @@ __global__ __launch_bounds__(kBlock) void k_reduce_parts(const int32_t* __restri
     }
   }
   reduce_slots<VEC, G>(acc);
-  if (slot == 0 && active) store_row<VEC>(y + (int64_t)giant_row[i] * ldy, f0, F, acc);
+  if (slot == 0 && active) store_row<VEC>(y + (int64_t)giant_row[i] * ldy, f0, F, acc, relu);
 }
 
 // ---- launch ------------------------------------------------------------------------
@@ -491,7 +498,7 @@ inline unsigned blocks_for_waves(int64_t waves) {
 }
 
 template <int VEC, int G, class Src>
-gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F,
+gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F, bool relu,
                       hipStream_t stream) {
   constexpr int E = 64 / G;
   const Plan& p = m.plan;
@@ -520,7 +527,7 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
     ProfScope ps("agg_short", stream);
     hipLaunchKernelGGL((k_short<VEC, G, Src>), dim3(blocks_for_waves(waves), tiles), dim3(kBlock),
                        0, stream, (const int64_t*)m.ptr, (const Ent*)m.ent,
-                       (const int32_t*)p.rows, sa, src, y, ldy, F);
+                       (const int32_t*)p.rows, sa, src, y, ldy, F, relu);
     GCN_HIP(hipGetLastError());
   }
   // medium rows
@@ -529,7 +536,8 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
     ProfScope ps("agg_medium", stream);
     hipLaunchKernelGGL((k_medium<VEC, G, Src>), dim3(blocks_for_waves(n_med), tiles), dim3(kBlock),
                        0, stream, (const int64_t*)m.ptr, (const Ent*)m.ent,
-                       (const int32_t*)(p.rows + p.class_off[kMedium]), n_med, src, y, ldy, F);
+                       (const int32_t*)(p.rows + p.class_off[kMedium]), n_med, src, y, ldy, F,
+                       relu);
     GCN_HIP(hipGetLastError());
   }
   // long rows
@@ -542,7 +550,7 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
       hipLaunchKernelGGL((k_chunk<VEC, G, Src>), dim3((unsigned)p.n_chunks, tiles), dim3(kBlock), 0,
                          stream, (const Ent*)m.ent, (const int32_t*)p.chunk_row,
                          (const int64_t*)p.chunk_beg, (const int64_t*)p.chunk_end,
-                         (const int32_t*)p.chunk_part, src, y, ldy, parts, ldp, F);
+                         (const int32_t*)p.chunk_part, src, y, ldy, parts, ldp, F, relu);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) {
         tfree(parts, stream);
@@ -554,7 +562,7 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
       hipLaunchKernelGGL((k_reduce_parts<VEC, G>), dim3(blocks_for_waves(p.n_giant), tiles),
                          dim3(kBlock), 0, stream, (const int32_t*)p.giant_row,
                          (const int32_t*)p.giant_part_off, p.n_giant, (const float*)parts, ldp, y,
-                         ldy, F);
+                         ldy, F, relu);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) {
         tfree(parts, stream);
@@ -578,14 +586,14 @@ int lanes_for(int F, bool vec4) {
 
 template <template <int> class SrcT, class Make>
 gcn_status dispatch(const Mat& m, bool vec4, int F, float* y, int64_t ldy, hipStream_t stream,
-                    Make make) {
-  if (!vec4) return launch_all<1, 64>(m, make(SrcT<1>{}), y, ldy, F, stream);
+                    Make make, bool relu = false) {
+  if (!vec4) return launch_all<1, 64>(m, make(SrcT<1>{}), y, ldy, F, relu, stream);
   switch (lanes_for(F, true)) {
-    case 4: return launch_all<4, 4>(m, make(SrcT<4>{}), y, ldy, F, stream);
-    case 8: return launch_all<4, 8>(m, make(SrcT<4>{}), y, ldy, F, stream);
-    case 16: return launch_all<4, 16>(m, make(SrcT<4>{}), y, ldy, F, stream);
-    case 32: return launch_all<4, 32>(m, make(SrcT<4>{}), y, ldy, F, stream);
-    default: return launch_all<4, 64>(m, make(SrcT<4>{}), y, ldy, F, stream);
+    case 4: return launch_all<4, 4>(m, make(SrcT<4>{}), y, ldy, F, relu, stream);
+    case 8: return launch_all<4, 8>(m, make(SrcT<4>{}), y, ldy, F, relu, stream);
+    case 16: return launch_all<4, 16>(m, make(SrcT<4>{}), y, ldy, F, relu, stream);
+    case 32: return launch_all<4, 32>(m, make(SrcT<4>{}), y, ldy, F, relu, stream);
+    default: return launch_all<4, 64>(m, make(SrcT<4>{}), y, ldy, F, relu, stream);
   }
 }
 
@@ -639,15 +647,18 @@ gcn_status aggregate(const gcn_graph* g, const Mat& m, const void* X, int64_t ld
 }  // namespace
 
 gcn_status aggregate_f32(const Mat& m, const float* X, int64_t ldx, float* Y, int64_t ldy,
-                         int64_t F, hipStream_t stream) {
+                         int64_t F, bool relu, hipStream_t stream) {
   const int Fi = (int)F;
   const bool vec4 = aligned(Y, 16) && ldy % 4 == 0 && aligned(X, 16) && ldx % 4 == 0;
-  return dispatch<SrcF32>(m, vec4, Fi, Y, ldy, stream, [&](auto t) {
-    t.x = X;
-    t.ld = ldx;
-    t.F = Fi;
-    return t;
-  });
+  return dispatch<SrcF32>(
+      m, vec4, Fi, Y, ldy, stream,
+      [&](auto t) {
+        t.x = X;
+        t.ld = ldx;
+        t.F = Fi;
+        return t;
+      },
+      relu);
 }
 
 }  // namespace gcn

@@ -132,11 +132,13 @@ gcn_status radix_pass_u64(const uint64_t* in, uint64_t* out, int64_t n, int shif
 gcn_status scan_i64(const int64_t* in, int64_t* out, int64_t n, hipStream_t stream);
 
 // ---- aggregation and dense operations (aggregate.hip, dense.hip) -------------
-// Y = M X for fp32 X (M is a graph's CSR or CSC).
+// Y = M X for fp32 X (M is a graph's CSR or CSC); relu clamps the result at 0.
 gcn_status aggregate_f32(const Mat& m, const float* X, int64_t ldx, float* Y, int64_t ldy,
-                         int64_t F, hipStream_t stream);
+                         int64_t F, bool relu, hipStream_t stream);
+// mask (optional, [M x N], ldm): C[i, j] = 0 where mask[i, j] <= 0 (NN and NT)
 gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
-                    const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream);
+                    const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream,
+                    const float* mask = nullptr, int64_t ldm = 0);
 gcn_status relu_fwd(int64_t n, int64_t F, float* H, int64_t ld, hipStream_t stream);
 gcn_status relu_bwd(int64_t n, int64_t F, const float* H, int64_t ldh, float* dH, int64_t ld,
                     hipStream_t stream);

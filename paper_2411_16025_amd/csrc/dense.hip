@@ -151,6 +151,141 @@ __global__ __launch_bounds__(kThreads) void k_gemm_tn_partial(int64_t M, int64_t
   }
 }
 
+// Features [c, c + 4) of row `row` of a row-major matrix with `cols` columns,
+// zero outside it: one 16-byte load when the four are inside (the caller
+// guarantees 16-byte alignment of every row start and of c), else per element.
+__device__ inline f4 load4(const float* __restrict__ p, int64_t row, int64_t rows, int64_t ld,
+                           int64_t c, int64_t cols) {
+  f4 v = {0.f, 0.f, 0.f, 0.f};
+  if (row >= rows) return v;
+  const float* q = p + row * ld + c;
+  if (c + 4 <= cols) return *reinterpret_cast<const f4*>(q);
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (c + e < cols) v[e] = q[e];
+  return v;
+}
+
+// Wide-tile C = A op(B) for 16-byte aligned operands: a 64 x BN tile per
+// 256-thread workgroup (BN up to 256, so the tall operand is read once per
+// BN columns), 16-byte global loads, 32-deep K slices in LDS.
+template <int OP, int BN>
+__global__ __launch_bounds__(kThreads) void k_gemm_tall_v(int64_t M, int64_t N, int64_t K,
+                                                          const float* __restrict__ A, int64_t lda,
+                                                          const float* __restrict__ B, int64_t ldb,
+                                                          float* __restrict__ C, int64_t ldc,
+                                                          const float* __restrict__ mask,
+                                                          int64_t ldm) {
+  constexpr int NB = BN / 16;
+  __shared__ __align__(16) float As[kTile][kKc + 4];
+  __shared__ __align__(16) float Bs[kKc][BN + 4];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int64_t m0 = (int64_t)blockIdx.x * kTile;
+  const int64_t n0 = (int64_t)blockIdx.y * BN;
+  f4 acc[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+  for (int64_t k0 = 0; k0 < K; k0 += kKc) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {  // A: 64 x 32 = 512 float4
+      const int idx = t + kThreads * j, r = idx >> 3, c = (idx & 7) * 4;
+      *reinterpret_cast<f4*>(&As[r][c]) = load4(A, m0 + r, M, lda, k0 + c, K);
+    }
+    if (OP == kNN) {  // B: 32 x BN
+#pragma unroll
+      for (int j = 0; j < BN / 32; ++j) {
+        const int idx = t + kThreads * j, r = idx / (BN / 4), c = (idx % (BN / 4)) * 4;
+        *reinterpret_cast<f4*>(&Bs[r][c]) = load4(B, k0 + r, K, ldb, n0 + c, N);
+      }
+    } else {  // B stored N x K: BN rows of 32 k, transposed into Bs
+#pragma unroll
+      for (int j = 0; j < BN / 32; ++j) {
+        const int idx = t + kThreads * j, r = idx >> 3, c = (idx & 7) * 4;
+        const f4 v = load4(B, n0 + r, N, ldb, k0 + c, K);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) Bs[c + e][r] = v[e];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < kKc; kk += 4) {
+      const float a = As[16 * w + (lane & 15)][kk + (lane >> 4)];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const float b = Bs[kk + (lane >> 4)][16 * j + (lane & 15)];
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[j], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int64_t gn = n0 + 16 * j + (lane & 15);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t gm = m0 + 16 * w + 4 * (lane >> 4) + i;
+      if (gm < M && gn < N)
+        C[gm * ldc + gn] = (mask && !(mask[gm * ldm + gn] > 0.f)) ? 0.f : acc[j][i];
+    }
+  }
+}
+
+// Wide-tile partial C = A^T B over one K chunk for 16-byte aligned operands:
+// a (16 * WAVES) x BN tile per workgroup, so for C up to 128 x 256 each row
+// of A and B is read once per chunk.
+template <int WAVES, int BN>
+__global__ __launch_bounds__(WAVES * 64) void k_gemm_tn_v(int64_t M, int64_t N, int64_t K,
+                                                          int64_t split,
+                                                          const float* __restrict__ A, int64_t lda,
+                                                          const float* __restrict__ B, int64_t ldb,
+                                                          float* __restrict__ part) {
+  constexpr int BM = 16 * WAVES, NT = 64 * WAVES, NB = BN / 16;
+  __shared__ __align__(16) float As[kKc][BM + 4];
+  __shared__ __align__(16) float Bs[kKc][BN + 4];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int64_t m0 = (int64_t)blockIdx.x * BM;
+  const int64_t n0 = (int64_t)blockIdx.y * BN;
+  const int64_t chunk = blockIdx.z;
+  const int64_t kb = chunk * split;
+  const int64_t ke = std::min(K, kb + split);
+  f4 acc[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+  for (int64_t k0 = kb; k0 < ke; k0 += kKc) {
+#pragma unroll
+    for (int j = 0; j < kKc * BM / 4 / NT; ++j) {
+      const int idx = t + NT * j, r = idx / (BM / 4), c = (idx % (BM / 4)) * 4;
+      *reinterpret_cast<f4*>(&As[r][c]) = load4(A, k0 + r, ke, lda, m0 + c, M);
+    }
+#pragma unroll
+    for (int j = 0; j < kKc * BN / 4 / NT; ++j) {
+      const int idx = t + NT * j, r = idx / (BN / 4), c = (idx % (BN / 4)) * 4;
+      *reinterpret_cast<f4*>(&Bs[r][c]) = load4(B, k0 + r, ke, ldb, n0 + c, N);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < kKc; kk += 4) {
+      const float a = As[kk + (lane >> 4)][16 * w + (lane & 15)];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const float b = Bs[kk + (lane >> 4)][16 * j + (lane & 15)];
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[j], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+  float* out = part + chunk * M * N;
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int64_t gn = n0 + 16 * j + (lane & 15);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t gm = m0 + 16 * w + 4 * (lane >> 4) + i;
+      if (gm < M && gn < N) out[gm * N + gn] = acc[j][i];
+    }
+  }
+}
+
 // C[m][n] = sum over chunks, in chunk order, of part[chunk][m][n].
 __global__ __launch_bounds__(kThreads) void k_sum_partials(int64_t M, int64_t N, int64_t n_chunks,
                                                            const float* __restrict__ part,
@@ -181,9 +316,12 @@ __global__ __launch_bounds__(kThreads) void k_relu_bwd(int64_t n, int64_t F,
     if (!(h[i * ldh + f] > 0.f)) dh[i * ld + f] = 0.f;
 }
 
-// One wavefront per row (C <= 64 classes, lane = class): log-softmax with the
-// row maximum subtracted, per-row loss lse - z[y] accumulated in double per
-// workgroup in a fixed order, and dz = (softmax - onehot(y)) / n.
+constexpr int kSoftmaxRowsPerWave = 16;
+
+// One wavefront per row at a time (C <= 64 classes, lane = class), 16 rows
+// per wavefront: log-softmax with the row maximum subtracted, row losses
+// lse - z[y] added in row order in double, wavefront sums added in
+// wavefront order, and dz = (softmax - onehot(y)) / n.
 __global__ __launch_bounds__(kThreads) void k_softmax_xent(int64_t n, int C,
                                                            const float* __restrict__ z, int64_t ldz,
                                                            const int32_t* __restrict__ y,
@@ -191,7 +329,9 @@ __global__ __launch_bounds__(kThreads) void k_softmax_xent(int64_t n, int C,
                                                            double* __restrict__ block_loss) {
   __shared__ double wl[kThreads / 64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int64_t i = (int64_t)blockIdx.x * (kThreads / 64) + w;
+  double wave_loss = 0.0;
+  for (int rr = 0; rr < kSoftmaxRowsPerWave; ++rr) {
+  const int64_t i = ((int64_t)blockIdx.x * (kThreads / 64) + w) * kSoftmaxRowsPerWave + rr;
   double row_loss = 0.0;
   if (i < n) {
     const float v = lane < C ? z[i * ldz + lane] : -INFINITY;
@@ -208,7 +348,9 @@ __global__ __launch_bounds__(kThreads) void k_softmax_xent(int64_t n, int C,
     row_loss = (double)(lse - zy);
     if (lane < C) dz[i * ldd + lane] = (ex / s - (lane == yi ? 1.f : 0.f)) / (float)n;
   }
-  if (lane == 0) wl[w] = row_loss;
+  wave_loss += row_loss;
+  }
+  if (lane == 0) wl[w] = wave_loss;
   __syncthreads();
   if (threadIdx.x == 0) {
     double s = 0.0;
@@ -237,9 +379,53 @@ __global__ __launch_bounds__(kThreads) void k_loss_total(int64_t nb, int64_t n,
 
 }  // namespace
 
+namespace {
+
+bool aligned16(const void* p, int64_t ld) { return ((uintptr_t)p % 16) == 0 && ld % 4 == 0; }
+
+// widest tile of 64, 128 or 256 columns that is not mostly padding
+int tile_n(int64_t N) { return N <= 64 ? 64 : (N <= 128 ? 128 : 256); }
+
+template <int OP>
+void launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
+                 int64_t ldb, float* C, int64_t ldc, const float* mask, int64_t ldm,
+                 hipStream_t stream) {
+  const int bn = tile_n(N);
+  const dim3 grid((unsigned)ceil_div(M, kTile), (unsigned)ceil_div(N, bn));
+  if (bn == 64)
+    hipLaunchKernelGGL((k_gemm_tall_v<OP, 64>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda, B,
+                       ldb, C, ldc, mask, ldm);
+  else if (bn == 128)
+    hipLaunchKernelGGL((k_gemm_tall_v<OP, 128>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda,
+                       B, ldb, C, ldc, mask, ldm);
+  else
+    hipLaunchKernelGGL((k_gemm_tall_v<OP, 256>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda,
+                       B, ldb, C, ldc, mask, ldm);
+}
+
+void launch_tn(int64_t M, int64_t N, int64_t K, int64_t split, int64_t n_chunks, const float* A,
+               int64_t lda, const float* B, int64_t ldb, float* part, hipStream_t stream) {
+  constexpr int kWaves = 8, kBm = 16 * kWaves;
+  const int bn = tile_n(N);
+  const dim3 grid((unsigned)ceil_div(M, kBm), (unsigned)ceil_div(N, bn), (unsigned)n_chunks);
+  if (bn == 64)
+    hipLaunchKernelGGL((k_gemm_tn_v<kWaves, 64>), grid, dim3(64 * kWaves), 0, stream, M, N, K,
+                       split, A, lda, B, ldb, part);
+  else if (bn == 128)
+    hipLaunchKernelGGL((k_gemm_tn_v<kWaves, 128>), grid, dim3(64 * kWaves), 0, stream, M, N, K,
+                       split, A, lda, B, ldb, part);
+  else
+    hipLaunchKernelGGL((k_gemm_tn_v<kWaves, 256>), grid, dim3(64 * kWaves), 0, stream, M, N, K,
+                       split, A, lda, B, ldb, part);
+}
+
+}  // namespace
+
 gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
-                    const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream) {
+                    const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream,
+                    const float* mask, int64_t ldm) {
   if (M == 0 || N == 0) return GCN_OK;
+  const bool vec = aligned16(A, lda) && aligned16(B, ldb);
   if (op == GCN_GEMM_TN) {
     // chunk length: kSplitRows, grown so the chunk count fits the grid's z range
     const int64_t split = std::max<int64_t>(kSplitRows, ceil_div(ceil_div(K, 65535), kKc) * kKc);
@@ -248,9 +434,13 @@ gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int
     GCN_CHECK(talloc(&part, n_chunks * M * N, stream, "GEMM partials"));
     {
       ProfScope ps("gemm_tn_partial", stream);
-      hipLaunchKernelGGL(k_gemm_tn_partial, dim3((unsigned)ceil_div(M, kTile),
-                                                 (unsigned)ceil_div(N, kTile), (unsigned)n_chunks),
-                         dim3(kThreads), 0, stream, M, N, K, split, A, lda, B, ldb, part);
+      if (vec)
+        launch_tn(M, N, K, split, n_chunks, A, lda, B, ldb, part, stream);
+      else
+        hipLaunchKernelGGL(k_gemm_tn_partial, dim3((unsigned)ceil_div(M, kTile),
+                                                   (unsigned)ceil_div(N, kTile),
+                                                   (unsigned)n_chunks),
+                           dim3(kThreads), 0, stream, M, N, K, split, A, lda, B, ldb, part);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) {
         tfree(part, stream);
@@ -269,13 +459,18 @@ gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int
   }
   const dim3 grid((unsigned)ceil_div(M, kTile), (unsigned)ceil_div(N, kTile));
   ProfScope ps(op == GCN_GEMM_NN ? "gemm_nn" : "gemm_nt", stream);
-  if (op == GCN_GEMM_NN)
+  if (vec && op == GCN_GEMM_NN)
+    launch_tall<kNN>(M, N, K, A, lda, B, ldb, C, ldc, mask, ldm, stream);
+  else if (vec)
+    launch_tall<kNT>(M, N, K, A, lda, B, ldb, C, ldc, mask, ldm, stream);
+  else if (op == GCN_GEMM_NN)
     hipLaunchKernelGGL(k_gemm_tall<kNN>, grid, dim3(kThreads), 0, stream, M, N, K, A, lda, B, ldb,
                        C, ldc);
   else
     hipLaunchKernelGGL(k_gemm_tall<kNT>, grid, dim3(kThreads), 0, stream, M, N, K, A, lda, B, ldb,
                        C, ldc);
   GCN_HIP(hipGetLastError());
+  if (mask && !vec) return relu_bwd(M, N, mask, ldm, C, ldc, stream);
   return GCN_OK;
 }
 
@@ -300,7 +495,7 @@ gcn_status relu_bwd(int64_t n, int64_t F, const float* H, int64_t ldh, float* dH
 
 gcn_status softmax_xent(int64_t n, int C, const float* z, int64_t ldz, const int32_t* y,
                         float* dz, int64_t ldd, double* loss, hipStream_t stream) {
-  const int64_t nb = std::max<int64_t>(1, ceil_div(n, kThreads / 64));
+  const int64_t nb = std::max<int64_t>(1, ceil_div(n, (kThreads / 64) * kSoftmaxRowsPerWave));
   double* bl = nullptr;
   GCN_CHECK(talloc(&bl, nb, stream, "block losses"));
   {

@@ -27,7 +27,14 @@ extern "C" gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t 
   const int64_t ldh = (hidden + 3) & ~int64_t(3);
   const int64_t ldc = (n_classes + 3) & ~int64_t(3);
   float *z1 = nullptr, *h1 = nullptr, *z2 = nullptr, *lg = nullptr, *dl = nullptr, *dz2 = nullptr;
+  float* w2p = nullptr;  // W2 with rows padded to a multiple of 4 floats (16-byte aligned rows)
   gcn_status st = talloc(&z1, n * ldh, s, "Z1");
+  if (st == GCN_OK) st = talloc(&w2p, hidden * ldc, s, "W2 copy");
+  if (st == GCN_OK) {
+    hipError_t e = hipMemcpy2DAsync(w2p, ldc * sizeof(float), W2, n_classes * sizeof(float),
+                                    n_classes * sizeof(float), hidden, hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) st = hip_fail(e, "hipMemcpy2DAsync", __FILE__, __LINE__);
+  }
   if (st == GCN_OK) st = talloc(&h1, n * ldh, s, "H1");
   if (st == GCN_OK) st = talloc(&z2, n * ldc, s, "Z2");
   if (st == GCN_OK) st = talloc(&lg, n * ldc, s, "logits");
@@ -35,22 +42,20 @@ extern "C" gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t 
   if (st == GCN_OK) st = talloc(&dz2, n * ldc, s, "dZ2");
   // forward
   if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NN, n, hidden, f_in, X, ldx, W1, hidden, z1, ldh, s);
-  if (st == GCN_OK) st = aggregate_f32(g->csr, z1, ldh, h1, ldh, hidden, s);
-  if (st == GCN_OK) st = relu_fwd(n, hidden, h1, ldh, s);
-  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NN, n, n_classes, hidden, h1, ldh, W2, n_classes, z2,
-                                  ldc, s);
-  if (st == GCN_OK) st = aggregate_f32(g->csr, z2, ldc, lg, ldc, n_classes, s);
+  if (st == GCN_OK) st = aggregate_f32(g->csr, z1, ldh, h1, ldh, hidden, true, s);  // + ReLU
+  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NN, n, n_classes, hidden, h1, ldh, w2p, ldc, z2, ldc, s);
+  if (st == GCN_OK) st = aggregate_f32(g->csr, z2, ldc, lg, ldc, n_classes, false, s);
   if (st == GCN_OK) st = softmax_xent(n, (int)n_classes, lg, ldc, labels, dl, ldc, loss, s);
   // backward
-  if (st == GCN_OK) st = aggregate_f32(g->csc, dl, ldc, dz2, ldc, n_classes, s);
+  if (st == GCN_OK) st = aggregate_f32(g->csc, dl, ldc, dz2, ldc, n_classes, false, s);
   if (st == GCN_OK) st = gemm_f32(GCN_GEMM_TN, hidden, n_classes, n, h1, ldh, dz2, ldc, dW2,
                                   n_classes, s);
   float* dh1 = z1;  // Z1 is dead after the first aggregation
-  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NT, n, hidden, n_classes, dz2, ldc, W2, n_classes, dh1,
-                                  ldh, s);
-  if (st == GCN_OK) st = relu_bwd(n, hidden, h1, ldh, dh1, ldh, s);
+  // dH1 = dZ2 W2^T with the ReLU mask (H1 > 0) applied as it is stored
+  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NT, n, hidden, n_classes, dz2, ldc, w2p, ldc, dh1, ldh,
+                                  s, h1, ldh);
   float* dz1 = h1;  // H1 is dead once the ReLU mask is applied
-  if (st == GCN_OK) st = aggregate_f32(g->csc, dh1, ldh, dz1, ldh, hidden, s);
+  if (st == GCN_OK) st = aggregate_f32(g->csc, dh1, ldh, dz1, ldh, hidden, false, s);
   if (st == GCN_OK) st = gemm_f32(GCN_GEMM_TN, f_in, hidden, n, X, ldx, dz1, ldh, dW1, hidden, s);
   tfree(dz2, s);
   tfree(dl, s);
@@ -58,5 +63,6 @@ extern "C" gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t 
   tfree(z2, s);
   tfree(h1, s);
   tfree(z1, s);
+  tfree(w2p, s);
   return st;
 }

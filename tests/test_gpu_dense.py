@@ -152,3 +152,4 @@ def test_gcn_step_product_like(G):
     assert abs(loss - np.log(47)) < 0.5
     gc.collect()
     torch.cuda.empty_cache()
+
