@@ -67,7 +67,11 @@ enum {
 enum { GCN_DT_F32 = 0, GCN_DT_BF16 = 1 };
 
 /* gcn_aggregate_fwd_q8halo flags */
-enum { GCN_Q8_USE_CSC = 1u /* aggregate with A_hat^T instead of A_hat */ };
+enum {
+  GCN_Q8_USE_CSC = 1u, /* aggregate with A_hat^T instead of A_hat */
+  GCN_Q_CODES_2BIT = 2u /* halo codes are 2-bit, packed four per byte (see
+                           gcn_layernorm_quantize); ldq >= (F + 3) / 4 */
+};
 
 /* Build the sparse structure of A (or A + I) from an edge list: the
  * "clustering and sorting" step of Section 4 done on the device. Entries are
@@ -121,7 +125,9 @@ gcn_status gcn_aggregate_bwd(const gcn_graph* g, const void* G, int64_t ldg, int
  *   Y = A_hat x   (or A_hat^T x with GCN_Q8_USE_CSC; then x has n_rows rows
  *                  and Y has n_cols rows).
  *  X_local     fp32 [n_local_cols x F] (ldx); may be NULL if n_local_cols == 0.
- *  Q_halo      uint8 [n_in - n_local_cols x F] (ldq), n_in = rows of x.
+ *  Q_halo      uint8 [n_in - n_local_cols x F] (ldq), n_in = rows of x; with
+ *              GCN_Q_CODES_2BIT the codes are 2-bit (Section 7.3's Int2),
+ *              packed four per byte, and the code is taken from byte f / 4.
  *  halo_min, halo_scale   fp32 zero point Z and scale S of halo row h at
  *              element h * ldp (ldp >= 1). ldp = 1: two plain arrays;
  *              ldp = 2 with halo_scale == halo_min + 1: (Z, S) pairs side by
@@ -191,6 +197,27 @@ gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t ldx, int64_
                          const float* W1, int64_t hidden, const float* W2, int64_t n_classes,
                          const int32_t* labels, float* dW1, float* dW2, double* loss,
                          void* stream);
+
+/* LayerNorm-then-quantize producer for boundary rows (Section 6.1 steps 2
+ * and 3; Section 7.3 computes the parameters and the codes in one fused pass
+ * and fixes the bit width at 2).
+ *  flags   GCN_LAYERNORM: first y = (x - mean) / sqrt(var + eps) * gamma + beta
+ *          per row over the F features (biased variance, computed in double,
+ *          rounded once to fp32; gamma/beta fp32 [F] or NULL for 1 and 0);
+ *          without it y = x.
+ *  bits    8: one code byte per feature (as gcn_quantize_rows_u8);
+ *          2: codes 0..3 packed four per byte, feature f in bits
+ *             [2 (f % 4), 2 (f % 4) + 2) of byte f / 4 (padding codes 0).
+ *  Codes: Z = min y, S = (max y - min y) / (2^bits - 1), q = clamp(rint((y - Z)
+ *  / S), 0, 2^bits - 1) in fp32, all 0 when S == 0; Z and S at zmin[i * ldp],
+ *  scale[i * ldp]. Q [n x ldq] needs ldq >= F (8-bit) or (F + 3) / 4 (2-bit).
+ *  Y (optional, [n x F], ldy) receives the normalized rows. */
+enum { GCN_LAYERNORM = 1u };
+gcn_status gcn_layernorm_quantize(int64_t n, int64_t F, const float* X, int64_t ldx,
+                                  const float* gamma, const float* beta, double eps,
+                                  uint32_t flags, int bits, float* Y, int64_t ldy, uint8_t* Q,
+                                  int64_t ldq, float* zmin, float* scale, int64_t ldp,
+                                  void* stream);
 
 /* ---- support calls ---------------------------------------------------- */
 

@@ -68,6 +68,11 @@ def _L():
         lib.orc_dequant_rows.argtypes = [i64, i64, P, i64, P, P, P, i64]
         lib.orc_spmm_q8.argtypes = [i64, P, P, P, i64, P, i64, P, i64, P, P, i64, P, P]
         lib.orc_quantize_rows.argtypes = [i64, i64, P, i64, P, i64, P, P]
+        lib.orc_layernorm_rows.argtypes = [i64, i64, P, i64, P, P, ctypes.c_double, P, i64]
+        lib.orc_quantize_rows_bits.argtypes = [i64, i64, ctypes.c_int, P, i64, P, i64, P, P, i64]
+        lib.orc_dequant_rows_bits.argtypes = [i64, i64, ctypes.c_int, P, i64, P, P, i64, P, i64]
+        lib.orc_spmm_qbits.argtypes = [i64, P, P, P, i64, P, i64, ctypes.c_int, P, i64, P, P, i64,
+                                       i64, P, P]
         lib.orc_num_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -216,6 +221,57 @@ def quantize_rows(X):
     scale = np.empty(n, np.float32)
     _L().orc_quantize_rows(n, F, X.ctypes.data, X.strides[0] // 4, _p(Q), F, _p(zmin), _p(scale))
     return Q, zmin, scale
+
+
+def layernorm_rows(X, gamma=None, beta=None, eps=1e-5):
+    """Row LayerNorm in double, rounded once to fp32 (biased variance)."""
+    X = np.ascontiguousarray(X, np.float32)
+    n, F = X.shape
+    Y = np.empty((n, F), np.float32)
+    g = None if gamma is None else _c(gamma, np.float32)
+    b = None if beta is None else _c(beta, np.float32)
+    _L().orc_layernorm_rows(n, F, _p(X), F, _p(g), _p(b), float(eps), _p(Y), F)
+    return Y
+
+
+def code_bytes(F, bits):
+    return F if bits == 8 else (F + 3) // 4
+
+
+def quantize_rows_bits(X, bits):
+    """(Q, zmin, scale) with b-bit codes; 2-bit codes packed 4 per byte."""
+    X = np.ascontiguousarray(X, np.float32)
+    n, F = X.shape
+    Q = np.zeros((n, code_bytes(F, bits)), np.uint8)
+    zmin = np.empty(n, np.float32)
+    scale = np.empty(n, np.float32)
+    _L().orc_quantize_rows_bits(n, F, bits, _p(X), F, _p(Q), Q.shape[1], _p(zmin), _p(scale), 1)
+    return Q, zmin, scale
+
+
+def dequant_rows_bits(Q, zmin, scale, F, bits):
+    Q = _c(Q, np.uint8)
+    n = Q.shape[0]
+    out = np.empty((n, F), np.float32)
+    _L().orc_dequant_rows_bits(n, F, bits, _p(Q), Q.shape[1], _p(_c(zmin, np.float32)),
+                               _p(_c(scale, np.float32)), 1, _p(out), F)
+    return out
+
+
+def spmm_qbits(ptr, idx, val, n_local_cols, X_local, Q, zmin, scale, F, bits):
+    """(Y, S) with halo columns holding b-bit codes."""
+    ptr = _c(ptr, np.int64)
+    idx = _c(idx, np.int32)
+    val = _c(val, np.float32)
+    X_local = np.ascontiguousarray(X_local, np.float32)
+    Q = _c(Q, np.uint8)
+    n = len(ptr) - 1
+    Y = np.empty((n, F), np.float64)
+    S = np.empty((n, F), np.float64)
+    _L().orc_spmm_qbits(n, _p(ptr), _p(idx), _p(val), n_local_cols, _p(X_local),
+                        X_local.shape[1] if X_local.ndim == 2 else F, bits, _p(Q), Q.shape[1],
+                        _p(_c(zmin, np.float32)), _p(_c(scale, np.float32)), 1, F, _p(Y), _p(S))
+    return Y, S
 
 
 # ---------------------------------------------------------------------------

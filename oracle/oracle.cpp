@@ -298,6 +298,106 @@ void orc_quantize_rows(int64_t n, int64_t F, const float* X, int64_t ldx, uint8_
   }
 }
 
+// LayerNorm of each row over its F features (Section 6.1, step 2: applied to
+// the embedding table before quantization to remove outliers):
+// y = (x - mean) / sqrt(var + eps) * gamma + beta with the biased variance,
+// all in double, rounded once to fp32. gamma/beta may be null (1 and 0).
+void orc_layernorm_rows(int64_t n, int64_t F, const float* X, int64_t ldx, const float* gamma,
+                        const float* beta, double eps, float* Y, int64_t ldy) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    const float* x = X + i * ldx;
+    double mean = 0.0;
+    for (int64_t f = 0; f < F; ++f) mean += (double)x[f];
+    mean /= (double)F;
+    double var = 0.0;
+    for (int64_t f = 0; f < F; ++f) var += ((double)x[f] - mean) * ((double)x[f] - mean);
+    var /= (double)F;
+    const double inv = 1.0 / std::sqrt(var + eps);
+    for (int64_t f = 0; f < F; ++f) {
+      const double g = gamma ? (double)gamma[f] : 1.0;
+      const double b = beta ? (double)beta[f] : 0.0;
+      Y[i * ldy + f] = (float)(((double)x[f] - mean) * inv * g + b);
+    }
+  }
+}
+
+// b-bit per-row quantization (Section 2.4), b = 8 or 2:
+// Z = min, S = (max - min) / (2^b - 1), q = clamp(nearbyint((x - Z) / S), 0, 2^b - 1)
+// in fp32; codes 0 when S == 0. 8-bit codes are bytes; 2-bit codes are packed
+// four per byte, feature f of a row in bits [2 (f % 4), 2 (f % 4) + 2) of byte
+// f / 4 (pad codes 0). Params at zmin[i * ldp], scale[i * ldp].
+void orc_quantize_rows_bits(int64_t n, int64_t F, int bits, const float* X, int64_t ldx,
+                            uint8_t* Q, int64_t ldq, float* zmin, float* scale, int64_t ldp) {
+  const float levels = (float)((1 << bits) - 1);
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    const float* x = X + i * ldx;
+    float mn = x[0], mx = x[0];
+    for (int64_t f = 1; f < F; ++f) {
+      mn = std::min(mn, x[f]);
+      mx = std::max(mx, x[f]);
+    }
+    const float s = (mx - mn) / levels;
+    zmin[i * ldp] = mn;
+    scale[i * ldp] = s;
+    uint8_t* q = Q + i * ldq;
+    if (bits == 2)
+      for (int64_t k = 0; k < (F + 3) / 4; ++k) q[k] = 0;
+    for (int64_t f = 0; f < F; ++f) {
+      float c = 0.0f;
+      if (s != 0.0f) c = std::nearbyint((x[f] - mn) / s);
+      c = std::min(levels, std::max(0.0f, c));
+      if (bits == 8)
+        q[f] = (uint8_t)c;
+      else
+        q[f / 4] |= (uint8_t)((uint32_t)c << (2 * (f % 4)));
+    }
+  }
+}
+
+// Code of feature f of a b-bit row.
+static inline uint32_t code_of(const uint8_t* row, int64_t f, int bits) {
+  return bits == 8 ? row[f] : (row[f / 4] >> (2 * (f % 4))) & 3u;
+}
+
+// Dequantize b-bit rows: out[i, f] = fmaf(q, scale[i * ldp], zmin[i * ldp]).
+void orc_dequant_rows_bits(int64_t n, int64_t F, int bits, const uint8_t* Q, int64_t ldq,
+                           const float* zmin, const float* scale, int64_t ldp, float* out,
+                           int64_t ldo) {
+  for (int64_t i = 0; i < n; ++i)
+    for (int64_t f = 0; f < F; ++f)
+      out[i * ldo + f] =
+          std::fmaf((float)code_of(Q + i * ldq, f, bits), scale[i * ldp], zmin[i * ldp]);
+}
+
+// orc_spmm_q8 for b-bit halo codes.
+void orc_spmm_qbits(int64_t n_major, const int64_t* ptr, const int32_t* idx, const float* val,
+                    int64_t n_local_cols, const float* X, int64_t ldx, int bits, const uint8_t* Q,
+                    int64_t ldq, const float* zmin, const float* scale, int64_t ldp, int64_t F,
+                    double* Y, double* S) {
+#pragma omp parallel for schedule(dynamic, 256)
+  for (int64_t r = 0; r < n_major; ++r)
+    for (int64_t f = 0; f < F; ++f) {
+      double acc = 0.0, mag = 0.0;
+      for (int64_t k = ptr[r]; k < ptr[r + 1]; ++k) {
+        const int64_t j = idx[k];
+        float x;
+        if (j < n_local_cols) {
+          x = X[j * ldx + f];
+        } else {
+          const int64_t h = j - n_local_cols;
+          x = std::fmaf((float)code_of(Q + h * ldq, f, bits), scale[h * ldp], zmin[h * ldp]);
+        }
+        const double t = (double)val[k] * (double)x;
+        acc += t;
+        mag += std::fabs(t);
+      }
+      Y[r * F + f] = acc;
+      if (S) S[r * F + f] = mag;
+    }
+}
+
 int orc_num_threads(void) { return omp_get_max_threads(); }
 
 }  // extern "C"

@@ -123,6 +123,7 @@ struct SrcQ8 {
   const float* __restrict__ scale;
   int64_t ldp;
   bool paired;  // (Z, S) side by side: one 8-byte load
+  bool two_bit;  // 2-bit codes, four per byte
   int F;
   struct Raw {
     float v[VEC < 3 ? 3 : VEC];  // local: features; halo: {codes, Z, S}
@@ -146,7 +147,11 @@ struct SrcQ8 {
       r.v[2] = scale[h * ldp];
     }
     uint32_t c;
-    if constexpr (VEC == 4) {
+    if (two_bit) {
+      // byte f0 / 4 holds the codes of features f0 .. f0 + 3 (VEC = 4: f0 % 4 == 0)
+      const uint32_t byte = q[h * ldq + (f0 >> 2)];
+      c = VEC == 4 ? byte : (byte >> (2 * (f0 & 3))) & 3u;
+    } else if constexpr (VEC == 4) {
       if (f0 + 4 <= F) {
         c = *reinterpret_cast<const uint32_t*>(p);
       } else {
@@ -163,9 +168,11 @@ struct SrcQ8 {
   __device__ inline void decode(const Raw& r, int32_t j, float* out) const {
     if ((int64_t)j >= n_local) {
       const uint32_t c = __float_as_uint(r.v[0]);
+      const int w = two_bit ? 2 : 8;
+      const uint32_t m = two_bit ? 3u : 255u;
 #pragma unroll
       for (int v = 0; v < VEC; ++v)
-        out[v] = __builtin_fmaf((float)((c >> (8 * v)) & 255u), r.v[2], r.v[1]);
+        out[v] = __builtin_fmaf((float)((c >> (w * v)) & m), r.v[2], r.v[1]);
     } else {
 #pragma unroll
       for (int v = 0; v < VEC; ++v) out[v] = r.v[v];
@@ -687,7 +694,7 @@ extern "C" gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_loc
                                                uint32_t flags, void* stream) {
   clear_error();
   GCN_CHECK(check_common(g, F));
-  if (flags & ~(uint32_t)GCN_Q8_USE_CSC) {
+  if (flags & ~(uint32_t)(GCN_Q8_USE_CSC | GCN_Q_CODES_2BIT)) {
     set_error("unknown q8halo flag bits 0x%x", flags);
     return GCN_EINVAL;
   }
@@ -705,16 +712,18 @@ extern "C" gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_loc
     set_error("X_local must be non-NULL with ldx >= F when n_local_cols > 0");
     return GCN_EINVAL;
   }
-  if (n_local_cols < n_in && (!Q_halo || !halo_min || !halo_scale || ldq < F || ldp < 1)) {
-    set_error("Q_halo, halo_min, halo_scale must be non-NULL with ldq >= F and ldp >= 1 when "
-              "halo rows exist");
+  const bool two_bit = (flags & GCN_Q_CODES_2BIT) != 0;
+  const int64_t qbytes = two_bit ? (F + 3) / 4 : F;
+  if (n_local_cols < n_in && (!Q_halo || !halo_min || !halo_scale || ldq < qbytes || ldp < 1)) {
+    set_error("Q_halo, halo_min, halo_scale must be non-NULL with ldq >= code bytes per row and "
+              "ldp >= 1 when halo rows exist");
     return GCN_EINVAL;
   }
   const bool paired = ldp == 2 && halo_scale == halo_min + 1 && aligned(halo_min, 8);
   const int Fi = (int)F;
   const bool vec4 = aligned(Y, 16) && ldy % 4 == 0 && (n_local_cols == 0 ||
                     (aligned(X_local, 16) && ldx % 4 == 0)) &&
-                    (n_local_cols == n_in || (aligned(Q_halo, 4) && ldq % 4 == 0));
+                    (n_local_cols == n_in || two_bit || (aligned(Q_halo, 4) && ldq % 4 == 0));
   return dispatch<SrcQ8>(m, vec4, Fi, Y, ldy, (hipStream_t)stream, [&](auto t) {
     t.x = X_local;
     t.ldx = ldx;
@@ -725,6 +734,7 @@ extern "C" gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_loc
     t.scale = halo_scale;
     t.ldp = ldp;
     t.paired = paired;
+    t.two_bit = two_bit;
     t.F = Fi;
     return t;
   });

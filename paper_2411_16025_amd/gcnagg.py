@@ -21,6 +21,8 @@ GCN_ADD_SELF_LOOPS = 2
 GCN_DT_F32 = 0
 GCN_DT_BF16 = 1
 GCN_Q8_USE_CSC = 1
+GCN_Q_CODES_2BIT = 2
+GCN_LAYERNORM = 1
 
 STATUS = {0: "GCN_OK", 1: "GCN_EINVAL", 2: "GCN_ERANGE", 3: "GCN_ENOMEM", 4: "GCN_EHIP",
           5: "GCN_ESTATE"}
@@ -29,7 +31,8 @@ STATUS = {0: "GCN_OK", 1: "GCN_EINVAL", 2: "GCN_ERANGE", 3: "GCN_ENOMEM", 4: "GC
 GCN_GEMM_NN, GCN_GEMM_NT, GCN_GEMM_TN = 0, 1, 2
 
 EXPORTS = ("gcn_build_csr", "gcn_normalize", "gcn_aggregate_fwd", "gcn_aggregate_bwd",
-           "gcn_aggregate_fwd_q8halo", "gcn_quantize_rows_u8", "gcn_gemm_f32", "gcn_relu",
+           "gcn_aggregate_fwd_q8halo", "gcn_quantize_rows_u8", "gcn_layernorm_quantize",
+           "gcn_gemm_f32", "gcn_relu",
            "gcn_relu_bwd", "gcn_softmax_xent", "gcn_gcn2_step", "gcn_graph_free",
            "gcn_graph_info", "gcn_graph_export", "gcn_graph_bins", "gcn_profile_enable",
            "gcn_profile_read", "gcn_last_error")
@@ -61,6 +64,8 @@ def lib():
         L.gcn_aggregate_fwd_q8halo.argtypes = [P, i64, P, i64, P, i64, P, P, i64, P, i64, i64, u32,
                                                P]
         L.gcn_quantize_rows_u8.argtypes = [i64, i64, P, i64, P, i64, P, P, i64, P]
+        L.gcn_layernorm_quantize.argtypes = [i64, i64, P, i64, P, P, ctypes.c_double, u32, i32, P,
+                                             i64, P, i64, P, P, i64, P]
         L.gcn_gemm_f32.argtypes = [i32, i64, i64, i64, P, i64, P, i64, P, i64, P]
         L.gcn_relu.argtypes = [i64, i64, P, i64, P]
         L.gcn_relu_bwd.argtypes = [i64, i64, P, i64, P, i64, P]
@@ -201,7 +206,7 @@ def gcn_aggregate_bwd(g: Graph, G: torch.Tensor, dX: torch.Tensor | None = None,
 
 def gcn_aggregate_fwd_q8halo(g: Graph, n_local_cols: int, X_local, Q_halo, halo_min, halo_scale,
                              Y: torch.Tensor | None = None, use_csc: bool = False, F=None,
-                             stream=None):
+                             bits: int = 8, stream=None):
     """Y = A_hat [X_local; fmaf(Q, S, Z)] (or A_hat^T with use_csc).
 
     halo_min / halo_scale are 1-D tensors with a common stride ldp; the
@@ -218,6 +223,8 @@ def gcn_aggregate_fwd_q8halo(g: Graph, n_local_cols: int, X_local, Q_halo, halo_
     if Q_halo is not None:
         _dev(Q_halo, torch.uint8, "Q_halo")
         ldq = _rowmajor(Q_halo, "Q_halo")
+        if F is None and bits == 2:
+            raise ValueError("F must be given for 2-bit codes without X_local")
         F = Q_halo.shape[1] if F is None else F
         n_h = n_in - n_local_cols
         if Q_halo.shape[0] < n_h:
@@ -241,7 +248,8 @@ def gcn_aggregate_fwd_q8halo(g: Graph, n_local_cols: int, X_local, Q_halo, halo_
     ptr = lambda t: t.data_ptr() if t is not None else None
     _check(lib().gcn_aggregate_fwd_q8halo(
         g.handle, n_local_cols, ptr(X_local), ldx, ptr(Q_halo), ldq, ptr(halo_min),
-        ptr(halo_scale), ldp, Y.data_ptr(), ldy, F, GCN_Q8_USE_CSC if use_csc else 0,
+        ptr(halo_scale), ldp, Y.data_ptr(), ldy, F,
+        (GCN_Q8_USE_CSC if use_csc else 0) | (GCN_Q_CODES_2BIT if bits == 2 else 0),
         _stream(stream)))
     return Y
 
@@ -271,6 +279,33 @@ def gcn_quantize_rows_u8(X: torch.Tensor, Q=None, zmin=None, scale=None, paired=
     _check(lib().gcn_quantize_rows_u8(n, F, X.data_ptr(), ldx, Q.data_ptr(), ldq, zmin.data_ptr(),
                                       scale.data_ptr(), ldp, _stream(stream)))
     return Q, zmin, scale
+
+
+def gcn_layernorm_quantize(X: torch.Tensor, bits: int = 8, layernorm: bool = True, gamma=None,
+                           beta=None, eps: float = 1e-5, paired: bool = True, with_y: bool = False,
+                           stream=None):
+    """(Q, zmin, scale[, Y]): optional row LayerNorm, then b-bit codes (8 or 2,
+    2-bit packed four per byte) with per-row zero point and scale."""
+    _dev(X, torch.float32, "X")
+    ldx = _rowmajor(X, "X")
+    n, F = X.shape
+    qb = F if bits == 8 else (F + 3) // 4
+    Q = torch.empty((n, qb), dtype=torch.uint8, device=X.device)
+    zs = torch.empty((n, 2), dtype=torch.float32, device=X.device)
+    zmin, scale = (zs[:, 0], zs[:, 1]) if paired else (zs[:, 0].clone(), zs[:, 1].clone())
+    Y = torch.empty((n, F), dtype=torch.float32, device=X.device) if with_y else None
+    for t, nm in ((gamma, "gamma"), (beta, "beta")):
+        if t is not None:
+            _dev(t, torch.float32, nm)
+            if t.numel() != F or not t.is_contiguous():
+                raise ValueError("%s must hold F contiguous values" % nm)
+    ptr = lambda t: t.data_ptr() if t is not None else None
+    _check(lib().gcn_layernorm_quantize(n, F, X.data_ptr(), ldx, ptr(gamma), ptr(beta), eps,
+                                        GCN_LAYERNORM if layernorm else 0, bits, ptr(Y),
+                                        F if Y is not None else 0, Q.data_ptr(), qb,
+                                        zmin.data_ptr(), scale.data_ptr(), zmin.stride(0),
+                                        _stream(stream)))
+    return (Q, zmin, scale, Y) if with_y else (Q, zmin, scale)
 
 
 def gcn_gemm_f32(op: int, A: torch.Tensor, B: torch.Tensor, C: torch.Tensor | None = None,

@@ -394,3 +394,74 @@ def test_double_input_aggregation_matches_dense():
     H = np.random.default_rng(3).standard_normal((n, 7))
     got = oracle._agg64(g.csr_ptr, g.csr_idx, g.csr_val, H)
     assert np.allclose(got, Ah @ H, rtol=1e-13, atol=1e-13)
+
+
+# ---------------------------------------------------------------------------
+# Producer side: LayerNorm (Section 6.1 step 2) and b-bit quantization.
+# ---------------------------------------------------------------------------
+
+def test_layernorm_moments_and_affine():
+    X = synth.normal(40, 300, 100) * 7 + 3
+    Y = oracle.layernorm_rows(X, eps=0.0).astype(np.float64)
+    assert np.allclose(Y.mean(axis=1), 0, atol=1e-6)
+    assert np.allclose(Y.var(axis=1), 1, rtol=1e-5)
+    g = synth.uniform(41, 1, 100)[0]
+    b = synth.uniform(42, 1, 100)[0]
+    Y2 = oracle.layernorm_rows(X, g, b, eps=0.0).astype(np.float64)
+    assert np.allclose(Y2, Y * g + b, rtol=1e-5, atol=1e-5)
+    # a hand case: row (1, 2, 3, 4): mean 2.5, var 1.25
+    Y3 = oracle.layernorm_rows(np.array([[1, 2, 3, 4]], np.float32), eps=0.0)
+    assert np.allclose(Y3[0], (np.array([1, 2, 3, 4]) - 2.5) / np.sqrt(1.25), rtol=1e-6)
+    # a constant row normalizes to beta (here 0) for eps > 0
+    assert np.all(oracle.layernorm_rows(np.full((1, 9), 5.0, np.float32)) == 0)
+
+
+@pytest.mark.parametrize("bits", [8, 2])
+def test_bit_quantizer_nearest_code(bits):
+    X = synth.normal(43, 200, 37)
+    X[7] = -2.0
+    Q, Z, S = oracle.quantize_rows_bits(X, bits)
+    levels = (1 << bits) - 1
+    D = oracle.dequant_rows_bits(Q, Z, S, 37, bits).astype(np.float64)
+    assert S[7] == 0 and np.all(D[7] == -2.0)
+    assert np.allclose(S[S > 0], (X.max(1) - X.min(1))[S > 0] / levels, rtol=1e-6)
+    grid = np.arange(levels + 1, dtype=np.float64)
+    F = X.shape[1]
+    codes = Q[:, :F] if bits == 8 else (Q[:, np.arange(F) // 4] >> (2 * (np.arange(F) % 4))) & 3
+    assert codes.max() <= levels
+    for i in range(X.shape[0]):
+        if S[i] == 0:
+            continue
+        cand = grid[None, :] * np.float64(S[i]) + np.float64(Z[i])
+        best = np.abs(X[i].astype(np.float64)[:, None] - cand).min(axis=1)
+        chosen = np.abs(X[i].astype(np.float64) - (codes[i] * np.float64(S[i]) + np.float64(Z[i])))
+        assert np.all(chosen <= best + 1e-6 * S[i])
+        # the dequantized fp32 value is that code's grid point, rounded once
+        assert np.all(D[i] == (codes[i] * np.float64(S[i]) + np.float64(Z[i])).astype(np.float32))
+    if bits == 8:
+        Q8, Z8, S8 = oracle.quantize_rows(X)
+        assert np.array_equal(Q, Q8) and np.array_equal(Z, Z8) and np.array_equal(S, S8)
+
+
+def test_int2_packing_layout():
+    # feature f of a row sits in bits [2(f % 4), 2(f % 4) + 2) of byte f / 4
+    X = np.array([[0.0, 1.0, 2.0, 3.0, 3.0, 0.0]], np.float32)
+    Q, Z, S = oracle.quantize_rows_bits(X, 2)
+    assert Z[0] == 0 and S[0] == 1
+    assert Q.shape == (1, 2)
+    assert Q[0, 0] == 0 | (1 << 2) | (2 << 4) | (3 << 6)
+    assert Q[0, 1] == 3  # features 4, 5 = (3, 0); padding codes are 0
+
+
+def test_int2_halo_aggregation_matches_dequantized_plain():
+    n = 500
+    src, dst = synth.rmat_edges(44, n, 5000, perm_seed=45)
+    g = oracle.Graph(n, n, src, dst, SYM | LOOPS)
+    nlc, F = 375, 19
+    X = synth.normal(46, n, F)
+    Q, Z, S = oracle.quantize_rows_bits(X[nlc:], 2)
+    Xd = X.copy()
+    Xd[nlc:] = oracle.dequant_rows_bits(Q, Z, S, F, 2)
+    Y1, S1 = oracle.spmm_qbits(g.csr_ptr, g.csr_idx, g.csr_val, nlc, X[:nlc], Q, Z, S, F, 2)
+    Y2, S2 = g.fwd(Xd)
+    assert np.array_equal(Y1, Y2) and np.array_equal(S1, S2)
