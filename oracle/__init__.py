@@ -73,6 +73,8 @@ def _L():
         lib.orc_dequant_rows_bits.argtypes = [i64, i64, ctypes.c_int, P, i64, P, P, i64, P, i64]
         lib.orc_spmm_qbits.argtypes = [i64, P, P, P, i64, P, i64, ctypes.c_int, P, i64, P, P, i64,
                                        i64, P, P]
+        lib.orc_bipartite_cover.argtypes = [i64, i64, i64, P, P, P, P]
+        lib.orc_bipartite_cover.restype = i64
         lib.orc_num_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -272,6 +274,34 @@ def spmm_qbits(ptr, idx, val, n_local_cols, X_local, Q, zmin, scale, F, bits):
                         X_local.shape[1] if X_local.ndim == 2 else F, bits, _p(Q), Q.shape[1],
                         _p(_c(zmin, np.float32)), _p(_c(scale, np.float32)), 1, F, _p(Y), _p(S))
     return Y, S
+
+
+def bipartite_cover(eu, ev, n_u=None, n_v=None):
+    """(matching size, cover_u bool[n_u], cover_v bool[n_v]) of a bipartite graph."""
+    eu = _c(eu, np.int32)
+    ev = _c(ev, np.int32)
+    n_u = int(eu.max()) + 1 if n_u is None else n_u
+    n_v = int(ev.max()) + 1 if n_v is None else n_v
+    cu = np.zeros(max(n_u, 1), np.uint8)
+    cv = np.zeros(max(n_v, 1), np.uint8)
+    m = _L().orc_bipartite_cover(n_u, n_v, len(eu), _p(eu), _p(ev), _p(cu), _p(cv))
+    return int(m), cu[:n_u].astype(bool), cv[:n_v].astype(bool)
+
+
+def prepost_split(src, dst):
+    """Algorithm 1 of Section 5.2 on a remote edge list (src on the sending
+    worker, dst on the receiving one): the two endpoint sets are the sides of
+    a bipartite graph, a minimum vertex cover is found, and an edge is a post-
+    aggregation edge when its source is in the cover, else a pre-aggregation
+    edge. Returns (is_post bool[n_edges], volume = |cover|, cover sources,
+    cover destinations)."""
+    src = np.asarray(src)
+    dst = np.asarray(dst)
+    us, eu = np.unique(src, return_inverse=True)
+    vs, ev = np.unique(dst, return_inverse=True)
+    m, cu, cv = bipartite_cover(eu.astype(np.int32), ev.astype(np.int32), len(us), len(vs))
+    is_post = cu[eu]
+    return is_post, m, us[cu], vs[cv]
 
 
 # ---------------------------------------------------------------------------

@@ -398,6 +398,86 @@ void orc_spmm_qbits(int64_t n_major, const int64_t* ptr, const int32_t* idx, con
     }
 }
 
+// Minimum vertex cover of a bipartite graph (Section 5.3): a maximum matching
+// by augmenting paths (Kuhn's method: for each left vertex, search an
+// alternating path to a free right vertex), then Koenig's construction: Z =
+// vertices reachable from free left vertices along alternating paths (left to
+// right on any edge, right to left on matched edges); the cover is
+// (left not in Z) plus (right in Z). Edge e joins left eu[e] and right ev[e].
+// Returns the matching size, which equals the cover size.
+int64_t orc_bipartite_cover(int64_t n_u, int64_t n_v, int64_t n_edges, const int32_t* eu,
+                            const int32_t* ev, uint8_t* cover_u, uint8_t* cover_v) {
+  std::vector<int64_t> off((size_t)n_u + 1, 0);
+  for (int64_t e = 0; e < n_edges; ++e) off[eu[e] + 1] += 1;
+  for (int64_t u = 0; u < n_u; ++u) off[u + 1] += off[u];
+  std::vector<int32_t> adj((size_t)n_edges);
+  std::vector<int64_t> pos(off.begin(), off.end() - 1);
+  for (int64_t e = 0; e < n_edges; ++e) adj[pos[eu[e]]++] = ev[e];
+  std::vector<int32_t> match_u((size_t)n_u, -1), match_v((size_t)n_v, -1);
+  std::vector<int64_t> seen((size_t)n_v, -1);
+  std::vector<int32_t> stack_u, stack_v;
+  std::vector<int64_t> stack_k;
+  int64_t size = 0;
+  for (int64_t root = 0; root < n_u; ++root) {
+    // depth-first search for an augmenting path from root (explicit stack)
+    stack_u.assign(1, (int32_t)root);
+    stack_k.assign(1, off[root]);
+    stack_v.clear();
+    bool found = false;
+    while (!stack_u.empty() && !found) {
+      const int32_t u = stack_u.back();
+      int64_t& k = stack_k.back();
+      if (k == off[u + 1]) {
+        stack_u.pop_back();
+        stack_k.pop_back();
+        if (!stack_v.empty()) stack_v.pop_back();
+        continue;
+      }
+      const int32_t v = adj[k++];
+      if (seen[v] == root) continue;
+      seen[v] = root;
+      if (match_v[v] < 0) {
+        // augment along the stack: u_0 v_0 u_1 v_1 ... u_last v
+        stack_v.push_back(v);
+        for (size_t i = 0; i < stack_u.size(); ++i) {
+          match_u[stack_u[i]] = stack_v[i];
+          match_v[stack_v[i]] = stack_u[i];
+        }
+        found = true;
+      } else {
+        stack_v.push_back(v);
+        stack_u.push_back(match_v[v]);
+        stack_k.push_back(off[match_v[v]]);
+      }
+    }
+    size += found;
+  }
+  // Koenig: alternating reachability from free left vertices
+  std::vector<uint8_t> zu((size_t)n_u, 0), zv((size_t)n_v, 0);
+  std::vector<int32_t> queue;
+  for (int64_t u = 0; u < n_u; ++u)
+    if (match_u[u] < 0) {
+      zu[u] = 1;
+      queue.push_back((int32_t)u);
+    }
+  for (size_t qi = 0; qi < queue.size(); ++qi) {
+    const int32_t u = queue[qi];
+    for (int64_t k = off[u]; k < off[u + 1]; ++k) {
+      const int32_t v = adj[k];
+      if (zv[v]) continue;
+      zv[v] = 1;
+      const int32_t w = match_v[v];
+      if (w >= 0 && !zu[w]) {
+        zu[w] = 1;
+        queue.push_back(w);
+      }
+    }
+  }
+  for (int64_t u = 0; u < n_u; ++u) cover_u[u] = !zu[u];
+  for (int64_t v = 0; v < n_v; ++v) cover_v[v] = zv[v];
+  return size;
+}
+
 int orc_num_threads(void) { return omp_get_max_threads(); }
 
 }  // extern "C"

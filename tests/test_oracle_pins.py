@@ -465,3 +465,66 @@ def test_int2_halo_aggregation_matches_dequantized_plain():
     Y1, S1 = oracle.spmm_qbits(g.csr_ptr, g.csr_idx, g.csr_val, nlc, X[:nlc], Q, Z, S, F, 2)
     Y2, S2 = g.fwd(Xd)
     assert np.array_equal(Y1, Y2) and np.array_equal(S1, S2)
+
+
+# ---------------------------------------------------------------------------
+# Algorithm 1 (Section 5.2): minimum vertex cover and the pre/post split.
+# ---------------------------------------------------------------------------
+
+def _brute_force_cover(eu, ev, n_u, n_v):
+    import itertools
+    verts = [("u", i) for i in range(n_u)] + [("v", j) for j in range(n_v)]
+    for k in range(len(verts) + 1):
+        for comb in itertools.combinations(verts, k):
+            c = set(comb)
+            if all(("u", a) in c or ("v", b) in c for a, b in zip(eu, ev)):
+                return k
+    return len(verts)
+
+
+def test_golden_prepost_fig4():
+    edges, expect = [], {}
+    for line in open(os.path.join(GOLDEN, "prepost_fig4.txt")):
+        line = line.split("#", 1)[0].split()
+        if not line:
+            continue
+        if line[0].isdigit():
+            edges.append((int(line[0]), int(line[1])))
+        else:
+            expect.setdefault(line[0], []).append([int(t) for t in line[1:]])
+    src = np.array([e[0] for e in edges])
+    dst = np.array([e[1] for e in edges])
+    is_post, vol, cov_src, cov_dst = oracle.prepost_split(src, dst)
+    assert len(edges) == expect["volume_edges"][0][0]
+    assert len(np.unique(dst)) == expect["volume_pre"][0][0]
+    assert len(np.unique(src)) == expect["volume_post"][0][0]
+    assert vol == expect["volume_hybrid"][0][0]
+    assert sorted(list(cov_src) + list(cov_dst)) == expect["cover"][0]
+    got = {("post" if p else "pre", int(s), int(d)) for p, s, d in zip(is_post, src, dst)}
+    want = {(k, a, b) for k in ("post", "pre") for a, b in expect.get(k, [])}
+    assert got == want
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_cover_is_minimum_brute_force(seed):
+    # Koenig: cover size = maximum matching = the brute-force minimum cover
+    rng = np.random.default_rng(seed)
+    n_u, n_v = int(rng.integers(1, 7)), int(rng.integers(1, 7))
+    m = int(rng.integers(1, 14))
+    eu = rng.integers(0, n_u, m).astype(np.int32)
+    ev = rng.integers(0, n_v, m).astype(np.int32)
+    size, cu, cv = oracle.bipartite_cover(eu, ev, n_u, n_v)
+    assert np.all(cu[eu] | cv[ev])
+    assert cu.sum() + cv.sum() == size
+    assert size == _brute_force_cover(eu, ev, n_u, n_v)
+
+
+def test_split_covers_every_edge_on_random_remote_graph():
+    src, dst = synth.rmat_edges(47, 5000, 20000, perm_seed=48)
+    dst = dst + 10000  # the two workers' node ids are disjoint
+    is_post, vol, cs, cd = oracle.prepost_split(src, dst)
+    cover_s, cover_d = set(cs.tolist()), set(cd.tolist())
+    assert all((s in cover_s) == p for s, p in zip(src, is_post))
+    assert all(d in cover_d for d, p in zip(dst, is_post) if not p)
+    assert vol == len(cover_s) + len(cover_d)
+    assert vol <= min(len(np.unique(src)), len(np.unique(dst)))
