@@ -57,7 +57,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="rmat24_q8",
                     choices=["rmat24_q8", "rmat24", "rmat20", "er4096", "product", "partition",
-                             "gcn_step"])
+                             "gcn_step", "prepost"])
+    ap.add_argument("--senders", type=int, default=7,
+                    help="prepost: number of workers that own the halo nodes")
     ap.add_argument("--cpu-target-s", type=float, default=12.0,
                     help="approximate seconds of oracle work for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -168,6 +170,110 @@ def run_gcn_step(args):
     print(json.dumps(out_json), flush=True)
 
 
+def run_prepost(args):
+    """Hybrid pre/post-aggregation on the 14M x 20M partition: the halo nodes
+    belong to --senders workers (contiguous id ranges). Per sender, the host
+    split (Algorithm 1), the sender's pre-aggregation SpMM, and the receiver's
+    post-aggregation SpMM plus the partial-sum combine, against the plain
+    aggregation that receives every halo row with a cut edge."""
+    import torch
+    import synth
+    import paper_2411_16025_amd as G
+
+    dev = torch.device("cuda:0")
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    t0 = time.time()
+    w = synth.partition_111m()
+    F, nl, nh = w.F, w.n_rows, w.n_cols - w.n_rows
+    log("generated %s: %d entries in %.1f s" % (w.name, len(w.src), time.time() - t0))
+    X = synth.normal(3004, w.n_cols, F)
+    g_full = G.gcn_build_csr(w.n_rows, w.n_cols, d(w.src), d(w.dst), w.flags)
+    deg_d = d(w.deg)
+    G.gcn_normalize(g_full, deg_d)
+    cut = w.src >= nl
+    local = ~cut
+    s_all, d_all = w.src[cut] - nl, w.dst[cut]
+    owner = (s_all.astype(np.int64) * args.senders) // nh
+    split_s, vol, senders = 0.0, np.zeros(4, np.int64), []
+    post_src, post_dst, col_ids, n_cols = [], [], [np.arange(nl)], nl
+    for o in range(args.senders):
+        lo, hi = -(-o * nh // args.senders), -(-(o + 1) * nh // args.senders)
+        m = owner == o
+        sl, dd = (s_all[m] - lo).astype(np.int32), d_all[m]
+        ts = time.time()
+        is_post, src_slot, dst_slot, v = G.gcn_prepost_split(sl, dd, hi - lo, nl)
+        split_s += time.time() - ts
+        vol += (len(sl), len(np.unique(dd)), len(np.unique(sl)), v)
+        cov_src = np.flatnonzero(src_slot >= 0)
+        cov_dst = np.flatnonzero(dst_slot >= 0).astype(np.int32)
+        pre = ~is_post
+        gp = G.gcn_build_csr(len(cov_dst), hi - lo, d(sl[pre]), d(dst_slot[dd[pre]]), 0)
+        G.gcn_normalize_rc(gp, d(w.deg[cov_dst]), deg_d[nl + lo: nl + hi].contiguous())
+        senders.append((gp, d(X[nl + lo: nl + hi]), d(cov_dst)))
+        col_ids.append(nl + lo + cov_src)
+        post_src.append(n_cols + src_slot[sl[is_post]])
+        post_dst.append(dd[is_post])
+        n_cols += len(cov_src)
+        log("sender %d: %d cut edges, rows sent %d (post-only %d, pre-only %d)"
+            % (o, len(sl), v, len(np.unique(sl)), len(np.unique(dd))))
+    col_ids = np.concatenate(col_ids)
+    g_recv = G.gcn_build_csr(nl, n_cols, d(np.concatenate([w.src[local]] + post_src).astype(np.int32)),
+                             d(np.concatenate([w.dst[local]] + post_dst).astype(np.int32)),
+                             synth.ADD_SELF_LOOPS)
+    G.gcn_normalize_rc(g_recv, deg_d[:nl].contiguous(), d(w.deg[col_ids]))
+    X_full = d(X)
+    X_recv = d(X[col_ids])
+    Y_full = torch.empty(nl, F, device=dev)
+    Y_recv = torch.empty(nl, F, device=dev)
+    partials = [torch.empty(gp.n_rows, F, device=dev) for gp, _, _ in senders]
+
+    def full():
+        G.gcn_aggregate_fwd(g_full, X_full, Y_full)
+
+    def send():
+        for (gp, xs, _), P in zip(senders, partials):
+            G.gcn_aggregate_fwd(gp, xs, P)
+
+    def recv():
+        G.gcn_aggregate_fwd(g_recv, X_recv, Y_recv)
+        for (_, _, idx), P in zip(senders, partials):
+            G.gcn_add_rows(P, idx, Y_recv)
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        t = time.time()
+        for _ in range(args.steps):
+            fn()
+        torch.cuda.synchronize()
+        return (time.time() - t) * 1e3 / args.steps
+
+    full_ms, send_ms = timed(full), timed(send)
+    recv_ms = timed(recv)
+    S = torch.abs(Y_full).max().item()
+    diff = torch.abs(Y_full - Y_recv).max().item()
+    row_bytes = 4 * F
+    out = {
+        "metric": "hybrid pre/post aggregation: rows sent to one receiver and its aggregation time",
+        "value": int(vol[3]), "unit": "rows", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(recv_ms, 3), "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name + "_prepost", "senders": args.senders, "F": F,
+                   "cut_edges": int(vol[0])},
+        "rows_sent": {"edges": int(vol[0]), "pre_only": int(vol[1]), "post_only": int(vol[2]),
+                      "hybrid": int(vol[3])},
+        "bytes_sent_fp32": {"post_only": int(vol[2]) * row_bytes, "hybrid": int(vol[3]) * row_bytes},
+        "split_host_s": round(split_s, 3),
+        "receiver_full_ms": round(full_ms, 3), "receiver_hybrid_ms": round(recv_ms, 3),
+        "senders_pre_ms_total": round(send_ms, 3),
+        "max_abs_diff_vs_full": diff, "max_abs_output": S,
+        "nnz_full": g_full.nnz, "nnz_receiver_hybrid": g_recv.nnz,
+        "nnz_senders_pre": int(sum(gp.nnz for gp, _, _ in senders)),
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -177,6 +283,9 @@ def main():
         sys.exit(2)
     if args.workload == "gcn_step":
         run_gcn_step(args)
+        return
+    if args.workload == "prepost":
+        run_prepost(args)
         return
 
     import torch

@@ -107,6 +107,19 @@ gcn_status gcn_build_csr(int64_t n_rows, int64_t n_cols, int64_t n_edges, const 
  *  Synchronizes `stream` when deg is supplied (the degrees are checked). */
 gcn_status gcn_normalize(gcn_graph* g, const int32_t* deg, void* stream);
 
+/* As gcn_normalize, with separate degree arrays for the rows and for the
+ * columns: entry (r, c) becomes
+ * (float)(1 / sqrt((double)(deg_rows[r] + 1) * (double)(deg_cols[c] + 1))).
+ * This normalizes an operator whose row and column ids are different node
+ * sets, such as the pre-aggregation matrix of Section 5.2 (rows: the
+ * receiver's nodes in the vertex cover; columns: the sender's nodes) or a
+ * receiver whose columns are its own nodes followed by received rows.
+ *  deg_rows  int32 device array [n_rows], degrees without the self-loop, >= 0.
+ *  deg_cols  int32 device array [n_cols], likewise.
+ *  Negative degrees or NULL arrays -> GCN_EINVAL. Synchronizes `stream`. */
+gcn_status gcn_normalize_rc(gcn_graph* g, const int32_t* deg_rows, const int32_t* deg_cols,
+                            void* stream);
+
 /* Y[n_rows x F] = A_hat X. X is [n_cols x F] (ldx), fp32 or bf16 (dtype);
  * Y is fp32 (ldy). Accumulation is fp32; each output element is summed in
  * an order fixed by the graph alone, so repeated calls give identical bits. */
@@ -218,6 +231,46 @@ gcn_status gcn_layernorm_quantize(int64_t n, int64_t F, const float* X, int64_t 
                                   uint32_t flags, int bits, float* Y, int64_t ldy, uint8_t* Q,
                                   int64_t ldq, float* zmin, float* scale, int64_t ldp,
                                   void* stream);
+
+/* ---- hybrid pre/post-aggregation (Algorithm 1, Sections 5.2 and 5.3) ---- */
+
+/* Split the cut edges that a sending worker has into a receiving worker.
+ * Sending a source node's row serves all of its cut edges (post-aggregation
+ * on the receiver); sending the sender's partial sum for a destination node
+ * serves all of that node's cut edges (pre-aggregation on the sender). The
+ * split takes a minimum vertex cover of the bipartite remote graph (Eq. 1;
+ * each connected component is solved separately by Hopcroft-Karp maximum
+ * matching and Koenig's construction, in parallel host threads): an edge whose
+ * source is in the cover is a post-aggregation edge, every other edge is a
+ * pre-aggregation edge (its destination is then in the cover). The rows to
+ * send are the cover's nodes, as many as a maximum matching has edges.
+ * Host-side; every array is a host array.
+ *  n_src, n_dst  sender-local source ids [0, n_src), receiver-local
+ *                destination ids [0, n_dst); n_src + n_dst < 2^31.
+ *  src, dst      int32 [n_edges]; repeated pairs are allowed (out of range
+ *                -> GCN_ERANGE, nothing written).
+ *  is_post       uint8 [n_edges] or NULL: 1 for post-, 0 for pre-aggregation.
+ *  src_slot      int32 [n_src] or NULL: position of the source among the
+ *                covered sources (their send-buffer row, in increasing id
+ *                order), -1 if not covered.
+ *  dst_slot      int32 [n_dst] or NULL: likewise for covered destinations
+ *                (the row of the sender's partial-sum buffer).
+ *  volume        int64 or NULL: rows to send = size of the cover.
+ * Which minimum cover is returned when several exist is unspecified; its
+ * size is not. Host memory: about 40 bytes per edge and node. */
+gcn_status gcn_prepost_split(int64_t n_src, int64_t n_dst, int64_t n_edges, const int32_t* src,
+                             const int32_t* dst, uint8_t* is_post, int32_t* src_slot,
+                             int32_t* dst_slot, int64_t* volume);
+
+/* Post-aggregation combine on the receiver (Section 5.2): add the received
+ * partial sums to the rows they belong to, Y[idx[j], :] += P[j, :] for
+ * j < n, in fp32. P [n x F] (ldp) and Y [n_y x F] (ldy) are fp32 device
+ * arrays; idx is an int32 device array [n] of distinct row ids (the covered
+ * destinations, e.g. those with dst_slot >= 0 in slot order). Rows whose idx
+ * lies outside [0, n_y) are skipped, no error is reported for them; repeated
+ * ids race. Asynchronous on `stream`. */
+gcn_status gcn_add_rows(int64_t n, int64_t F, const float* P, int64_t ldp, const int32_t* idx,
+                        int64_t n_y, float* Y, int64_t ldy, void* stream);
 
 /* ---- support calls ---------------------------------------------------- */
 

@@ -261,11 +261,13 @@ __device__ inline int64_t row_of(const int64_t* ptr, int64_t lo, int64_t hi, int
   return lo;
 }
 
-// val of entry (r, c) = fp32(1 / sqrt((deg[r] + 1) * (deg[c] + 1))) in IEEE double
+// val of entry (r, c) = fp32(1 / sqrt((deg_major[r] + 1) * (deg_minor[c] + 1))) in
+// IEEE double
 __global__ __launch_bounds__(kThreads) void k_normalize(const int64_t* __restrict__ ptr,
                                                         int64_t n_major, Ent* __restrict__ ent,
                                                         int64_t nnz,
-                                                        const int32_t* __restrict__ deg) {
+                                                        const int32_t* __restrict__ deg_major,
+                                                        const int32_t* __restrict__ deg_minor) {
   __shared__ int64_t r_lo, r_hi;
   const int64_t k0 = (int64_t)blockIdx.x * kNormTile;
   const int64_t k1 = std::min(nnz, k0 + kNormTile) - 1;
@@ -276,8 +278,8 @@ __global__ __launch_bounds__(kThreads) void k_normalize(const int64_t* __restric
     const int64_t k = k0 + (int64_t)j * kThreads + threadIdx.x;
     if (k > k1) break;
     const int64_t r = row_of(ptr, r_lo, r_hi, k);
-    const double dr = (double)deg[r] + 1.0;
-    const double dc = (double)deg[ent[k].col] + 1.0;
+    const double dr = (double)deg_major[r] + 1.0;
+    const double dc = (double)deg_minor[ent[k].col] + 1.0;
     ent[k].val = (float)(1.0 / sqrt(dr * dc));
   }
 }
@@ -650,6 +652,50 @@ extern "C" gcn_status gcn_graph_info(const gcn_graph* g, int64_t* n_rows, int64_
   return GCN_OK;
 }
 
+namespace {
+
+// 1 if any of deg[0, n) is negative (synchronizes the stream)
+gcn_status check_degrees(const int32_t* deg, int64_t n, hipStream_t stream) {
+  if (n == 0) return GCN_OK;
+  int* err = nullptr;
+  GCN_CHECK(talloc(&err, 1, stream, "error flag"));
+  int host_err = 0;
+  hipError_t e = hipMemsetAsync(err, 0, sizeof(int), stream);
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL(k_check_degrees, dim3(grid_for(n)), dim3(kThreads), 0, stream, deg, n, err);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess) e = hipMemcpyAsync(&host_err, err, sizeof(int), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  tfree(err, stream);
+  if (e != hipSuccess) return hip_fail(e, "degree check", __FILE__, __LINE__);
+  if (host_err) {
+    set_error("supplied degrees must be >= 0");
+    return GCN_EINVAL;
+  }
+  return GCN_OK;
+}
+
+// values of A from row degrees and column degrees; A^T takes them swapped
+gcn_status normalize_with(gcn_graph* g, const int32_t* deg_rows, const int32_t* deg_cols,
+                          hipStream_t stream) {
+  for (int which = 0; which < 2; ++which) {
+    if (which == 1 && g->csc_shared) break;
+    Mat& m = which ? g->csc : g->csr;
+    if (m.nnz == 0) continue;
+    ProfScope ps("normalize", stream);
+    hipLaunchKernelGGL(k_normalize, dim3(grid_for(m.nnz, (int)kNormTile)), dim3(kThreads), 0,
+                       stream, (const int64_t*)m.ptr, m.n_major, m.ent, m.nnz,
+                       which ? deg_cols : deg_rows, which ? deg_rows : deg_cols);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "k_normalize", __FILE__, __LINE__);
+  }
+  g->normalized = true;
+  return GCN_OK;
+}
+
+}  // namespace
+
 extern "C" gcn_status gcn_normalize(gcn_graph* g, const int32_t* deg, void* stream_) {
   clear_error();
   GCN_CHECK(check_graph(g));
@@ -658,49 +704,33 @@ extern "C" gcn_status gcn_normalize(gcn_graph* g, const int32_t* deg, void* stre
     set_error("a rectangular graph needs a supplied degree array");
     return GCN_EINVAL;
   }
-  int32_t* own = nullptr;
-  const int32_t* d = deg;
-  gcn_status st = GCN_OK;
   if (deg) {
-    int* err = nullptr;
-    GCN_CHECK(talloc(&err, 1, stream, "error flag"));
-    int host_err = 0;
-    const int64_t n_nodes = std::max(g->n_rows, g->n_cols);
-    hipError_t e = hipMemsetAsync(err, 0, sizeof(int), stream);
-    if (e == hipSuccess) {
-      hipLaunchKernelGGL(k_check_degrees, dim3(grid_for(n_nodes)), dim3(kThreads), 0, stream,
-                         deg, n_nodes, err);
-      e = hipGetLastError();
-    }
-    if (e == hipSuccess) e = hipMemcpyAsync(&host_err, err, sizeof(int), hipMemcpyDeviceToHost, stream);
-    if (e == hipSuccess) e = hipStreamSynchronize(stream);
-    tfree(err, stream);
-    if (e != hipSuccess) return hip_fail(e, "degree check", __FILE__, __LINE__);
-    if (host_err) {
-      set_error("supplied degrees must be >= 0");
-      return GCN_EINVAL;
-    }
-  } else {
-    GCN_CHECK(talloc(&own, g->n_rows, stream, "degrees"));
-    hipLaunchKernelGGL(k_degrees, dim3(grid_for(g->n_rows)), dim3(kThreads), 0, stream, g->csr.ptr,
-                       (const Ent*)g->csr.ent, g->n_rows, own);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) st = hip_fail(e, "k_degrees", __FILE__, __LINE__);
-    d = own;
+    GCN_CHECK(check_degrees(deg, std::max(g->n_rows, g->n_cols), stream));
+    return normalize_with(g, deg, deg, stream);
   }
-  for (int which = 0; which < 2 && st == GCN_OK; ++which) {
-    if (which == 1 && g->csc_shared) break;
-    Mat& m = which ? g->csc : g->csr;
-    if (m.nnz == 0) continue;
-    ProfScope ps("normalize", stream);
-    hipLaunchKernelGGL(k_normalize, dim3(grid_for(m.nnz, (int)kNormTile)), dim3(kThreads), 0,
-                       stream, (const int64_t*)m.ptr, m.n_major, m.ent, m.nnz, d);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) st = hip_fail(e, "k_normalize", __FILE__, __LINE__);
-  }
+  int32_t* own = nullptr;
+  GCN_CHECK(talloc(&own, g->n_rows, stream, "degrees"));
+  hipLaunchKernelGGL(k_degrees, dim3(grid_for(g->n_rows)), dim3(kThreads), 0, stream, g->csr.ptr,
+                     (const Ent*)g->csr.ent, g->n_rows, own);
+  hipError_t e = hipGetLastError();
+  gcn_status st = e != hipSuccess ? hip_fail(e, "k_degrees", __FILE__, __LINE__)
+                                  : normalize_with(g, own, own, stream);
   tfree(own, stream);
-  if (st == GCN_OK) g->normalized = true;
   return st;
+}
+
+extern "C" gcn_status gcn_normalize_rc(gcn_graph* g, const int32_t* deg_rows,
+                                       const int32_t* deg_cols, void* stream_) {
+  clear_error();
+  GCN_CHECK(check_graph(g));
+  hipStream_t stream = (hipStream_t)stream_;
+  if (!deg_rows || !deg_cols) {
+    set_error("deg_rows and deg_cols must not be NULL");
+    return GCN_EINVAL;
+  }
+  GCN_CHECK(check_degrees(deg_rows, g->n_rows, stream));
+  GCN_CHECK(check_degrees(deg_cols, g->n_cols, stream));
+  return normalize_with(g, deg_rows, deg_cols, stream);
 }
 
 extern "C" gcn_status gcn_graph_export(const gcn_graph* g, int which, int64_t* ptr, int32_t* idx,

@@ -30,7 +30,8 @@ STATUS = {0: "GCN_OK", 1: "GCN_EINVAL", 2: "GCN_ERANGE", 3: "GCN_ENOMEM", 4: "GC
 # every symbol include/gcnagg.h declares
 GCN_GEMM_NN, GCN_GEMM_NT, GCN_GEMM_TN = 0, 1, 2
 
-EXPORTS = ("gcn_build_csr", "gcn_normalize", "gcn_aggregate_fwd", "gcn_aggregate_bwd",
+EXPORTS = ("gcn_build_csr", "gcn_normalize", "gcn_normalize_rc", "gcn_prepost_split",
+           "gcn_add_rows", "gcn_aggregate_fwd", "gcn_aggregate_bwd",
            "gcn_aggregate_fwd_q8halo", "gcn_quantize_rows_u8", "gcn_layernorm_quantize",
            "gcn_gemm_f32", "gcn_relu",
            "gcn_relu_bwd", "gcn_softmax_xent", "gcn_gcn2_step", "gcn_graph_free",
@@ -59,6 +60,9 @@ def lib():
         P, i64, u32, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint32, ctypes.c_int
         L.gcn_build_csr.argtypes = [i64, i64, i64, P, P, u32, P, ctypes.POINTER(P)]
         L.gcn_normalize.argtypes = [P, P, P]
+        L.gcn_normalize_rc.argtypes = [P, P, P, P]
+        L.gcn_prepost_split.argtypes = [i64, i64, i64, P, P, P, P, P, P]
+        L.gcn_add_rows.argtypes = [i64, i64, P, i64, P, i64, P, i64, P]
         L.gcn_aggregate_fwd.argtypes = [P, P, i64, i32, P, i64, i64, P]
         L.gcn_aggregate_bwd.argtypes = [P, P, i64, i32, P, i64, i64, P]
         L.gcn_aggregate_fwd_q8halo.argtypes = [P, i64, P, i64, P, i64, P, P, i64, P, i64, i64, u32,
@@ -158,6 +162,50 @@ def gcn_normalize(g: Graph, deg: torch.Tensor | None = None, stream=None):
             raise ValueError("deg must be contiguous with max(n_rows, n_cols) entries")
     _check(lib().gcn_normalize(g.handle, deg.data_ptr() if deg is not None else None,
                                _stream(stream)))
+
+
+def gcn_normalize_rc(g: Graph, deg_rows: torch.Tensor, deg_cols: torch.Tensor, stream=None):
+    """Normalize with row degrees [n_rows] and column degrees [n_cols]."""
+    for t, n, name in ((deg_rows, g.n_rows, "deg_rows"), (deg_cols, g.n_cols, "deg_cols")):
+        _dev(t, torch.int32, name)
+        if not t.is_contiguous() or t.numel() != n:
+            raise ValueError("%s must be contiguous with %d entries" % (name, n))
+    _check(lib().gcn_normalize_rc(g.handle, deg_rows.data_ptr(), deg_cols.data_ptr(),
+                                  _stream(stream)))
+
+
+def gcn_prepost_split(src, dst, n_src: int | None = None, n_dst: int | None = None):
+    """Algorithm 1 on host int32 edge arrays: (is_post bool[n_edges],
+    src_slot int32[n_src], dst_slot int32[n_dst], volume)."""
+    src = np.ascontiguousarray(src, dtype=np.int32)
+    dst = np.ascontiguousarray(dst, dtype=np.int32)
+    if src.shape != dst.shape or src.ndim != 1:
+        raise ValueError("src and dst must be 1-D arrays of one length")
+    n_src = int(src.max()) + 1 if n_src is None else int(n_src)
+    n_dst = int(dst.max()) + 1 if n_dst is None else int(n_dst)
+    is_post = np.zeros(len(src), np.uint8)
+    src_slot = np.zeros(max(n_src, 0), np.int32)
+    dst_slot = np.zeros(max(n_dst, 0), np.int32)
+    vol = ctypes.c_int64(0)
+    ptr = lambda a: a.ctypes.data if a.size else None  # noqa: E731
+    _check(lib().gcn_prepost_split(n_src, n_dst, len(src), ptr(src), ptr(dst), ptr(is_post),
+                                   ptr(src_slot), ptr(dst_slot), ctypes.byref(vol)))
+    return is_post.astype(bool), src_slot, dst_slot, int(vol.value)
+
+
+def gcn_add_rows(P: torch.Tensor, idx: torch.Tensor, Y: torch.Tensor, stream=None):
+    """Y[idx[j]] += P[j] in place (distinct idx)."""
+    _dev(P, torch.float32, "P")
+    _dev(Y, torch.float32, "Y")
+    _dev(idx, torch.int32, "idx")
+    if P.dim() != 2 or Y.dim() != 2 or P.shape[1] != Y.shape[1] or idx.numel() != P.shape[0]:
+        raise ValueError("need P [n x F], idx [n], Y [m x F]")
+    if not idx.is_contiguous():
+        raise ValueError("idx must be contiguous")
+    _check(lib().gcn_add_rows(P.shape[0], P.shape[1], P.data_ptr(), _rowmajor(P, "P"),
+                              idx.data_ptr(), Y.shape[0], Y.data_ptr(), _rowmajor(Y, "Y"),
+                              _stream(stream)))
+    return Y
 
 
 def _dtype_code(t):
