@@ -57,7 +57,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="rmat24_q8",
                     choices=["rmat24_q8", "rmat24", "rmat20", "er4096", "product", "partition",
-                             "gcn_step", "prepost"])
+                             "gcn_step", "prepost", "producer"])
+    ap.add_argument("--halo-bits", type=int, default=8, choices=[8, 2],
+                    help="code width of the halo rows (8: one byte per feature; 2: four per byte)")
     ap.add_argument("--senders", type=int, default=7,
                     help="prepost: number of workers that own the halo nodes")
     ap.add_argument("--cpu-target-s", type=float, default=12.0,
@@ -71,12 +73,17 @@ def parse():
     return ap.parse_args()
 
 
-def model_bytes(rows, entries, halo_entries, F, halo=True):
+def code_bytes(F, bits=8):
+    return F if bits == 8 else (F + 3) // 4
+
+
+def model_bytes(rows, entries, halo_entries, F, bits=8):
     """Minimum traffic: row pointer (8 B/row), column + value (8 B/entry),
-    gathered rows (4F B for fp32, F + 8 B for a uint8 row with its min and
-    scale), output rows (4F B)."""
+    gathered rows (4F B for fp32; the code bytes + 8 B for a quantized halo
+    row with its min and scale), output rows (4F B)."""
     local = entries - halo_entries
-    return 8 * rows + 8 * entries + 4 * F * local + (F + 8) * halo_entries + 4 * F * rows
+    return (8 * rows + 8 * entries + 4 * F * local + (code_bytes(F, bits) + 8) * halo_entries
+            + 4 * F * rows)
 
 
 def file_sha256(path):
@@ -274,6 +281,54 @@ def run_prepost(args):
     print(json.dumps(out), flush=True)
 
 
+def run_producer(args):
+    """The sender side of the quantized exchange on the RMAT-24 halo share
+    (4,194,304 rows x 128 fp32, N(0, 1)): row LayerNorm fused with 2-bit
+    quantization (codes packed four per byte, paired (min, scale)), plus the
+    8-bit and no-LayerNorm variants. Modeled bytes per call: the rows read
+    (4F B), the codes and the 8-byte parameter pair written."""
+    import torch
+    import synth
+    import paper_2411_16025_amd as G
+
+    dev = torch.device("cuda:0")
+    n, F = 1 << 22, 128
+    X = torch.from_numpy(synth.normal(3005, n, F)).to(dev)
+    variants = [("layernorm+int2", True, 2), ("int2", False, 2), ("layernorm+u8", True, 8),
+                ("u8", False, 8)]
+    res = {}
+    for name, ln, bits in variants:
+        fn = lambda: G.gcn_layernorm_quantize(X, bits=bits, layernorm=ln)  # noqa: E731
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
+        for _ in range(args.steps):
+            fn()
+        ev[1].record()
+        ev[1].synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / args.steps
+        B = n * (4 * F + code_bytes(F, bits) + 8)
+        res[name] = {"ms": round(ms, 4), "modeled_GB": round(B / 1e9, 3),
+                     "GBps": round(B / (ms * 1e-3) / 1e9, 1),
+                     "frac": round(B / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        log("%s: %.3f ms, %.1f GB/s" % (name, ms, res[name]["GBps"]))
+    main_v = res["layernorm+int2"]
+    out = {
+        "metric": "fused LayerNorm + 2-bit quantize of the halo rows, GB/s",
+        "value": main_v["GBps"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": main_v["ms"], "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "rmat24 halo rows 4194304 x 128 N(0,1)", "rows": n, "F": F},
+        "variants": res,
+        "roofline": {"bound": "hbm", "kernel": "ln_quantize", "achieved": main_v["GBps"],
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": main_v["frac"],
+                     "traffic": None},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -286,6 +341,9 @@ def main():
         return
     if args.workload == "prepost":
         run_prepost(args)
+        return
+    if args.workload == "producer":
+        run_producer(args)
         return
 
     import torch
@@ -342,9 +400,14 @@ def main():
     if args.no_cpu_baseline:
         X_h = None
     nlc = w.n_local_cols
-    if q8:
+    bits = args.halo_bits if q8 else 8
+    if q8 and bits == 8:
         QX, ZX, SX = G.gcn_quantize_rows_u8(X[nlc:], paired=True)
         QG, ZG, SG = G.gcn_quantize_rows_u8(Gd[nlc:], paired=True)
+    elif q8:
+        QX, ZX, SX = G.gcn_layernorm_quantize(X[nlc:], bits=bits, layernorm=False)
+        QG, ZG, SG = G.gcn_layernorm_quantize(Gd[nlc:], bits=bits, layernorm=False)
+    if q8:
         X_loc, G_loc = X[:nlc], Gd[:nlc]
     Y = torch.empty((w.n_rows, F), dtype=torch.float32, device=dev)
     dX = torch.empty((w.n_cols, F), dtype=torch.float32, device=dev)
@@ -353,10 +416,11 @@ def main():
 
     if q8:
         def fwd():
-            G.gcn_aggregate_fwd_q8halo(g, nlc, X_loc, QX, ZX, SX, Y=Y)
+            G.gcn_aggregate_fwd_q8halo(g, nlc, X_loc, QX, ZX, SX, Y=Y, F=F, bits=bits)
 
         def bwd():
-            G.gcn_aggregate_fwd_q8halo(g, nlc, G_loc, QG, ZG, SG, Y=dX, use_csc=True)
+            G.gcn_aggregate_fwd_q8halo(g, nlc, G_loc, QG, ZG, SG, Y=dX, use_csc=True, F=F,
+                                       bits=bits)
     else:
         def fwd():
             G.gcn_aggregate_fwd(g, X, Y=Y)
@@ -408,7 +472,7 @@ def main():
         rows = sum(b["rows"] for b in bins)
         ents = sum(b["entries"] for b in bins)
         halo = sum(b["halo_entries"] for b in bins)
-        return model_bytes(rows, ents, halo, F) + 8, ents, halo
+        return model_bytes(rows, ents, halo, F, bits) + 8, ents, halo
 
     Bf, nnz_f, halo_f = pass_bytes(bins_f)
     Bb, nnz_b, _ = pass_bytes(bins_b)
@@ -422,13 +486,14 @@ def main():
         dom = max(agg, key=lambda k: agg[k][1])
         launches, tot_ms = agg[dom]
         per_launch_bytes = 0.5 * sum(
-            model_bytes(b["rows"], b["entries"], b["halo_entries"], F)
+            model_bytes(b["rows"], b["entries"], b["halo_entries"], F, bits)
             for bins in (bins_f, bins_b) for c, b in enumerate(bins) if c in KERNEL_CLASSES[dom])
         avg_ms = tot_ms / launches
         achieved = per_launch_bytes / (avg_ms * 1e-3) / 1e9
         roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": read_counters(dom),
+                    "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": read_counters(dom) if bits == 8 else None,
                     "bytes_per_launch": int(per_launch_bytes), "avg_launch_ms": round(avg_ms, 4)}
 
     out = {
@@ -438,8 +503,10 @@ def main():
         "dtype": "f32", "data": "synthetic",
         "config": {"workload": w.name, "n_rows": w.n_rows, "n_cols": w.n_cols, "nnz": g.nnz,
                    "F": F, "halo_rows": (w.n_cols - nlc) if q8 else 0,
-                   "halo_storage": "u8 codes + fp32 (min, scale) pair per row" if q8 else None,
-                   "step": "fwd A_hat x + bwd A_hat^T g" + (" with fused uint8 halo dequant" if q8 else "")},
+                   "halo_storage": ("%s codes + fp32 (min, scale) pair per row"
+                                    % ("u8" if bits == 8 else "2-bit packed")) if q8 else None,
+                   "step": "fwd A_hat x + bwd A_hat^T g"
+                           + (" with fused %d-bit halo dequant" % bits if q8 else "")},
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),
         "edge_features_per_s": float("%.4g" % ef_per_s),
         "fwd_ms": round(fwd_ms, 4), "bwd_ms": round(bwd_ms, 4),
@@ -453,26 +520,30 @@ def main():
 
     # ---- CPU baseline: the oracle on a bounded sample of the same workload ----
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, X_h, nlc, F, args.cpu_target_s)
+        out["cpu_baseline"] = cpu_baseline(w, X_h, nlc, F, args.cpu_target_s, bits)
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(w, X_h, nlc, F, target_s):
+def cpu_baseline(w, X_h, nlc, F, target_s, bits=8):
     import oracle
     import synth
 
     order = synth.permutation(778, w.n_rows)  # rows in a seeded random order
     q8 = nlc is not None
-    if q8:
+    if q8 and bits == 8:
         Q, Z, S = oracle.quantize_rows(X_h[nlc:])
+    elif q8:
+        Q, Z, S = oracle.quantize_rows_bits(X_h[nlc:], bits)
 
     def run(n_sel):
         sel = np.sort(order[:n_sel]).astype(np.int32)
         ptr, idx = oracle.rows_of(w.n_rows, w.n_cols, w.src, w.dst, w.flags, sel)
         val = np.ones(len(idx), np.float32)  # unit weights: the cost does not depend on them
         t = time.time()
-        if q8:
+        if q8 and bits == 8:
             oracle.spmm_q8(ptr, idx, val, nlc, X_h[:nlc], Q, Z, S)
+        elif q8:
+            oracle.spmm_qbits(ptr, idx, val, nlc, X_h[:nlc], Q, Z, S, F, bits)
         else:
             oracle.spmm(ptr, idx, val, X_h)
         dt = time.time() - t
@@ -486,14 +557,14 @@ def cpu_baseline(w, X_h, nlc, F, target_s):
             break
         n = int(min(w.n_rows, n * min(8.0, target_s / max(dt, 1e-3))))
         dt, rows, ents, halo = run(n)
-    B = model_bytes(rows, ents, halo, F)
+    B = model_bytes(rows, ents, halo, F, bits)
     return {"value": round(B / dt / 1e9, 3), "unit": "GB/s", "cores": oracle.num_threads(),
             "kind": "oracle", "edge_features_per_s": float("%.4g" % (ents * F / dt)),
             "seconds": round(dt, 2),
             "sample": "forward aggregation (fp64 accumulation%s) over %d uniformly sampled rows "
                       "(%d entries) of %s, unit weights; structure of the sampled rows built by "
                       "the oracle from the edge list beforehand (untimed)"
-                      % (", uint8 halo dequantized" if q8 else "", rows, ents, w.name)}
+                      % (", %d-bit halo dequantized" % bits if q8 else "", rows, ents, w.name)}
 
 
 if __name__ == "__main__":

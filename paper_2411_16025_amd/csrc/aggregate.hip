@@ -108,12 +108,13 @@ struct SrcBF16 {
   }
 };
 
-// Input rows j < n_local are fp32; rows j >= n_local are uint8 codes with a
-// per-row zero point and scale: x = fmaf(q, S, Z), exactly one rounding. A
-// halo row's raw registers hold the packed codes, Z and S in the slots a
-// local row uses for its features, so both kinds cost the same registers.
-template <int VEC>
-struct SrcQ8 {
+// Input rows j < n_local are fp32; rows j >= n_local are BITS-bit codes (8:
+// one byte per feature; 2: four per byte) with a per-row zero point and
+// scale: x = fmaf(q, S, Z), exactly one rounding. A halo row's raw registers
+// hold the packed codes, Z and S in the slots a local row uses for its
+// features, so both kinds cost the same registers.
+template <int VEC, int BITS>
+struct SrcQ {
   const float* __restrict__ x;
   int64_t ldx;
   int64_t n_local;
@@ -123,7 +124,6 @@ struct SrcQ8 {
   const float* __restrict__ scale;
   int64_t ldp;
   bool paired;  // (Z, S) side by side: one 8-byte load
-  bool two_bit;  // 2-bit codes, four per byte
   int F;
   struct Raw {
     float v[VEC < 3 ? 3 : VEC];  // local: features; halo: {codes, Z, S}
@@ -147,7 +147,7 @@ struct SrcQ8 {
       r.v[2] = scale[h * ldp];
     }
     uint32_t c;
-    if (two_bit) {
+    if constexpr (BITS == 2) {
       // byte f0 / 4 holds the codes of features f0 .. f0 + 3 (VEC = 4: f0 % 4 == 0)
       const uint32_t byte = q[h * ldq + (f0 >> 2)];
       c = VEC == 4 ? byte : (byte >> (2 * (f0 & 3))) & 3u;
@@ -168,8 +168,8 @@ struct SrcQ8 {
   __device__ inline void decode(const Raw& r, int32_t j, float* out) const {
     if ((int64_t)j >= n_local) {
       const uint32_t c = __float_as_uint(r.v[0]);
-      const int w = two_bit ? 2 : 8;
-      const uint32_t m = two_bit ? 3u : 255u;
+      constexpr int w = BITS;
+      constexpr uint32_t m = (1u << BITS) - 1u;
 #pragma unroll
       for (int v = 0; v < VEC; ++v)
         out[v] = __builtin_fmaf((float)((c >> (w * v)) & m), r.v[2], r.v[1]);
@@ -180,16 +180,20 @@ struct SrcQ8 {
   }
 };
 
+template <int VEC>
+using SrcQ8 = SrcQ<VEC, 8>;
+template <int VEC>
+using SrcQ2 = SrcQ<VEC, 2>;
+
 // ---- helpers -------------------------------------------------------------------
 
 // Store a finished output row tile; relu clamps it at 0 (the activation of a
 // layer fused into the aggregation that produces it).
-template <int VEC>
-__device__ inline void store_row(float* __restrict__ y, int f0, int F, const float* acc_in,
-                                 bool relu = false) {
+template <int VEC, bool RELU = false>
+__device__ inline void store_row(float* __restrict__ y, int f0, int F, const float* acc_in) {
   float acc[VEC];
 #pragma unroll
-  for (int v = 0; v < VEC; ++v) acc[v] = relu ? fmaxf(acc_in[v], 0.f) : acc_in[v];
+  for (int v = 0; v < VEC; ++v) acc[v] = RELU ? fmaxf(acc_in[v], 0.f) : acc_in[v];
   if constexpr (VEC == 4) {
     if (f0 + 4 <= F) {
       f4 v = {acc[0], acc[1], acc[2], acc[3]};
@@ -324,12 +328,12 @@ __global__ __launch_bounds__(kBlock) void k_zero_rows(const int32_t* __restrict_
 // row's (column, value) pairs with one coalesced access and share them by
 // lane shuffles; the loop bound is the class's longest row, so every lane
 // of the wavefront runs the same iterations.
-template <int VEC, int G, class Src>
+template <int VEC, int G, class Src, bool RELU>
 __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* __restrict__ ptr,
                                                   const Ent* __restrict__ ent,
                                                   const int32_t* __restrict__ rows, ShortArgs sa,
                                                   Src src, float* __restrict__ y, int64_t ldy,
-                                                  int F, bool relu) {
+                                                  int F) {
   constexpr int E = 64 / G;
   constexpr int NS = kLastShort - kFirstShort + 1;
   constexpr int U = 4;
@@ -383,16 +387,16 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* 
       }
     }
   }
-  if (active) store_row<VEC>(y + (int64_t)r * ldy, f0, F, acc, relu);
+  if (active) store_row<VEC, RELU>(y + (int64_t)r * ldy, f0, F, acc);
 }
 
 // Rows with 33..medium_max entries: one wavefront per row.
-template <int VEC, int G, class Src>
+template <int VEC, int G, class Src, bool RELU>
 __global__ __launch_bounds__(kBlock) void k_medium(const int64_t* __restrict__ ptr,
                                                    const Ent* __restrict__ ent,
                                                    const int32_t* __restrict__ rows, int64_t n,
                                                    Src src, float* __restrict__ y, int64_t ldy,
-                                                   int F, bool relu) {
+                                                   int F) {
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
   if (i >= n) return;  // whole wavefront leaves together
@@ -406,22 +410,21 @@ __global__ __launch_bounds__(kBlock) void k_medium(const int64_t* __restrict__ p
   for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
   accumulate_blocks<VEC, G, GCN_AGG_UNROLL>(ent, b, e, 0, 1, src, f0, active, acc);
   reduce_slots<VEC, G>(acc);
-  if (slot == 0 && active) store_row<VEC>(y + (int64_t)r * ldy, f0, F, acc, relu);
+  if (slot == 0 && active) store_row<VEC, RELU>(y + (int64_t)r * ldy, f0, F, acc);
 }
 
 // One workgroup per chunk of a long row. Wavefront w of the workgroup takes
 // the chunk's 64-entry blocks w, w + 4, w + 8, ...; wavefront sums meet in
 // LDS and are added in wavefront order. Single-chunk rows write Y, others a
 // partial row.
-template <int VEC, int G, class Src>
+template <int VEC, int G, class Src, bool RELU>
 __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_chunk(const Ent* __restrict__ ent,
                                                   const int32_t* __restrict__ chunk_row,
                                                   const int64_t* __restrict__ chunk_beg,
                                                   const int64_t* __restrict__ chunk_end,
                                                   const int32_t* __restrict__ chunk_part, Src src,
                                                   float* __restrict__ y, int64_t ldy,
-                                                  float* __restrict__ parts, int64_t ldp, int F,
-                                                  bool relu) {
+                                                  float* __restrict__ parts, int64_t ldp, int F) {
   __shared__ float red[kWavesPerBlock][G * VEC];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int slot = lane / G, gl = lane % G;
@@ -452,7 +455,7 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_chunk(const Ent* __re
     }
     const int32_t part = chunk_part[c];
     if (part < 0)
-      store_row<VEC>(y + (int64_t)r * ldy, f0, F, acc, relu);
+      store_row<VEC, RELU>(y + (int64_t)r * ldy, f0, F, acc);
     else
       store_row<VEC>(parts + (int64_t)part * ldp, f0, F, acc);
   }
@@ -460,13 +463,13 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_chunk(const Ent* __re
 
 // Sum the partial rows of each multi-chunk row in chunk order: slot s adds
 // partials s, s + E, ...; the slots are then combined by the butterfly.
-template <int VEC, int G>
+template <int VEC, int G, bool RELU>
 __global__ __launch_bounds__(kBlock) void k_reduce_parts(const int32_t* __restrict__ giant_row,
                                                          const int32_t* __restrict__ part_off,
                                                          int64_t n_giant,
                                                          const float* __restrict__ parts,
                                                          int64_t ldp, float* __restrict__ y,
-                                                         int64_t ldy, int F, bool relu) {
+                                                         int64_t ldy, int F) {
   constexpr int E = 64 / G;
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
@@ -495,7 +498,7 @@ __global__ __launch_bounds__(kBlock) void k_reduce_parts(const int32_t* __restri
     }
   }
   reduce_slots<VEC, G>(acc);
-  if (slot == 0 && active) store_row<VEC>(y + (int64_t)giant_row[i] * ldy, f0, F, acc, relu);
+  if (slot == 0 && active) store_row<VEC, RELU>(y + (int64_t)giant_row[i] * ldy, f0, F, acc);
 }
 
 // ---- launch ------------------------------------------------------------------------
@@ -504,8 +507,8 @@ inline unsigned blocks_for_waves(int64_t waves) {
   return (unsigned)std::max<int64_t>(1, ceil_div(waves, kWavesPerBlock));
 }
 
-template <int VEC, int G, class Src>
-gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F, bool relu,
+template <int VEC, int G, bool RELU, class Src>
+gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F,
                       hipStream_t stream) {
   constexpr int E = 64 / G;
   const Plan& p = m.plan;
@@ -532,19 +535,18 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
   }
   if (waves > 0) {
     ProfScope ps("agg_short", stream);
-    hipLaunchKernelGGL((k_short<VEC, G, Src>), dim3(blocks_for_waves(waves), tiles), dim3(kBlock),
-                       0, stream, (const int64_t*)m.ptr, (const Ent*)m.ent,
-                       (const int32_t*)p.rows, sa, src, y, ldy, F, relu);
+    hipLaunchKernelGGL((k_short<VEC, G, Src, RELU>), dim3(blocks_for_waves(waves), tiles),
+                       dim3(kBlock), 0, stream, (const int64_t*)m.ptr, (const Ent*)m.ent,
+                       (const int32_t*)p.rows, sa, src, y, ldy, F);
     GCN_HIP(hipGetLastError());
   }
   // medium rows
   const int64_t n_med = p.class_off[kMedium + 1] - p.class_off[kMedium];
   if (n_med > 0) {
     ProfScope ps("agg_medium", stream);
-    hipLaunchKernelGGL((k_medium<VEC, G, Src>), dim3(blocks_for_waves(n_med), tiles), dim3(kBlock),
-                       0, stream, (const int64_t*)m.ptr, (const Ent*)m.ent,
-                       (const int32_t*)(p.rows + p.class_off[kMedium]), n_med, src, y, ldy, F,
-                       relu);
+    hipLaunchKernelGGL((k_medium<VEC, G, Src, RELU>), dim3(blocks_for_waves(n_med), tiles),
+                       dim3(kBlock), 0, stream, (const int64_t*)m.ptr, (const Ent*)m.ent,
+                       (const int32_t*)(p.rows + p.class_off[kMedium]), n_med, src, y, ldy, F);
     GCN_HIP(hipGetLastError());
   }
   // long rows
@@ -554,10 +556,10 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
     if (p.n_parts > 0) GCN_CHECK(talloc(&parts, p.n_parts * ldp, stream, "partial rows"));
     {
       ProfScope ps("agg_chunk", stream);
-      hipLaunchKernelGGL((k_chunk<VEC, G, Src>), dim3((unsigned)p.n_chunks, tiles), dim3(kBlock), 0,
-                         stream, (const Ent*)m.ent, (const int32_t*)p.chunk_row,
+      hipLaunchKernelGGL((k_chunk<VEC, G, Src, RELU>), dim3((unsigned)p.n_chunks, tiles),
+                         dim3(kBlock), 0, stream, (const Ent*)m.ent, (const int32_t*)p.chunk_row,
                          (const int64_t*)p.chunk_beg, (const int64_t*)p.chunk_end,
-                         (const int32_t*)p.chunk_part, src, y, ldy, parts, ldp, F, relu);
+                         (const int32_t*)p.chunk_part, src, y, ldy, parts, ldp, F);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) {
         tfree(parts, stream);
@@ -566,10 +568,10 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
     }
     if (p.n_giant > 0) {
       ProfScope ps("agg_reduce_parts", stream);
-      hipLaunchKernelGGL((k_reduce_parts<VEC, G>), dim3(blocks_for_waves(p.n_giant), tiles),
+      hipLaunchKernelGGL((k_reduce_parts<VEC, G, RELU>), dim3(blocks_for_waves(p.n_giant), tiles),
                          dim3(kBlock), 0, stream, (const int32_t*)p.giant_row,
                          (const int32_t*)p.giant_part_off, p.n_giant, (const float*)parts, ldp, y,
-                         ldy, F, relu);
+                         ldy, F);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) {
         tfree(parts, stream);
@@ -591,16 +593,16 @@ int lanes_for(int F, bool vec4) {
   return g;
 }
 
-template <template <int> class SrcT, class Make>
+template <template <int> class SrcT, bool RELU = false, class Make>
 gcn_status dispatch(const Mat& m, bool vec4, int F, float* y, int64_t ldy, hipStream_t stream,
-                    Make make, bool relu = false) {
-  if (!vec4) return launch_all<1, 64>(m, make(SrcT<1>{}), y, ldy, F, relu, stream);
+                    Make make) {
+  if (!vec4) return launch_all<1, 64, RELU>(m, make(SrcT<1>{}), y, ldy, F, stream);
   switch (lanes_for(F, true)) {
-    case 4: return launch_all<4, 4>(m, make(SrcT<4>{}), y, ldy, F, relu, stream);
-    case 8: return launch_all<4, 8>(m, make(SrcT<4>{}), y, ldy, F, relu, stream);
-    case 16: return launch_all<4, 16>(m, make(SrcT<4>{}), y, ldy, F, relu, stream);
-    case 32: return launch_all<4, 32>(m, make(SrcT<4>{}), y, ldy, F, relu, stream);
-    default: return launch_all<4, 64>(m, make(SrcT<4>{}), y, ldy, F, relu, stream);
+    case 4: return launch_all<4, 4, RELU>(m, make(SrcT<4>{}), y, ldy, F, stream);
+    case 8: return launch_all<4, 8, RELU>(m, make(SrcT<4>{}), y, ldy, F, stream);
+    case 16: return launch_all<4, 16, RELU>(m, make(SrcT<4>{}), y, ldy, F, stream);
+    case 32: return launch_all<4, 32, RELU>(m, make(SrcT<4>{}), y, ldy, F, stream);
+    default: return launch_all<4, 64, RELU>(m, make(SrcT<4>{}), y, ldy, F, stream);
   }
 }
 
@@ -657,15 +659,14 @@ gcn_status aggregate_f32(const Mat& m, const float* X, int64_t ldx, float* Y, in
                          int64_t F, bool relu, hipStream_t stream) {
   const int Fi = (int)F;
   const bool vec4 = aligned(Y, 16) && ldy % 4 == 0 && aligned(X, 16) && ldx % 4 == 0;
-  return dispatch<SrcF32>(
-      m, vec4, Fi, Y, ldy, stream,
-      [&](auto t) {
-        t.x = X;
-        t.ld = ldx;
-        t.F = Fi;
-        return t;
-      },
-      relu);
+  auto make = [&](auto t) {
+    t.x = X;
+    t.ld = ldx;
+    t.F = Fi;
+    return t;
+  };
+  return relu ? dispatch<SrcF32, true>(m, vec4, Fi, Y, ldy, stream, make)
+              : dispatch<SrcF32, false>(m, vec4, Fi, Y, ldy, stream, make);
 }
 
 }  // namespace gcn
@@ -724,7 +725,7 @@ extern "C" gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_loc
   const bool vec4 = aligned(Y, 16) && ldy % 4 == 0 && (n_local_cols == 0 ||
                     (aligned(X_local, 16) && ldx % 4 == 0)) &&
                     (n_local_cols == n_in || two_bit || (aligned(Q_halo, 4) && ldq % 4 == 0));
-  return dispatch<SrcQ8>(m, vec4, Fi, Y, ldy, (hipStream_t)stream, [&](auto t) {
+  auto make = [&](auto t) {
     t.x = X_local;
     t.ldx = ldx;
     t.n_local = n_local_cols;
@@ -734,8 +735,9 @@ extern "C" gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_loc
     t.scale = halo_scale;
     t.ldp = ldp;
     t.paired = paired;
-    t.two_bit = two_bit;
     t.F = Fi;
     return t;
-  });
+  };
+  if (two_bit) return dispatch<SrcQ2>(m, vec4, Fi, Y, ldy, (hipStream_t)stream, make);
+  return dispatch<SrcQ8>(m, vec4, Fi, Y, ldy, (hipStream_t)stream, make);
 }

@@ -133,6 +133,204 @@ __global__ __launch_bounds__(kBlock) void k_ln_quantize(int64_t n, int F, const 
   }
 }
 
+// Register-resident variant for rows of at most 4 * G * NV features in
+// 16-byte aligned storage (ldx % 4 == 0): a slot of G lanes holds a whole row
+// (NV float4 per lane), so the row is read from memory once; a wavefront
+// holds 64 / G rows per group and R groups are loaded before any arithmetic.
+// Same values as k_ln_quantize: statistics in double (only their summation
+// order differs), values rounded once to fp32, codes from IEEE fp32
+// division.
+template <int G>
+__device__ inline double slot_sum(double v) {
+#pragma unroll
+  for (int off = 1; off < G; off <<= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+template <int G>
+__device__ inline void slot_minmax(float& mn, float& mx) {
+#pragma unroll
+  for (int off = 1; off < G; off <<= 1) {
+    mn = fminf(mn, __shfl_xor(mn, off, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+  }
+}
+
+// clamp(rint((t - Z) / S), 0, levels) with IEEE fp32 division
+__device__ inline uint32_t code_of(float a, float s, float levels) {
+  return (uint32_t)fminf(levels, fmaxf(0.0f, __builtin_rintf(a / s)));
+}
+
+struct QuantArgs {
+  int64_t n;
+  int F;
+  const float* x;
+  int64_t ldx;
+  const float* gamma;
+  const float* beta;
+  double eps;
+  int ln, bits;
+  float* y;
+  int64_t ldy;
+  uint8_t* q;
+  int64_t ldq;
+  float* zmin;
+  float* scale;
+  int64_t ldp;
+  bool q_dword, y_vec;  // Q rows 4-byte aligned; Y rows 16-byte aligned
+};
+
+template <int G, int NV, int R, bool AFFINE>
+__global__ __launch_bounds__(kBlock) void k_ln_quantize_v(QuantArgs a) {
+  constexpr int E = 64 / G;
+  const int lane = threadIdx.x & 63;
+  const int sl = lane % G;
+  const int64_t base = ((int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6)) * (E * R) + lane / G;
+  float v[R][NV][4];
+  // every load of every group first
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int64_t i = base + (int64_t)r * E;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int f = 4 * (sl + j * G);
+      if (i < a.n && f + 4 <= a.F) {
+        const float4 t = *reinterpret_cast<const float4*>(a.x + i * a.ldx + f);
+        v[r][j][0] = t.x;
+        v[r][j][1] = t.y;
+        v[r][j][2] = t.z;
+        v[r][j][3] = t.w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          v[r][j][e] = (i < a.n && f + e < a.F) ? a.x[i * a.ldx + f + e] : 0.0f;
+      }
+    }
+  }
+  const float levels = (float)((1 << a.bits) - 1);
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int64_t i = base + (int64_t)r * E;
+    const bool live = i < a.n;
+    if (a.ln) {
+      double s = 0.0;
+#pragma unroll
+      for (int j = 0; j < NV; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s += (double)v[r][j][e];  // masked entries are 0
+      const double mean = slot_sum<G>(s) / (double)a.F;
+      double var = 0.0;
+#pragma unroll
+      for (int j = 0; j < NV; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const double d = (double)v[r][j][e] - mean;
+          if (4 * (sl + j * G) + e < a.F) var += d * d;
+        }
+      const double inv = 1.0 / sqrt(slot_sum<G>(var) / (double)a.F + a.eps);
+#pragma unroll
+      for (int j = 0; j < NV; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int f = 4 * (sl + j * G) + e;
+          if (f < a.F) {
+            const double d = ((double)v[r][j][e] - mean) * inv;
+            if (AFFINE) {
+              const double g = a.gamma ? (double)a.gamma[f] : 1.0;
+              const double b = a.beta ? (double)a.beta[f] : 0.0;
+              v[r][j][e] = (float)(d * g + b);
+            } else {
+              v[r][j][e] = (float)(d + 0.0);  // times 1 is exact; + 0 turns -0 into +0
+            }
+          }
+        }
+    }
+    float mn = __builtin_inff(), mx = -__builtin_inff();
+#pragma unroll
+    for (int j = 0; j < NV; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (4 * (sl + j * G) + e < a.F) {
+          mn = fminf(mn, v[r][j][e]);
+          mx = fmaxf(mx, v[r][j][e]);
+        }
+    slot_minmax<G>(mn, mx);
+    if (!live) continue;
+    const float s = (mx - mn) / levels;
+    if (sl == 0) {
+      a.zmin[i * a.ldp] = mn;
+      a.scale[i * a.ldp] = s;
+    }
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int f = 4 * (sl + j * G);
+      if (f >= a.F) continue;
+      uint32_t c[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        c[e] = (f + e < a.F && s != 0.0f) ? code_of(v[r][j][e] - mn, s, levels) : 0u;
+      uint8_t* qr = a.q + i * a.ldq;
+      const bool whole = f + 4 <= a.F;
+      if (a.bits == 2) {
+        qr[f / 4] = (uint8_t)(c[0] | (c[1] << 2) | (c[2] << 4) | (c[3] << 6));
+      } else if (whole && a.q_dword) {
+        *reinterpret_cast<uint32_t*>(qr + f) = c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24);
+      } else {
+        for (int e = 0; e < 4 && f + e < a.F; ++e) qr[f + e] = (uint8_t)c[e];
+      }
+      if (a.y) {
+        float* yr = a.y + i * a.ldy;
+        if (whole && a.y_vec)
+          *reinterpret_cast<float4*>(yr + f) = make_float4(v[r][j][0], v[r][j][1], v[r][j][2], v[r][j][3]);
+        else
+          for (int e = 0; e < 4 && f + e < a.F; ++e) yr[f + e] = v[r][j][e];
+      }
+    }
+  }
+}
+
+template <int G, int NV, int R>
+gcn_status launch_v(const QuantArgs& a, hipStream_t s) {
+  const int64_t rows_per_block = (int64_t)(kBlock / 64) * (64 / G) * R;
+  const dim3 grid((unsigned)ceil_div(a.n, rows_per_block));
+  if (a.ln && (a.gamma || a.beta))
+    hipLaunchKernelGGL((k_ln_quantize_v<G, NV, R, true>), grid, dim3(kBlock), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_ln_quantize_v<G, NV, R, false>), grid, dim3(kBlock), 0, s, a);
+  GCN_HIP(hipGetLastError());
+  return GCN_OK;
+}
+
+// The register-resident kernel when the layout allows it (returns false
+// otherwise, and the row-per-wavefront kernel runs). Up to 16 features per
+// lane and 8 lanes or more per row.
+bool try_vector(const QuantArgs& a, hipStream_t s, gcn_status* st) {
+  if (a.ldx % 4 != 0 || reinterpret_cast<uintptr_t>(a.x) % 16 != 0 || a.F > 1024) return false;
+  if (a.F <= 32)
+    *st = launch_v<8, 1, 2>(a, s);
+  else if (a.F <= 64)
+    *st = launch_v<8, 2, 2>(a, s);
+  else if (a.F <= 128)
+    *st = launch_v<8, 4, 2>(a, s);
+  else if (a.F <= 256)
+    *st = launch_v<16, 4, 1>(a, s);
+  else if (a.F <= 512)
+    *st = launch_v<32, 4, 1>(a, s);
+  else
+    *st = launch_v<64, 4, 1>(a, s);
+  return true;
+}
+
+QuantArgs make_args(int64_t n, int64_t F, const float* X, int64_t ldx, const float* gamma,
+                    const float* beta, double eps, int ln, int bits, float* Y, int64_t ldy,
+                    uint8_t* Q, int64_t ldq, float* zmin, float* scale, int64_t ldp) {
+  QuantArgs a{n, (int)F, X, ldx, gamma, beta, eps, ln, bits, Y, ldy, Q, ldq, zmin, scale, ldp,
+              false, false};
+  a.q_dword = reinterpret_cast<uintptr_t>(Q) % 4 == 0 && ldq % 4 == 0;
+  a.y_vec = Y && reinterpret_cast<uintptr_t>(Y) % 16 == 0 && ldy % 4 == 0;
+  return a;
+}
+
 }  // namespace
 }  // namespace gcn
 
@@ -158,6 +356,11 @@ extern "C" gcn_status gcn_layernorm_quantize(int64_t n, int64_t F, const float* 
   }
   hipStream_t s = (hipStream_t)stream;
   ProfScope ps("layernorm_quantize", s);
+  gcn_status st = GCN_OK;
+  if (try_vector(make_args(n, F, X, ldx, gamma, beta, eps, (int)(flags & GCN_LAYERNORM), bits, Y,
+                           ldy, Q, ldq, zmin, scale, ldp),
+                 s, &st))
+    return st;
   hipLaunchKernelGGL(k_ln_quantize, dim3((unsigned)ceil_div(n, kBlock / 64)), dim3(kBlock), 0, s, n,
                      (int)F, X, ldx, gamma, beta, eps, (int)(flags & GCN_LAYERNORM), bits, Y, ldy,
                      Q, ldq, zmin, scale, ldp);
@@ -180,6 +383,11 @@ extern "C" gcn_status gcn_quantize_rows_u8(int64_t n, int64_t F, const float* X,
   }
   hipStream_t s = (hipStream_t)stream;
   ProfScope ps("quantize_rows_u8", s);
+  gcn_status st = GCN_OK;
+  if (try_vector(make_args(n, F, X, ldx, nullptr, nullptr, 0.0, 0, 8, nullptr, 0, Q, ldq, zmin,
+                           scale, ldp),
+                 s, &st))
+    return st;
   const int64_t blocks = ceil_div(n, kBlock / 64);
   hipLaunchKernelGGL(k_quantize_rows, dim3((unsigned)blocks), dim3(kBlock), 0, s, n, (int)F, X, ldx,
                      Q, ldq, zmin, scale, ldp);

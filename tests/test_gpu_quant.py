@@ -101,3 +101,36 @@ def test_int2_permutation_dequant_bit_exact(G, F):
                                         dev(Z), dev(S), bits=2))
     D = oracle.dequant_rows_bits(Q, Z, S, F, 2)
     assert np.array_equal(Y.view(np.uint32), D[perm].view(np.uint32))
+
+
+@pytest.mark.parametrize("bits", [8, 2])
+@pytest.mark.parametrize("F,ld", [(64, 64), (256, 256), (512, 512), (1000, 1000), (47, 48),
+                                  (1025, 1028), (6, 8)])
+def test_quantize_register_kernel_shapes(G, bits, F, ld):
+    # every row-width class of the register-resident kernel, ragged tails on a
+    # padded leading dimension, and the row-per-wavefront kernel beyond 1024
+    import torch
+    note("quantize shapes bits=%d F=%d ld=%d" % (bits, F, ld))
+    n = 1531  # not a multiple of any rows-per-block figure
+    Xp = synth.normal(320 + F, n, ld)
+    X = Xp[:, :F]
+    Q, Z, S = oracle.quantize_rows_bits(X, bits)
+    q, z, s = G.gcn_layernorm_quantize(dev(Xp)[:, :F], bits=bits, layernorm=False)
+    assert np.array_equal(host(q), Q)
+    assert np.array_equal(host(z).view(np.uint32), Z.view(np.uint32))
+    assert np.array_equal(host(s).view(np.uint32), S.view(np.uint32))
+    Yr = oracle.layernorm_rows(X)
+    Qr, Zr, Sr = oracle.quantize_rows_bits(Yr, bits)
+    q, z, s, y = G.gcn_layernorm_quantize(dev(Xp)[:, :F], bits=bits, with_y=True)
+    y, q, z, s = host(y), host(q), host(z), host(s)
+    ulp = np.abs(y.view(np.int32).astype(np.int64) - Yr.view(np.int32).astype(np.int64))
+    assert ulp.max() <= 1
+    same = np.all(ulp == 0, axis=1)
+    assert same.mean() >= 0.99
+    assert np.array_equal(q[same], Qr[same])
+    assert np.array_equal(s[same].view(np.uint32), Sr[same].view(np.uint32))
+    if bits == 8:  # the plain u8 entry point shares the kernels
+        qu, zu, su = G.gcn_quantize_rows_u8(dev(Xp)[:, :F])
+        assert np.array_equal(host(qu), Q)
+        assert np.array_equal(host(su).view(np.uint32), S.view(np.uint32))
+    torch.cuda.synchronize()
