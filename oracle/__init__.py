@@ -312,10 +312,14 @@ class Graph:
     """Oracle matrices of one workload: CSR (rows = dst) and CSC, both with
     normalized values unless normalized=False (then every value is 1)."""
 
-    def __init__(self, n_rows, n_cols, src, dst, flags, deg=None, normalized=True):
+    def __init__(self, n_rows, n_cols, src, dst, flags, deg=None, normalized=True, mean=False):
         self.n_rows, self.n_cols = n_rows, n_cols
         self.csr_ptr, self.csr_idx = structure(n_rows, n_cols, src, dst, flags, False)
         self.csc_ptr, self.csc_idx = structure(n_rows, n_cols, src, dst, flags, True)
+        if mean:
+            self.deg = None
+            self.csr_val, self.csc_val = mean_values(self.csr_ptr, self.csr_idx, self.csc_idx)
+            return
         if deg is None:
             if n_rows != n_cols:
                 raise ValueError("a rectangular graph needs a supplied degree array")
@@ -339,6 +343,19 @@ class Graph:
 
     def bwd(self, G):
         return spmm(self.csc_ptr, self.csc_idx, self.csc_val, G)
+
+
+def mean_values(csr_ptr, csr_idx, csc_idx):
+    """Values of the mean operator D^-1 A (GraphSAGE's mean AGGREGATE, Section
+    2.1): entry (r, c) of A is 1 / (number of stored entries of row r), computed
+    in double and rounded once to fp32; an empty row has no entries. Returns
+    the values for A's CSR and for its transpose (whose entry (c, r) carries
+    the value of row r of A)."""
+    lens = np.diff(np.asarray(csr_ptr, np.int64)).astype(np.float64)
+    rows = np.repeat(np.arange(len(lens)), np.diff(csr_ptr))
+    csr_val = (1.0 / lens[rows]).astype(np.float32)
+    csc_val = (1.0 / lens[np.asarray(csc_idx, np.int64)]).astype(np.float32)
+    return csr_val, csc_val
 
 
 def sampled(n_rows, n_cols, src, dst, flags, sel, transpose=False, deg=None):
@@ -414,3 +431,87 @@ def gcn_step(graph: Graph, X, W1, W2, labels):
     dW1 = X.T @ dZ1
     return dict(loss=loss, dW1=dW1, dW2=dW2, Z1=Z1, A1=A1, H1=H1, Z2=Z2, logits=logits,
                 dlogits=dlogits, dZ2=dZ2, dH1=dH1, dZ1=dZ1)
+
+
+# ---------------------------------------------------------------------------
+# 3-layer GraphSAGE training step with LayerNorm before each layer (the model
+# of the evaluation, Table 2) and masked label propagation (Section 6.1 step 1,
+# Lemma 2), all in float64.
+# ---------------------------------------------------------------------------
+
+def layernorm64(H, eps):
+    """Row LayerNorm without affine parameters: (y, 1/sqrt(var + eps)) with the
+    biased variance, in float64."""
+    mu = H.mean(axis=1, keepdims=True)
+    var = ((H - mu) ** 2).mean(axis=1, keepdims=True)
+    rstd = 1.0 / np.sqrt(var + eps)
+    return (H - mu) * rstd, rstd[:, 0]
+
+
+def layernorm64_bwd(Y, rstd, dY):
+    """Gradient of the row LayerNorm: rstd * (dY - mean(dY) - Y * mean(dY * Y))."""
+    return rstd[:, None] * (dY - dY.mean(axis=1, keepdims=True)
+                            - Y * (dY * Y).mean(axis=1, keepdims=True))
+
+
+def sage_step(graph: Graph, X, params, labels, lp_mask=None, E=None, eps=1e-5):
+    """Loss and gradients of one step of the 3-layer GraphSAGE-mean model.
+
+    graph: mean-normalized (Graph(..., mean=True)); params: the list
+    [W_self1, W_neigh1, b1, W_self2, W_neigh2, b2, W_self3, W_neigh3, b3]
+    (W [f_in x f_out], b [f_out]). Layer l: Y = LayerNorm(H), Z = D^-1 A Y,
+    O = Y W_self + Z W_neigh + b, H = relu(O) after layers 1 and 2; the last O
+    are the logits. Masked label propagation: rows with lp_mask = 1 get the
+    embedding E[label] added to their input features and are left out of the
+    loss; the loss is the mean softmax cross-entropy over the other rows (all
+    rows without lp_mask). Returns dict(loss, grads (same order as params),
+    dE or None, logits)."""
+    H = np.asarray(X, np.float64).copy()
+    y = np.asarray(labels)
+    n = H.shape[0]
+    P = [np.asarray(p, np.float64) for p in params]
+    if lp_mask is not None:
+        m = np.asarray(lp_mask).astype(bool)
+        H[m] += np.asarray(E, np.float64)[y[m]]
+        loss_rows = ~m
+    else:
+        m = None
+        loss_rows = np.ones(n, bool)
+    fwd = lambda T: _agg64(graph.csr_ptr, graph.csr_idx, graph.csr_val, T)
+    bwd = lambda T: _agg64(graph.csc_ptr, graph.csc_idx, graph.csc_val, T)
+    saved = []
+    for l in range(3):
+        Ws, Wn, b = P[3 * l], P[3 * l + 1], P[3 * l + 2]
+        Yl, rstd = layernorm64(H, eps)
+        Zl = fwd(Yl)
+        O = Yl @ Ws + Zl @ Wn + b
+        saved.append((Yl, rstd, Zl, O))
+        H = np.maximum(O, 0.0) if l < 2 else O
+    logits = H
+    mx = logits.max(axis=1, keepdims=True)
+    lse = mx[:, 0] + np.log(np.exp(logits - mx).sum(axis=1))
+    n_loss = int(loss_rows.sum())
+    idx = np.flatnonzero(loss_rows)
+    loss = float(np.sum(lse[idx] - logits[idx, y[idx]]) / n_loss)
+    dO = np.exp(logits - lse[:, None])
+    dO[idx, y[idx]] -= 1.0
+    dO[~loss_rows] = 0.0
+    dO /= n_loss
+    grads = [None] * 9
+    dE = None
+    for l in (2, 1, 0):
+        Yl, rstd, Zl, O = saved[l]
+        grads[3 * l] = Yl.T @ dO
+        grads[3 * l + 1] = Zl.T @ dO
+        grads[3 * l + 2] = dO.sum(axis=0)
+        if l == 0 and m is None:
+            break
+        dY = dO @ P[3 * l].T + bwd(dO @ P[3 * l + 1].T)
+        dH = layernorm64_bwd(Yl, rstd, dY)
+        if l > 0:
+            dO = dH * (saved[l - 1][3] > 0)
+        else:
+            dE = np.zeros_like(np.asarray(E, np.float64))
+            np.add.at(dE, y[m], dH[m])
+    return dict(loss=loss, grads=grads, dE=dE, logits=logits)
+

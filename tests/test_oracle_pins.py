@@ -528,3 +528,149 @@ def test_split_covers_every_edge_on_random_remote_graph():
     assert all(d in cover_d for d, p in zip(dst, is_post) if not p)
     assert vol == len(cover_s) + len(cover_d)
     assert vol <= min(len(np.unique(src)), len(np.unique(dst)))
+
+
+# ---------------------------------------------------------------------------
+# GraphSAGE-mean (Section 2.1 with AGGREGATE = mean; the evaluation model of
+# Table 2) and masked label propagation (Section 6.1 step 1, Lemma 2).
+# ---------------------------------------------------------------------------
+
+def _dense_binary(n, src, dst, flags):
+    A = np.zeros((n, n))
+    for s, d in zip(src, dst):
+        if s == d and flags & LOOPS:
+            continue
+        A[d, s] = 1
+        if flags & SYM:
+            A[s, d] = 1
+    if flags & LOOPS:
+        A[np.arange(n), np.arange(n)] = 1
+    return A
+
+
+@pytest.mark.parametrize("flags", [SYM, 0, SYM | LOOPS])
+def test_mean_values_match_dense(flags):
+    n = 40
+    src, dst = synth.er_edges(50 + flags, n, 90)
+    g = oracle.Graph(n, n, src, dst, flags, mean=True)
+    A = _dense_binary(n, src, dst, flags)
+    lens = A.sum(axis=1)
+    M = np.divide(A, lens[:, None], out=np.zeros_like(A), where=lens[:, None] > 0)
+    D = np.zeros((n, n))
+    rows = np.repeat(np.arange(n), np.diff(g.csr_ptr))
+    D[rows, g.csr_idx] = g.csr_val
+    assert np.array_equal(D != 0, A != 0)
+    assert np.array_equal(D, M.astype(np.float32).astype(np.float64))
+    T = np.zeros((n, n))
+    cols = np.repeat(np.arange(n), np.diff(g.csc_ptr))
+    T[cols, g.csc_idx] = g.csc_val
+    assert np.array_equal(T, D.T)
+    # D^-1 A 1 = 1 on rows with entries
+    ones, _ = g.fwd(np.ones((n, 1), np.float32))
+    assert np.allclose(ones[lens > 0, 0], 1.0, atol=1e-6) and np.all(ones[lens == 0] == 0)
+
+
+def test_mean_values_star_closed_form():
+    k = 7
+    src = np.arange(1, k + 1, dtype=np.int32)
+    dst = np.zeros(k, np.int32)
+    g = oracle.Graph(k + 1, k + 1, src, dst, SYM, mean=True)
+    assert np.all(g.csr_val[g.csr_ptr[0]:g.csr_ptr[1]] == np.float32(1.0 / k))
+    assert np.all(g.csr_val[g.csr_ptr[1]:] == 1.0)
+
+
+def _sage_case(seed, n=50, f_in=6, hidden=5, C=4, lp=False):
+    src, dst = synth.er_edges(seed, n, 3 * n)
+    g = oracle.Graph(n, n, src, dst, SYM, mean=True)
+    rng = np.random.default_rng(seed)
+    X = rng.normal(size=(n, f_in))
+    dims = [(f_in, hidden), (hidden, hidden), (hidden, C)]
+    params = []
+    for a, b in dims:
+        params += [rng.normal(size=(a, b)) * 0.5, rng.normal(size=(a, b)) * 0.5, rng.normal(size=b) * 0.1]
+    y = rng.integers(0, C, n)
+    mask = (rng.random(n) < 0.4).astype(np.uint8) if lp else None
+    E = rng.normal(size=(C, f_in)) if lp else None
+    return g, X, params, y, mask, E, src, dst
+
+
+@pytest.mark.parametrize("lp", [False, True])
+def test_sage_step_gradients_finite_difference(lp):
+    g, X, params, y, mask, E, _, _ = _sage_case(60, lp=lp)
+    out = oracle.sage_step(g, X, params, y, mask, E)
+    rng = np.random.default_rng(61)
+    h = 1e-6
+    targets = [(k, params) for k in range(9)] + ([("E", None)] if lp else [])
+    for k, _ in targets:
+        P = E if k == "E" else params[k]
+        G = out["dE"] if k == "E" else out["grads"][k]
+        assert G.shape == P.shape
+        for _ in range(4):
+            i = tuple(rng.integers(0, s) for s in P.shape)
+            old = P[i]
+            P[i] = old + h
+            lp_ = oracle.sage_step(g, X, params, y, mask, E)["loss"]
+            P[i] = old - h
+            lm = oracle.sage_step(g, X, params, y, mask, E)["loss"]
+            P[i] = old
+            fd = (lp_ - lm) / (2 * h)
+            assert abs(fd - G[i]) <= 1e-6 * max(1.0, abs(fd)) + 1e-8, (k, i, fd, G[i])
+
+
+def test_sage_forward_brute_force_loops():
+    g, X, params, y, _, _, src, dst = _sage_case(62, n=12, f_in=3, hidden=4, C=3)
+    n = X.shape[0]
+    # neighbours: the deduplicated, symmetrized edge list; a drawn self pair
+    # counts as an edge (no self-loop is added, the root term is separate)
+    nbr = [set() for _ in range(n)]
+    for s, d in zip(src, dst):
+        nbr[d].add(int(s))
+        nbr[s].add(int(d))
+    H = [list(map(float, row)) for row in X]
+    for l in range(3):
+        Ws, Wn, b = params[3 * l], params[3 * l + 1], params[3 * l + 2]
+        Y = []
+        for row in H:
+            mu = sum(row) / len(row)
+            var = sum((v - mu) ** 2 for v in row) / len(row)
+            Y.append([(v - mu) / math.sqrt(var + 1e-5) for v in row])
+        Z = []
+        for i in range(n):
+            nb = sorted(nbr[i])
+            Z.append([sum(Y[j][f] for j in nb) / len(nb) if nb else 0.0 for f in range(len(Y[0]))])
+        out = []
+        for i in range(n):
+            o = [b[c] + sum(Y[i][f] * Ws[f][c] + Z[i][f] * Wn[f][c] for f in range(len(Y[0])))
+                 for c in range(len(b))]
+            out.append([max(v, 0.0) for v in o] if l < 2 else o)
+        H = out
+    logits = oracle.sage_step(g, X, params, y)["logits"]
+    # the oracle aggregates with fp32-rounded 1/len values: within 2^-24 relative
+    assert np.allclose(logits, np.array(H), rtol=1e-6, atol=1e-6)
+
+
+def test_sage_label_propagation_reduces_to_plain_step():
+    g, X, params, y, _, _, _, _ = _sage_case(63)
+    base = oracle.sage_step(g, X, params, y)
+    zero = oracle.sage_step(g, X, params, y, np.zeros(len(y), np.uint8), np.ones((4, 6)))
+    assert zero["loss"] == base["loss"]
+    assert all(np.array_equal(a, b) for a, b in zip(zero["grads"], base["grads"]))
+    assert np.all(zero["dE"] == 0)
+    # an embedded row's input is X + E[label]: the same as adding it to X directly
+    mask = np.zeros(len(y), np.uint8)
+    mask[5] = 1
+    E = np.arange(24, dtype=np.float64).reshape(4, 6)
+    a = oracle.sage_step(g, X, params, y, mask, E)
+    X2 = X.copy()
+    X2[5] += E[y[5]]
+    keep = np.ones(len(y), np.uint8)
+    keep[5] = 0
+    b = oracle.sage_step(g, X2, params, y, np.where(keep == 1, 0, 1).astype(np.uint8),
+                         np.zeros((4, 6)))
+    assert abs(a["loss"] - b["loss"]) < 1e-12
+
+
+def test_sage_initial_loss_near_log_classes():
+    g, X, params, y, _, _, _, _ = _sage_case(64, n=200, C=10)
+    small = [p * 1e-3 for p in params]
+    assert abs(oracle.sage_step(g, X, small, y)["loss"] - math.log(10)) < 1e-3
