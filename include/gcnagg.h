@@ -120,6 +120,16 @@ gcn_status gcn_normalize(gcn_graph* g, const int32_t* deg, void* stream);
 gcn_status gcn_normalize_rc(gcn_graph* g, const int32_t* deg_rows, const int32_t* deg_cols,
                             void* stream);
 
+/* Overwrite the stored values with those of the mean operator D^-1 A
+ * (GraphSAGE's mean AGGREGATE, Section 2.1, the model of the evaluation):
+ * entry (r, c) becomes (float)(1 / (double)len(r)), len(r) = stored entries of
+ * row r of A (self-loops and drawn self pairs count when stored; a graph
+ * built without GCN_ADD_SELF_LOOPS gives the mean over neighbours). A^T
+ * receives the transposed values; for a symmetric graph it then keeps the
+ * shared structure but gets entries of its own (8 bytes per entry more).
+ * Asynchronous on `stream`. */
+gcn_status gcn_normalize_mean(gcn_graph* g, void* stream);
+
 /* Y[n_rows x F] = A_hat X. X is [n_cols x F] (ldx), fp32 or bf16 (dtype);
  * Y is fp32 (ldy). Accumulation is fp32; each output element is summed in
  * an order fixed by the graph alone, so repeated calls give identical bits. */
@@ -231,6 +241,65 @@ gcn_status gcn_layernorm_quantize(int64_t n, int64_t F, const float* X, int64_t 
                                   uint32_t flags, int bits, float* Y, int64_t ldy, uint8_t* Q,
                                   int64_t ldq, float* zmin, float* scale, int64_t ldp,
                                   void* stream);
+
+/* Row LayerNorm without affine parameters (applied before every layer,
+ * Section 6.1 step 2 and Table 2): Y = (X - mean) / sqrt(var + eps) per row
+ * over the F features, biased variance, statistics in double, each value
+ * rounded once to fp32. rstd (optional, fp32 [n]) receives 1 / sqrt(var + eps).
+ * Asynchronous. */
+gcn_status gcn_layernorm_fwd(int64_t n, int64_t F, const float* X, int64_t ldx, double eps,
+                             float* Y, int64_t ldy, float* rstd, void* stream);
+
+/* Gradient of gcn_layernorm_fwd: dX = rstd * (g - mean(g) - Y * mean(g * Y))
+ * per row, with g = dY + dY2 (dY2 optional, NULL for none) and Y, rstd from
+ * the forward pass; with mask (optional) dX is zeroed where mask <= 0 (the
+ * ReLU of the layer below: pass its output). mask may be dX itself (same ld).
+ * Row means in double. Asynchronous. */
+gcn_status gcn_layernorm_bwd(int64_t n, int64_t F, const float* Y, int64_t ldy, const float* rstd,
+                             const float* dY, int64_t lddy, const float* dY2, int64_t lddy2,
+                             const float* mask, int64_t ldm, float* dX, int64_t lddx,
+                             void* stream);
+
+/* Forward pass (inference) of the 3-layer GraphSAGE model of gcn_sage3_step,
+ * the same kernels in the same order, so its outputs are bit-identical to the
+ * step's activations. Arguments as for gcn_sage3_step (labels may be NULL
+ * without lp_mask); outputs, each optional (NULL) and fp32 device row-major:
+ * H1, H2 [n x hidden] the ReLU outputs of layers 1 and 2, logits
+ * [n x n_classes]. Asynchronous. */
+gcn_status gcn_sage3_forward(const gcn_graph* g, const float* X, int64_t ldx, int64_t f_in,
+                             int64_t hidden, int64_t n_classes, const float* const* params,
+                             const int32_t* labels, const uint8_t* lp_mask, const float* E,
+                             double eps, float* H1, int64_t ldh1, float* H2, int64_t ldh2,
+                             float* logits, int64_t ldl, void* stream);
+
+/* One training step (forward, loss, backward) of the 3-layer GraphSAGE model
+ * of the evaluation (Section 8, Table 2), with optional masked label
+ * propagation (Section 6.1 step 1, Lemma 2). Layer l (l = 1, 2, 3):
+ *   Y = LayerNorm(H) (as gcn_layernorm_fwd), Z = A Y with the graph's values
+ *   (after gcn_normalize_mean: the neighbour mean), O = Y W_self + Z W_neigh + b,
+ *   H = relu(O) for l = 1, 2; the logits are O of layer 3.
+ * Loss: mean softmax cross-entropy over the rows that count (all rows, or
+ * those with lp_mask = 0). Label propagation: rows with lp_mask = 1 get E[label]
+ * added to their input features and are left out of the loss. Dropout is not
+ * applied.
+ *  g        square graph, aggregated as stored (A for the forward, A^T for the
+ *           backward).
+ *  X        fp32 device [n x f_in] (ldx); labels int32 [n] in [0, n_classes).
+ *  params   host array of 9 device pointers, fp32 row-major:
+ *           W_self1, W_neigh1 [f_in x hidden], b1 [hidden],
+ *           W_self2, W_neigh2 [hidden x hidden], b2 [hidden],
+ *           W_self3, W_neigh3 [hidden x n_classes], b3 [n_classes].
+ *  grads    host array of 9 device pointers of the same shapes (outputs).
+ *  lp_mask  uint8 device [n] or NULL; E fp32 [n_classes x f_in] and dE (output,
+ *           same shape) are required with it.
+ *  eps      LayerNorm epsilon; loss: device double, the mean loss.
+ *  1 <= n_classes <= 64. Asynchronous; temporaries are stream-ordered
+ *  (about 4 n (2 f_in + 3 (2 hidden + 4) + 4 hidden) bytes). */
+gcn_status gcn_sage3_step(const gcn_graph* g, const float* X, int64_t ldx, int64_t f_in,
+                          int64_t hidden, int64_t n_classes, const float* const* params,
+                          const int32_t* labels, const uint8_t* lp_mask, const float* E,
+                          double eps, float* const* grads, float* dE, double* loss,
+                          void* stream);
 
 /* ---- hybrid pre/post-aggregation (Algorithm 1, Sections 5.2 and 5.3) ---- */
 

@@ -454,7 +454,8 @@ def layernorm64_bwd(Y, rstd, dY):
                             - Y * (dY * Y).mean(axis=1, keepdims=True))
 
 
-def sage_step(graph: Graph, X, params, labels, lp_mask=None, E=None, eps=1e-5):
+def sage_step(graph: Graph, X, params, labels, lp_mask=None, E=None, eps=1e-5, masks=None,
+              with_margins=True):
     """Loss and gradients of one step of the 3-layer GraphSAGE-mean model.
 
     graph: mean-normalized (Graph(..., mean=True)); params: the list
@@ -464,8 +465,12 @@ def sage_step(graph: Graph, X, params, labels, lp_mask=None, E=None, eps=1e-5):
     are the logits. Masked label propagation: rows with lp_mask = 1 get the
     embedding E[label] added to their input features and are left out of the
     loss; the loss is the mean softmax cross-entropy over the other rows (all
-    rows without lp_mask). Returns dict(loss, grads (same order as params),
-    dE or None, logits)."""
+    rows without lp_mask). masks (optional): the ReLU patterns of layers 1 and
+    2 to use in place of O > 0 (a unit whose pre-activation lies within
+    rounding of 0 may fall either way in another precision). Returns
+    dict(loss, grads (same order as params), dE or None, logits, margins: per
+    hidden layer |O| / (sum of the magnitudes of its terms), acts: the float64
+    patterns O > 0)."""
     H = np.asarray(X, np.float64).copy()
     y = np.asarray(labels)
     n = H.shape[0]
@@ -480,13 +485,23 @@ def sage_step(graph: Graph, X, params, labels, lp_mask=None, E=None, eps=1e-5):
     fwd = lambda T: _agg64(graph.csr_ptr, graph.csr_idx, graph.csr_val, T)
     bwd = lambda T: _agg64(graph.csc_ptr, graph.csc_idx, graph.csc_val, T)
     saved = []
+    margins, acts = [], []
     for l in range(3):
         Ws, Wn, b = P[3 * l], P[3 * l + 1], P[3 * l + 2]
         Yl, rstd = layernorm64(H, eps)
         Zl = fwd(Yl)
         O = Yl @ Ws + Zl @ Wn + b
-        saved.append((Yl, rstd, Zl, O))
-        H = np.maximum(O, 0.0) if l < 2 else O
+        if l < 2:
+            act = (O > 0) if masks is None else np.asarray(masks[l], bool)
+            if with_margins:
+                margins.append(np.abs(O) / (np.abs(Yl) @ np.abs(Ws) + np.abs(Zl) @ np.abs(Wn)
+                                            + np.abs(b)))
+            acts.append(O > 0)
+            H = O * act
+        else:
+            act = None
+            H = O
+        saved.append((Yl, rstd, Zl, act))
     logits = H
     mx = logits.max(axis=1, keepdims=True)
     lse = mx[:, 0] + np.log(np.exp(logits - mx).sum(axis=1))
@@ -500,7 +515,7 @@ def sage_step(graph: Graph, X, params, labels, lp_mask=None, E=None, eps=1e-5):
     grads = [None] * 9
     dE = None
     for l in (2, 1, 0):
-        Yl, rstd, Zl, O = saved[l]
+        Yl, rstd, Zl, _ = saved[l]
         grads[3 * l] = Yl.T @ dO
         grads[3 * l + 1] = Zl.T @ dO
         grads[3 * l + 2] = dO.sum(axis=0)
@@ -509,9 +524,9 @@ def sage_step(graph: Graph, X, params, labels, lp_mask=None, E=None, eps=1e-5):
         dY = dO @ P[3 * l].T + bwd(dO @ P[3 * l + 1].T)
         dH = layernorm64_bwd(Yl, rstd, dY)
         if l > 0:
-            dO = dH * (saved[l - 1][3] > 0)
+            dO = dH * saved[l - 1][3]
         else:
             dE = np.zeros_like(np.asarray(E, np.float64))
             np.add.at(dE, y[m], dH[m])
-    return dict(loss=loss, grads=grads, dE=dE, logits=logits)
+    return dict(loss=loss, grads=grads, dE=dE, logits=logits, margins=margins, acts=acts)
 

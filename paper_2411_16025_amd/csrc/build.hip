@@ -284,6 +284,30 @@ __global__ __launch_bounds__(kThreads) void k_normalize(const int64_t* __restric
   }
 }
 
+// val of entry k = fp32(1 / (stored entries of the row of A it belongs to)) in
+// IEEE double: for A's CSR that row is the entry's major row, for the CSC it is
+// the entry's minor index. a_ptr is A's row pointer.
+__global__ __launch_bounds__(kThreads) void k_normalize_mean(const int64_t* __restrict__ ptr,
+                                                             int64_t n_major,
+                                                             Ent* __restrict__ ent, int64_t nnz,
+                                                             const int64_t* __restrict__ a_ptr,
+                                                             bool by_minor) {
+  __shared__ int64_t r_lo, r_hi;
+  const int64_t k0 = (int64_t)blockIdx.x * kNormTile;
+  const int64_t k1 = std::min(nnz, k0 + kNormTile) - 1;
+  if (!by_minor) {
+    if (threadIdx.x == 0) r_lo = row_of(ptr, 0, n_major - 1, k0);
+    if (threadIdx.x == 1) r_hi = row_of(ptr, 0, n_major - 1, k1);
+    __syncthreads();
+  }
+  for (int j = 0; j < kNormPerThread; ++j) {
+    const int64_t k = k0 + (int64_t)j * kThreads + threadIdx.x;
+    if (k > k1) break;
+    const int64_t r = by_minor ? (int64_t)ent[k].col : row_of(ptr, r_lo, r_hi, k);
+    ent[k].val = (float)(1.0 / (double)(a_ptr[r + 1] - a_ptr[r]));
+  }
+}
+
 // ---- export ----------------------------------------------------------------------
 
 __global__ void k_split(const Ent* __restrict__ ent, int64_t nnz, int32_t* __restrict__ idx,
@@ -497,6 +521,7 @@ namespace {
 void destroy(gcn_graph* g) {
   if (!g) return;
   if (!g->csc_shared) free_mat(g->csc, true);
+  if (g->csc_shared && g->csc_own_ent) dfree(g->csc.ent);
   free_mat(g->csr, true);
   g->magic = kFreed;
   delete g;
@@ -626,6 +651,8 @@ extern "C" gcn_status gcn_build_csr(int64_t n_rows, int64_t n_cols, int64_t n_ed
   g->n_cols = n_cols;
   g->flags = flags;
   g->normalized = false;
+  g->norm_mode = 0;
+  g->csc_own_ent = false;
   g->csc_shared = false;
   gcn_status st = build_impl(n_rows, n_cols, n_edges, src, dst, flags, (hipStream_t)stream, g);
   if (st != GCN_OK) {
@@ -680,7 +707,7 @@ gcn_status check_degrees(const int32_t* deg, int64_t n, hipStream_t stream) {
 gcn_status normalize_with(gcn_graph* g, const int32_t* deg_rows, const int32_t* deg_cols,
                           hipStream_t stream) {
   for (int which = 0; which < 2; ++which) {
-    if (which == 1 && g->csc_shared) break;
+    if (which == 1 && g->csc_shared && !g->csc_own_ent) break;
     Mat& m = which ? g->csc : g->csr;
     if (m.nnz == 0) continue;
     ProfScope ps("normalize", stream);
@@ -691,6 +718,7 @@ gcn_status normalize_with(gcn_graph* g, const int32_t* deg_rows, const int32_t* 
     if (e != hipSuccess) return hip_fail(e, "k_normalize", __FILE__, __LINE__);
   }
   g->normalized = true;
+  g->norm_mode = 1;
   return GCN_OK;
 }
 
@@ -717,6 +745,39 @@ extern "C" gcn_status gcn_normalize(gcn_graph* g, const int32_t* deg, void* stre
                                   : normalize_with(g, own, own, stream);
   tfree(own, stream);
   return st;
+}
+
+extern "C" gcn_status gcn_normalize_mean(gcn_graph* g, void* stream_) {
+  clear_error();
+  GCN_CHECK(check_graph(g));
+  hipStream_t stream = (hipStream_t)stream_;
+  const int64_t nnz = g->csr.nnz;
+  if (g->csc_shared && !g->csc_own_ent) {
+    // the transpose keeps the shared structure but needs values of its own
+    Ent* e = nullptr;
+    GCN_CHECK(dalloc(&e, nnz, "transpose entries"));
+    hipError_t err = nnz > 0 ? hipMemcpyAsync(e, g->csr.ent, nnz * sizeof(Ent),
+                                              hipMemcpyDeviceToDevice, stream)
+                             : hipSuccess;
+    if (err != hipSuccess) {
+      dfree(e);
+      return hip_fail(err, "hipMemcpyAsync(transpose entries)", __FILE__, __LINE__);
+    }
+    g->csc.ent = e;
+    g->csc_own_ent = true;
+  }
+  for (int which = 0; which < 2; ++which) {
+    Mat& m = which ? g->csc : g->csr;
+    if (m.nnz == 0) continue;
+    ProfScope ps("normalize", stream);
+    hipLaunchKernelGGL(k_normalize_mean, dim3(grid_for(m.nnz, (int)kNormTile)), dim3(kThreads), 0,
+                       stream, (const int64_t*)m.ptr, m.n_major, m.ent, m.nnz,
+                       (const int64_t*)g->csr.ptr, which == 1);
+    GCN_HIP(hipGetLastError());
+  }
+  g->normalized = true;
+  g->norm_mode = 2;
+  return GCN_OK;
 }
 
 extern "C" gcn_status gcn_normalize_rc(gcn_graph* g, const int32_t* deg_rows,

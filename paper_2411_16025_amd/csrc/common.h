@@ -68,8 +68,10 @@ struct gcn_graph {
   int device;
   int64_t n_rows, n_cols;
   uint32_t flags;
-  bool csc_shared;  // symmetric graph: A^T is A, csc aliases csr
+  bool csc_shared;   // symmetric structure: csc aliases csr's ptr and plan
+  bool csc_own_ent;  // ... but csc holds its own entries (mean values are not symmetric)
   bool normalized;
+  int norm_mode;     // 0 none (values 1), 1 symmetric D^-1/2 (A+I) D^-1/2, 2 mean D^-1 A
   gcn::Mat csr;     // rows = destination nodes
   gcn::Mat csc;     // rows = source nodes (A^T)
 };
@@ -143,7 +145,18 @@ gcn_status relu_fwd(int64_t n, int64_t F, float* H, int64_t ld, hipStream_t stre
 gcn_status relu_bwd(int64_t n, int64_t F, const float* H, int64_t ldh, float* dH, int64_t ld,
                     hipStream_t stream);
 gcn_status softmax_xent(int64_t n, int C, const float* z, int64_t ldz, const int32_t* y,
-                        float* dz, int64_t ldd, double* loss, hipStream_t stream);
+                        float* dz, int64_t ldd, double* loss, hipStream_t stream,
+                        const uint8_t* skip = nullptr);
+// Row LayerNorm without affine parameters (statistics in double); rstd
+// (optional) receives 1 / sqrt(var + eps) per row.
+gcn_status layernorm_fwd(int64_t n, int64_t F, const float* X, int64_t ldx, double eps, float* Y,
+                         int64_t ldy, float* rstd, hipStream_t stream);
+// dX = rstd * (g - mean(g) - Y * mean(g * Y)), g = G1 (+ G2), times (mask > 0)
+// when mask is given (mask may be dX itself).
+gcn_status layernorm_bwd(int64_t n, int64_t F, const float* Y, int64_t ldy, const float* rstd,
+                         const float* G1, int64_t ld1, const float* G2, int64_t ld2,
+                         const float* mask, int64_t ldm, float* dX, int64_t lddx,
+                         hipStream_t stream);
 
 // ---- plan building (build.hip) ----------------------------------------------
 gcn_status build_plan(Mat& m, hipStream_t stream);

@@ -318,22 +318,43 @@ __global__ __launch_bounds__(kThreads) void k_relu_bwd(int64_t n, int64_t F,
 
 constexpr int kSoftmaxRowsPerWave = 16;
 
+__global__ void k_zero_count(unsigned long long* __restrict__ cnt) {
+  if (threadIdx.x == 0) *cnt = 0ull;
+}
+
+// Rows that count in the loss: those with skip[i] == 0 (all rows without a
+// skip array). cnt receives their number (integer atomics: exact).
+__global__ __launch_bounds__(kThreads) void k_count_kept(int64_t n, const uint8_t* __restrict__ skip,
+                                                         unsigned long long* __restrict__ cnt) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const bool keep = i < n && skip[i] == 0;
+  const unsigned long long b = __ballot(keep);
+  if ((threadIdx.x & 63) == 0 && b) atomicAdd(cnt, (unsigned long long)__popcll(b));
+}
+
 // One wavefront per row at a time (C <= 64 classes, lane = class), 16 rows
 // per wavefront: log-softmax with the row maximum subtracted, row losses
 // lse - z[y] added in row order in double, wavefront sums added in
-// wavefront order, and dz = (softmax - onehot(y)) / n.
+// wavefront order, and dz = (softmax - onehot(y)) / m, where m is the number
+// of rows in the loss (n, or *n_kept when skip is given; skipped rows get
+// dz = 0 and add nothing).
 __global__ __launch_bounds__(kThreads) void k_softmax_xent(int64_t n, int C,
                                                            const float* __restrict__ z, int64_t ldz,
                                                            const int32_t* __restrict__ y,
                                                            float* __restrict__ dz, int64_t ldd,
-                                                           double* __restrict__ block_loss) {
+                                                           double* __restrict__ block_loss,
+                                                           const uint8_t* __restrict__ skip,
+                                                           const unsigned long long* __restrict__ n_kept) {
   __shared__ double wl[kThreads / 64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   double wave_loss = 0.0;
   for (int rr = 0; rr < kSoftmaxRowsPerWave; ++rr) {
   const int64_t i = ((int64_t)blockIdx.x * (kThreads / 64) + w) * kSoftmaxRowsPerWave + rr;
   double row_loss = 0.0;
-  if (i < n) {
+  if (i < n && skip && skip[i]) {
+    if (lane < C) dz[i * ldd + lane] = 0.f;
+  } else if (i < n) {
+    const float m_rows = skip ? (float)*n_kept : (float)n;
     const float v = lane < C ? z[i * ldz + lane] : -INFINITY;
     float m = v;
 #pragma unroll
@@ -346,7 +367,7 @@ __global__ __launch_bounds__(kThreads) void k_softmax_xent(int64_t n, int C,
     const float zy = __shfl(v, yi, 64);
     const float lse = m + logf(s);
     row_loss = (double)(lse - zy);
-    if (lane < C) dz[i * ldd + lane] = (ex / s - (lane == yi ? 1.f : 0.f)) / (float)n;
+    if (lane < C) dz[i * ldd + lane] = (ex / s - (lane == yi ? 1.f : 0.f)) / m_rows;
   }
   wave_loss += row_loss;
   }
@@ -364,7 +385,8 @@ __global__ __launch_bounds__(kThreads) void k_softmax_xent(int64_t n, int C,
 // the 256 sums.
 __global__ __launch_bounds__(kThreads) void k_loss_total(int64_t nb, int64_t n,
                                                          const double* __restrict__ block_loss,
-                                                         double* __restrict__ loss) {
+                                                         double* __restrict__ loss,
+                                                         const unsigned long long* __restrict__ n_kept) {
   __shared__ double part[kThreads];
   double s = 0.0;
   for (int64_t b = threadIdx.x; b < nb; b += kThreads) s += block_loss[b];
@@ -374,7 +396,10 @@ __global__ __launch_bounds__(kThreads) void k_loss_total(int64_t nb, int64_t n,
     if ((int)threadIdx.x < off) part[threadIdx.x] += part[threadIdx.x + off];
     __syncthreads();
   }
-  if (threadIdx.x == 0) *loss = part[0] / (double)n;
+  if (threadIdx.x == 0) {
+    const double m = n_kept ? (double)*n_kept : (double)n;
+    *loss = m > 0 ? part[0] / m : 0.0;
+  }
 }
 
 }  // namespace
@@ -494,22 +519,41 @@ gcn_status relu_bwd(int64_t n, int64_t F, const float* H, int64_t ldh, float* dH
 }
 
 gcn_status softmax_xent(int64_t n, int C, const float* z, int64_t ldz, const int32_t* y,
-                        float* dz, int64_t ldd, double* loss, hipStream_t stream) {
+                        float* dz, int64_t ldd, double* loss, hipStream_t stream,
+                        const uint8_t* skip) {
   const int64_t nb = std::max<int64_t>(1, ceil_div(n, (kThreads / 64) * kSoftmaxRowsPerWave));
   double* bl = nullptr;
+  unsigned long long* cnt = nullptr;
   GCN_CHECK(talloc(&bl, nb, stream, "block losses"));
-  {
+  hipError_t e = hipSuccess;
+  if (skip) {
+    gcn_status st = talloc(&cnt, 1, stream, "loss row count");
+    if (st != GCN_OK) {
+      tfree(bl, stream);
+      return st;
+    }
+    // a kernel, not a memset node, clears the counter (safe under stream capture)
+    hipLaunchKernelGGL(k_zero_count, dim3(1), dim3(64), 0, stream, cnt);
+    e = hipGetLastError();
+    if (e == hipSuccess) {
+      hipLaunchKernelGGL(k_count_kept, dim3((unsigned)std::max<int64_t>(1, ceil_div(n, kThreads))),
+                         dim3(kThreads), 0, stream, n, skip, cnt);
+      e = hipGetLastError();
+    }
+  }
+  if (e == hipSuccess) {
     ProfScope ps("softmax_xent", stream);
     hipLaunchKernelGGL(k_softmax_xent, dim3((unsigned)nb), dim3(kThreads), 0, stream, n, C, z, ldz,
-                       y, dz, ldd, bl);
+                       y, dz, ldd, bl, skip, (const unsigned long long*)cnt);
+    e = hipGetLastError();
   }
-  hipError_t e = hipGetLastError();
   if (e == hipSuccess) {
     ProfScope ps("loss_total", stream);
     hipLaunchKernelGGL(k_loss_total, dim3(1), dim3(kThreads), 0, stream, nb, n, (const double*)bl,
-                       loss);
+                       loss, (const unsigned long long*)cnt);
     e = hipGetLastError();
   }
+  tfree(cnt, stream);
   tfree(bl, stream);
   if (e != hipSuccess) return hip_fail(e, "softmax_xent", __FILE__, __LINE__);
   return GCN_OK;

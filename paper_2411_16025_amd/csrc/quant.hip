@@ -76,7 +76,8 @@ __global__ __launch_bounds__(kBlock) void k_ln_quantize(int64_t n, int F, const 
                                                         int ln, int bits, float* __restrict__ y,
                                                         int64_t ldy, uint8_t* __restrict__ q,
                                                         int64_t ldq, float* __restrict__ zmin,
-                                                        float* __restrict__ scale, int64_t ldp) {
+                                                        float* __restrict__ scale, int64_t ldp,
+                                                        float* __restrict__ rstd) {
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
   if (i >= n) return;
@@ -93,6 +94,11 @@ __global__ __launch_bounds__(kBlock) void k_ln_quantize(int64_t n, int F, const 
     }
     nm.mean = mean;
     nm.inv = 1.0 / sqrt(wave_sum(v) / (double)F + eps);
+    if (rstd && lane == 0) rstd[i] = (float)nm.inv;
+  }
+  if (bits == 0) {  // LayerNorm only
+    for (int f = lane; f < F; f += 64) y[i * ldy + f] = nm.apply(row[f], f);
+    return;
   }
   float mn = nm.apply(row[0], 0), mx = mn;
   for (int f = lane; f < F; f += 64) {
@@ -178,6 +184,7 @@ struct QuantArgs {
   float* scale;
   int64_t ldp;
   bool q_dword, y_vec;  // Q rows 4-byte aligned; Y rows 16-byte aligned
+  float* rstd;          // optional 1 / sqrt(var + eps) per row (bits == 0 only)
 };
 
 template <int G, int NV, int R, bool AFFINE>
@@ -228,6 +235,7 @@ __global__ __launch_bounds__(kBlock) void k_ln_quantize_v(QuantArgs a) {
           if (4 * (sl + j * G) + e < a.F) var += d * d;
         }
       const double inv = 1.0 / sqrt(slot_sum<G>(var) / (double)a.F + a.eps);
+      if (a.rstd && live && sl == 0) a.rstd[i] = (float)inv;
 #pragma unroll
       for (int j = 0; j < NV; ++j)
 #pragma unroll
@@ -244,6 +252,20 @@ __global__ __launch_bounds__(kBlock) void k_ln_quantize_v(QuantArgs a) {
             }
           }
         }
+    }
+    if (a.bits == 0) {  // LayerNorm only
+      if (!live) continue;
+      float* yr = a.y + i * a.ldy;
+#pragma unroll
+      for (int j = 0; j < NV; ++j) {
+        const int f = 4 * (sl + j * G);
+        if (f >= a.F) continue;
+        if (f + 4 <= a.F && a.y_vec)
+          *reinterpret_cast<float4*>(yr + f) = make_float4(v[r][j][0], v[r][j][1], v[r][j][2], v[r][j][3]);
+        else
+          for (int e = 0; e < 4 && f + e < a.F; ++e) yr[f + e] = v[r][j][e];
+      }
+      continue;
     }
     float mn = __builtin_inff(), mx = -__builtin_inff();
 #pragma unroll
@@ -325,16 +347,212 @@ QuantArgs make_args(int64_t n, int64_t F, const float* X, int64_t ldx, const flo
                     const float* beta, double eps, int ln, int bits, float* Y, int64_t ldy,
                     uint8_t* Q, int64_t ldq, float* zmin, float* scale, int64_t ldp) {
   QuantArgs a{n, (int)F, X, ldx, gamma, beta, eps, ln, bits, Y, ldy, Q, ldq, zmin, scale, ldp,
-              false, false};
+              false, false, nullptr};
   a.q_dword = reinterpret_cast<uintptr_t>(Q) % 4 == 0 && ldq % 4 == 0;
   a.y_vec = Y && reinterpret_cast<uintptr_t>(Y) % 16 == 0 && ldy % 4 == 0;
   return a;
 }
 
+// ---- LayerNorm backward -----------------------------------------------------------
+
+// dx = rstd * (g - mean(g) - y * mean(g * y)) per row, g = g1 (+ g2), then
+// optionally dx *= (mask > 0) (the ReLU of the layer below). y is the
+// normalized output of the forward pass. Row means in double.
+struct LnBwdArgs {
+  int64_t n;
+  int F;
+  const float* y;
+  int64_t ldy;
+  const float* rstd;
+  const float* g1;
+  int64_t ld1;
+  const float* g2;
+  int64_t ld2;
+  const float* mask;  // may alias dx (read before dx is written, by the same lane)
+  int64_t ldm;
+  float* dx;
+  int64_t ldx;
+};
+
+template <int G, int NV>
+__global__ __launch_bounds__(kBlock) void k_ln_bwd_v(LnBwdArgs a) {
+  constexpr int E = 64 / G;
+  const int lane = threadIdx.x & 63;
+  const int sl = lane % G;
+  const int64_t i = ((int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6)) * E + lane / G;
+  const bool live = i < a.n;
+  float yv[NV][4], gv[NV][4], mv[NV][4];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int f = 4 * (sl + j * G);
+    if (live && f + 4 <= a.F) {
+      const float4 t = *reinterpret_cast<const float4*>(a.y + i * a.ldy + f);
+      float4 u = *reinterpret_cast<const float4*>(a.g1 + i * a.ld1 + f);
+      if (a.g2) {
+        const float4 w = *reinterpret_cast<const float4*>(a.g2 + i * a.ld2 + f);
+        u.x += w.x;
+        u.y += w.y;
+        u.z += w.z;
+        u.w += w.w;
+      }
+      float4 m = make_float4(1.f, 1.f, 1.f, 1.f);
+      if (a.mask) m = *reinterpret_cast<const float4*>(a.mask + i * a.ldm + f);
+      yv[j][0] = t.x; yv[j][1] = t.y; yv[j][2] = t.z; yv[j][3] = t.w;
+      gv[j][0] = u.x; gv[j][1] = u.y; gv[j][2] = u.z; gv[j][3] = u.w;
+      mv[j][0] = m.x; mv[j][1] = m.y; mv[j][2] = m.z; mv[j][3] = m.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bool ok = live && f + e < a.F;
+        yv[j][e] = ok ? a.y[i * a.ldy + f + e] : 0.f;
+        gv[j][e] = ok ? a.g1[i * a.ld1 + f + e] + (a.g2 ? a.g2[i * a.ld2 + f + e] : 0.f) : 0.f;
+        mv[j][e] = ok && a.mask ? a.mask[i * a.ldm + f + e] : 1.f;
+      }
+    }
+  }
+  double s1 = 0.0, s2 = 0.0;
+#pragma unroll
+  for (int j = 0; j < NV; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {  // masked entries are 0
+      s1 += (double)gv[j][e];
+      s2 += (double)gv[j][e] * (double)yv[j][e];
+    }
+  const double m1 = slot_sum<G>(s1) / (double)a.F;
+  const double m2 = slot_sum<G>(s2) / (double)a.F;
+  if (!live) return;
+  const double r = (double)a.rstd[i];
+  float* out = a.dx + i * a.ldx;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int f = 4 * (sl + j * G);
+    if (f >= a.F) continue;
+    float o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float d = (float)(r * ((double)gv[j][e] - m1 - (double)yv[j][e] * m2));
+      o[e] = mv[j][e] > 0.f ? d : 0.f;
+    }
+    if (f + 4 <= a.F)
+      *reinterpret_cast<float4*>(out + f) = make_float4(o[0], o[1], o[2], o[3]);
+    else
+      for (int e = 0; e < 4 && f + e < a.F; ++e) out[f + e] = o[e];
+  }
+}
+
+// One wavefront per row for wide rows or unaligned storage.
+__global__ __launch_bounds__(kBlock) void k_ln_bwd(LnBwdArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t i = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  if (i >= a.n) return;
+  auto g_at = [&](int f) {
+    return a.g1[i * a.ld1 + f] + (a.g2 ? a.g2[i * a.ld2 + f] : 0.f);
+  };
+  double s1 = 0.0, s2 = 0.0;
+  for (int f = lane; f < a.F; f += 64) {
+    const double gf = (double)g_at(f);
+    s1 += gf;
+    s2 += gf * (double)a.y[i * a.ldy + f];
+  }
+  const double m1 = wave_sum(s1) / (double)a.F;
+  const double m2 = wave_sum(s2) / (double)a.F;
+  const double r = (double)a.rstd[i];
+  for (int f = lane; f < a.F; f += 64) {
+    const float d = (float)(r * ((double)g_at(f) - m1 - (double)a.y[i * a.ldy + f] * m2));
+    const bool keep = !a.mask || a.mask[i * a.ldm + f] > 0.f;
+    a.dx[i * a.ldx + f] = keep ? d : 0.f;
+  }
+}
+
+template <int G, int NV>
+void launch_bwd_v(const LnBwdArgs& a, hipStream_t s) {
+  const int64_t rows_per_block = (int64_t)(kBlock / 64) * (64 / G);
+  hipLaunchKernelGGL((k_ln_bwd_v<G, NV>), dim3((unsigned)ceil_div(a.n, rows_per_block)),
+                     dim3(kBlock), 0, s, a);
+}
+
+bool al16(const void* p, int64_t ld) { return reinterpret_cast<uintptr_t>(p) % 16 == 0 && ld % 4 == 0; }
+
 }  // namespace
+
+gcn_status layernorm_fwd(int64_t n, int64_t F, const float* X, int64_t ldx, double eps, float* Y,
+                         int64_t ldy, float* rstd, hipStream_t s) {
+  if (n == 0) return GCN_OK;
+  ProfScope ps("layernorm_fwd", s);
+  QuantArgs a = make_args(n, F, X, ldx, nullptr, nullptr, eps, 1, 0, Y, ldy, nullptr, 0, nullptr,
+                          nullptr, 1);
+  a.rstd = rstd;
+  gcn_status st = GCN_OK;
+  if (try_vector(a, s, &st)) return st;
+  hipLaunchKernelGGL(k_ln_quantize, dim3((unsigned)ceil_div(n, kBlock / 64)), dim3(kBlock), 0, s,
+                     n, (int)F, X, ldx, nullptr, nullptr, eps, 1, 0, Y, ldy, nullptr, 0, nullptr,
+                     nullptr, 1, rstd);
+  GCN_HIP(hipGetLastError());
+  return GCN_OK;
+}
+
+gcn_status layernorm_bwd(int64_t n, int64_t F, const float* Y, int64_t ldy, const float* rstd,
+                         const float* G1, int64_t ld1, const float* G2, int64_t ld2,
+                         const float* mask, int64_t ldm, float* dX, int64_t lddx, hipStream_t s) {
+  if (n == 0) return GCN_OK;
+  ProfScope ps("layernorm_bwd", s);
+  const LnBwdArgs a{n, (int)F, Y, ldy, rstd, G1, ld1, G2, ld2, mask, ldm, dX, lddx};
+  const bool vec = al16(Y, ldy) && al16(G1, ld1) && (!G2 || al16(G2, ld2)) &&
+                   (!mask || al16(mask, ldm)) && al16(dX, lddx) && F <= 1024;
+  if (!vec)
+    hipLaunchKernelGGL(k_ln_bwd, dim3((unsigned)ceil_div(n, kBlock / 64)), dim3(kBlock), 0, s, a);
+  else if (F <= 32)
+    launch_bwd_v<8, 1>(a, s);
+  else if (F <= 64)
+    launch_bwd_v<8, 2>(a, s);
+  else if (F <= 128)
+    launch_bwd_v<8, 4>(a, s);
+  else if (F <= 256)
+    launch_bwd_v<16, 4>(a, s);
+  else if (F <= 512)
+    launch_bwd_v<32, 4>(a, s);
+  else
+    launch_bwd_v<64, 4>(a, s);
+  GCN_HIP(hipGetLastError());
+  return GCN_OK;
+}
+
 }  // namespace gcn
 
 using namespace gcn;
+
+extern "C" gcn_status gcn_layernorm_fwd(int64_t n, int64_t F, const float* X, int64_t ldx,
+                                        double eps, float* Y, int64_t ldy, float* rstd,
+                                        void* stream) {
+  clear_error();
+  if (n < 0 || F <= 0 || F >= (1ll << 31) || !(eps >= 0.0)) {
+    set_error("need n >= 0, F in [1, 2^31) and eps >= 0");
+    return GCN_EINVAL;
+  }
+  if (n > 0 && (!X || !Y || ldx < F || ldy < F)) {
+    set_error("X and Y must be non-NULL with ldx, ldy >= F");
+    return GCN_EINVAL;
+  }
+  return layernorm_fwd(n, F, X, ldx, eps, Y, ldy, rstd, (hipStream_t)stream);
+}
+
+extern "C" gcn_status gcn_layernorm_bwd(int64_t n, int64_t F, const float* Y, int64_t ldy,
+                                        const float* rstd, const float* dY, int64_t lddy,
+                                        const float* dY2, int64_t lddy2, const float* mask,
+                                        int64_t ldm, float* dX, int64_t lddx, void* stream) {
+  clear_error();
+  if (n < 0 || F <= 0 || F >= (1ll << 31)) {
+    set_error("need n >= 0 and F in [1, 2^31)");
+    return GCN_EINVAL;
+  }
+  if (n > 0 && (!Y || !rstd || !dY || !dX || ldy < F || lddy < F || lddx < F ||
+                (dY2 && lddy2 < F) || (mask && ldm < F))) {
+    set_error("Y, rstd, dY, dX must be non-NULL with leading dimensions >= F");
+    return GCN_EINVAL;
+  }
+  return layernorm_bwd(n, F, Y, ldy, rstd, dY, lddy, dY2, lddy2, mask, ldm, dX, lddx,
+                       (hipStream_t)stream);
+}
 
 extern "C" gcn_status gcn_layernorm_quantize(int64_t n, int64_t F, const float* X, int64_t ldx,
                                              const float* gamma, const float* beta, double eps,
@@ -363,7 +581,7 @@ extern "C" gcn_status gcn_layernorm_quantize(int64_t n, int64_t F, const float* 
     return st;
   hipLaunchKernelGGL(k_ln_quantize, dim3((unsigned)ceil_div(n, kBlock / 64)), dim3(kBlock), 0, s, n,
                      (int)F, X, ldx, gamma, beta, eps, (int)(flags & GCN_LAYERNORM), bits, Y, ldy,
-                     Q, ldq, zmin, scale, ldp);
+                     Q, ldq, zmin, scale, ldp, nullptr);
   GCN_HIP(hipGetLastError());
   return GCN_OK;
 }

@@ -1,0 +1,382 @@
+// One training step of the 3-layer GraphSAGE model the paper evaluates
+// (Section 8, Table 2: LayerNorm before each layer, mean aggregation), with
+// optional masked label propagation (Section 6.1 step 1, Lemma 2), built from
+// the library's kernels on the caller's stream without host synchronization.
+//
+// Layer l reads H (n x f), and writes the row-major concatenation
+//   C = [ LayerNorm(H) | D^-1 A LayerNorm(H) | 1 | 0 0 0 ]
+// (each block padded to a multiple of 4 columns), so that the layer's UPDATE
+//   O = Y W_self + Z W_neigh + b
+// is one MFMA product C Wp with the packed weights Wp = [W_self; W_neigh; b; 0].
+// The aggregation writes straight into the middle block through its row
+// stride; the ones column carries the bias, and the weight gradient of the
+// same product yields dW_self, dW_neigh and db together.
+
+#include "common.h"
+
+namespace gcn {
+namespace {
+
+constexpr int kThreadsS = 256;
+
+inline int64_t round4(int64_t v) { return (v + 3) & ~int64_t(3); }
+
+// Columns of C that no kernel of the layer writes: the padding after each
+// f-wide block, the ones column and the three zero columns after it.
+__global__ __launch_bounds__(kThreadsS) void k_concat_tail(int64_t n, int64_t f, int64_t fp,
+                                                           float* __restrict__ c, int64_t ldc) {
+  const int64_t pad = fp - f;
+  const int64_t per_row = 2 * pad + 4;
+  const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
+  if (t >= n * per_row) return;
+  const int64_t i = t / per_row, k = t % per_row;
+  int64_t col;
+  if (k < pad)
+    col = f + k;
+  else if (k < 2 * pad)
+    col = fp + f + (k - pad);
+  else
+    col = 2 * fp + (k - 2 * pad);
+  c[i * ldc + col] = (col == 2 * fp) ? 1.f : 0.f;
+}
+
+// Wp [(2 fp + 4) x fop]: rows [0, f) = W_self, [fp, fp + f) = W_neigh,
+// row 2 fp = b, every other entry 0 (fo columns used of fop).
+__global__ __launch_bounds__(kThreadsS) void k_pack_weights(int64_t f, int64_t fp, int64_t fo,
+                                                            int64_t fop,
+                                                            const float* __restrict__ ws,
+                                                            const float* __restrict__ wn,
+                                                            const float* __restrict__ b,
+                                                            float* __restrict__ wp) {
+  const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
+  const int64_t rows = 2 * fp + 4;
+  if (t >= rows * fop) return;
+  const int64_t r = t / fop, c = t % fop;
+  float v = 0.f;
+  if (c < fo) {
+    if (r < f)
+      v = ws[r * fo + c];
+    else if (r >= fp && r < fp + f)
+      v = wn[(r - fp) * fo + c];
+    else if (r == 2 * fp)
+      v = b[c];
+  }
+  wp[t] = v;
+}
+
+// The inverse of k_pack_weights for the gradient.
+__global__ __launch_bounds__(kThreadsS) void k_unpack_grads(int64_t f, int64_t fp, int64_t fo,
+                                                            int64_t fop,
+                                                            const float* __restrict__ dwp,
+                                                            float* __restrict__ dws,
+                                                            float* __restrict__ dwn,
+                                                            float* __restrict__ db) {
+  const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
+  if (t >= (2 * f + 1) * fo) return;
+  const int64_t r = t / fo, c = t % fo;
+  if (r < f)
+    dws[r * fo + c] = dwp[r * fop + c];
+  else if (r < 2 * f)
+    dwn[(r - f) * fo + c] = dwp[(fp + r - f) * fop + c];
+  else
+    db[c] = dwp[2 * fp * fop + c];
+}
+
+// Masked label propagation, forward: Xp = X + E[y] on rows with mask = 1.
+__global__ __launch_bounds__(kThreadsS) void k_embed_labels(int64_t n, int64_t f, int C,
+                                                            const float* __restrict__ x,
+                                                            int64_t ldx,
+                                                            const uint8_t* __restrict__ mask,
+                                                            const int32_t* __restrict__ y,
+                                                            const float* __restrict__ e,
+                                                            float* __restrict__ xp, int64_t ldp) {
+  const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
+  if (t >= n * f) return;
+  const int64_t i = t / f, c = t % f;
+  float v = x[i * ldx + c];
+  const int32_t k = y[i];
+  if (mask[i] && k >= 0 && k < C) v += e[(int64_t)k * f + c];
+  xp[i * ldp + c] = v;
+}
+
+// Masked label propagation, backward: dE[k] = sum of dXp rows with mask = 1
+// and label k. Workgroup b sums its range of rows in row order into an LDS
+// table (thread = feature, so no two threads touch one entry), then writes
+// the table as partial b; k_embed_grad_reduce adds the partials in order.
+constexpr int kEmbedRows = 2048;
+
+__global__ __launch_bounds__(kThreadsS) void k_embed_grad_partial(
+    int64_t n, int64_t f, int C, const float* __restrict__ dx, int64_t ldx,
+    const uint8_t* __restrict__ mask, const int32_t* __restrict__ y, float* __restrict__ part) {
+  __shared__ float acc[64][kThreadsS];
+  const int t = threadIdx.x;
+  const int64_t c = (int64_t)blockIdx.y * kThreadsS + t;
+  for (int k = 0; k < C; ++k) acc[k][t] = 0.f;
+  const int64_t i0 = (int64_t)blockIdx.x * kEmbedRows;
+  const int64_t i1 = std::min(n, i0 + kEmbedRows);
+  if (c < f)
+    for (int64_t i = i0; i < i1; ++i)
+      if (mask[i] && y[i] >= 0 && y[i] < C) acc[y[i]][t] += dx[i * ldx + c];
+  if (c < f)
+    for (int k = 0; k < C; ++k) part[((int64_t)blockIdx.x * C + k) * f + c] = acc[k][t];
+}
+
+__global__ __launch_bounds__(kThreadsS) void k_embed_grad_reduce(int64_t nb, int64_t f, int C,
+                                                                 const float* __restrict__ part,
+                                                                 float* __restrict__ de) {
+  const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
+  if (t >= (int64_t)C * f) return;
+  float s = 0.f;
+  for (int64_t b = 0; b < nb; ++b) s += part[b * C * f + t];
+  de[t] = s;
+}
+
+inline unsigned blocks(int64_t work) {
+  return (unsigned)std::max<int64_t>(1, ceil_div(work, kThreadsS));
+}
+
+// Buffers of one layer.
+struct Layer {
+  int64_t f = 0, fp = 0, fo = 0, fop = 0, ldc = 0;
+  float* c = nullptr;     // [n x ldc] = [Y | Z | 1 000]
+  float* rstd = nullptr;  // [n]
+  float* wp = nullptr;    // [ldc x fop]
+  float* o = nullptr;     // [n x fop] pre-activation; after ReLU the layer output
+};
+
+struct Sage {
+  int64_t n = 0;
+  Layer L[3];
+  float* xp = nullptr;  // input with label embeddings ([n x fp of layer 1])
+};
+
+gcn_status check_args(const gcn_graph* g, const float* X, int64_t ldx, int64_t f_in,
+                      int64_t hidden, int64_t n_classes, const float* const* params,
+                      const int32_t* labels, const uint8_t* lp_mask, const float* E, double eps) {
+  GCN_CHECK(check_graph(g));
+  if (g->n_rows != g->n_cols) {
+    set_error("the GraphSAGE model needs a square graph");
+    return GCN_EINVAL;
+  }
+  if (!X || !params || f_in <= 0 || hidden <= 0 || n_classes <= 0 || n_classes > 64 ||
+      ldx < f_in || !(eps >= 0.0)) {
+    set_error("invalid GraphSAGE arguments (1 <= n_classes <= 64, ldx >= f_in, eps >= 0)");
+    return GCN_EINVAL;
+  }
+  for (int k = 0; k < 9; ++k)
+    if (!params[k]) {
+      set_error("params[%d] must be non-NULL", k);
+      return GCN_EINVAL;
+    }
+  if (lp_mask && (!E || !labels)) {
+    set_error("label propagation needs the labels and the embedding E");
+    return GCN_EINVAL;
+  }
+  return GCN_OK;
+}
+
+void sage_free(Sage& m, hipStream_t s) {
+  tfree(m.xp, s);
+  for (int l = 2; l >= 0; --l) {
+    tfree(m.L[l].o, s);
+    tfree(m.L[l].wp, s);
+    tfree(m.L[l].rstd, s);
+    tfree(m.L[l].c, s);
+    m.L[l] = Layer();
+  }
+  m.xp = nullptr;
+}
+
+// Shapes, buffers, packed weights and the forward pass; on return L[2].o
+// holds the logits and L[0..1].o the ReLU outputs of layers 1 and 2.
+gcn_status sage_forward(const gcn_graph* g, const float* X, int64_t ldx, int64_t f_in,
+                        int64_t hidden, int64_t n_classes, const float* const* params,
+                        const int32_t* labels, const uint8_t* lp_mask, const float* E, double eps,
+                        Sage& m, hipStream_t s) {
+  const int64_t n = g->n_rows;
+  m.n = n;
+  Layer* L = m.L;
+  const int64_t dims[4] = {f_in, hidden, hidden, n_classes};
+  for (int l = 0; l < 3; ++l) {
+    L[l].f = dims[l];
+    L[l].fp = round4(dims[l]);
+    L[l].fo = dims[l + 1];
+    L[l].fop = round4(dims[l + 1]);
+    L[l].ldc = 2 * L[l].fp + 4;
+  }
+  gcn_status st = GCN_OK;
+  for (int l = 0; l < 3 && st == GCN_OK; ++l) {
+    st = talloc(&L[l].c, n * L[l].ldc, s, "concatenated layer input");
+    if (st == GCN_OK) st = talloc(&L[l].rstd, n, s, "LayerNorm 1/std");
+    if (st == GCN_OK) st = talloc(&L[l].wp, L[l].ldc * L[l].fop, s, "packed weights");
+    if (st == GCN_OK) st = talloc(&L[l].o, n * L[l].fop, s, "layer output");
+  }
+  if (st == GCN_OK && lp_mask) st = talloc(&m.xp, n * L[0].fp, s, "input with label embeddings");
+  GCN_CHECK(st);
+  // packed weights and the constant columns of each C
+  for (int l = 0; l < 3; ++l) {
+    Layer& y = L[l];
+    hipLaunchKernelGGL(k_pack_weights, dim3(blocks(y.ldc * y.fop)), dim3(kThreadsS), 0, s, y.f,
+                       y.fp, y.fo, y.fop, params[3 * l], params[3 * l + 1], params[3 * l + 2], y.wp);
+    GCN_HIP(hipGetLastError());
+    hipLaunchKernelGGL(k_concat_tail, dim3(blocks(n * (2 * (y.fp - y.f) + 4))), dim3(kThreadsS),
+                       0, s, n, y.f, y.fp, y.c, y.ldc);
+    GCN_HIP(hipGetLastError());
+  }
+  const float* h = X;
+  int64_t ldh = ldx;
+  if (lp_mask) {
+    hipLaunchKernelGGL(k_embed_labels, dim3(blocks(n * f_in)), dim3(kThreadsS), 0, s, n, f_in,
+                       (int)n_classes, X, ldx, lp_mask, labels, E, m.xp, L[0].fp);
+    GCN_HIP(hipGetLastError());
+    h = m.xp;
+    ldh = L[0].fp;
+  }
+  for (int l = 0; l < 3; ++l) {
+    Layer& y = L[l];
+    GCN_CHECK(layernorm_fwd(n, y.f, h, ldh, eps, y.c, y.ldc, y.rstd, s));
+    GCN_CHECK(aggregate_f32(g->csr, y.c, y.ldc, y.c + y.fp, y.ldc, y.f, false, s));
+    GCN_CHECK(gemm_f32(GCN_GEMM_NN, n, y.fop, y.ldc, y.c, y.ldc, y.wp, y.fop, y.o, y.fop, s));
+    if (l < 2) GCN_CHECK(relu_fwd(n, y.fo, y.o, y.fop, s));
+    h = y.o;
+    ldh = y.fop;
+  }
+  return GCN_OK;
+}
+
+// Backward pass and loss after sage_forward.
+gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
+                         const int32_t* labels, const uint8_t* lp_mask, float* const* grads,
+                         float* dE, double* loss, Sage& m, hipStream_t s) {
+  const int64_t n = m.n;
+  const int C = (int)n_classes;
+  Layer* L = m.L;
+  float *dlogits = nullptr, *dc = nullptr, *t = nullptr, *dwp = nullptr, *part = nullptr;
+  const int64_t ld_dc = std::max(std::max(L[0].ldc, L[1].ldc), L[2].ldc);
+  const int64_t ld_t = std::max(L[0].fp, L[1].fp);
+  int64_t w_max = 0;
+  for (int l = 0; l < 3; ++l) w_max = std::max(w_max, L[l].ldc * L[l].fop);
+  gcn_status st = talloc(&dlogits, n * L[2].fop, s, "dlogits");
+  if (st == GCN_OK) st = talloc(&dc, n * ld_dc, s, "dC");
+  if (st == GCN_OK) st = talloc(&t, n * ld_t, s, "transposed aggregation");
+  if (st == GCN_OK) st = talloc(&dwp, w_max, s, "packed weight gradient");
+  if (st == GCN_OK)
+    st = softmax_xent(n, C, L[2].o, L[2].fop, labels, dlogits, L[2].fop, loss, s, lp_mask);
+  float* dO = dlogits;
+  int64_t ld_do = L[2].fop;
+  for (int l = 2; l >= 0 && st == GCN_OK; --l) {
+    Layer& y = L[l];
+    st = gemm_f32(GCN_GEMM_TN, y.ldc, y.fop, n, y.c, y.ldc, dO, ld_do, dwp, y.fop, s);
+    if (st != GCN_OK) break;
+    hipLaunchKernelGGL(k_unpack_grads, dim3(blocks((2 * y.f + 1) * y.fo)), dim3(kThreadsS), 0, s,
+                       y.f, y.fp, y.fo, y.fop, (const float*)dwp, grads[3 * l], grads[3 * l + 1],
+                       grads[3 * l + 2]);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) {
+      st = hip_fail(e, "k_unpack_grads", __FILE__, __LINE__);
+      break;
+    }
+    if (l == 0 && !lp_mask) break;
+    // dC = dO Wp^T; the input gradient of the layer is
+    // dY = dC[:, Y block] + A^T dC[:, Z block], then the LayerNorm backward
+    st = gemm_f32(GCN_GEMM_NT, n, y.ldc, y.fop, dO, ld_do, y.wp, y.fop, dc, y.ldc, s);
+    if (st == GCN_OK) st = aggregate_f32(g->csc, dc + y.fp, y.ldc, t, y.fp, y.f, false, s);
+    if (st != GCN_OK) break;
+    if (l > 0) {
+      // the gradient of the layer below, masked by its ReLU, overwrites its output
+      Layer& below = L[l - 1];
+      st = layernorm_bwd(n, y.f, y.c, y.ldc, y.rstd, dc, y.ldc, t, y.fp, below.o, below.fop,
+                         below.o, below.fop, s);
+      dO = below.o;
+      ld_do = below.fop;
+    } else {
+      // label propagation: dXp, then the embedding gradient
+      st = layernorm_bwd(n, y.f, y.c, y.ldc, y.rstd, dc, y.ldc, t, y.fp, nullptr, 0, m.xp, y.fp,
+                         s);
+      const int64_t nb = std::max<int64_t>(1, ceil_div(n, kEmbedRows));
+      if (st == GCN_OK) st = talloc(&part, nb * C * f_in, s, "embedding gradient partials");
+      if (st == GCN_OK) {
+        hipLaunchKernelGGL(k_embed_grad_partial,
+                           dim3((unsigned)nb, (unsigned)ceil_div(f_in, kThreadsS)),
+                           dim3(kThreadsS), 0, s, n, f_in, C, (const float*)m.xp, y.fp, lp_mask,
+                           labels, part);
+        e = hipGetLastError();
+        if (e == hipSuccess) {
+          hipLaunchKernelGGL(k_embed_grad_reduce, dim3(blocks((int64_t)C * f_in)),
+                             dim3(kThreadsS), 0, s, nb, f_in, C, (const float*)part, dE);
+          e = hipGetLastError();
+        }
+        if (e != hipSuccess) st = hip_fail(e, "embedding gradient", __FILE__, __LINE__);
+      }
+    }
+  }
+  tfree(part, s);
+  tfree(dwp, s);
+  tfree(t, s);
+  tfree(dc, s);
+  tfree(dlogits, s);
+  return st;
+}
+
+gcn_status copy_rows(float* dst, int64_t ldd, const float* src, int64_t lds, int64_t n,
+                     int64_t cols, hipStream_t s) {
+  if (!dst || n == 0) return GCN_OK;
+  GCN_HIP(hipMemcpy2DAsync(dst, ldd * sizeof(float), src, lds * sizeof(float),
+                           cols * sizeof(float), n, hipMemcpyDeviceToDevice, s));
+  return GCN_OK;
+}
+
+}  // namespace
+}  // namespace gcn
+
+using namespace gcn;
+
+extern "C" gcn_status gcn_sage3_forward(const gcn_graph* g, const float* X, int64_t ldx,
+                                        int64_t f_in, int64_t hidden, int64_t n_classes,
+                                        const float* const* params, const int32_t* labels,
+                                        const uint8_t* lp_mask, const float* E, double eps,
+                                        float* H1, int64_t ldh1, float* H2, int64_t ldh2,
+                                        float* logits, int64_t ldl, void* stream_) {
+  clear_error();
+  GCN_CHECK(check_args(g, X, ldx, f_in, hidden, n_classes, params, labels, lp_mask, E, eps));
+  if ((H1 && ldh1 < hidden) || (H2 && ldh2 < hidden) || (logits && ldl < n_classes)) {
+    set_error("output leading dimensions must cover the output widths");
+    return GCN_EINVAL;
+  }
+  hipStream_t s = (hipStream_t)stream_;
+  Sage m;
+  gcn_status st = sage_forward(g, X, ldx, f_in, hidden, n_classes, params, labels, lp_mask, E,
+                               eps, m, s);
+  if (st == GCN_OK) st = copy_rows(H1, ldh1, m.L[0].o, m.L[0].fop, m.n, hidden, s);
+  if (st == GCN_OK) st = copy_rows(H2, ldh2, m.L[1].o, m.L[1].fop, m.n, hidden, s);
+  if (st == GCN_OK) st = copy_rows(logits, ldl, m.L[2].o, m.L[2].fop, m.n, n_classes, s);
+  sage_free(m, s);
+  return st;
+}
+
+extern "C" gcn_status gcn_sage3_step(const gcn_graph* g, const float* X, int64_t ldx, int64_t f_in,
+                                     int64_t hidden, int64_t n_classes,
+                                     const float* const* params, const int32_t* labels,
+                                     const uint8_t* lp_mask, const float* E, double eps,
+                                     float* const* grads, float* dE, double* loss,
+                                     void* stream_) {
+  clear_error();
+  GCN_CHECK(check_args(g, X, ldx, f_in, hidden, n_classes, params, labels, lp_mask, E, eps));
+  if (!grads || !labels || !loss || (lp_mask && !dE)) {
+    set_error("the step needs labels, grads, loss (and dE with label propagation)");
+    return GCN_EINVAL;
+  }
+  for (int k = 0; k < 9; ++k)
+    if (!grads[k]) {
+      set_error("grads[%d] must be non-NULL", k);
+      return GCN_EINVAL;
+    }
+  hipStream_t s = (hipStream_t)stream_;
+  Sage m;
+  gcn_status st = sage_forward(g, X, ldx, f_in, hidden, n_classes, params, labels, lp_mask, E,
+                               eps, m, s);
+  if (st == GCN_OK)
+    st = sage_backward(g, f_in, n_classes, labels, lp_mask, grads, dE, loss, m, s);
+  sage_free(m, s);
+  return st;
+}

@@ -30,7 +30,9 @@ STATUS = {0: "GCN_OK", 1: "GCN_EINVAL", 2: "GCN_ERANGE", 3: "GCN_ENOMEM", 4: "GC
 # every symbol include/gcnagg.h declares
 GCN_GEMM_NN, GCN_GEMM_NT, GCN_GEMM_TN = 0, 1, 2
 
-EXPORTS = ("gcn_build_csr", "gcn_normalize", "gcn_normalize_rc", "gcn_prepost_split",
+EXPORTS = ("gcn_build_csr", "gcn_normalize", "gcn_normalize_rc", "gcn_normalize_mean",
+           "gcn_layernorm_fwd", "gcn_layernorm_bwd", "gcn_sage3_forward", "gcn_sage3_step",
+           "gcn_prepost_split",
            "gcn_add_rows", "gcn_aggregate_fwd", "gcn_aggregate_bwd",
            "gcn_aggregate_fwd_q8halo", "gcn_quantize_rows_u8", "gcn_layernorm_quantize",
            "gcn_gemm_f32", "gcn_relu",
@@ -75,6 +77,13 @@ def lib():
         L.gcn_relu_bwd.argtypes = [i64, i64, P, i64, P, i64, P]
         L.gcn_softmax_xent.argtypes = [i64, i64, P, i64, P, P, i64, P, P]
         L.gcn_gcn2_step.argtypes = [P, P, i64, i64, P, i64, P, i64, P, P, P, P, P]
+        L.gcn_normalize_mean.argtypes = [P, P]
+        L.gcn_layernorm_fwd.argtypes = [i64, i64, P, i64, ctypes.c_double, P, i64, P, P]
+        L.gcn_layernorm_bwd.argtypes = [i64, i64, P, i64, P, P, i64, P, i64, P, i64, P, i64, P]
+        L.gcn_sage3_step.argtypes = [P, P, i64, i64, i64, i64, P, P, P, P, ctypes.c_double, P,
+                                     P, P, P]
+        L.gcn_sage3_forward.argtypes = [P, P, i64, i64, i64, i64, P, P, P, P, ctypes.c_double, P,
+                                        i64, P, i64, P, i64, P]
         L.gcn_graph_free.argtypes = [P]
         L.gcn_graph_free.restype = None
         L.gcn_graph_info.argtypes = [P, P, P, P]
@@ -437,6 +446,111 @@ def gcn_gcn2_step(g: Graph, X: torch.Tensor, W1: torch.Tensor, W2: torch.Tensor,
                                hidden, W2.data_ptr(), n_classes, labels.data_ptr(),
                                dW1.data_ptr(), dW2.data_ptr(), loss.data_ptr(), _stream(stream)))
     return loss, dW1, dW2
+
+
+def gcn_normalize_mean(g: Graph, stream=None):
+    """Values of the mean operator D^-1 A (and its transpose)."""
+    _check(lib().gcn_normalize_mean(g.handle, _stream(stream)))
+
+
+def gcn_layernorm_fwd(X: torch.Tensor, eps: float = 1e-5, Y: torch.Tensor | None = None,
+                      stream=None):
+    """(Y, rstd): row LayerNorm without affine parameters, and 1/sqrt(var + eps)."""
+    _dev(X, torch.float32, "X")
+    n, F = X.shape
+    if Y is None:
+        Y = torch.empty((n, F), dtype=torch.float32, device=X.device)
+    _dev(Y, torch.float32, "Y")
+    rstd = torch.empty(n, dtype=torch.float32, device=X.device)
+    _check(lib().gcn_layernorm_fwd(n, F, X.data_ptr(), _rowmajor(X, "X"), eps, Y.data_ptr(),
+                                   _rowmajor(Y, "Y"), rstd.data_ptr(), _stream(stream)))
+    return Y, rstd
+
+
+def gcn_layernorm_bwd(Y: torch.Tensor, rstd: torch.Tensor, dY: torch.Tensor, dY2=None,
+                      mask=None, dX: torch.Tensor | None = None, stream=None):
+    """dX of the row LayerNorm for g = dY (+ dY2), zeroed where mask <= 0."""
+    for t, nm in ((Y, "Y"), (rstd, "rstd"), (dY, "dY")):
+        _dev(t, torch.float32, nm)
+    n, F = Y.shape
+    if dX is None:
+        dX = torch.empty((n, F), dtype=torch.float32, device=Y.device)
+    ptr = lambda t: t.data_ptr() if t is not None else None  # noqa: E731
+    ld = lambda t, nm: _rowmajor(t, nm) if t is not None else 0  # noqa: E731
+    _check(lib().gcn_layernorm_bwd(n, F, Y.data_ptr(), _rowmajor(Y, "Y"), rstd.data_ptr(),
+                                   dY.data_ptr(), _rowmajor(dY, "dY"), ptr(dY2), ld(dY2, "dY2"),
+                                   ptr(mask), ld(mask, "mask"), dX.data_ptr(), _rowmajor(dX, "dX"),
+                                   _stream(stream)))
+    return dX
+
+
+def _sage_shapes(g, X, params):
+    _dev(X, torch.float32, "X")
+    if len(params) != 9:
+        raise ValueError("params holds 9 tensors")
+    for k, t in enumerate(params):
+        _dev(t, torch.float32, "params[%d]" % k)
+        if not t.is_contiguous():
+            raise ValueError("params[%d] must be contiguous" % k)
+    f_in, hidden = params[0].shape
+    n_classes = params[6].shape[1]
+    shapes = [(f_in, hidden), (f_in, hidden), (hidden,), (hidden, hidden), (hidden, hidden),
+              (hidden,), (hidden, n_classes), (hidden, n_classes), (n_classes,)]
+    if [tuple(t.shape) for t in params] != shapes:
+        raise ValueError("parameter shapes must be %s" % shapes)
+    if X.shape != (g.n_rows, f_in):
+        raise ValueError("X must be [n x f_in]")
+    return f_in, hidden, n_classes
+
+
+def gcn_sage3_forward(g: Graph, X: torch.Tensor, params, labels=None, lp_mask=None, E=None,
+                      eps: float = 1e-5, stream=None):
+    """(H1, H2, logits) of the 3-layer GraphSAGE model (the step's forward pass)."""
+    f_in, hidden, n_classes = _sage_shapes(g, X, params)
+    if lp_mask is not None:
+        _dev(lp_mask, torch.uint8, "lp_mask")
+        _dev(E, torch.float32, "E")
+        _dev(labels, torch.int32, "labels")
+    n = g.n_rows
+    H1 = torch.empty((n, hidden), dtype=torch.float32, device=X.device)
+    H2 = torch.empty_like(H1)
+    logits = torch.empty((n, n_classes), dtype=torch.float32, device=X.device)
+    pa = (ctypes.c_void_p * 9)(*[t.data_ptr() for t in params])
+    ptr = lambda t: t.data_ptr() if t is not None else None  # noqa: E731
+    _check(lib().gcn_sage3_forward(g.handle, X.data_ptr(), _rowmajor(X, "X"), f_in, hidden,
+                                   n_classes, pa, ptr(labels), ptr(lp_mask), ptr(E), eps,
+                                   H1.data_ptr(), hidden, H2.data_ptr(), hidden, logits.data_ptr(),
+                                   n_classes, _stream(stream)))
+    return H1, H2, logits
+
+
+def gcn_sage3_step(g: Graph, X: torch.Tensor, params, labels: torch.Tensor, lp_mask=None, E=None,
+                   eps: float = 1e-5, stream=None):
+    """(loss, grads, dE) of one step of the 3-layer GraphSAGE model.
+
+    params: [W_self1, W_neigh1, b1, W_self2, W_neigh2, b2, W_self3, W_neigh3, b3]."""
+    f_in, hidden, n_classes = _sage_shapes(g, X, params)
+    _dev(labels, torch.int32, "labels")
+    if labels.numel() != g.n_rows:
+        raise ValueError("labels must have n entries")
+    grads = [torch.empty_like(t) for t in params]
+    dE = None
+    if lp_mask is not None:
+        _dev(lp_mask, torch.uint8, "lp_mask")
+        _dev(E, torch.float32, "E")
+        if tuple(E.shape) != (n_classes, f_in) or not E.is_contiguous():
+            raise ValueError("E must be contiguous [n_classes x f_in]")
+        dE = torch.empty_like(E)
+    loss = torch.empty((), dtype=torch.float64, device=X.device)
+    pa = (ctypes.c_void_p * 9)(*[t.data_ptr() for t in params])
+    ga = (ctypes.c_void_p * 9)(*[t.data_ptr() for t in grads])
+    _check(lib().gcn_sage3_step(g.handle, X.data_ptr(), _rowmajor(X, "X"), f_in, hidden, n_classes,
+                                pa, labels.data_ptr(),
+                                lp_mask.data_ptr() if lp_mask is not None else None,
+                                E.data_ptr() if E is not None else None, eps, ga,
+                                dE.data_ptr() if dE is not None else None, loss.data_ptr(),
+                                _stream(stream)))
+    return loss, grads, dE
 
 
 def gcn_graph_info(g: Graph):
