@@ -57,7 +57,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="rmat24_q8",
                     choices=["rmat24_q8", "rmat24", "rmat20", "er4096", "product", "partition",
-                             "gcn_step", "prepost", "producer"])
+                             "gcn_step", "sage_step", "prepost", "producer"])
     ap.add_argument("--halo-bits", type=int, default=8, choices=[8, 2],
                     help="code width of the halo rows (8: one byte per feature; 2: four per byte)")
     ap.add_argument("--senders", type=int, default=7,
@@ -169,6 +169,80 @@ def run_gcn_step(args):
                                              / FP32_MFMA_PEAK_TFLOPS, 4),
         "kernels_ms_per_step": {k: round(v[1] / ps, 4) for k, v in prof.items()},
         "roofline": {"bound": "hbm", "kernel": "aggregation (4 passes)",
+                     "achieved": round(agg_bytes / (agg_ms * 1e-3) / 1e9, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(agg_bytes / (agg_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": None},
+    }
+    print(json.dumps(out_json), flush=True)
+
+
+def run_sage_step(args):
+    """One training step of the 3-layer GraphSAGE model of the evaluation
+    (LayerNorm before each layer, mean aggregation, F_in 100, hidden 256, 47
+    classes) on the product-shaped graph without self-loops, with the labels
+    of half of the nodes embedded (masked label propagation)."""
+    import torch
+    import synth
+    import paper_2411_16025_amd as G
+
+    dev = torch.device("cuda:0")
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    w = synth.product_like()
+    n, f_in, hidden, C = w.n_rows, 100, 256, 47
+    g = G.gcn_build_csr(n, n, d(w.src), d(w.dst), synth.SYMMETRIZE)
+    G.gcn_normalize_mean(g)
+    X = d(synth.normal(3003, n, f_in))
+    params = []
+    for k, (a, b) in enumerate([(f_in, hidden), (hidden, hidden), (hidden, C)]):
+        params += [d(synth.glorot(5003 + 3 * k, a, b)), d(synth.glorot(5004 + 3 * k, a, b)),
+                   d(0.1 * synth.uniform(5005 + 3 * k, 1, b)[0])]
+    y = d(synth.labels(5203, n, C))
+    mask = d((synth.uniform(5204, n, 1)[:, 0] < 0.0).astype(np.uint8))
+    E = d(0.5 * synth.normal(5205, C, f_in))
+    step = lambda: G.gcn_sage3_step(g, X, params, y, mask, E)  # noqa: E731
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ts = time.time()
+    for _ in range(args.steps):
+        out = step()
+    torch.cuda.synchronize()
+    step_ms = (time.time() - ts) * 1e3 / args.steps
+    G.gcn_profile_enable(True)
+    for _ in range(max(1, args.profile_steps)):
+        step()
+    torch.cuda.synchronize()
+    prof = G.gcn_profile_read()
+    G.gcn_profile_enable(False)
+    ps = max(1, args.profile_steps)
+    dims = [(f_in, hidden), (hidden, hidden), (hidden, C)]
+    # algorithmic flops: Y W_self + Z W_neigh (forward), the weight gradients,
+    # and the input gradients of all three layers (label propagation needs layer 1's)
+    flop = sum(2 * n * 2 * f * fo * 3 for f, fo in dims)
+    gemm_ms = sum(v[1] for k, v in prof.items() if k.startswith("gemm")) / ps
+    agg_ms = sum(v[1] for k, v in prof.items() if k.startswith("agg")) / ps
+    bins = G.gcn_graph_bins(g, 0)
+    rows = sum(b["rows"] for b in bins)
+    ents = sum(b["entries"] for b in bins)
+    agg_bytes = 2 * sum(model_bytes(rows, ents, 0, f) for f, _ in dims)  # forward + transposed
+    out_json = {
+        "metric": "3-layer GraphSAGE training step (fwd + bwd, LayerNorm, masked label "
+                  "propagation), product-shaped graph",
+        "value": round(step_ms, 3), "unit": "ms", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(step_ms, 3), "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name + "_sage3", "nodes": n, "nnz": g.nnz, "f_in": f_in,
+                   "hidden": hidden, "classes": C, "lp_fraction": 0.5},
+        "loss": float(out[0]),
+        "aggregation_ms_per_step": round(agg_ms, 3),
+        "aggregation_modeled_GBps": round(agg_bytes / (agg_ms * 1e-3) / 1e9, 1),
+        "gemm_ms_per_step": round(gemm_ms, 3),
+        "gemm_TFLOPs": round(flop / (gemm_ms * 1e-3) / 1e12, 2),
+        "gemm_frac_of_fp32_mfma_peak": round(flop / (gemm_ms * 1e-3) / 1e12
+                                             / FP32_MFMA_PEAK_TFLOPS, 4),
+        "kernels_ms_per_step": {k: round(v[1] / ps, 4) for k, v in prof.items()},
+        "roofline": {"bound": "hbm", "kernel": "aggregation (6 passes)",
                      "achieved": round(agg_bytes / (agg_ms * 1e-3) / 1e9, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(agg_bytes / (agg_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
@@ -341,6 +415,9 @@ def main():
         return
     if args.workload == "prepost":
         run_prepost(args)
+        return
+    if args.workload == "sage_step":
+        run_sage_step(args)
         return
     if args.workload == "producer":
         run_producer(args)

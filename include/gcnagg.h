@@ -273,7 +273,7 @@ gcn_status gcn_sage3_forward(const gcn_graph* g, const float* X, int64_t ldx, in
                              float* logits, int64_t ldl, void* stream);
 
 /* One training step (forward, loss, backward) of the 3-layer GraphSAGE model
- * of the evaluation (Section 8, Table 2), with optional masked label
+ * of the evaluation (Section 8.1, Table 2), with optional masked label
  * propagation (Section 6.1 step 1, Lemma 2). Layer l (l = 1, 2, 3):
  *   Y = LayerNorm(H) (as gcn_layernorm_fwd), Z = A Y with the graph's values
  *   (after gcn_normalize_mean: the neighbour mean), O = Y W_self + Z W_neigh + b,

@@ -1,5 +1,5 @@
 // One training step of the 3-layer GraphSAGE model the paper evaluates
-// (Section 8, Table 2: LayerNorm before each layer, mean aggregation), with
+// (Section 8.1, Table 2: LayerNorm before each layer, mean aggregation), with
 // optional masked label propagation (Section 6.1 step 1, Lemma 2), built from
 // the library's kernels on the caller's stream without host synchronization.
 //
