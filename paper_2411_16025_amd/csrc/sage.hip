@@ -5,12 +5,17 @@
 //
 // Layer l reads H (n x f), and writes the row-major concatenation
 //   C = [ LayerNorm(H) | D^-1 A LayerNorm(H) | 1 | 0 0 0 ]
-// (each block padded to a multiple of 4 columns), so that the layer's UPDATE
+// so that the layer's UPDATE
 //   O = Y W_self + Z W_neigh + b
 // is one MFMA product C Wp with the packed weights Wp = [W_self; W_neigh; b; 0].
 // The aggregation writes straight into the middle block through its row
 // stride; the ones column carries the bias, and the weight gradient of the
-// same product yields dW_self, dW_neigh and db together.
+// same product yields dW_self, dW_neigh and db together. Column layout of a
+// row: Y in [0, f), Z in [zo, zo + f), the ones column at oc, zero padding up
+// to K (the GEMMs' inner size); rows are ldc >= K floats apart. Wide layers
+// (f >= 128) start Z on a 128-byte boundary and every row is a multiple of
+// 128 bytes, so the gathered rows of the aggregations touch no extra cache
+// line (a 516-float stride costs 28% at f = 256).
 
 #include "common.h"
 
@@ -21,52 +26,52 @@ constexpr int kThreadsS = 256;
 
 inline int64_t round4(int64_t v) { return (v + 3) & ~int64_t(3); }
 
-// Columns of C that no kernel of the layer writes: the padding after each
-// f-wide block, the ones column and the three zero columns after it.
-__global__ __launch_bounds__(kThreadsS) void k_concat_tail(int64_t n, int64_t f, int64_t fp,
+// Columns of C below K that no kernel of the layer writes: [f, zo),
+// [zo + f, oc), the ones column oc and (oc, K).
+__global__ __launch_bounds__(kThreadsS) void k_concat_tail(int64_t n, int64_t f, int64_t zo,
+                                                           int64_t oc, int64_t K,
                                                            float* __restrict__ c, int64_t ldc) {
-  const int64_t pad = fp - f;
-  const int64_t per_row = 2 * pad + 4;
+  const int64_t a = zo - f, b = oc - zo - f;  // the two padding runs
+  const int64_t per_row = K - 2 * f;
   const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
   if (t >= n * per_row) return;
   const int64_t i = t / per_row, k = t % per_row;
   int64_t col;
-  if (k < pad)
+  if (k < a)
     col = f + k;
-  else if (k < 2 * pad)
-    col = fp + f + (k - pad);
+  else if (k < a + b)
+    col = zo + f + (k - a);
   else
-    col = 2 * fp + (k - 2 * pad);
-  c[i * ldc + col] = (col == 2 * fp) ? 1.f : 0.f;
+    col = oc + (k - a - b);
+  c[i * ldc + col] = (col == oc) ? 1.f : 0.f;
 }
 
-// Wp [(2 fp + 4) x fop]: rows [0, f) = W_self, [fp, fp + f) = W_neigh,
-// row 2 fp = b, every other entry 0 (fo columns used of fop).
-__global__ __launch_bounds__(kThreadsS) void k_pack_weights(int64_t f, int64_t fp, int64_t fo,
-                                                            int64_t fop,
+// Wp [K x fop]: rows [0, f) = W_self, [zo, zo + f) = W_neigh, row oc = b,
+// every other entry 0 (fo columns used of fop).
+__global__ __launch_bounds__(kThreadsS) void k_pack_weights(int64_t f, int64_t zo, int64_t oc,
+                                                            int64_t K, int64_t fo, int64_t fop,
                                                             const float* __restrict__ ws,
                                                             const float* __restrict__ wn,
                                                             const float* __restrict__ b,
                                                             float* __restrict__ wp) {
   const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
-  const int64_t rows = 2 * fp + 4;
-  if (t >= rows * fop) return;
+  if (t >= K * fop) return;
   const int64_t r = t / fop, c = t % fop;
   float v = 0.f;
   if (c < fo) {
     if (r < f)
       v = ws[r * fo + c];
-    else if (r >= fp && r < fp + f)
-      v = wn[(r - fp) * fo + c];
-    else if (r == 2 * fp)
+    else if (r >= zo && r < zo + f)
+      v = wn[(r - zo) * fo + c];
+    else if (r == oc)
       v = b[c];
   }
   wp[t] = v;
 }
 
 // The inverse of k_pack_weights for the gradient.
-__global__ __launch_bounds__(kThreadsS) void k_unpack_grads(int64_t f, int64_t fp, int64_t fo,
-                                                            int64_t fop,
+__global__ __launch_bounds__(kThreadsS) void k_unpack_grads(int64_t f, int64_t zo, int64_t oc,
+                                                            int64_t fo, int64_t fop,
                                                             const float* __restrict__ dwp,
                                                             float* __restrict__ dws,
                                                             float* __restrict__ dwn,
@@ -77,9 +82,9 @@ __global__ __launch_bounds__(kThreadsS) void k_unpack_grads(int64_t f, int64_t f
   if (r < f)
     dws[r * fo + c] = dwp[r * fop + c];
   else if (r < 2 * f)
-    dwn[(r - f) * fo + c] = dwp[(fp + r - f) * fop + c];
+    dwn[(r - f) * fo + c] = dwp[(zo + r - f) * fop + c];
   else
-    db[c] = dwp[2 * fp * fop + c];
+    db[c] = dwp[oc * fop + c];
 }
 
 // Masked label propagation, forward: Xp = X + E[y] on rows with mask = 1.
@@ -137,12 +142,25 @@ inline unsigned blocks(int64_t work) {
 
 // Buffers of one layer.
 struct Layer {
-  int64_t f = 0, fp = 0, fo = 0, fop = 0, ldc = 0;
+  int64_t f = 0, fp = 0, zo = 0, oc = 0, K = 0, ldc = 0, fo = 0, fop = 0;
   float* c = nullptr;     // [n x ldc] = [Y | Z | 1 000]
   float* rstd = nullptr;  // [n]
-  float* wp = nullptr;    // [ldc x fop]
+  float* wp = nullptr;    // [K x fop]
   float* o = nullptr;     // [n x fop] pre-activation; after ReLU the layer output
 };
+
+inline int64_t round32(int64_t v) { return (v + 31) & ~int64_t(31); }
+
+void set_layout(Layer& y, int64_t f, int64_t fo) {
+  y.f = f;
+  y.fp = round4(f);
+  y.zo = f >= 128 ? round32(f) : y.fp;
+  y.oc = y.zo + y.fp;
+  y.K = y.oc + 4;
+  y.ldc = round32(y.K);
+  y.fo = fo;
+  y.fop = round4(fo);
+}
 
 struct Sage {
   int64_t n = 0;
@@ -197,18 +215,12 @@ gcn_status sage_forward(const gcn_graph* g, const float* X, int64_t ldx, int64_t
   m.n = n;
   Layer* L = m.L;
   const int64_t dims[4] = {f_in, hidden, hidden, n_classes};
-  for (int l = 0; l < 3; ++l) {
-    L[l].f = dims[l];
-    L[l].fp = round4(dims[l]);
-    L[l].fo = dims[l + 1];
-    L[l].fop = round4(dims[l + 1]);
-    L[l].ldc = 2 * L[l].fp + 4;
-  }
+  for (int l = 0; l < 3; ++l) set_layout(L[l], dims[l], dims[l + 1]);
   gcn_status st = GCN_OK;
   for (int l = 0; l < 3 && st == GCN_OK; ++l) {
     st = talloc(&L[l].c, n * L[l].ldc, s, "concatenated layer input");
     if (st == GCN_OK) st = talloc(&L[l].rstd, n, s, "LayerNorm 1/std");
-    if (st == GCN_OK) st = talloc(&L[l].wp, L[l].ldc * L[l].fop, s, "packed weights");
+    if (st == GCN_OK) st = talloc(&L[l].wp, L[l].K * L[l].fop, s, "packed weights");
     if (st == GCN_OK) st = talloc(&L[l].o, n * L[l].fop, s, "layer output");
   }
   if (st == GCN_OK && lp_mask) st = talloc(&m.xp, n * L[0].fp, s, "input with label embeddings");
@@ -216,11 +228,12 @@ gcn_status sage_forward(const gcn_graph* g, const float* X, int64_t ldx, int64_t
   // packed weights and the constant columns of each C
   for (int l = 0; l < 3; ++l) {
     Layer& y = L[l];
-    hipLaunchKernelGGL(k_pack_weights, dim3(blocks(y.ldc * y.fop)), dim3(kThreadsS), 0, s, y.f,
-                       y.fp, y.fo, y.fop, params[3 * l], params[3 * l + 1], params[3 * l + 2], y.wp);
+    hipLaunchKernelGGL(k_pack_weights, dim3(blocks(y.K * y.fop)), dim3(kThreadsS), 0, s, y.f,
+                       y.zo, y.oc, y.K, y.fo, y.fop, params[3 * l], params[3 * l + 1],
+                       params[3 * l + 2], y.wp);
     GCN_HIP(hipGetLastError());
-    hipLaunchKernelGGL(k_concat_tail, dim3(blocks(n * (2 * (y.fp - y.f) + 4))), dim3(kThreadsS),
-                       0, s, n, y.f, y.fp, y.c, y.ldc);
+    hipLaunchKernelGGL(k_concat_tail, dim3(blocks(n * (y.K - 2 * y.f))), dim3(kThreadsS), 0, s, n,
+                       y.f, y.zo, y.oc, y.K, y.c, y.ldc);
     GCN_HIP(hipGetLastError());
   }
   const float* h = X;
@@ -235,8 +248,8 @@ gcn_status sage_forward(const gcn_graph* g, const float* X, int64_t ldx, int64_t
   for (int l = 0; l < 3; ++l) {
     Layer& y = L[l];
     GCN_CHECK(layernorm_fwd(n, y.f, h, ldh, eps, y.c, y.ldc, y.rstd, s));
-    GCN_CHECK(aggregate_f32(g->csr, y.c, y.ldc, y.c + y.fp, y.ldc, y.f, false, s));
-    GCN_CHECK(gemm_f32(GCN_GEMM_NN, n, y.fop, y.ldc, y.c, y.ldc, y.wp, y.fop, y.o, y.fop, s));
+    GCN_CHECK(aggregate_f32(g->csr, y.c, y.ldc, y.c + y.zo, y.ldc, y.f, false, s));
+    GCN_CHECK(gemm_f32(GCN_GEMM_NN, n, y.fop, y.K, y.c, y.ldc, y.wp, y.fop, y.o, y.fop, s));
     if (l < 2) GCN_CHECK(relu_fwd(n, y.fo, y.o, y.fop, s));
     h = y.o;
     ldh = y.fop;
@@ -255,7 +268,7 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
   const int64_t ld_dc = std::max(std::max(L[0].ldc, L[1].ldc), L[2].ldc);
   const int64_t ld_t = std::max(L[0].fp, L[1].fp);
   int64_t w_max = 0;
-  for (int l = 0; l < 3; ++l) w_max = std::max(w_max, L[l].ldc * L[l].fop);
+  for (int l = 0; l < 3; ++l) w_max = std::max(w_max, L[l].K * L[l].fop);
   gcn_status st = talloc(&dlogits, n * L[2].fop, s, "dlogits");
   if (st == GCN_OK) st = talloc(&dc, n * ld_dc, s, "dC");
   if (st == GCN_OK) st = talloc(&t, n * ld_t, s, "transposed aggregation");
@@ -266,11 +279,13 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
   int64_t ld_do = L[2].fop;
   for (int l = 2; l >= 0 && st == GCN_OK; --l) {
     Layer& y = L[l];
-    st = gemm_f32(GCN_GEMM_TN, y.ldc, y.fop, n, y.c, y.ldc, dO, ld_do, dwp, y.fop, s);
+    // only the fo real columns of dO enter the products: the padding columns of
+    // the logits gradient are never written
+    st = gemm_f32(GCN_GEMM_TN, y.K, y.fo, n, y.c, y.ldc, dO, ld_do, dwp, y.fop, s);
     if (st != GCN_OK) break;
     hipLaunchKernelGGL(k_unpack_grads, dim3(blocks((2 * y.f + 1) * y.fo)), dim3(kThreadsS), 0, s,
-                       y.f, y.fp, y.fo, y.fop, (const float*)dwp, grads[3 * l], grads[3 * l + 1],
-                       grads[3 * l + 2]);
+                       y.f, y.zo, y.oc, y.fo, y.fop, (const float*)dwp, grads[3 * l],
+                       grads[3 * l + 1], grads[3 * l + 2]);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) {
       st = hip_fail(e, "k_unpack_grads", __FILE__, __LINE__);
@@ -279,8 +294,8 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
     if (l == 0 && !lp_mask) break;
     // dC = dO Wp^T; the input gradient of the layer is
     // dY = dC[:, Y block] + A^T dC[:, Z block], then the LayerNorm backward
-    st = gemm_f32(GCN_GEMM_NT, n, y.ldc, y.fop, dO, ld_do, y.wp, y.fop, dc, y.ldc, s);
-    if (st == GCN_OK) st = aggregate_f32(g->csc, dc + y.fp, y.ldc, t, y.fp, y.f, false, s);
+    st = gemm_f32(GCN_GEMM_NT, n, y.K, y.fo, dO, ld_do, y.wp, y.fop, dc, y.ldc, s);
+    if (st == GCN_OK) st = aggregate_f32(g->csc, dc + y.zo, y.ldc, t, y.fp, y.f, false, s);
     if (st != GCN_OK) break;
     if (l > 0) {
       // the gradient of the layer below, masked by its ReLU, overwrites its output
