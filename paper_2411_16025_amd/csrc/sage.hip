@@ -136,6 +136,51 @@ __global__ __launch_bounds__(kThreadsS) void k_embed_grad_reduce(int64_t nb, int
   de[t] = s;
 }
 
+// Column sums of dO (the bias gradient) in a fixed order: workgroup b adds
+// rows [b R, (b + 1) R) in row order (thread = column, eight rows loaded
+// ahead of the additions), then k_colsum_reduce runs one workgroup per
+// column: thread t adds the partials t, t + 256, ... in turn, and a fixed
+// tree combines the 256 sums.
+constexpr int kColsumRows = 1024;
+constexpr int kColsumAhead = 8;
+
+__global__ __launch_bounds__(kThreadsS) void k_colsum_partial(int64_t n, int64_t N,
+                                                              const float* __restrict__ d,
+                                                              int64_t ld,
+                                                              float* __restrict__ part) {
+  const int64_t c = (int64_t)blockIdx.y * kThreadsS + threadIdx.x;
+  if (c >= N) return;
+  const int64_t i0 = (int64_t)blockIdx.x * kColsumRows;
+  const int64_t i1 = std::min(n, i0 + kColsumRows);
+  float s = 0.f;
+  int64_t i = i0;
+  for (; i + kColsumAhead <= i1; i += kColsumAhead) {
+    float v[kColsumAhead];
+#pragma unroll
+    for (int k = 0; k < kColsumAhead; ++k) v[k] = d[(i + k) * ld + c];
+#pragma unroll
+    for (int k = 0; k < kColsumAhead; ++k) s += v[k];
+  }
+  for (; i < i1; ++i) s += d[i * ld + c];
+  part[(int64_t)blockIdx.x * N + c] = s;
+}
+
+__global__ __launch_bounds__(kThreadsS) void k_colsum_reduce(int64_t nb, int64_t N,
+                                                             const float* __restrict__ part,
+                                                             float* __restrict__ out) {
+  __shared__ float red[kThreadsS];
+  const int64_t c = blockIdx.x;
+  float s = 0.f;
+  for (int64_t b = threadIdx.x; b < nb; b += kThreadsS) s += part[b * N + c];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int off = kThreadsS / 2; off > 0; off >>= 1) {
+    if ((int)threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[c] = red[0];
+}
+
 inline unsigned blocks(int64_t work) {
   return (unsigned)std::max<int64_t>(1, ceil_div(work, kThreadsS));
 }
@@ -265,6 +310,8 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
   const int C = (int)n_classes;
   Layer* L = m.L;
   float *dlogits = nullptr, *dc = nullptr, *t = nullptr, *dwp = nullptr, *part = nullptr;
+  float* colpart = nullptr;
+  const int64_t n_colsum = std::max<int64_t>(1, ceil_div(n, kColsumRows));
   const int64_t ld_dc = std::max(std::max(L[0].ldc, L[1].ldc), L[2].ldc);
   const int64_t ld_t = std::max(L[0].fp, L[1].fp);
   int64_t w_max = 0;
@@ -274,15 +321,32 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
   if (st == GCN_OK) st = talloc(&t, n * ld_t, s, "transposed aggregation");
   if (st == GCN_OK) st = talloc(&dwp, w_max, s, "packed weight gradient");
   if (st == GCN_OK)
+    st = talloc(&colpart, n_colsum * std::max(L[1].fop, L[2].fop), s, "bias gradient partials");
+  if (st == GCN_OK)
     st = softmax_xent(n, C, L[2].o, L[2].fop, labels, dlogits, L[2].fop, loss, s, lp_mask);
   float* dO = dlogits;
   int64_t ld_do = L[2].fop;
   for (int l = 2; l >= 0 && st == GCN_OK; --l) {
     Layer& y = L[l];
     // only the fo real columns of dO enter the products: the padding columns of
-    // the logits gradient are never written
-    st = gemm_f32(GCN_GEMM_TN, y.K, y.fo, n, y.c, y.ldc, dO, ld_do, dwp, y.fop, s);
+    // the logits gradient are never written. The product covers rows [0, oc)
+    // of the packed gradient (the W blocks); the bias row oc is the column sum
+    // of dO, computed on its own so that a 2f + 4 row count does not cost a
+    // whole extra tile of the product.
+    st = gemm_f32(GCN_GEMM_TN, y.oc, y.fo, n, y.c, y.ldc, dO, ld_do, dwp, y.fop, s);
     if (st != GCN_OK) break;
+    {
+      ProfScope ps("bias_grad", s);
+      hipLaunchKernelGGL(k_colsum_partial,
+                         dim3((unsigned)n_colsum, (unsigned)ceil_div(y.fo, kThreadsS)),
+                         dim3(kThreadsS), 0, s, n, y.fo, (const float*)dO, ld_do, colpart);
+      hipLaunchKernelGGL(k_colsum_reduce, dim3((unsigned)y.fo), dim3(kThreadsS), 0, s, n_colsum,
+                         y.fo, (const float*)colpart, dwp + y.oc * y.fop);
+    }
+    if (hipGetLastError() != hipSuccess) {
+      st = hip_fail(hipErrorLaunchFailure, "bias gradient", __FILE__, __LINE__);
+      break;
+    }
     hipLaunchKernelGGL(k_unpack_grads, dim3(blocks((2 * y.f + 1) * y.fo)), dim3(kThreadsS), 0, s,
                        y.f, y.zo, y.oc, y.fo, y.fop, (const float*)dwp, grads[3 * l],
                        grads[3 * l + 1], grads[3 * l + 2]);
@@ -294,7 +358,8 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
     if (l == 0 && !lp_mask) break;
     // dC = dO Wp^T; the input gradient of the layer is
     // dY = dC[:, Y block] + A^T dC[:, Z block], then the LayerNorm backward
-    st = gemm_f32(GCN_GEMM_NT, n, y.K, y.fo, dO, ld_do, y.wp, y.fop, dc, y.ldc, s);
+    // dC over the Y and Z blocks only (the ones and padding columns are not read)
+    st = gemm_f32(GCN_GEMM_NT, n, y.zo + y.f, y.fo, dO, ld_do, y.wp, y.fop, dc, y.ldc, s);
     if (st == GCN_OK) st = aggregate_f32(g->csc, dc + y.zo, y.ldc, t, y.fp, y.f, false, s);
     if (st != GCN_OK) break;
     if (l > 0) {
@@ -326,6 +391,7 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
     }
   }
   tfree(part, s);
+  tfree(colpart, s);
   tfree(dwp, s);
   tfree(t, s);
   tfree(dc, s);
