@@ -217,6 +217,17 @@ __device__ inline void store_row(float* __restrict__ y, int f0, int F, const flo
 #ifndef GCN_GROUP_UNROLL
 #define GCN_GROUP_UNROLL 1
 #endif
+// Gathers in flight per lane in the one-wavefront-per-row kernel.
+#ifndef GCN_MEDIUM_UNROLL
+#define GCN_MEDIUM_UNROLL GCN_AGG_UNROLL
+#endif
+// Row groups per wavefront of the one-entry and two-entry row kernels.
+#ifndef GCN_TINY_GROUPS1
+#define GCN_TINY_GROUPS1 4
+#endif
+#ifndef GCN_TINY_GROUPS2
+#define GCN_TINY_GROUPS2 2
+#endif
 // Waves per SIMD the entry-loop kernels must fit (caps their registers).
 #ifndef GCN_MIN_WAVES
 #define GCN_MIN_WAVES 8
@@ -323,6 +334,63 @@ __global__ __launch_bounds__(kBlock) void k_zero_rows(const int32_t* __restrict_
   store_row<VEC>(y + (int64_t)rows[i] * ldy, f0, F, z);
 }
 
+// Rows with exactly L entries (L = 1 or 2): one row per slot and R groups of
+// E rows per wavefront, every load of the R groups issued before any
+// arithmetic. Such rows have no other work to hide their chain of dependent
+// loads (row id, row start, entries, feature rows) behind, so the wavefront
+// keeps R * L gathers per lane in flight instead of L. The terms of a row are
+// added in entry order, as in k_short.
+template <int VEC, int G, class Src, bool RELU, int L, int R>
+__global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_tiny(const int64_t* __restrict__ ptr,
+                                                  const Ent* __restrict__ ent,
+                                                  const int32_t* __restrict__ rows, int64_t n,
+                                                  Src src, float* __restrict__ y, int64_t ldy,
+                                                  int F) {
+  constexpr int E = 64 / G;
+  const int lane = threadIdx.x & 63;
+  const int slot = lane / G;
+  const int64_t wave = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+  const int f0 = (int)blockIdx.y * G * VEC + (lane % G) * VEC;
+  const bool fa = f0 < F;
+  int32_t r[R];
+  bool has[R];
+#pragma unroll
+  for (int g = 0; g < R; ++g) {
+    const int64_t i = (wave * R + g) * E + slot;
+    has[g] = i < n;
+    r[g] = has[g] ? rows[i] : 0;
+  }
+  int64_t b[R];
+#pragma unroll
+  for (int g = 0; g < R; ++g) b[g] = has[g] ? ptr[r[g]] : 0;
+  Ent e[R][L];
+#pragma unroll
+  for (int g = 0; g < R; ++g)
+#pragma unroll
+    for (int k = 0; k < L; ++k) e[g][k] = has[g] ? load_ent(ent + b[g] + k) : Ent{0, 0.f};
+  typename Src::Raw raw[R][L];
+#pragma unroll
+  for (int g = 0; g < R; ++g)
+#pragma unroll
+    for (int k = 0; k < L; ++k)
+      if (has[g] && fa) src.fetch(e[g][k].col, f0, raw[g][k]);
+#pragma unroll
+  for (int g = 0; g < R; ++g) {
+    if (!(has[g] && fa)) continue;
+    float acc[VEC];
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
+#pragma unroll
+    for (int k = 0; k < L; ++k) {
+      float xv[VEC];
+      src.decode(raw[g][k], e[g][k].col, xv);
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) acc[v] = __builtin_fmaf(e[g][k].val, xv[v], acc[v]);
+    }
+    store_row<VEC, RELU>(y + (int64_t)r[g] * ldy, f0, F, acc);
+  }
+}
+
 // Rows with 1..32 entries: one row per slot, E rows per wavefront, the rows
 // of one wavefront from one length class. The G lanes of a slot load the
 // row's (column, value) pairs with one coalesced access and share them by
@@ -408,7 +476,7 @@ __global__ __launch_bounds__(kBlock) void k_medium(const int64_t* __restrict__ p
   float acc[VEC];
 #pragma unroll
   for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
-  accumulate_blocks<VEC, G, GCN_AGG_UNROLL>(ent, b, e, 0, 1, src, f0, active, acc);
+  accumulate_blocks<VEC, G, GCN_MEDIUM_UNROLL>(ent, b, e, 0, 1, src, f0, active, acc);
   reduce_slots<VEC, G>(acc);
   if (slot == 0 && active) store_row<VEC, RELU>(y + (int64_t)r * ldy, f0, F, acc);
 }
@@ -522,14 +590,37 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
                        n_empty, y, ldy, F);
     GCN_HIP(hipGetLastError());
   }
-  // short rows
+  // rows of exactly one and exactly two entries
+  {
+    const int64_t n1 = p.class_off[kFirstShort + 1] - p.class_off[kFirstShort];
+    const int64_t n2 = p.class_off[kFirstShort + 2] - p.class_off[kFirstShort + 1];
+    constexpr int R1 = GCN_TINY_GROUPS1, R2 = GCN_TINY_GROUPS2;
+    if (n1 > 0) {
+      ProfScope ps("agg_tiny", stream);
+      hipLaunchKernelGGL((k_tiny<VEC, G, Src, RELU, 1, R1>),
+                         dim3(blocks_for_waves(ceil_div(n1, E * R1)), tiles), dim3(kBlock), 0,
+                         stream, (const int64_t*)m.ptr, (const Ent*)m.ent,
+                         (const int32_t*)(p.rows + p.class_off[kFirstShort]), n1, src, y, ldy, F);
+      GCN_HIP(hipGetLastError());
+    }
+    if (n2 > 0) {
+      ProfScope ps("agg_tiny", stream);
+      hipLaunchKernelGGL((k_tiny<VEC, G, Src, RELU, 2, R2>),
+                         dim3(blocks_for_waves(ceil_div(n2, E * R2)), tiles), dim3(kBlock), 0,
+                         stream, (const int64_t*)m.ptr, (const Ent*)m.ent,
+                         (const int32_t*)(p.rows + p.class_off[kFirstShort + 1]), n2, src, y, ldy,
+                         F);
+      GCN_HIP(hipGetLastError());
+    }
+  }
+  // rows of 3..32 entries (the classes of one and two entries get no waves)
   ShortArgs sa;
   int64_t waves = 0;
   for (int c = kFirstShort; c <= kLastShort + 1; ++c) {
     sa.row_off[c - kFirstShort] = p.class_off[c];
     sa.wave_off[c - kFirstShort] = waves;
     if (c <= kLastShort) {
-      waves += ceil_div(p.class_off[c + 1] - p.class_off[c], E);
+      if (c >= kFirstShort + 2) waves += ceil_div(p.class_off[c + 1] - p.class_off[c], E);
       sa.len_hi[c - kFirstShort] = kClassHi[c];
     }
   }
