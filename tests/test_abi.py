@@ -99,3 +99,39 @@ def test_profile_toggle_without_launches(L):
     assert L.gcn_profile_read(None, None, None, 0, ctypes.byref(n)) == 0
     assert n.value == 0
     assert L.gcn_profile_enable(0) == 0
+
+
+def test_new_entry_points_reject_bad_arguments(L):
+    import ctypes
+    fake = ctypes.c_void_p(0x1000)
+    junk = (ctypes.c_uint64 * 64)()
+    jh = ctypes.cast(junk, ctypes.c_void_p)
+    # normalization variants
+    assert L.gcn_normalize_mean(None, None) == 1
+    assert L.gcn_normalize_mean(jh, None) == 5
+    assert L.gcn_normalize_rc(None, fake, fake, None) == 1
+    assert L.gcn_normalize_rc(jh, fake, fake, None) == 5
+    # LayerNorm forward / backward
+    assert L.gcn_layernorm_fwd(-1, 4, fake, 4, 1e-5, fake, 4, None, None) == 1
+    assert L.gcn_layernorm_fwd(4, 0, fake, 4, 1e-5, fake, 4, None, None) == 1
+    assert L.gcn_layernorm_fwd(4, 8, fake, 4, 1e-5, fake, 8, None, None) == 1  # ldx < F
+    assert L.gcn_layernorm_fwd(4, 8, None, 8, 1e-5, fake, 8, None, None) == 1
+    assert L.gcn_layernorm_fwd(4, 8, fake, 8, -1.0, fake, 8, None, None) == 1  # eps < 0
+    assert L.gcn_layernorm_fwd(0, 8, None, 8, 1e-5, None, 8, None, None) == 0  # no rows
+    assert L.gcn_layernorm_bwd(4, 8, fake, 8, None, fake, 8, None, 0, None, 0, fake, 8, None) == 1
+    assert L.gcn_layernorm_bwd(4, 8, fake, 8, fake, fake, 8, fake, 4, None, 0, fake, 8, None) == 1
+    assert L.gcn_layernorm_bwd(0, 8, None, 8, None, None, 8, None, 0, None, 0, None, 8, None) == 0
+    # GraphSAGE step and forward
+    params = (ctypes.c_void_p * 9)(*([0x1000] * 9))
+    grads = (ctypes.c_void_p * 9)(*([0x1000] * 9))
+    assert L.gcn_sage3_step(None, fake, 4, 4, 8, 3, params, fake, None, None, 1e-5, grads, None,
+                            fake, None) == 1
+    assert L.gcn_sage3_step(jh, fake, 4, 4, 8, 3, params, fake, None, None, 1e-5, grads, None,
+                            fake, None) == 5
+    assert L.gcn_sage3_forward(None, fake, 4, 4, 8, 3, params, None, None, None, 1e-5, None, 0,
+                               None, 0, None, 0, None) == 1
+    # combine of received partial sums
+    assert L.gcn_add_rows(0, 4, None, 4, None, 10, None, 4, None) == 0
+    assert L.gcn_add_rows(3, 0, fake, 4, fake, 10, fake, 4, None) == 1
+    assert L.gcn_add_rows(3, 8, fake, 4, fake, 10, fake, 8, None) == 1  # ldp < F
+    assert L.gcn_add_rows(3, 4, None, 4, fake, 10, fake, 4, None) == 1
