@@ -168,55 +168,93 @@ __device__ inline f4 load4(const float* __restrict__ p, int64_t row, int64_t row
 
 // Wide-tile C = A op(B) for 16-byte aligned operands: a 64 x BN tile per
 // 256-thread workgroup (BN up to 256, so the tall operand is read once per
-// BN columns), 16-byte global loads, 32-deep K slices in LDS.
+// BN columns), 32-deep K slices in LDS, software-pipelined: the next slice's
+// A and B tiles are loaded into registers while the current slice is
+// multiplied from LDS, so the loads' latency overlaps the matrix-core work.
+// B is kept k-major for NN and n-major for NT (both written with 16-byte
+// LDS stores). With mask, C = 0 where mask <= 0 (a ReLU backward).
+#ifndef GCN_GEMM_MIN_BLOCKS
+#define GCN_GEMM_MIN_BLOCKS 2
+#endif
+#ifndef GCN_GEMM_KK_UNROLL
+#define GCN_GEMM_KK_UNROLL 8
+#endif
+#define GCN_GEMM_PRAGMA(x) _Pragma(#x)
+#define GCN_GEMM_UNROLL(n) GCN_GEMM_PRAGMA(unroll n)
+
 template <int OP, int BN>
-__global__ __launch_bounds__(kThreads) void k_gemm_tall_v(int64_t M, int64_t N, int64_t K,
+__global__ __launch_bounds__(kThreads, GCN_GEMM_MIN_BLOCKS) void k_gemm_tall_v(int64_t M, int64_t N, int64_t K,
                                                           const float* __restrict__ A, int64_t lda,
                                                           const float* __restrict__ B, int64_t ldb,
                                                           float* __restrict__ C, int64_t ldc,
                                                           const float* __restrict__ mask,
                                                           int64_t ldm) {
   constexpr int NB = BN / 16;
+  constexpr int BL = BN / 32;  // 16-byte B loads per thread per slice
+  constexpr int BR = OP == kNN ? kKc : BN;
+  constexpr int BC = OP == kNN ? BN + 4 : kKc + 4;
   __shared__ __align__(16) float As[kTile][kKc + 4];
-  __shared__ __align__(16) float Bs[kKc][BN + 4];
+  __shared__ __align__(16) float Bs[BR][BC];
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int64_t m0 = (int64_t)blockIdx.x * kTile;
   const int64_t n0 = (int64_t)blockIdx.y * BN;
   f4 acc[NB];
 #pragma unroll
   for (int j = 0; j < NB; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
-  for (int64_t k0 = 0; k0 < K; k0 += kKc) {
+  f4 ra[2], rb[BL];
+  auto load_slice = [&](int64_t k0) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) {  // A: 64 x 32 = 512 float4
       const int idx = t + kThreads * j, r = idx >> 3, c = (idx & 7) * 4;
-      *reinterpret_cast<f4*>(&As[r][c]) = load4(A, m0 + r, M, lda, k0 + c, K);
+      ra[j] = load4(A, m0 + r, M, lda, k0 + c, K);
     }
-    if (OP == kNN) {  // B: 32 x BN
 #pragma unroll
-      for (int j = 0; j < BN / 32; ++j) {
-        const int idx = t + kThreads * j, r = idx / (BN / 4), c = (idx % (BN / 4)) * 4;
-        *reinterpret_cast<f4*>(&Bs[r][c]) = load4(B, k0 + r, K, ldb, n0 + c, N);
-      }
-    } else {  // B stored N x K: BN rows of 32 k, transposed into Bs
-#pragma unroll
-      for (int j = 0; j < BN / 32; ++j) {
-        const int idx = t + kThreads * j, r = idx >> 3, c = (idx & 7) * 4;
-        const f4 v = load4(B, n0 + r, N, ldb, k0 + c, K);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) Bs[c + e][r] = v[e];
+    for (int j = 0; j < BL; ++j) {
+      const int idx = t + kThreads * j;
+      if (OP == kNN) {  // B rows k0 .. k0 + 31, columns n0 .. n0 + BN - 1
+        const int r = idx / (BN / 4), c = (idx % (BN / 4)) * 4;
+        rb[j] = load4(B, k0 + r, K, ldb, n0 + c, N);
+      } else {  // B stored N x K: rows n0 .. n0 + BN - 1, columns k0 .. k0 + 31
+        const int r = idx >> 3, c = (idx & 7) * 4;
+        rb[j] = load4(B, n0 + r, N, ldb, k0 + c, K);
       }
     }
-    __syncthreads();
+  };
+  auto store_slice = [&]() {
 #pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int idx = t + kThreads * j, r = idx >> 3, c = (idx & 7) * 4;
+      *reinterpret_cast<f4*>(&As[r][c]) = ra[j];
+    }
+#pragma unroll
+    for (int j = 0; j < BL; ++j) {
+      const int idx = t + kThreads * j;
+      const int r = OP == kNN ? idx / (BN / 4) : idx >> 3;
+      const int c = OP == kNN ? (idx % (BN / 4)) * 4 : (idx & 7) * 4;
+      *reinterpret_cast<f4*>(&Bs[r][c]) = rb[j];
+    }
+  };
+  load_slice(0);
+  store_slice();
+  __syncthreads();
+  for (int64_t k0 = 0; k0 < K; k0 += kKc) {
+    const bool more = k0 + kKc < K;
+    if (more) load_slice(k0 + kKc);
+    GCN_GEMM_UNROLL(GCN_GEMM_KK_UNROLL)
     for (int kk = 0; kk < kKc; kk += 4) {
       const float a = As[16 * w + (lane & 15)][kk + (lane >> 4)];
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
-        const float b = Bs[kk + (lane >> 4)][16 * j + (lane & 15)];
+        const float b = OP == kNN ? Bs[kk + (lane >> 4)][16 * j + (lane & 15)]
+                                  : Bs[16 * j + (lane & 15)][kk + (lane >> 4)];
         acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[j], 0, 0, 0);
       }
     }
     __syncthreads();
+    if (more) {
+      store_slice();
+      __syncthreads();
+    }
   }
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
