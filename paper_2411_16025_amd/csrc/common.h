@@ -138,9 +138,10 @@ gcn_status scan_i64(const int64_t* in, int64_t* out, int64_t n, hipStream_t stre
 gcn_status aggregate_f32(const Mat& m, const float* X, int64_t ldx, float* Y, int64_t ldy,
                          int64_t F, bool relu, hipStream_t stream);
 // mask (optional, [M x N], ldm): C[i, j] = 0 where mask[i, j] <= 0 (NN and NT)
+// C = A op(B); with mask, C = 0 where mask <= 0; with relu, C = max(C, 0).
 gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
                     const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream,
-                    const float* mask = nullptr, int64_t ldm = 0);
+                    const float* mask = nullptr, int64_t ldm = 0, bool relu = false);
 gcn_status relu_fwd(int64_t n, int64_t F, float* H, int64_t ld, hipStream_t stream);
 gcn_status relu_bwd(int64_t n, int64_t F, const float* H, int64_t ldh, float* dH, int64_t ld,
                     hipStream_t stream);

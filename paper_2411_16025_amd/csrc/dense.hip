@@ -172,7 +172,8 @@ __device__ inline f4 load4(const float* __restrict__ p, int64_t row, int64_t row
 // A and B tiles are loaded into registers while the current slice is
 // multiplied from LDS, so the loads' latency overlaps the matrix-core work.
 // B is kept k-major for NN and n-major for NT (both written with 16-byte
-// LDS stores). With mask, C = 0 where mask <= 0 (a ReLU backward).
+// LDS stores). With mask, C = 0 where mask <= 0 (a ReLU backward); with
+// relu, C = max(C, 0) (a ReLU forward).
 #ifndef GCN_GEMM_MIN_BLOCKS
 #define GCN_GEMM_MIN_BLOCKS 2
 #endif
@@ -188,7 +189,7 @@ __global__ __launch_bounds__(kThreads, GCN_GEMM_MIN_BLOCKS) void k_gemm_tall_v(i
                                                           const float* __restrict__ B, int64_t ldb,
                                                           float* __restrict__ C, int64_t ldc,
                                                           const float* __restrict__ mask,
-                                                          int64_t ldm) {
+                                                          int64_t ldm, bool relu) {
   constexpr int NB = BN / 16;
   constexpr int BL = BN / 32;  // 16-byte B loads per thread per slice
   constexpr int BR = OP == kNN ? kKc : BN;
@@ -262,8 +263,11 @@ __global__ __launch_bounds__(kThreads, GCN_GEMM_MIN_BLOCKS) void k_gemm_tall_v(i
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int64_t gm = m0 + 16 * w + 4 * (lane >> 4) + i;
-      if (gm < M && gn < N)
-        C[gm * ldc + gn] = (mask && !(mask[gm * ldm + gn] > 0.f)) ? 0.f : acc[j][i];
+      if (gm < M && gn < N) {
+        float v = (mask && !(mask[gm * ldm + gn] > 0.f)) ? 0.f : acc[j][i];
+        if (relu) v = fmaxf(v, 0.f);
+        C[gm * ldc + gn] = v;
+      }
     }
   }
 }
@@ -452,18 +456,18 @@ int tile_n(int64_t N) { return N <= 64 ? 64 : (N <= 128 ? 128 : 256); }
 template <int OP>
 void launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
                  int64_t ldb, float* C, int64_t ldc, const float* mask, int64_t ldm,
-                 hipStream_t stream) {
+                 bool relu, hipStream_t stream) {
   const int bn = tile_n(N);
   const dim3 grid((unsigned)ceil_div(M, kTile), (unsigned)ceil_div(N, bn));
   if (bn == 64)
     hipLaunchKernelGGL((k_gemm_tall_v<OP, 64>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda, B,
-                       ldb, C, ldc, mask, ldm);
+                       ldb, C, ldc, mask, ldm, relu);
   else if (bn == 128)
     hipLaunchKernelGGL((k_gemm_tall_v<OP, 128>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda,
-                       B, ldb, C, ldc, mask, ldm);
+                       B, ldb, C, ldc, mask, ldm, relu);
   else
     hipLaunchKernelGGL((k_gemm_tall_v<OP, 256>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda,
-                       B, ldb, C, ldc, mask, ldm);
+                       B, ldb, C, ldc, mask, ldm, relu);
 }
 
 void launch_tn(int64_t M, int64_t N, int64_t K, int64_t split, int64_t n_chunks, const float* A,
@@ -486,7 +490,7 @@ void launch_tn(int64_t M, int64_t N, int64_t K, int64_t split, int64_t n_chunks,
 
 gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
                     const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream,
-                    const float* mask, int64_t ldm) {
+                    const float* mask, int64_t ldm, bool relu) {
   if (M == 0 || N == 0) return GCN_OK;
   const bool vec = aligned16(A, lda) && aligned16(B, ldb);
   if (op == GCN_GEMM_TN) {
@@ -518,14 +522,16 @@ gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int
       tfree(part, stream);
       if (e != hipSuccess) return hip_fail(e, "k_sum_partials", __FILE__, __LINE__);
     }
+    if (mask) GCN_CHECK(relu_bwd(M, N, mask, ldm, C, ldc, stream));
+    if (relu) GCN_CHECK(relu_fwd(M, N, C, ldc, stream));
     return GCN_OK;
   }
   const dim3 grid((unsigned)ceil_div(M, kTile), (unsigned)ceil_div(N, kTile));
   ProfScope ps(op == GCN_GEMM_NN ? "gemm_nn" : "gemm_nt", stream);
   if (vec && op == GCN_GEMM_NN)
-    launch_tall<kNN>(M, N, K, A, lda, B, ldb, C, ldc, mask, ldm, stream);
+    launch_tall<kNN>(M, N, K, A, lda, B, ldb, C, ldc, mask, ldm, relu, stream);
   else if (vec)
-    launch_tall<kNT>(M, N, K, A, lda, B, ldb, C, ldc, mask, ldm, stream);
+    launch_tall<kNT>(M, N, K, A, lda, B, ldb, C, ldc, mask, ldm, relu, stream);
   else if (op == GCN_GEMM_NN)
     hipLaunchKernelGGL(k_gemm_tall<kNN>, grid, dim3(kThreads), 0, stream, M, N, K, A, lda, B, ldb,
                        C, ldc);
@@ -533,7 +539,8 @@ gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int
     hipLaunchKernelGGL(k_gemm_tall<kNT>, grid, dim3(kThreads), 0, stream, M, N, K, A, lda, B, ldb,
                        C, ldc);
   GCN_HIP(hipGetLastError());
-  if (mask && !vec) return relu_bwd(M, N, mask, ldm, C, ldc, stream);
+  if (mask && !vec) GCN_CHECK(relu_bwd(M, N, mask, ldm, C, ldc, stream));
+  if (relu && !vec) GCN_CHECK(relu_fwd(M, N, C, ldc, stream));
   return GCN_OK;
 }
 

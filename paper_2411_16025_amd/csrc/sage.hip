@@ -294,8 +294,9 @@ gcn_status sage_forward(const gcn_graph* g, const float* X, int64_t ldx, int64_t
     Layer& y = L[l];
     GCN_CHECK(layernorm_fwd(n, y.f, h, ldh, eps, y.c, y.ldc, y.rstd, s));
     GCN_CHECK(aggregate_f32(g->csr, y.c, y.ldc, y.c + y.zo, y.ldc, y.f, false, s));
-    GCN_CHECK(gemm_f32(GCN_GEMM_NN, n, y.fop, y.K, y.c, y.ldc, y.wp, y.fop, y.o, y.fop, s));
-    if (l < 2) GCN_CHECK(relu_fwd(n, y.fo, y.o, y.fop, s));
+    // the ReLU of layers 1 and 2 is applied as the product is stored
+    GCN_CHECK(gemm_f32(GCN_GEMM_NN, n, y.fop, y.K, y.c, y.ldc, y.wp, y.fop, y.o, y.fop, s,
+                       nullptr, 0, l < 2));
     h = y.o;
     ldh = y.fop;
   }
