@@ -523,6 +523,7 @@ def main():
     # fwd / bwd split, HIP events on the stream the library launches on
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
     fwd_ms = bwd_ms = 0.0
+    per_step = []
     for _ in range(args.steps):
         ev[0].record()
         fwd()
@@ -532,6 +533,7 @@ def main():
         ev[2].synchronize()
         fwd_ms += ev[0].elapsed_time(ev[1]) / args.steps
         bwd_ms += ev[1].elapsed_time(ev[2]) / args.steps
+        per_step.append(ev[0].elapsed_time(ev[2]))
 
     # per-kernel durations (events around every launch, separate from the timed region)
     G.gcn_profile_enable(True)
@@ -553,6 +555,12 @@ def main():
 
     Bf, nnz_f, halo_f = pass_bytes(bins_f)
     Bb, nnz_b, _ = pass_bytes(bins_b)
+    # compulsory traffic of the step: CSR/CSC, each input row once, the outputs
+    def read_once(n_in):  # input rows [0, n_in) of one pass, halo rows quantized
+        n_loc = min(nlc, n_in) if q8 else n_in
+        return 4 * F * n_loc + (code_bytes(F, bits) + 8) * (n_in - n_loc)
+    compulsory = sum(8 * (r + 1) + 8 * e + 4 * F * r + read_once(n_in)
+                     for r, e, n_in in ((w.n_rows, nnz_f, w.n_cols), (w.n_cols, nnz_b, w.n_rows)))
     value = (Bf + Bb) / (step_ms * 1e-3) / 1e9
     ef_per_s = (nnz_f + nnz_b) * F / (step_ms * 1e-3)
 
@@ -587,6 +595,10 @@ def main():
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),
         "edge_features_per_s": float("%.4g" % ef_per_s),
         "fwd_ms": round(fwd_ms, 4), "bwd_ms": round(bwd_ms, 4),
+        "step_ms_median": round(float(np.median(per_step)), 4),
+        "step_ms_min": round(float(np.min(per_step)), 4),
+        # secondary: every input row read once (not reachable by a gather)
+        "compulsory_GBps": round(compulsory / (step_ms * 1e-3) / 1e9, 1),
         "modeled_bytes_per_step": int(Bf + Bb),
         "build_ms": round(build_ms, 1), "normalize_ms": round(norm_ms, 1),
         "kernels_ms_per_step": {k: round(v[1] / max(args.profile_steps, 1), 4)
@@ -635,7 +647,16 @@ def cpu_baseline(w, X_h, nlc, F, target_s, bits=8):
         n = int(min(w.n_rows, n * min(8.0, target_s / max(dt, 1e-3))))
         dt, rows, ents, halo = run(n)
     B = model_bytes(rows, ents, halo, F, bits)
+    cpu = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {"value": round(B / dt / 1e9, 3), "unit": "GB/s", "cores": oracle.num_threads(),
+            "cpu_model": cpu, "host_cpus": os.cpu_count(),
             "kind": "oracle", "edge_features_per_s": float("%.4g" % (ents * F / dt)),
             "seconds": round(dt, 2),
             "sample": "forward aggregation (fp64 accumulation%s) over %d uniformly sampled rows "
