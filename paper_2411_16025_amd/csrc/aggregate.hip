@@ -217,6 +217,11 @@ __device__ inline void store_row(float* __restrict__ y, int f0, int F, const flo
 #ifndef GCN_GROUP_UNROLL
 #define GCN_GROUP_UNROLL 1
 #endif
+// Medium rows (33 .. medium_max entries) run one per lane group in k_short (1)
+// or one per wavefront in k_medium (0).
+#ifndef GCN_MEDIUM_BY_SLOTS
+#define GCN_MEDIUM_BY_SLOTS 1
+#endif
 // Gathers in flight per lane in the one-wavefront-per-row kernel.
 #ifndef GCN_MEDIUM_UNROLL
 #define GCN_MEDIUM_UNROLL GCN_AGG_UNROLL
@@ -310,10 +315,13 @@ __device__ inline void reduce_slots(float* acc) {
   }
 }
 
+// Classes run one row per lane group by k_short: kFirstShort .. kMedium (the
+// one- and two-entry classes get no wavefronts there, and the medium class
+// only with GCN_MEDIUM_BY_SLOTS).
+constexpr int kSlotClasses = kMedium - kFirstShort + 1;
 struct ShortArgs {
-  int64_t row_off[kLastShort - kFirstShort + 2];   // rows of short class c start at row_off[c-1]
-  int64_t wave_off[kLastShort - kFirstShort + 2];  // first wavefront of each short class
-  int32_t len_hi[kLastShort - kFirstShort + 1];    // longest row of each short class
+  int64_t row_off[kSlotClasses + 1];   // rows of class kFirstShort + k start at row_off[k]
+  int64_t wave_off[kSlotClasses + 1];  // first wavefront of each class; [kSlotClasses] = total
 };
 
 // ---- kernels ---------------------------------------------------------------------
@@ -391,11 +399,13 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_tiny(const int64_t* _
   }
 }
 
-// Rows with 1..32 entries: one row per slot, E rows per wavefront, the rows
-// of one wavefront from one length class. The G lanes of a slot load the
-// row's (column, value) pairs with one coalesced access and share them by
-// lane shuffles; the loop bound is the class's longest row, so every lane
-// of the wavefront runs the same iterations.
+// Rows of 3 .. medium_max entries: one row per slot, E rows per wavefront, the
+// rows of one wavefront from one length class and, within it, of about the
+// same length (the plan orders them by decreasing length). The G lanes of a
+// slot load the row's (column, value) pairs G at a time with one coalesced
+// access (the next G travel with the current gathers) and share them by lane
+// shuffles; the loop bound is the wavefront's longest row, so every lane runs
+// the same iterations. A slot's terms are added in entry order.
 template <int VEC, int G, class Src, bool RELU>
 __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* __restrict__ ptr,
                                                   const Ent* __restrict__ ent,
@@ -403,7 +413,7 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* 
                                                   Src src, float* __restrict__ y, int64_t ldy,
                                                   int F) {
   constexpr int E = 64 / G;
-  constexpr int NS = kLastShort - kFirstShort + 1;
+  constexpr int NS = kSlotClasses;
   constexpr int U = 4;
   const int lane = threadIdx.x & 63;
   const int slot = lane / G, gl = lane % G;
@@ -428,10 +438,14 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* 
   float acc[VEC];
 #pragma unroll
   for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
-  const int hi = sa.len_hi[c];
+  int hi = len;  // the wavefront's longest row
+#pragma unroll
+  for (int off = G; off < 64; off <<= 1) hi = max(hi, __shfl_xor(hi, off, 64));
+  Ent me = {0, 0.f};
+  if (gl < len) me = load_ent(ent + b + gl);
   for (int p0 = 0; p0 < hi; p0 += G) {
-    Ent me = {0, 0.f};
-    if (p0 + gl < len) me = load_ent(ent + b + p0 + gl);
+    Ent nx = {0, 0.f};
+    if (p0 + G + gl < len) nx = load_ent(ent + b + p0 + G + gl);
     const int np = (hi - p0) < G ? (hi - p0) : G;
     for (int p = 0; p < np; p += U) {
       float w[U];
@@ -454,6 +468,7 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* 
         }
       }
     }
+    me = nx;
   }
   if (active) store_row<VEC, RELU>(y + (int64_t)r * ldy, f0, F, acc);
 }
@@ -613,16 +628,16 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
       GCN_HIP(hipGetLastError());
     }
   }
-  // rows of 3..32 entries (the classes of one and two entries get no waves)
+  // rows of 3 .. 32 entries, and of the medium class with GCN_MEDIUM_BY_SLOTS (the
+  // classes of one and two entries get no waves here)
+  constexpr int last_slot_class = GCN_MEDIUM_BY_SLOTS ? kMedium : kLastShort;
   ShortArgs sa;
   int64_t waves = 0;
-  for (int c = kFirstShort; c <= kLastShort + 1; ++c) {
+  for (int c = kFirstShort; c <= kMedium + 1; ++c) {
     sa.row_off[c - kFirstShort] = p.class_off[c];
     sa.wave_off[c - kFirstShort] = waves;
-    if (c <= kLastShort) {
-      if (c >= kFirstShort + 2) waves += ceil_div(p.class_off[c + 1] - p.class_off[c], E);
-      sa.len_hi[c - kFirstShort] = kClassHi[c];
-    }
+    if (c >= kFirstShort + 2 && c <= last_slot_class)
+      waves += ceil_div(p.class_off[c + 1] - p.class_off[c], E);
   }
   if (waves > 0) {
     ProfScope ps("agg_short", stream);
@@ -631,8 +646,8 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
                        (const int32_t*)p.rows, sa, src, y, ldy, F);
     GCN_HIP(hipGetLastError());
   }
-  // medium rows
-  const int64_t n_med = p.class_off[kMedium + 1] - p.class_off[kMedium];
+  // medium rows, one wavefront per row (unless they ran one per lane group above)
+  const int64_t n_med = GCN_MEDIUM_BY_SLOTS ? 0 : p.class_off[kMedium + 1] - p.class_off[kMedium];
   if (n_med > 0) {
     ProfScope ps("agg_medium", stream);
     hipLaunchKernelGGL((k_medium<VEC, G, Src, RELU>), dim3(blocks_for_waves(n_med), tiles),
