@@ -120,19 +120,21 @@ __device__ inline int row_class(int64_t len, int64_t medium_max) {
   return kChunked;
 }
 
-// Sort key of a row: class in bits [41, 45), then, for the classes whose rows
-// are processed one per lane group (3 entries up to medium_max), decreasing
-// length (511 - min(len, 511)) in bits [32, 41), so the rows of a wavefront
-// have about the same length; then the row id.
+// Sort key of a row: class in bits [60, 64), then, for the classes of 3 or
+// more entries, decreasing length (kLenMask - min(len, kLenMask)) in bits
+// [32, 60), then the row id. Rows a wavefront takes together then have about
+// the same length, and long rows and full chunks start first.
+constexpr uint64_t kLenMask = (1ull << 28) - 1;
+
 __global__ void k_class_keys(const int64_t* __restrict__ ptr, int64_t n_major, int64_t medium_max,
                              uint64_t* __restrict__ keys) {
   const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= n_major) return;
   const int64_t len = ptr[r + 1] - ptr[r];
   const int c = row_class(len, medium_max);
-  const uint64_t lcode =
-      (c >= kFirstShort + 2 && c <= kMedium) ? (uint64_t)(511 - (len < 511 ? len : 511)) : 0;
-  keys[r] = ((uint64_t)c << 41) | (lcode << 32) | (uint64_t)r;
+  const uint64_t l = (uint64_t)len < kLenMask ? (uint64_t)len : kLenMask;
+  const uint64_t lcode = c >= kFirstShort + 2 ? kLenMask - l : 0;
+  keys[r] = ((uint64_t)c << 60) | (lcode << 32) | (uint64_t)r;
 }
 
 // per-class row and entry counts (integer sums, so the atomics are exact)
@@ -441,9 +443,11 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
   hipLaunchKernelGGL(k_class_count, dim3(grid_for(n)), dim3(kThreads), 0, stream, m.ptr, n,
                      p.medium_max, counts);
   GCN_HIP(hipGetLastError());
-  // two stable 8-bit passes over bits [32, 48): by length code, then by class
+  // four stable 8-bit passes over bits [32, 64): by length code, then by class
   GCN_CHECK(radix_pass_u64(keys, sorted, n, 32, stream));
   GCN_CHECK(radix_pass_u64(sorted, keys, n, 40, stream));
+  GCN_CHECK(radix_pass_u64(keys, sorted, n, 48, stream));
+  GCN_CHECK(radix_pass_u64(sorted, keys, n, 56, stream));
   hipLaunchKernelGGL(k_low32, dim3(grid_for(n)), dim3(kThreads), 0, stream,
                      (const uint64_t*)keys, n, p.rows);
   GCN_HIP(hipGetLastError());
