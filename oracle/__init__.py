@@ -507,11 +507,12 @@ def sage_step(graph: Graph, X, params, labels, lp_mask=None, E=None, eps=1e-5, m
     lse = mx[:, 0] + np.log(np.exp(logits - mx).sum(axis=1))
     n_loss = int(loss_rows.sum())
     idx = np.flatnonzero(loss_rows)
-    loss = float(np.sum(lse[idx] - logits[idx, y[idx]]) / n_loss)
+    # no row in the loss (every label embedded): loss 0 and no gradient
+    loss = float(np.sum(lse[idx] - logits[idx, y[idx]]) / n_loss) if n_loss else 0.0
     dO = np.exp(logits - lse[:, None])
     dO[idx, y[idx]] -= 1.0
     dO[~loss_rows] = 0.0
-    dO /= n_loss
+    dO /= max(n_loss, 1)
     grads = [None] * 9
     dE = None
     for l in (2, 1, 0):

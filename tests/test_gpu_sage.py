@@ -217,3 +217,32 @@ def test_sage_step_product_full(G):
     assert max(errs) <= 1e-5
     del ref, og
     gc.collect()
+
+
+@pytest.mark.parametrize("n,f_in,hidden,C,mask_kind", [
+    (1500, 30, 20, 64, "half"),     # the widest class count, narrow rows (8-lane LayerNorm)
+    (1200, 1030, 40, 7, "half"),    # inputs wider than the register LayerNorm kernel
+    (1000, 16, 16, 3, "all"),       # every label embedded: no row in the loss
+])
+def test_sage_step_edge_cases(G, n, f_in, hidden, C, mask_kind):
+    note("sage edge n=%d f_in=%d hidden=%d C=%d mask=%s" % (n, f_in, hidden, C, mask_kind))
+    src, dst, X, params, y, mask, E = sage_case(n, 10 * n, f_in, hidden, C, 460 + f_in, True)
+    if mask_kind == "all":
+        mask[:] = 1
+    og = oracle.Graph(n, n, src, dst, synth.SYMMETRIZE, mean=True)
+    g = G.gcn_build_csr(n, n, dev(src), dev(dst), synth.SYMMETRIZE)
+    G.gcn_normalize_mean(g)
+    pd = [dev(p) for p in params]
+    args = (dev(y), dev(mask), dev(E))
+    H1, H2, _ = G.gcn_sage3_forward(g, dev(X), pd, *args)
+    masks = [host(H1) > 0, host(H2) > 0]
+    ref = oracle.sage_step(og, X, params, y, mask, E, masks=masks, with_margins=False)
+    loss, grads, dE = G.gcn_sage3_step(g, dev(X), pd, *args)
+    got_loss = float(host(loss))
+    if mask_kind == "all":
+        assert got_loss == 0.0 and ref["loss"] == 0.0
+        assert all(np.all(host(t) == 0) for t in grads) and np.all(host(dE) == 0)
+        return
+    assert abs(got_loss - ref["loss"]) <= 1e-5 * abs(ref["loss"])
+    for a, b in zip([host(t) for t in grads] + [host(dE)], ref["grads"] + [ref["dE"]]):
+        assert np.linalg.norm(a - b) <= 1e-5 * np.linalg.norm(b)
