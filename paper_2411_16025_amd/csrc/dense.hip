@@ -189,13 +189,18 @@ __global__ __launch_bounds__(kThreads, GCN_GEMM_MIN_BLOCKS) void k_gemm_tall_v(i
                                                           const float* __restrict__ B, int64_t ldb,
                                                           float* __restrict__ C, int64_t ldc,
                                                           const float* __restrict__ mask,
-                                                          int64_t ldm, bool relu) {
+                                                          int64_t ldm, bool relu, bool cvec) {
   constexpr int NB = BN / 16;
   constexpr int BL = BN / 32;  // 16-byte B loads per thread per slice
   constexpr int BR = OP == kNN ? kKc : BN;
   constexpr int BC = OP == kNN ? BN + 4 : kKc + 4;
-  __shared__ __align__(16) float As[kTile][kKc + 4];
-  __shared__ __align__(16) float Bs[BR][BC];
+  // the output tile is staged through the same LDS, CW columns at a time
+  constexpr int CW = BN < 128 ? BN : 128;
+  constexpr int kOperands = kTile * (kKc + 4) + BR * BC;
+  constexpr int kStage = kTile * (CW + 4);
+  __shared__ __align__(16) float smem[kOperands > kStage ? kOperands : kStage];
+  auto& As = *reinterpret_cast<float (*)[kTile][kKc + 4]>(smem);
+  auto& Bs = *reinterpret_cast<float (*)[BR][BC]>(smem + kTile * (kKc + 4));
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int64_t m0 = (int64_t)blockIdx.x * kTile;
   const int64_t n0 = (int64_t)blockIdx.y * BN;
@@ -256,6 +261,54 @@ __global__ __launch_bounds__(kThreads, GCN_GEMM_MIN_BLOCKS) void k_gemm_tall_v(i
       store_slice();
       __syncthreads();
     }
+  }
+  if (cvec) {
+    // CW columns at a time: the wave writes its 16 x CW block to LDS in the
+    // matrix-core layout, then stores it row by row with 16-byte accesses (the
+    // mask is read the same way)
+    float (*st)[CW + 4] = reinterpret_cast<float (*)[CW + 4]>(smem);
+    constexpr int LPR = CW / 4;    // lanes per row
+    constexpr int RPI = 64 / LPR;  // rows per store instruction
+#pragma unroll
+    for (int c0 = 0; c0 < BN; c0 += CW) {
+      __syncthreads();  // the operands (or the previous columns) are no longer read
+#pragma unroll
+      for (int j = c0 / 16; j < (c0 + CW) / 16; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          st[16 * w + 4 * (lane >> 4) + i][16 * j - c0 + (lane & 15)] = acc[j][i];
+      __syncthreads();
+#pragma unroll
+      for (int it = 0; it < 16 / RPI; ++it) {
+        const int rl = 16 * w + it * RPI + lane / LPR;
+        const int cl = 4 * (lane % LPR);
+        const int64_t gm = m0 + rl, gn = n0 + c0 + cl;
+        if (gm >= M || gn >= N) continue;
+        f4 v = *reinterpret_cast<const f4*>(&st[rl][cl]);
+        if (gn + 4 <= N) {
+          if (mask) {
+            const f4 mk = *reinterpret_cast<const f4*>(mask + gm * ldm + gn);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (!(mk[e] > 0.f)) v[e] = 0.f;
+          }
+          if (relu) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = fmaxf(v[e], 0.f);
+          }
+          *reinterpret_cast<f4*>(C + gm * ldc + gn) = v;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (gn + e >= N) break;
+            float x = (mask && !(mask[gm * ldm + gn + e] > 0.f)) ? 0.f : v[e];
+            if (relu) x = fmaxf(x, 0.f);
+            C[gm * ldc + gn + e] = x;
+          }
+        }
+      }
+    }
+    return;
   }
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
@@ -458,16 +511,18 @@ void launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, c
                  int64_t ldb, float* C, int64_t ldc, const float* mask, int64_t ldm,
                  bool relu, hipStream_t stream) {
   const int bn = tile_n(N);
+  // staged 16-byte stores need 16-byte aligned rows of C (and of the mask)
+  const bool cvec = aligned16(C, ldc) && (!mask || aligned16(mask, ldm));
   const dim3 grid((unsigned)ceil_div(M, kTile), (unsigned)ceil_div(N, bn));
   if (bn == 64)
     hipLaunchKernelGGL((k_gemm_tall_v<OP, 64>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda, B,
-                       ldb, C, ldc, mask, ldm, relu);
+                       ldb, C, ldc, mask, ldm, relu, cvec);
   else if (bn == 128)
     hipLaunchKernelGGL((k_gemm_tall_v<OP, 128>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda,
-                       B, ldb, C, ldc, mask, ldm, relu);
+                       B, ldb, C, ldc, mask, ldm, relu, cvec);
   else
     hipLaunchKernelGGL((k_gemm_tall_v<OP, 256>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda,
-                       B, ldb, C, ldc, mask, ldm, relu);
+                       B, ldb, C, ldc, mask, ldm, relu, cvec);
 }
 
 void launch_tn(int64_t M, int64_t N, int64_t K, int64_t split, int64_t n_chunks, const float* A,
