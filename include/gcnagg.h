@@ -53,7 +53,8 @@ typedef enum {
   GCN_ERANGE = 2, /* vertex id out of range, n_local_cols > n_cols, sizes beyond int32 ids */
   GCN_ENOMEM = 3, /* device allocation failed */
   GCN_EHIP = 4,   /* a HIP runtime call failed */
-  GCN_ESTATE = 5  /* freed / corrupted handle, or call out of order */
+  GCN_ESTATE = 5  /* freed / corrupted handle, a handle used while another device is
+                     current, or a call out of order */
 } gcn_status;
 
 /* gcn_build_csr flags */

@@ -113,6 +113,11 @@ gcn_status check_graph(const gcn_graph* g) {
     set_error("graph handle is freed or corrupted");
     return GCN_ESTATE;
   }
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != g->device) {
+    set_error("the graph lives on device %d, the current device is %d", g->device, dev);
+    return GCN_ESTATE;
+  }
   return GCN_OK;
 }
 
