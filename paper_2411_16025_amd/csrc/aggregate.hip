@@ -345,11 +345,12 @@ __global__ __launch_bounds__(kBlock) void k_zero_rows(const int32_t* __restrict_
 // Rows with exactly L entries (L = 1 or 2): one row per slot and R groups of
 // E rows per wavefront, every load of the R groups issued before any
 // arithmetic. Such rows have no other work to hide their chain of dependent
-// loads (row id, row start, entries, feature rows) behind, so the wavefront
-// keeps R * L gathers per lane in flight instead of L. The terms of a row are
-// added in entry order, as in k_short.
+// loads (row id and start, entries, feature rows) behind, so the wavefront
+// keeps R * L gathers per lane in flight instead of L; the plan stores their
+// starts next to their ids (beg[i] for rows[i]). The terms of a row are added
+// in entry order, as in k_short.
 template <int VEC, int G, class Src, bool RELU, int L, int R>
-__global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_tiny(const int64_t* __restrict__ ptr,
+__global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_tiny(const int64_t* __restrict__ beg,
                                                   const Ent* __restrict__ ent,
                                                   const int32_t* __restrict__ rows, int64_t n,
                                                   Src src, float* __restrict__ y, int64_t ldy,
@@ -361,16 +362,15 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_tiny(const int64_t* _
   const int f0 = (int)blockIdx.y * G * VEC + (lane % G) * VEC;
   const bool fa = f0 < F;
   int32_t r[R];
+  int64_t b[R];
   bool has[R];
 #pragma unroll
   for (int g = 0; g < R; ++g) {
     const int64_t i = (wave * R + g) * E + slot;
     has[g] = i < n;
     r[g] = has[g] ? rows[i] : 0;
+    b[g] = has[g] ? beg[i] : 0;
   }
-  int64_t b[R];
-#pragma unroll
-  for (int g = 0; g < R; ++g) b[g] = has[g] ? ptr[r[g]] : 0;
   Ent e[R][L];
 #pragma unroll
   for (int g = 0; g < R; ++g)
@@ -614,7 +614,7 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
       ProfScope ps("agg_tiny", stream);
       hipLaunchKernelGGL((k_tiny<VEC, G, Src, RELU, 1, R1>),
                          dim3(blocks_for_waves(ceil_div(n1, E * R1)), tiles), dim3(kBlock), 0,
-                         stream, (const int64_t*)m.ptr, (const Ent*)m.ent,
+                         stream, (const int64_t*)p.tiny_beg, (const Ent*)m.ent,
                          (const int32_t*)(p.rows + p.class_off[kFirstShort]), n1, src, y, ldy, F);
       GCN_HIP(hipGetLastError());
     }
@@ -622,7 +622,7 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
       ProfScope ps("agg_tiny", stream);
       hipLaunchKernelGGL((k_tiny<VEC, G, Src, RELU, 2, R2>),
                          dim3(blocks_for_waves(ceil_div(n2, E * R2)), tiles), dim3(kBlock), 0,
-                         stream, (const int64_t*)m.ptr, (const Ent*)m.ent,
+                         stream, (const int64_t*)(p.tiny_beg + n1), (const Ent*)m.ent,
                          (const int32_t*)(p.rows + p.class_off[kFirstShort + 1]), n2, src, y, ldy,
                          F);
       GCN_HIP(hipGetLastError());

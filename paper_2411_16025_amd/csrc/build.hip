@@ -160,6 +160,13 @@ __global__ void k_class_count(const int64_t* __restrict__ ptr, int64_t n_major, 
   }
 }
 
+// first entry of each row of a run of `rows`
+__global__ void k_row_begins(const int32_t* __restrict__ rows, int64_t n,
+                             const int64_t* __restrict__ ptr, int64_t* __restrict__ beg) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) beg[i] = ptr[rows[i]];
+}
+
 __global__ void k_low32(const uint64_t* __restrict__ keys, int64_t n, int32_t* __restrict__ out) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) out[i] = (int32_t)(keys[i] & 0xFFFFFFFFull);
@@ -462,6 +469,16 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
     p.class_off[c + 1] = p.class_off[c] + (int64_t)host_counts[c];
     p.class_nnz[c] = (int64_t)host_counts[kNumClasses + c];
   }
+  // the one- and two-entry rows read their first entry from here (one load
+  // fewer in their chain of dependent loads)
+  const int64_t n_tiny = p.class_off[kFirstShort + 2] - p.class_off[kFirstShort];
+  if (n_tiny > 0) {
+    GCN_CHECK(dalloc(&p.tiny_beg, n_tiny, "tiny row starts"));
+    hipLaunchKernelGGL(k_row_begins, dim3(grid_for(n_tiny)), dim3(kThreads), 0, stream,
+                       (const int32_t*)(p.rows + p.class_off[kFirstShort]), n_tiny,
+                       (const int64_t*)m.ptr, p.tiny_beg);
+    GCN_HIP(hipGetLastError());
+  }
   // chunk table over the rows of the chunked class
   const int64_t nc_rows = p.class_off[kChunked + 1] - p.class_off[kChunked];
   p.n_chunks = p.n_giant = p.n_parts = 0;
@@ -511,6 +528,7 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
 void free_mat(Mat& m, bool arrays) {
   Plan& p = m.plan;
   dfree(p.rows);
+  dfree(p.tiny_beg);
   dfree(p.chunk_row);
   dfree(p.chunk_beg);
   dfree(p.chunk_end);
