@@ -407,7 +407,8 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_tiny(const int64_t* _
 // shuffles; the loop bound is the wavefront's longest row, so every lane runs
 // the same iterations. A slot's terms are added in entry order.
 template <int VEC, int G, class Src, bool RELU>
-__global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* __restrict__ ptr,
+__global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* __restrict__ rbeg,
+                                                  const int32_t* __restrict__ rlen,
                                                   const Ent* __restrict__ ent,
                                                   const int32_t* __restrict__ rows, ShortArgs sa,
                                                   Src src, float* __restrict__ y, int64_t ldy,
@@ -430,10 +431,10 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* 
   int32_t r = 0;
   int64_t b = 0;
   int len = 0;
-  if (has_row) {
+  if (has_row) {  // start and length come with the row id (rbeg, rlen follow rows from row_off[0])
     r = rows[i];
-    b = ptr[r];
-    len = (int)(ptr[r + 1] - b);
+    b = rbeg[i - sa.row_off[0]];
+    len = rlen[i - sa.row_off[0]];
   }
   float acc[VEC];
 #pragma unroll
@@ -614,7 +615,7 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
       ProfScope ps("agg_tiny", stream);
       hipLaunchKernelGGL((k_tiny<VEC, G, Src, RELU, 1, R1>),
                          dim3(blocks_for_waves(ceil_div(n1, E * R1)), tiles), dim3(kBlock), 0,
-                         stream, (const int64_t*)p.tiny_beg, (const Ent*)m.ent,
+                         stream, (const int64_t*)p.rbeg, (const Ent*)m.ent,
                          (const int32_t*)(p.rows + p.class_off[kFirstShort]), n1, src, y, ldy, F);
       GCN_HIP(hipGetLastError());
     }
@@ -622,7 +623,7 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
       ProfScope ps("agg_tiny", stream);
       hipLaunchKernelGGL((k_tiny<VEC, G, Src, RELU, 2, R2>),
                          dim3(blocks_for_waves(ceil_div(n2, E * R2)), tiles), dim3(kBlock), 0,
-                         stream, (const int64_t*)(p.tiny_beg + n1), (const Ent*)m.ent,
+                         stream, (const int64_t*)(p.rbeg + n1), (const Ent*)m.ent,
                          (const int32_t*)(p.rows + p.class_off[kFirstShort + 1]), n2, src, y, ldy,
                          F);
       GCN_HIP(hipGetLastError());
@@ -642,8 +643,8 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
   if (waves > 0) {
     ProfScope ps("agg_short", stream);
     hipLaunchKernelGGL((k_short<VEC, G, Src, RELU>), dim3(blocks_for_waves(waves), tiles),
-                       dim3(kBlock), 0, stream, (const int64_t*)m.ptr, (const Ent*)m.ent,
-                       (const int32_t*)p.rows, sa, src, y, ldy, F);
+                       dim3(kBlock), 0, stream, (const int64_t*)p.rbeg, (const int32_t*)p.rlen,
+                       (const Ent*)m.ent, (const int32_t*)p.rows, sa, src, y, ldy, F);
     GCN_HIP(hipGetLastError());
   }
   // medium rows, one wavefront per row (unless they ran one per lane group above)

@@ -160,11 +160,15 @@ __global__ void k_class_count(const int64_t* __restrict__ ptr, int64_t n_major, 
   }
 }
 
-// first entry of each row of a run of `rows`
+// first entry and length of each row of a run of `rows`
 __global__ void k_row_begins(const int32_t* __restrict__ rows, int64_t n,
-                             const int64_t* __restrict__ ptr, int64_t* __restrict__ beg) {
+                             const int64_t* __restrict__ ptr, int64_t* __restrict__ beg,
+                             int32_t* __restrict__ len) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) beg[i] = ptr[rows[i]];
+  if (i >= n) return;
+  const int64_t b = ptr[rows[i]];
+  beg[i] = b;
+  len[i] = (int32_t)(ptr[rows[i] + 1] - b);
 }
 
 __global__ void k_low32(const uint64_t* __restrict__ keys, int64_t n, int32_t* __restrict__ out) {
@@ -469,14 +473,15 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
     p.class_off[c + 1] = p.class_off[c] + (int64_t)host_counts[c];
     p.class_nnz[c] = (int64_t)host_counts[kNumClasses + c];
   }
-  // the one- and two-entry rows read their first entry from here (one load
-  // fewer in their chain of dependent loads)
-  const int64_t n_tiny = p.class_off[kFirstShort + 2] - p.class_off[kFirstShort];
-  if (n_tiny > 0) {
-    GCN_CHECK(dalloc(&p.tiny_beg, n_tiny, "tiny row starts"));
-    hipLaunchKernelGGL(k_row_begins, dim3(grid_for(n_tiny)), dim3(kThreads), 0, stream,
-                       (const int32_t*)(p.rows + p.class_off[kFirstShort]), n_tiny,
-                       (const int64_t*)m.ptr, p.tiny_beg);
+  // rows up to the medium class read their start and length from here (one
+  // load fewer in their chain of dependent loads)
+  const int64_t n_rowk = p.class_off[kMedium + 1] - p.class_off[kFirstShort];
+  if (n_rowk > 0) {
+    GCN_CHECK(dalloc(&p.rbeg, n_rowk, "row starts"));
+    GCN_CHECK(dalloc(&p.rlen, n_rowk, "row lengths"));
+    hipLaunchKernelGGL(k_row_begins, dim3(grid_for(n_rowk)), dim3(kThreads), 0, stream,
+                       (const int32_t*)(p.rows + p.class_off[kFirstShort]), n_rowk,
+                       (const int64_t*)m.ptr, p.rbeg, p.rlen);
     GCN_HIP(hipGetLastError());
   }
   // chunk table over the rows of the chunked class
@@ -528,7 +533,8 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
 void free_mat(Mat& m, bool arrays) {
   Plan& p = m.plan;
   dfree(p.rows);
-  dfree(p.tiny_beg);
+  dfree(p.rbeg);
+  dfree(p.rlen);
   dfree(p.chunk_row);
   dfree(p.chunk_beg);
   dfree(p.chunk_end);

@@ -37,8 +37,11 @@ constexpr int kClassHi[kLastShort + 1] = {0, 1, 2, 4, 8, 16, 32};
 
 struct Plan {
   int32_t* rows = nullptr;        // [n_major] row ids grouped by class (order: see build_plan)
-  int64_t* tiny_beg = nullptr;    // first entry of each row of the 1- and 2-entry classes, in
-                                  // the order of `rows` from class_off[1]
+  // first entry and length of each row of the classes 1 .. kMedium, in the
+  // order of `rows` from class_off[1] (the row kernels read them with the
+  // row id instead of the row pointer)
+  int64_t* rbeg = nullptr;
+  int32_t* rlen = nullptr;
   int64_t class_off[kNumClasses + 1] = {};  // host copy of the class boundaries in `rows`
   int64_t class_nnz[kNumClasses] = {};      // host: stored entries per class
   int64_t medium_max = 256;                 // longest row of the medium class
