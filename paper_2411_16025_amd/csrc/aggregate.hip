@@ -210,7 +210,7 @@ __device__ inline void store_row(float* __restrict__ y, int f0, int F, const flo
 
 // Gathers in flight per lane in the entry loops.
 #ifndef GCN_AGG_UNROLL
-#define GCN_AGG_UNROLL 4
+#define GCN_AGG_UNROLL 3
 #endif
 // Unroll factor of the loop over gather groups inside a 64-entry block (1
 // keeps the register count, and so the occupancy, of one group).
