@@ -1,5 +1,5 @@
 // Aggregation kernels: Y = A_hat X, dX = A_hat^T G, and the variant whose
-// halo input rows are uint8 codes dequantized on read.
+// halo input rows are 8-bit or 2-bit codes dequantized on read.
 //
 // Paper: SuperGCN (arXiv 2411.16025) Section 4 -- the destination row is
 // accumulated in registers while its (sorted, clustered) source rows stream
@@ -13,10 +13,15 @@
 //  * A lane owns VEC consecutive features; G lanes ("a slot") cover one
 //    feature tile of G*VEC floats of one row; a wavefront holds E = 64/G
 //    slots. Feature tiles beyond G*VEC use blockIdx.y.
-//  * Rows are binned by length (see build.hip):
+//  * Rows are binned by length (see build.hip), and within the bins of 3 or
+//    more entries ordered by decreasing length:
 //      empty rows           -> zero fill
-//      1..32 entries        -> one row per slot, E rows per wavefront
-//      33..medium_max       -> one wavefront per row, slots interleave entries
+//      1 or 2 entries       -> one row per slot, several row groups per
+//                              wavefront with all their loads issued first
+//      3..medium_max        -> one row per slot, E rows of about the same
+//                              length per wavefront (or, with
+//                              GCN_MEDIUM_BY_SLOTS=0, one wavefront per row
+//                              from 33 entries, slots interleaving entries)
 //      longer rows          -> one 256-thread workgroup per chunk of entries,
 //                              slots reduced in fixed order through LDS; a row
 //                              with several chunks writes partial rows that a

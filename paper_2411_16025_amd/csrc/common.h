@@ -21,19 +21,18 @@ struct __align__(8) Ent {
   float val;
 };
 
-// Row-length classes (the binning that balances work across wavefronts).
-// Class c holds rows whose length lies in [kClassLo[c], kClassHi[c]].
-// Classes 0..kNumShort-1 are the "short" classes processed one row per lane
-// group; class kMedium runs one wavefront per row; class kChunked runs one
-// workgroup per chunk of at most chunk_len entries.
+// Row-length classes (the binning that balances work across wavefronts; the
+// bounds are in row_class in build.hip): 0 empty; 1 and 2 rows of exactly one
+// and two entries; 3..6 rows of 3-4, 5-8, 9-16 and 17-32 entries; kMedium
+// rows of 33 .. medium_max entries; kChunked longer rows, run one workgroup
+// per chunk of at most chunk_len entries. Classes 1 .. kMedium run one row
+// per lane group.
 constexpr int kNumClasses = 9;
 constexpr int kClassEmpty = 0;
 constexpr int kFirstShort = 1;
 constexpr int kLastShort = 6;
 constexpr int kMedium = 7;
 constexpr int kChunked = 8;
-// longest row of each class up to the short ones
-constexpr int kClassHi[kLastShort + 1] = {0, 1, 2, 4, 8, 16, 32};
 
 struct Plan {
   int32_t* rows = nullptr;        // [n_major] row ids grouped by class (order: see build_plan)

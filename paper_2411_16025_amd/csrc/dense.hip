@@ -5,9 +5,11 @@
 // GEMM shapes of full-batch GCN training are tall and skinny: the node count
 // is in the millions, feature and class counts are at most a few hundred.
 //  * C = A op(B) with M = nodes (NN, NT): one 256-thread workgroup computes a
-//    64 x 64 tile of C over all of K, staging 32-deep slices of A and B in
-//    LDS; each wavefront owns 16 rows and issues v_mfma_f32_16x16x4_f32 on
-//    four 16 x 16 blocks.
+//    64 x BN tile of C (BN = 64, 128 or 256) over all of K, staging 32-deep
+//    slices of A and B in LDS while the next slice is loaded into registers;
+//    each wavefront owns 16 rows and issues v_mfma_f32_16x16x4_f32 on BN / 16
+//    blocks of 16 x 16. The tile leaves through LDS as row-contiguous
+//    16-byte stores, with an optional ReLU or ReLU-backward mask.
 //  * C = A^T B with K = nodes (the weight gradients): K is split into fixed
 //    chunks; every chunk writes a partial C tile and a second kernel adds the
 //    partials in chunk order, so the result is the same on every run.

@@ -1,7 +1,9 @@
-// Per-row uint8 quantization, the producer side of the quantized boundary
-// exchange (SuperGCN, arXiv 2411.16025, Section 2.4 and Section 7.3): the
-// zero point and scale of a row are computed and the row is quantized in the
-// same pass, with round-half-even in place of stochastic rounding.
+// Row-wise kernels: per-row b-bit quantization (b = 8 or 2), the producer
+// side of the quantized boundary exchange (SuperGCN, arXiv 2411.16025,
+// Sections 2.4, 6.1 and 7.3: the zero point and scale of a row are computed
+// and the row is quantized in the same pass, with round-half-even in place of
+// stochastic rounding), optionally after a row LayerNorm (Section 6.1 step 2);
+// and the LayerNorm forward and backward of the GraphSAGE model (Table 2).
 
 #include "common.h"
 
