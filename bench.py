@@ -43,7 +43,7 @@ COUNTERS = os.path.join(ROOT, "profiles", "agg_counters_rmat24_q8.txt")
 
 # kernel name -> row-length classes whose rows it processes
 KERNEL_CLASSES = {"agg_zero_rows": [0], "agg_tiny": [1, 2], "agg_short": [3, 4, 5, 6],
-                  "agg_medium": [7], "agg_chunk": [8]}
+                  "agg_medium": [7], "agg_chunk": [8], "agg_pieces": [9]}
 
 
 def log(msg):

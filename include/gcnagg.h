@@ -361,8 +361,20 @@ gcn_status gcn_graph_export(const gcn_graph* g, int which, int64_t* ptr, int32_t
  * (which = 1). Writes up to `cap` records of 5 int64 each to host memory:
  * {first_len, last_len, rows, entries, entries with column >= halo_from},
  * last_len = -1 meaning unbounded (pass halo_from = -1 to skip the last
- * count, which is then 0). Returns the number of classes in *n_classes.
- * Synchronizes `stream` when halo_from >= 0. */
+ * count, which is then 0). Returns the number of classes in *n_classes (10:
+ * empty rows, 1, 2, 3-4, 5-8, 9-16, 17-32 entries, medium rows, rows cut into
+ * fixed-length chunks, and rows cut at column-block boundaries, the last bin
+ * empty when the plan blocks no row). Synchronizes `stream` when
+ * halo_from >= 0.
+ *
+ * The plan's bounds can be set at build time through the environment:
+ * GCN_MEDIUM_MAX (longest medium row, default 256), GCN_CHUNK_LEN (entries
+ * per chunk, 2048), GCN_BLOCKED_MIN (shortest column-blocked row, 257),
+ * GCN_COL_BLOCKS (column blocks, 64; 1 blocks nothing), GCN_SEGMENT_MIN
+ * (entries per segment a blocked row is cut for: about len / 32 segments, a
+ * power of two up to GCN_COL_BLOCKS; 0 cuts at every block), GCN_PIECE_MAX
+ * (entries per blocked piece, 256) and GCN_BLOCK_MIN_COLS (fewest columns
+ * for which rows are blocked, 2^20). Out-of-range values are ignored. */
 gcn_status gcn_graph_bins(const gcn_graph* g, int which, int64_t halo_from, int64_t* records,
                           int cap, int* n_classes, void* stream);
 

@@ -309,6 +309,55 @@ __device__ inline void accumulate_blocks(const Ent* __restrict__ ent, int64_t be
   }
 }
 
+// Slot s of a wavefront (lanes sG .. sG + G - 1) sums the len entries of
+// the run starting at entry b; acc receives the slot's features f0 .. f0 +
+// VEC - 1. The G lanes load the pairs G at a time with one coalesced access
+// (the next G travel with the current gathers) and share them by lane
+// shuffles; the loop bound is the wavefront's longest run, so every lane runs
+// the same iterations (all lanes of the wavefront must call this). Terms are
+// added in entry order.
+template <int VEC, int G, class Src>
+__device__ inline void accumulate_slot(const Ent* __restrict__ ent, int64_t b, int len,
+                                       const Src& src, int f0, bool active, float* acc) {
+  constexpr int U = 4;
+  const int lane = threadIdx.x & 63;
+  const int slot = lane / G, gl = lane % G;
+#pragma unroll
+  for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
+  int hi = len;  // the wavefront's longest run
+#pragma unroll
+  for (int off = G; off < 64; off <<= 1) hi = max(hi, __shfl_xor(hi, off, 64));
+  Ent me = {0, 0.f};
+  if (gl < len) me = load_ent(ent + b + gl);
+  for (int p0 = 0; p0 < hi; p0 += G) {
+    Ent nx = {0, 0.f};
+    if (p0 + G + gl < len) nx = load_ent(ent + b + p0 + G + gl);
+    const int np = (hi - p0) < G ? (hi - p0) : G;
+    for (int p = 0; p < np; p += U) {
+      float w[U];
+      int32_t col[U];
+      typename Src::Raw raw[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int pos = (p + u) < G ? (p + u) : (G - 1);
+        col[u] = __shfl(me.col, slot * G + pos, 64);
+        w[u] = __shfl(me.val, slot * G + pos, 64);
+        if (p + u < np && p0 + p + u < len && active) src.fetch(col[u], f0, raw[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (p + u < np && p0 + p + u < len && active) {
+          float xv[VEC];
+          src.decode(raw[u], col[u], xv);
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) acc[v] = __builtin_fmaf(w[u], xv[v], acc[v]);
+        }
+      }
+    }
+    me = nx;
+  }
+}
+
 // Sum the E slots of a wavefront (butterfly over lane distance G, 2G, ...).
 // Every slot ends with the same total, combined in the same fixed order.
 template <int VEC, int G>
@@ -404,13 +453,9 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_tiny(const int64_t* _
   }
 }
 
-// Rows of 3 .. medium_max entries: one row per slot, E rows per wavefront, the
-// rows of one wavefront from one length class and, within it, of about the
-// same length (the plan orders them by decreasing length). The G lanes of a
-// slot load the row's (column, value) pairs G at a time with one coalesced
-// access (the next G travel with the current gathers) and share them by lane
-// shuffles; the loop bound is the wavefront's longest row, so every lane runs
-// the same iterations. A slot's terms are added in entry order.
+// Rows of 3 .. medium_max entries: one row per slot (accumulate_slot), E rows
+// per wavefront, the rows of one wavefront from one length class and, within
+// it, of about the same length (the plan orders them by decreasing length).
 template <int VEC, int G, class Src, bool RELU>
 __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* __restrict__ rbeg,
                                                   const int32_t* __restrict__ rlen,
@@ -420,7 +465,6 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* 
                                                   int F) {
   constexpr int E = 64 / G;
   constexpr int NS = kSlotClasses;
-  constexpr int U = 4;
   const int lane = threadIdx.x & 63;
   const int slot = lane / G, gl = lane % G;
   const int64_t wave = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
@@ -442,40 +486,7 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* 
     len = rlen[i - sa.row_off[0]];
   }
   float acc[VEC];
-#pragma unroll
-  for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
-  int hi = len;  // the wavefront's longest row
-#pragma unroll
-  for (int off = G; off < 64; off <<= 1) hi = max(hi, __shfl_xor(hi, off, 64));
-  Ent me = {0, 0.f};
-  if (gl < len) me = load_ent(ent + b + gl);
-  for (int p0 = 0; p0 < hi; p0 += G) {
-    Ent nx = {0, 0.f};
-    if (p0 + G + gl < len) nx = load_ent(ent + b + p0 + G + gl);
-    const int np = (hi - p0) < G ? (hi - p0) : G;
-    for (int p = 0; p < np; p += U) {
-      float w[U];
-      int32_t col[U];
-      typename Src::Raw raw[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int pos = (p + u) < G ? (p + u) : (G - 1);
-        col[u] = __shfl(me.col, slot * G + pos, 64);
-        w[u] = __shfl(me.val, slot * G + pos, 64);
-        if (p + u < np && p0 + p + u < len && active) src.fetch(col[u], f0, raw[u]);
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        if (p + u < np && p0 + p + u < len && active) {
-          float xv[VEC];
-          src.decode(raw[u], col[u], xv);
-#pragma unroll
-          for (int v = 0; v < VEC; ++v) acc[v] = __builtin_fmaf(w[u], xv[v], acc[v]);
-        }
-      }
-    }
-    me = nx;
-  }
+  accumulate_slot<VEC, G>(ent, b, len, src, f0, active, acc);
   if (active) store_row<VEC, RELU>(y + (int64_t)r * ldy, f0, F, acc);
 }
 
@@ -550,6 +561,47 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_chunk(const Ent* __re
   }
 }
 
+// Column-blocked pieces (at most piece_max entries each), one per slot, in
+// the plan's launch order (column block by column block, decreasing length
+// within a block); each writes its partial row.
+template <int VEC, int G, class Src>
+__global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_pieces(const int64_t* __restrict__ pbeg,
+                                                   const int32_t* __restrict__ plen,
+                                                   const int32_t* __restrict__ ppart, int64_t n,
+                                                   const Ent* __restrict__ ent, Src src,
+                                                   float* __restrict__ parts, int64_t ldp, int F) {
+  constexpr int E = 64 / G;
+  const int lane = threadIdx.x & 63;
+  const int slot = lane / G, gl = lane % G;
+  const int64_t wave = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+  if (wave * E >= n) return;  // whole wavefront leaves together
+  const int64_t i = wave * E + slot;
+  const bool has = i < n;
+  const int f0 = (int)blockIdx.y * G * VEC + gl * VEC;
+  const bool active = has && f0 < F;
+  const int64_t b = has ? pbeg[i] : 0;
+  const int len = has ? plen[i] : 0;
+  float acc[VEC];
+  accumulate_slot<VEC, G>(ent, b, len, src, f0, active, acc);
+  if (active) store_row<VEC>(parts + (int64_t)ppart[i] * ldp, f0, F, acc);
+}
+
+// Features f0 .. f0 + VEC - 1 of a partial row (zeros past F).
+template <int VEC>
+__device__ inline void load_part(const float* __restrict__ row, int f0, int F, float* out) {
+  if constexpr (VEC == 4) {
+    if (f0 + 4 <= F) {
+      const f4 v4 = *reinterpret_cast<const f4*>(row + f0);
+      out[0] = v4.x; out[1] = v4.y; out[2] = v4.z; out[3] = v4.w;
+    } else {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) out[v] = f0 + v < F ? row[f0 + v] : 0.f;
+    }
+  } else {
+    out[0] = row[f0];
+  }
+}
+
 // Sum the partial rows of each multi-chunk row in chunk order: slot s adds
 // partials s, s + E, ...; the slots are then combined by the butterfly.
 template <int VEC, int G, bool RELU>
@@ -570,20 +622,25 @@ __global__ __launch_bounds__(kBlock) void k_reduce_parts(const int32_t* __restri
 #pragma unroll
   for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
   if (active) {
-    for (int64_t p = part_off[i] + slot; p < part_off[i + 1]; p += E) {
-      const float* src = parts + p * ldp + f0;
-      if constexpr (VEC == 4) {
-        if (f0 + 4 <= F) {
-          const f4 v4 = *reinterpret_cast<const f4*>(src);
-          acc[0] += v4.x; acc[1] += v4.y; acc[2] += v4.z; acc[3] += v4.w;
-        } else {
+    // U partial rows in flight per lane; each slot still adds its partials
+    // in increasing slot order
+    constexpr int U = 4;
+    const int64_t pe = part_off[i + 1];
+    int64_t p = part_off[i] + slot;
+    for (; p + (U - 1) * E < pe; p += U * E) {
+      float v[U][VEC];
 #pragma unroll
-          for (int v = 0; v < 4; ++v)
-            if (f0 + v < F) acc[v] += src[v];
-        }
-      } else {
-        acc[0] += src[0];
-      }
+      for (int u = 0; u < U; ++u) load_part<VEC>(parts + (p + u * E) * ldp, f0, F, v[u]);
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) acc[k] += v[u][k];
+    }
+    for (; p < pe; p += E) {
+      float v[VEC];
+      load_part<VEC>(parts + p * ldp, f0, F, v);
+#pragma unroll
+      for (int k = 0; k < VEC; ++k) acc[k] += v[k];
     }
   }
   reduce_slots<VEC, G>(acc);
@@ -661,12 +718,12 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
                        (const int32_t*)(p.rows + p.class_off[kMedium]), n_med, src, y, ldy, F);
     GCN_HIP(hipGetLastError());
   }
-  // long rows
-  if (p.n_chunks > 0) {
+  // long rows: chunk table, then column-blocked pieces, then the partial sums
+  if (p.n_chunks > 0 || p.n_pieces > 0) {
     float* parts = nullptr;
     const int64_t ldp = (F + 3) & ~3;
     if (p.n_parts > 0) GCN_CHECK(talloc(&parts, p.n_parts * ldp, stream, "partial rows"));
-    {
+    if (p.n_chunks > 0) {
       ProfScope ps("agg_chunk", stream);
       hipLaunchKernelGGL((k_chunk<VEC, G, Src, RELU>), dim3((unsigned)p.n_chunks, tiles),
                          dim3(kBlock), 0, stream, (const Ent*)m.ent, (const int32_t*)p.chunk_row,
@@ -676,6 +733,18 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
       if (e != hipSuccess) {
         tfree(parts, stream);
         return hip_fail(e, "k_chunk", __FILE__, __LINE__);
+      }
+    }
+    if (p.n_pieces > 0) {
+      ProfScope ps("agg_pieces", stream);
+      hipLaunchKernelGGL((k_pieces<VEC, G, Src>), dim3(blocks_for_waves(ceil_div(p.n_pieces, E)), tiles),
+                         dim3(kBlock), 0, stream, (const int64_t*)p.piece_beg,
+                         (const int32_t*)p.piece_len, (const int32_t*)p.piece_part, p.n_pieces,
+                         (const Ent*)m.ent, src, parts, ldp, F);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) {
+        tfree(parts, stream);
+        return hip_fail(e, "k_pieces", __FILE__, __LINE__);
       }
     }
     if (p.n_giant > 0) {

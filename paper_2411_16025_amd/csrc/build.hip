@@ -217,18 +217,144 @@ __global__ void k_chunks(const int32_t* __restrict__ rows, int64_t n, const int6
   if (i == n - 1) giant_part_off[n_giant] = (int32_t)part_off[n];
 }
 
+// ---- column-blocked pieces of the longest rows ----------------------------------
+
+struct BlockedCount {  // 1 for a row of at least min_len entries
+  const int32_t* rows;
+  const int64_t* ptr;
+  int64_t min_len;
+  __device__ int64_t operator()(int64_t i) const {
+    const int32_t r = rows[i];
+    return ptr[r + 1] - ptr[r] >= min_len ? 1 : 0;
+  }
+};
+
+// bnd[i * (B + 1) + k] = first entry of row rows[i] whose column is at least
+// k * width (k = 0 .. B; the columns of a row increase).
+__global__ void k_block_bounds(const int32_t* __restrict__ rows, int64_t n,
+                               const int64_t* __restrict__ ptr, const Ent* __restrict__ ent,
+                               int B, int64_t width, int64_t* __restrict__ bnd) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n * (B + 1)) return;
+  const int64_t i = t / (B + 1);
+  const int k = (int)(t % (B + 1));
+  const int32_t r = rows[i];
+  int64_t lo = ptr[r], hi = ptr[r + 1];
+  if (k == 0) {
+    bnd[t] = lo;
+    return;
+  }
+  if (k == B) {
+    bnd[t] = hi;
+    return;
+  }
+  const int64_t c = (int64_t)k * width;
+  while (lo < hi) {
+    const int64_t mid = lo + ((hi - lo) >> 1);
+    if ((int64_t)ent[mid].col < c)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  bnd[t] = lo;
+}
+
+struct RowLength {
+  const int32_t* rows;
+  const int64_t* ptr;
+  __device__ int64_t operator()(int64_t i) const {
+    const int32_t r = rows[i];
+    return ptr[r + 1] - ptr[r];
+  }
+};
+
+// Column blocks merged into one segment of a row of len entries: a row is
+// cut into about len / seg_min segments (a power of two, at most B), each
+// spanning ceil(B / segments) consecutive blocks; seg_min = 0 cuts every row
+// at every block boundary.
+__device__ inline int seg_span(int64_t len, int B, int64_t seg_min) {
+  if (seg_min <= 0) return 1;
+  const int64_t want = len / seg_min;
+  int segs = 1;
+  while (segs * 2 <= B && (int64_t)segs * 2 <= want) segs *= 2;
+  return (B + segs - 1) / segs;
+}
+
+struct PieceCount {  // pieces of the segment starting at block t % B of row t / B
+  const int64_t* bnd;
+  int B;
+  int64_t piece_max, seg_min;
+  __device__ int64_t operator()(int64_t t) const {
+    const int64_t* b = bnd + (t / B) * (B + 1);
+    const int k = (int)(t % B);
+    const int span = seg_span(b[B] - b[0], B, seg_min);
+    if (k % span) return 0;
+    const int e = k + span < B ? k + span : B;
+    return (b[e] - b[k] + piece_max - 1) / piece_max;
+  }
+};
+
+// Pieces in partial-slot order (row, segment, position): start, length and
+// the launch sort key (the segment's middle block, then decreasing length,
+// then slot). Block 0 of a row also records the row and its first partial
+// slot.
+__global__ void k_make_pieces(const int32_t* __restrict__ rows, int64_t n, int B,
+                              int64_t piece_max, int64_t seg_min, const int64_t* __restrict__ bnd,
+                              const int64_t* __restrict__ piece_off, int64_t part0,
+                              int64_t* __restrict__ tbeg, int32_t* __restrict__ tlen,
+                              uint64_t* __restrict__ keys, int32_t* __restrict__ giant_row,
+                              int32_t* __restrict__ giant_part_off) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n * B) return;
+  const int64_t i = t / B;
+  const int k = (int)(t % B);
+  const int64_t* rb = bnd + i * (B + 1);
+  const int span = seg_span(rb[B] - rb[0], B, seg_min);
+  if (k % span == 0) {
+    const int e = k + span < B ? k + span : B;
+    const uint64_t mid = (uint64_t)(k + (e - k - 1) / 2);
+    const int64_t s0 = rb[k], s1 = rb[e];
+    int64_t j = piece_off[t];
+    for (int64_t pos = s0; pos < s1; pos += piece_max, ++j) {
+      const int64_t len = s1 - pos < piece_max ? s1 - pos : piece_max;
+      tbeg[j] = pos;
+      tlen[j] = (int32_t)len;
+      keys[j] = (mid << 41) | ((uint64_t)(piece_max - len) << 32) | (uint64_t)j;
+    }
+  }
+  if (k == 0) {
+    giant_row[i] = rows[i];
+    giant_part_off[i] = (int32_t)(part0 + piece_off[t]);
+  }
+  if (t == n * B - 1) giant_part_off[n] = (int32_t)(part0 + piece_off[n * B]);
+}
+
+// launch-order piece table from the sorted keys
+__global__ void k_order_pieces(const uint64_t* __restrict__ keys, int64_t n,
+                               const int64_t* __restrict__ tbeg, const int32_t* __restrict__ tlen,
+                               int64_t part0, int64_t* __restrict__ pbeg,
+                               int32_t* __restrict__ plen, int32_t* __restrict__ ppart) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n) return;
+  const int64_t j = (int64_t)(keys[t] & 0xFFFFFFFFull);
+  pbeg[t] = tbeg[j];
+  plen[t] = tlen[j];
+  ppart[t] = (int32_t)(part0 + j);
+}
+
 // per-class count of entries whose column is >= halo_from
 __global__ void k_class_halo(const int64_t* __restrict__ ptr, const Ent* __restrict__ ent,
-                             int64_t n_major, int64_t medium_max, int64_t halo_from,
-                             unsigned long long* __restrict__ counts) {
-  __shared__ unsigned long long cnt[kNumClasses];
-  if (threadIdx.x < kNumClasses) cnt[threadIdx.x] = 0;
+                             int64_t n_major, int64_t medium_max, int64_t blocked_min,
+                             int64_t halo_from, unsigned long long* __restrict__ counts) {
+  __shared__ unsigned long long cnt[kNumClasses + 1];
+  if (threadIdx.x < kNumClasses + 1) cnt[threadIdx.x] = 0;
   __syncthreads();
   const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (r < n_major) {
     int64_t lo = ptr[r], hi = ptr[r + 1];
     const int64_t end = hi;
-    const int c = row_class(hi - lo, medium_max);
+    int c = row_class(hi - lo, medium_max);
+    if (c == kChunked && blocked_min > 0 && hi - lo >= blocked_min) c = kNumClasses;
     while (lo < hi) {  // first column >= halo_from
       const int64_t mid = (lo + hi) >> 1;
       if ((int64_t)ent[mid].col < halo_from)
@@ -239,7 +365,8 @@ __global__ void k_class_halo(const int64_t* __restrict__ ptr, const Ent* __restr
     if (end > lo) atomicAdd(&cnt[c], (unsigned long long)(end - lo));
   }
   __syncthreads();
-  if (threadIdx.x < kNumClasses && cnt[threadIdx.x]) atomicAdd(&counts[threadIdx.x], cnt[threadIdx.x]);
+  if (threadIdx.x < kNumClasses + 1 && cnt[threadIdx.x])
+    atomicAdd(&counts[threadIdx.x], cnt[threadIdx.x]);
 }
 
 // ---- normalization -------------------------------------------------------------
@@ -440,6 +567,12 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
   p.medium_max = env_int("GCN_MEDIUM_MAX", 256, 32, 1 << 20);
   p.chunk_len = env_int("GCN_CHUNK_LEN", 2048, 64, 1 << 24);
   if (p.chunk_len < p.medium_max) p.chunk_len = p.medium_max;
+  p.col_blocks = env_int("GCN_COL_BLOCKS", 64, 1, 256);
+  p.blocked_min = env_int("GCN_BLOCKED_MIN", 257, 1, (int64_t)kLenMask);
+  if (p.blocked_min <= p.medium_max) p.blocked_min = p.medium_max + 1;
+  p.piece_max = env_int("GCN_PIECE_MAX", 256, 16, 511);
+  p.seg_min = env_int("GCN_SEGMENT_MIN", 32, 0, 1 << 20);
+  const int64_t block_min_cols = env_int("GCN_BLOCK_MIN_COLS", 1 << 20, 0, 1ll << 40);
   const int64_t n = m.n_major;
   uint64_t *keys = nullptr, *sorted = nullptr;
   unsigned long long* counts = nullptr;
@@ -484,49 +617,126 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
                        (const int64_t*)m.ptr, p.rbeg, p.rlen);
     GCN_HIP(hipGetLastError());
   }
-  // chunk table over the rows of the chunked class
+  // chunked class: the longest rows (a prefix, the class being ordered by
+  // decreasing length) become column-blocked pieces when the matrix has
+  // enough columns for the gathered rows to outgrow the caches; the others
+  // get the chunk table
   const int64_t nc_rows = p.class_off[kChunked + 1] - p.class_off[kChunked];
   p.n_chunks = p.n_giant = p.n_parts = 0;
+  p.n_blocked = p.blocked_nnz = p.n_pieces = 0;
   if (nc_rows == 0) return GCN_OK;
   const int32_t* crow = p.rows + p.class_off[kChunked];
-  int64_t *chunk_off = nullptr, *part_off = nullptr, *giant_idx = nullptr, *scratch = nullptr;
-  GCN_CHECK(talloc(&chunk_off, nc_rows + 1, stream, "chunk offsets"));
-  GCN_CHECK(talloc(&part_off, nc_rows + 1, stream, "partial offsets"));
-  GCN_CHECK(talloc(&giant_idx, nc_rows + 1, stream, "giant index"));
+  const int B = (int)p.col_blocks;
+  const bool blocking = B > 1 && m.n_minor >= block_min_cols;
+  p.block_width = blocking ? ceil_div(m.n_minor, (int64_t)B) : 0;
+  int64_t* scratch = nullptr;
   GCN_CHECK(talloc(&scratch, scan_scratch_elems(nc_rows), stream, "scan scratch"));
-  GCN_CHECK(scan_functor(ChunkCount{crow, m.ptr, p.chunk_len, 0}, nc_rows, chunk_off, scratch,
-                         stream));
-  GCN_CHECK(scan_functor(ChunkCount{crow, m.ptr, p.chunk_len, 1}, nc_rows, part_off, scratch,
-                         stream));
-  GCN_CHECK(scan_functor(ChunkCount{crow, m.ptr, p.chunk_len, 2}, nc_rows, giant_idx, scratch,
-                         stream));
-  int64_t tot[3];
-  GCN_HIP(hipMemcpyAsync(&tot[0], chunk_off + nc_rows, 8, hipMemcpyDeviceToHost, stream));
-  GCN_HIP(hipMemcpyAsync(&tot[1], part_off + nc_rows, 8, hipMemcpyDeviceToHost, stream));
-  GCN_HIP(hipMemcpyAsync(&tot[2], giant_idx + nc_rows, 8, hipMemcpyDeviceToHost, stream));
+  if (blocking) {
+    int64_t* flag_off = nullptr;
+    GCN_CHECK(talloc(&flag_off, nc_rows + 1, stream, "blocked-row scan"));
+    GCN_CHECK(scan_functor(BlockedCount{crow, m.ptr, p.blocked_min}, nc_rows, flag_off, scratch,
+                           stream));
+    GCN_HIP(hipMemcpyAsync(&p.n_blocked, flag_off + nc_rows, 8, hipMemcpyDeviceToHost, stream));
+    GCN_HIP(hipStreamSynchronize(stream));
+    tfree(flag_off, stream);
+  }
+  const int64_t nb = p.n_blocked;
+  const int32_t* chrow = crow + nb;  // rows of the chunk table
+  const int64_t nch = nc_rows - nb;
+  int64_t *chunk_off = nullptr, *part_off = nullptr, *giant_idx = nullptr;
+  int64_t *bnd = nullptr, *piece_off = nullptr, *pscratch = nullptr, *len_off = nullptr;
+  int64_t tot[5] = {0, 0, 0, 0, 0};
+  if (nch > 0) {
+    GCN_CHECK(talloc(&chunk_off, nch + 1, stream, "chunk offsets"));
+    GCN_CHECK(talloc(&part_off, nch + 1, stream, "partial offsets"));
+    GCN_CHECK(talloc(&giant_idx, nch + 1, stream, "giant index"));
+    GCN_CHECK(scan_functor(ChunkCount{chrow, m.ptr, p.chunk_len, 0}, nch, chunk_off, scratch,
+                           stream));
+    GCN_CHECK(scan_functor(ChunkCount{chrow, m.ptr, p.chunk_len, 1}, nch, part_off, scratch,
+                           stream));
+    GCN_CHECK(scan_functor(ChunkCount{chrow, m.ptr, p.chunk_len, 2}, nch, giant_idx, scratch,
+                           stream));
+    GCN_HIP(hipMemcpyAsync(&tot[0], chunk_off + nch, 8, hipMemcpyDeviceToHost, stream));
+    GCN_HIP(hipMemcpyAsync(&tot[1], part_off + nch, 8, hipMemcpyDeviceToHost, stream));
+    GCN_HIP(hipMemcpyAsync(&tot[2], giant_idx + nch, 8, hipMemcpyDeviceToHost, stream));
+  }
+  if (nb > 0) {
+    GCN_CHECK(talloc(&bnd, nb * (B + 1), stream, "block bounds"));
+    GCN_CHECK(talloc(&piece_off, nb * B + 1, stream, "piece offsets"));
+    GCN_CHECK(talloc(&pscratch, scan_scratch_elems(nb * B), stream, "scan scratch"));
+    hipLaunchKernelGGL(k_block_bounds, dim3(grid_for(nb * (B + 1))), dim3(kThreads), 0, stream,
+                       crow, nb, (const int64_t*)m.ptr, (const Ent*)m.ent, B, p.block_width, bnd);
+    GCN_HIP(hipGetLastError());
+    GCN_CHECK(scan_functor(PieceCount{bnd, B, p.piece_max, p.seg_min}, nb * B, piece_off, pscratch,
+                           stream));
+    GCN_HIP(hipMemcpyAsync(&tot[3], piece_off + nb * B, 8, hipMemcpyDeviceToHost, stream));
+    // entries of the blocked rows
+    GCN_CHECK(talloc(&len_off, nb + 1, stream, "blocked entry scan"));
+    GCN_CHECK(scan_functor(RowLength{crow, m.ptr}, nb, len_off, pscratch, stream));
+    GCN_HIP(hipMemcpyAsync(&tot[4], len_off + nb, 8, hipMemcpyDeviceToHost, stream));
+  }
   GCN_HIP(hipStreamSynchronize(stream));
   p.n_chunks = tot[0];
-  p.n_parts = tot[1];
-  p.n_giant = tot[2];
+  const int64_t n_cparts = tot[1], n_cgiant = tot[2];
+  p.n_pieces = tot[3];
+  p.blocked_nnz = tot[4];
+  p.n_parts = n_cparts + p.n_pieces;
+  p.n_giant = n_cgiant + nb;
   if (p.n_parts >= (1ll << 31)) {
     set_error("too many partial rows (%lld)", (long long)p.n_parts);
     return GCN_ERANGE;
   }
-  GCN_CHECK(dalloc(&p.chunk_row, p.n_chunks, "chunk rows"));
-  GCN_CHECK(dalloc(&p.chunk_beg, p.n_chunks, "chunk starts"));
-  GCN_CHECK(dalloc(&p.chunk_end, p.n_chunks, "chunk ends"));
-  GCN_CHECK(dalloc(&p.chunk_part, p.n_chunks, "chunk partial slots"));
   GCN_CHECK(dalloc(&p.giant_row, p.n_giant, "giant rows"));
   GCN_CHECK(dalloc(&p.giant_part_off, p.n_giant + 1, "giant partial offsets"));
-  hipLaunchKernelGGL(k_chunks, dim3(grid_for(nc_rows)), dim3(kThreads), 0, stream, crow, nc_rows,
-                     m.ptr, p.chunk_len, (const int64_t*)chunk_off, (const int64_t*)part_off,
-                     (const int64_t*)giant_idx, p.chunk_row, p.chunk_beg, p.chunk_end, p.chunk_part,
-                     p.giant_row, p.giant_part_off, p.n_giant);
-  GCN_HIP(hipGetLastError());
-  tfree(scratch, stream);
+  if (nch > 0) {
+    GCN_CHECK(dalloc(&p.chunk_row, p.n_chunks, "chunk rows"));
+    GCN_CHECK(dalloc(&p.chunk_beg, p.n_chunks, "chunk starts"));
+    GCN_CHECK(dalloc(&p.chunk_end, p.n_chunks, "chunk ends"));
+    GCN_CHECK(dalloc(&p.chunk_part, p.n_chunks, "chunk partial slots"));
+    hipLaunchKernelGGL(k_chunks, dim3(grid_for(nch)), dim3(kThreads), 0, stream, chrow, nch,
+                       m.ptr, p.chunk_len, (const int64_t*)chunk_off, (const int64_t*)part_off,
+                       (const int64_t*)giant_idx, p.chunk_row, p.chunk_beg, p.chunk_end,
+                       p.chunk_part, p.giant_row, p.giant_part_off, n_cgiant);
+    GCN_HIP(hipGetLastError());
+  }
+  if (nb > 0) {
+    int64_t* tbeg = nullptr;
+    int32_t* tlen = nullptr;
+    uint64_t *keys = nullptr, *alt = nullptr;
+    GCN_CHECK(talloc(&tbeg, p.n_pieces, stream, "piece starts"));
+    GCN_CHECK(talloc(&tlen, p.n_pieces, stream, "piece lengths"));
+    GCN_CHECK(talloc(&keys, p.n_pieces, stream, "piece keys"));
+    GCN_CHECK(talloc(&alt, p.n_pieces, stream, "piece keys"));
+    hipLaunchKernelGGL(k_make_pieces, dim3(grid_for(nb * B)), dim3(kThreads), 0, stream, crow,
+                       nb, B, p.piece_max, p.seg_min, (const int64_t*)bnd,
+                       (const int64_t*)piece_off,
+                       n_cparts, tbeg, tlen, keys, p.giant_row + n_cgiant,
+                       p.giant_part_off + n_cgiant);
+    GCN_HIP(hipGetLastError());
+    // stable passes over bits [32, 56): decreasing length, then block
+    GCN_CHECK(radix_pass_u64(keys, alt, p.n_pieces, 32, stream));
+    GCN_CHECK(radix_pass_u64(alt, keys, p.n_pieces, 40, stream));
+    GCN_CHECK(radix_pass_u64(keys, alt, p.n_pieces, 48, stream));
+    GCN_CHECK(dalloc(&p.piece_beg, p.n_pieces, "piece starts"));
+    GCN_CHECK(dalloc(&p.piece_len, p.n_pieces, "piece lengths"));
+    GCN_CHECK(dalloc(&p.piece_part, p.n_pieces, "piece partial slots"));
+    hipLaunchKernelGGL(k_order_pieces, dim3(grid_for(p.n_pieces)), dim3(kThreads), 0, stream,
+                       (const uint64_t*)alt, p.n_pieces, (const int64_t*)tbeg,
+                       (const int32_t*)tlen, n_cparts, p.piece_beg, p.piece_len, p.piece_part);
+    GCN_HIP(hipGetLastError());
+    tfree(alt, stream);
+    tfree(keys, stream);
+    tfree(tlen, stream);
+    tfree(tbeg, stream);
+  }
+  tfree(len_off, stream);
+  tfree(pscratch, stream);
+  tfree(piece_off, stream);
+  tfree(bnd, stream);
   tfree(giant_idx, stream);
   tfree(part_off, stream);
   tfree(chunk_off, stream);
+  tfree(scratch, stream);
   return GCN_OK;
 }
 
@@ -541,6 +751,9 @@ void free_mat(Mat& m, bool arrays) {
   dfree(p.chunk_part);
   dfree(p.giant_row);
   dfree(p.giant_part_off);
+  dfree(p.piece_beg);
+  dfree(p.piece_len);
+  dfree(p.piece_part);
   p = Plan();
   if (arrays) {
     dfree(m.ptr);
@@ -874,15 +1087,19 @@ extern "C" gcn_status gcn_graph_bins(const gcn_graph* g, int which, int64_t halo
   }
   const Mat& m = which ? g->csc : g->csr;
   const Plan& p = m.plan;
-  unsigned long long halo[kNumClasses] = {};
+  // the chunked class is reported as two bins: chunk-table rows, then the
+  // column-blocked rows (none when the plan blocks nothing)
+  constexpr int kBins = kNumClasses + 1;
+  unsigned long long halo[kBins] = {};
+  const int64_t bmin = p.n_blocked > 0 ? p.blocked_min : 0;
   if (halo_from >= 0 && m.n_major > 0) {
     hipStream_t stream = (hipStream_t)stream_;
     unsigned long long* d = nullptr;
-    GCN_CHECK(talloc(&d, kNumClasses, stream, "halo counts"));
+    GCN_CHECK(talloc(&d, kBins, stream, "halo counts"));
     GCN_HIP(hipMemsetAsync(d, 0, sizeof(halo), stream));
     hipLaunchKernelGGL(k_class_halo, dim3(grid_for(m.n_major)), dim3(kThreads), 0, stream,
-                       (const int64_t*)m.ptr, (const Ent*)m.ent, m.n_major, p.medium_max, halo_from,
-                       d);
+                       (const int64_t*)m.ptr, (const Ent*)m.ent, m.n_major, p.medium_max, bmin,
+                       halo_from, d);
     GCN_HIP(hipGetLastError());
     GCN_HIP(hipMemcpyAsync(halo, d, sizeof(halo), hipMemcpyDeviceToHost, stream));
     tfree(d, stream);
@@ -890,13 +1107,26 @@ extern "C" gcn_status gcn_graph_bins(const gcn_graph* g, int which, int64_t halo
   }
   static const int64_t lo[kNumClasses] = {0, 1, 2, 3, 5, 9, 17, 33, -1};
   static const int64_t hi[kNumClasses] = {0, 1, 2, 4, 8, 16, 32, -1, -1};
-  for (int c = 0; c < kNumClasses && c < cap && records; ++c) {
-    records[5 * c + 0] = c == kChunked ? p.medium_max + 1 : lo[c];
-    records[5 * c + 1] = c == kMedium ? p.medium_max : hi[c];
-    records[5 * c + 2] = p.class_off[c + 1] - p.class_off[c];
-    records[5 * c + 3] = p.class_nnz[c];
-    records[5 * c + 4] = (int64_t)halo[c];
+  for (int c = 0; c < kBins && c < cap && records; ++c) {
+    int64_t* rec = records + 5 * c;
+    if (c < kChunked) {
+      rec[0] = lo[c];
+      rec[1] = c == kMedium ? p.medium_max : hi[c];
+      rec[2] = p.class_off[c + 1] - p.class_off[c];
+      rec[3] = p.class_nnz[c];
+    } else if (c == kChunked) {
+      rec[0] = p.medium_max + 1;
+      rec[1] = p.n_blocked > 0 ? p.blocked_min - 1 : -1;
+      rec[2] = p.class_off[c + 1] - p.class_off[c] - p.n_blocked;
+      rec[3] = p.class_nnz[c] - p.blocked_nnz;
+    } else {
+      rec[0] = p.blocked_min;
+      rec[1] = -1;
+      rec[2] = p.n_blocked;
+      rec[3] = p.blocked_nnz;
+    }
+    rec[4] = (int64_t)halo[c];
   }
-  if (n_classes) *n_classes = kNumClasses;
+  if (n_classes) *n_classes = kBins;
   return GCN_OK;
 }

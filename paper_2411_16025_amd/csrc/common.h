@@ -25,8 +25,9 @@ struct __align__(8) Ent {
 // bounds are in row_class in build.hip): 0 empty; 1 and 2 rows of exactly one
 // and two entries; 3..6 rows of 3-4, 5-8, 9-16 and 17-32 entries; kMedium
 // rows of 33 .. medium_max entries; kChunked longer rows, run one workgroup
-// per chunk of at most chunk_len entries. Classes 1 .. kMedium run one row
-// per lane group.
+// per chunk of at most chunk_len entries, or, from blocked_min entries on, as
+// column-blocked pieces (see Plan). Classes 1 .. kMedium run one row per lane
+// group.
 constexpr int kNumClasses = 9;
 constexpr int kClassEmpty = 0;
 constexpr int kFirstShort = 1;
@@ -51,7 +52,25 @@ struct Plan {
   int64_t* chunk_beg = nullptr;   // [n_chunks] first entry
   int64_t* chunk_end = nullptr;   // [n_chunks] one past the last entry
   int32_t* chunk_part = nullptr;  // [n_chunks] partial-row slot, -1 = writes the output row
-  // rows split over more than one chunk ("giant" rows) and their partials
+  // Column-blocked rows: the first n_blocked rows of the chunked class (those
+  // of at least blocked_min entries) are cut where the column crosses a
+  // multiple of block_width, and each segment into pieces of at most
+  // piece_max entries. The pieces run ordered by column block, so the rows
+  // the wavefronts in flight gather come from one column range and hub rows
+  // are reused in cache; every piece writes a partial row (slots from
+  // n_parts - n_pieces on, in entry order within each row).
+  int64_t col_blocks = 64;
+  int64_t blocked_min = 257;
+  int64_t piece_max = 256;
+  int64_t seg_min = 32;             // entries per segment aimed at (0: one per block)
+  int64_t block_width = 0;
+  int64_t n_blocked = 0;
+  int64_t blocked_nnz = 0;          // host: stored entries of the blocked rows
+  int64_t n_pieces = 0;
+  int64_t* piece_beg = nullptr;     // [n_pieces] first entry, in launch order
+  int32_t* piece_len = nullptr;     // [n_pieces] entries
+  int32_t* piece_part = nullptr;    // [n_pieces] partial-row slot
+  // rows summed from partial rows (multi-chunk rows, then the blocked rows)
   int64_t n_giant = 0;
   int64_t n_parts = 0;
   int32_t* giant_row = nullptr;       // [n_giant]
