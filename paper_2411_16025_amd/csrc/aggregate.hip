@@ -50,23 +50,28 @@ constexpr int kWavesPerBlock = kBlock / 64;
 // ---- gather policies ----------------------------------------------------------
 
 // Every policy splits a gather into fetch (issue the loads of features
-// [f0, f0 + VEC) of input row j into raw registers, f0 < F) and decode (turn
-// the raw registers into fp32 values). A loop issues the fetches of a whole
-// group of entries before it decodes any of them, so no load waits on the
-// arithmetic of another.
+// [f0, f0 + VEC) of input row j into raw registers) and decode (turn the raw
+// registers into fp32 values). A loop issues the fetches of a whole group of
+// entries before it decodes any of them, so no load waits on the arithmetic
+// of another. TAIL = false promises F % VEC == 0: every fetch is then one
+// unguarded vector load, and clamp() moves a lane's f0 past the row end back
+// into the row, so a loop may fetch on every lane and discard the values of
+// lanes or entries it does not use (no divergent branches around the loads).
+// TAIL = true guards each feature against F instead.
 
-template <int VEC>
+template <int VEC, bool TAIL>
 struct SrcF32 {
   const float* __restrict__ x;
-  int64_t ld;
+  uint32_t ld;  // row strides fit 32 bits (checked on the host): one 32 x 32 -> 64-bit multiply
   int F;
   struct Raw {
     float v[VEC];
   };
+  __device__ inline int clamp(int f0) const { return TAIL || f0 <= F - VEC ? f0 : F - VEC; }
   __device__ inline void fetch(int32_t j, int f0, Raw& r) const {
-    const float* p = x + (int64_t)j * ld + f0;
+    const float* p = x + (uint64_t)(uint32_t)j * ld + f0;
     if constexpr (VEC == 4) {
-      if (f0 + 4 <= F) {
+      if (!TAIL || f0 + 4 <= F) {
         const f4 v = *reinterpret_cast<const f4*>(p);
         r.v[0] = v.x; r.v[1] = v.y; r.v[2] = v.z; r.v[3] = v.w;
       } else {
@@ -85,18 +90,19 @@ struct SrcF32 {
 
 __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
-template <int VEC>
+template <int VEC, bool TAIL>
 struct SrcBF16 {
   const uint16_t* __restrict__ x;
-  int64_t ld;
+  uint32_t ld;
   int F;
   struct Raw {
     uint16_t v[VEC];
   };
+  __device__ inline int clamp(int f0) const { return TAIL || f0 <= F - VEC ? f0 : F - VEC; }
   __device__ inline void fetch(int32_t j, int f0, Raw& r) const {
-    const uint16_t* p = x + (int64_t)j * ld + f0;
+    const uint16_t* p = x + (uint64_t)(uint32_t)j * ld + f0;
     if constexpr (VEC == 4) {
-      if (f0 + 4 <= F) {
+      if (!TAIL || f0 + 4 <= F) {
         const us4 v = *reinterpret_cast<const us4*>(p);
         r.v[0] = v.x; r.v[1] = v.y; r.v[2] = v.z; r.v[3] = v.w;
       } else {
@@ -117,47 +123,44 @@ struct SrcBF16 {
 // one byte per feature; 2: four per byte) with a per-row zero point and
 // scale: x = fmaf(q, S, Z), exactly one rounding. A halo row's raw registers
 // hold the packed codes, Z and S in the slots a local row uses for its
-// features, so both kinds cost the same registers.
-template <int VEC, int BITS>
+// features, so both kinds cost the same registers (separate registers cost
+// occupancy and time).
+template <int VEC, int BITS, bool TAIL>
 struct SrcQ {
   const float* __restrict__ x;
-  int64_t ldx;
-  int64_t n_local;
+  uint32_t ldx;
+  uint32_t n_local;
   const uint8_t* __restrict__ q;
-  int64_t ldq;
+  uint32_t ldq;
   const float* __restrict__ zmin;
   const float* __restrict__ scale;
-  int64_t ldp;
-  bool paired;  // (Z, S) side by side: one 8-byte load
+  uint32_t ldp;
   int F;
   struct Raw {
     float v[VEC < 3 ? 3 : VEC];  // local: features; halo: {codes, Z, S}
   };
+  __device__ inline int clamp(int f0) const { return TAIL || f0 <= F - VEC ? f0 : F - VEC; }
   __device__ inline void fetch(int32_t j, int f0, Raw& r) const {
-    if ((int64_t)j < n_local) {
-      typename SrcF32<VEC>::Raw fr;
-      SrcF32<VEC>{x, ldx, F}.fetch(j, f0, fr);
+    if ((uint32_t)j < n_local) {
+      typename SrcF32<VEC, TAIL>::Raw fr;
+      SrcF32<VEC, TAIL>{x, ldx, F}.fetch(j, f0, fr);
 #pragma unroll
       for (int v = 0; v < VEC; ++v) r.v[v] = fr.v[v];
       return;
     }
-    const int64_t h = (int64_t)j - n_local;
-    const uint8_t* p = q + h * ldq + f0;
-    if (paired) {
-      const f2 zs = *reinterpret_cast<const f2*>(zmin + 2 * h);
-      r.v[1] = zs.x;
-      r.v[2] = zs.y;
-    } else {
-      r.v[1] = zmin[h * ldp];
-      r.v[2] = scale[h * ldp];
-    }
+    const uint32_t h = (uint32_t)j - n_local;
+    const uint8_t* qrow = q + (uint64_t)h * ldq;
+    const uint64_t po = (uint64_t)h * ldp;
+    const uint8_t* p = qrow + f0;
+    r.v[1] = zmin[po];
+    r.v[2] = scale[po];
     uint32_t c;
     if constexpr (BITS == 2) {
       // byte f0 / 4 holds the codes of features f0 .. f0 + 3 (VEC = 4: f0 % 4 == 0)
-      const uint32_t byte = q[h * ldq + (f0 >> 2)];
+      const uint32_t byte = qrow[f0 >> 2];
       c = VEC == 4 ? byte : (byte >> (2 * (f0 & 3))) & 3u;
     } else if constexpr (VEC == 4) {
-      if (f0 + 4 <= F) {
+      if (!TAIL || f0 + 4 <= F) {
         c = *reinterpret_cast<const uint32_t*>(p);
       } else {
         c = 0;
@@ -171,7 +174,7 @@ struct SrcQ {
     r.v[0] = __uint_as_float(c);
   }
   __device__ inline void decode(const Raw& r, int32_t j, float* out) const {
-    if ((int64_t)j >= n_local) {
+    if ((uint32_t)j >= n_local) {
       const uint32_t c = __float_as_uint(r.v[0]);
       constexpr int w = BITS;
       constexpr uint32_t m = (1u << BITS) - 1u;
@@ -185,10 +188,10 @@ struct SrcQ {
   }
 };
 
-template <int VEC>
-using SrcQ8 = SrcQ<VEC, 8>;
-template <int VEC>
-using SrcQ2 = SrcQ<VEC, 2>;
+template <int VEC, bool TAIL>
+using SrcQ8 = SrcQ<VEC, 8, TAIL>;
+template <int VEC, bool TAIL>
+using SrcQ2 = SrcQ<VEC, 2, TAIL>;
 
 // ---- helpers -------------------------------------------------------------------
 
@@ -242,6 +245,17 @@ __device__ inline void store_row(float* __restrict__ y, int f0, int F, const flo
 #ifndef GCN_MIN_WAVES
 #define GCN_MIN_WAVES 8
 #endif
+#ifndef GCN_PIECE_MIN_WAVES
+#define GCN_PIECE_MIN_WAVES GCN_MIN_WAVES
+#endif
+// Gathers in flight per lane in the one-run-per-slot loops of k_short and
+// k_pieces.
+#ifndef GCN_SLOT_UNROLL
+#define GCN_SLOT_UNROLL 4
+#endif
+#ifndef GCN_PIECE_UNROLL
+#define GCN_PIECE_UNROLL GCN_SLOT_UNROLL
+#endif
 #define GCN_PRAGMA(x) _Pragma(#x)
 #define GCN_UNROLL_N(n) GCN_PRAGMA(unroll n)
 
@@ -271,6 +285,7 @@ __device__ inline void accumulate_blocks(const Ent* __restrict__ ent, int64_t be
   constexpr int UU = U < G ? U : G;
   const int lane = threadIdx.x & 63;
   const int slot = lane / G;
+  const int fs = src.clamp(f0);
   int64_t base = beg + first * 64;
   const int64_t step = stride * 64;
   Ent cur = {0, 0.f};
@@ -286,21 +301,23 @@ __device__ inline void accumulate_blocks(const Ent* __restrict__ ent, int64_t be
       int32_t col[UU];
       typename Src::Raw raw[UU];
 #pragma unroll
-      for (int u = 0; u < UU; ++u) {
+      for (int u = 0; u < UU; ++u) {  // positions past n read row 0 (see accumulate_slot)
         const int pos = (p0 + u) * E + slot;
         col[u] = __shfl(cur.col, pos, 64);
         w[u] = __shfl(cur.val, pos, 64);
-        if (pos < n && active) src.fetch(col[u], f0, raw[u]);
+        src.fetch(col[u], fs, raw[u]);
       }
       // the next block's pairs travel with the first group's gathers
       if (p0 == 0 && nbase + lane < end) nxt = load_ent(ent + nbase + lane);
 #pragma unroll
       for (int u = 0; u < UU; ++u) {
-        if ((p0 + u) * E + slot < n && active) {
-          float xv[VEC];
-          src.decode(raw[u], col[u], xv);
+        float xv[VEC];
+        src.decode(raw[u], col[u], xv);
+        const bool ok = (p0 + u) * E + slot < n && active;
 #pragma unroll
-          for (int v = 0; v < VEC; ++v) acc[v] = __builtin_fmaf(w[u], xv[v], acc[v]);
+        for (int v = 0; v < VEC; ++v) {
+          const float t = __builtin_fmaf(w[u], xv[v], acc[v]);
+          acc[v] = ok ? t : acc[v];
         }
       }
     }
@@ -314,14 +331,17 @@ __device__ inline void accumulate_blocks(const Ent* __restrict__ ent, int64_t be
 // VEC - 1. The G lanes load the pairs G at a time with one coalesced access
 // (the next G travel with the current gathers) and share them by lane
 // shuffles; the loop bound is the wavefront's longest run, so every lane runs
-// the same iterations (all lanes of the wavefront must call this). Terms are
-// added in entry order.
-template <int VEC, int G, class Src>
+// the same iterations (all lanes of the wavefront must call this). Every
+// lane fetches on every iteration, positions past its run reading row 0
+// (a valid row whenever the matrix has entries) and lanes past F a clamped
+// feature offset, and a select drops those terms, so the loads are never
+// split by divergent branches. Terms are added in entry order.
+template <int VEC, int G, int U, class Src>
 __device__ inline void accumulate_slot(const Ent* __restrict__ ent, int64_t b, int len,
                                        const Src& src, int f0, bool active, float* acc) {
-  constexpr int U = 4;
   const int lane = threadIdx.x & 63;
   const int slot = lane / G, gl = lane % G;
+  const int fs = src.clamp(f0);
 #pragma unroll
   for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
   int hi = len;  // the wavefront's longest run
@@ -333,6 +353,7 @@ __device__ inline void accumulate_slot(const Ent* __restrict__ ent, int64_t b, i
     Ent nx = {0, 0.f};
     if (p0 + G + gl < len) nx = load_ent(ent + b + p0 + G + gl);
     const int np = (hi - p0) < G ? (hi - p0) : G;
+    const int nv = active ? len - p0 : 0;  // this slot's terms in the block (may be <= 0)
     for (int p = 0; p < np; p += U) {
       float w[U];
       int32_t col[U];
@@ -342,15 +363,17 @@ __device__ inline void accumulate_slot(const Ent* __restrict__ ent, int64_t b, i
         const int pos = (p + u) < G ? (p + u) : (G - 1);
         col[u] = __shfl(me.col, slot * G + pos, 64);
         w[u] = __shfl(me.val, slot * G + pos, 64);
-        if (p + u < np && p0 + p + u < len && active) src.fetch(col[u], f0, raw[u]);
+        src.fetch(col[u], fs, raw[u]);
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        if (p + u < np && p0 + p + u < len && active) {
-          float xv[VEC];
-          src.decode(raw[u], col[u], xv);
+        float xv[VEC];
+        src.decode(raw[u], col[u], xv);
+        const bool ok = p + u < nv;
 #pragma unroll
-          for (int v = 0; v < VEC; ++v) acc[v] = __builtin_fmaf(w[u], xv[v], acc[v]);
+        for (int v = 0; v < VEC; ++v) {
+          const float t = __builtin_fmaf(w[u], xv[v], acc[v]);
+          acc[v] = ok ? t : acc[v];
         }
       }
     }
@@ -415,6 +438,9 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_tiny(const int64_t* _
   const int64_t wave = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
   const int f0 = (int)blockIdx.y * G * VEC + (lane % G) * VEC;
   const bool fa = f0 < F;
+  const int fs = src.clamp(f0);
+  // slots past the last row repeat it and lanes past F read a clamped offset
+  // (see accumulate_slot), so every load is issued unconditionally
   int32_t r[R];
   int64_t b[R];
   bool has[R];
@@ -422,20 +448,20 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_tiny(const int64_t* _
   for (int g = 0; g < R; ++g) {
     const int64_t i = (wave * R + g) * E + slot;
     has[g] = i < n;
-    r[g] = has[g] ? rows[i] : 0;
-    b[g] = has[g] ? beg[i] : 0;
+    const int64_t ic = has[g] ? i : n - 1;
+    r[g] = rows[ic];
+    b[g] = beg[ic];
   }
   Ent e[R][L];
 #pragma unroll
   for (int g = 0; g < R; ++g)
 #pragma unroll
-    for (int k = 0; k < L; ++k) e[g][k] = has[g] ? load_ent(ent + b[g] + k) : Ent{0, 0.f};
+    for (int k = 0; k < L; ++k) e[g][k] = load_ent(ent + b[g] + k);
   typename Src::Raw raw[R][L];
 #pragma unroll
   for (int g = 0; g < R; ++g)
 #pragma unroll
-    for (int k = 0; k < L; ++k)
-      if (has[g] && fa) src.fetch(e[g][k].col, f0, raw[g][k]);
+    for (int k = 0; k < L; ++k) src.fetch(e[g][k].col, fs, raw[g][k]);
 #pragma unroll
   for (int g = 0; g < R; ++g) {
     if (!(has[g] && fa)) continue;
@@ -486,7 +512,7 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* 
     len = rlen[i - sa.row_off[0]];
   }
   float acc[VEC];
-  accumulate_slot<VEC, G>(ent, b, len, src, f0, active, acc);
+  accumulate_slot<VEC, G, GCN_SLOT_UNROLL>(ent, b, len, src, f0, active, acc);
   if (active) store_row<VEC, RELU>(y + (int64_t)r * ldy, f0, F, acc);
 }
 
@@ -565,7 +591,7 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_chunk(const Ent* __re
 // the plan's launch order (column block by column block, decreasing length
 // within a block); each writes its partial row.
 template <int VEC, int G, class Src>
-__global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_pieces(const int64_t* __restrict__ pbeg,
+__global__ __launch_bounds__(kBlock, GCN_PIECE_MIN_WAVES) void k_pieces(const int64_t* __restrict__ pbeg,
                                                    const int32_t* __restrict__ plen,
                                                    const int32_t* __restrict__ ppart, int64_t n,
                                                    const Ent* __restrict__ ent, Src src,
@@ -582,7 +608,7 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_pieces(const int64_t*
   const int64_t b = has ? pbeg[i] : 0;
   const int len = has ? plen[i] : 0;
   float acc[VEC];
-  accumulate_slot<VEC, G>(ent, b, len, src, f0, active, acc);
+  accumulate_slot<VEC, G, GCN_PIECE_UNROLL>(ent, b, len, src, f0, active, acc);
   if (active) store_row<VEC>(parts + (int64_t)ppart[i] * ldp, f0, F, acc);
 }
 
@@ -774,17 +800,24 @@ int lanes_for(int F, bool vec4) {
   return g;
 }
 
-template <template <int> class SrcT, bool RELU = false, class Make>
+template <class Src, bool RELU>
+gcn_status launch_vec4(const Mat& m, const Src& src, float* y, int64_t ldy, int F,
+                       hipStream_t stream) {
+  switch (lanes_for(F, true)) {
+    case 4: return launch_all<4, 4, RELU>(m, src, y, ldy, F, stream);
+    case 8: return launch_all<4, 8, RELU>(m, src, y, ldy, F, stream);
+    case 16: return launch_all<4, 16, RELU>(m, src, y, ldy, F, stream);
+    case 32: return launch_all<4, 32, RELU>(m, src, y, ldy, F, stream);
+    default: return launch_all<4, 64, RELU>(m, src, y, ldy, F, stream);
+  }
+}
+
+template <template <int, bool> class SrcT, bool RELU = false, class Make>
 gcn_status dispatch(const Mat& m, bool vec4, int F, float* y, int64_t ldy, hipStream_t stream,
                     Make make) {
-  if (!vec4) return launch_all<1, 64, RELU>(m, make(SrcT<1>{}), y, ldy, F, stream);
-  switch (lanes_for(F, true)) {
-    case 4: return launch_all<4, 4, RELU>(m, make(SrcT<4>{}), y, ldy, F, stream);
-    case 8: return launch_all<4, 8, RELU>(m, make(SrcT<4>{}), y, ldy, F, stream);
-    case 16: return launch_all<4, 16, RELU>(m, make(SrcT<4>{}), y, ldy, F, stream);
-    case 32: return launch_all<4, 32, RELU>(m, make(SrcT<4>{}), y, ldy, F, stream);
-    default: return launch_all<4, 64, RELU>(m, make(SrcT<4>{}), y, ldy, F, stream);
-  }
+  if (!vec4) return launch_all<1, 64, RELU>(m, make(SrcT<1, false>{}), y, ldy, F, stream);
+  if (F % 4 != 0) return launch_vec4<SrcT<4, true>, RELU>(m, make(SrcT<4, true>{}), y, ldy, F, stream);
+  return launch_vec4<SrcT<4, false>, RELU>(m, make(SrcT<4, false>{}), y, ldy, F, stream);
 }
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
@@ -804,6 +837,10 @@ gcn_status aggregate(const gcn_graph* g, const Mat& m, const void* X, int64_t ld
     set_error("input and output pointers must be non-NULL");
     return GCN_EINVAL;
   }
+  if (ldx > (int64_t)UINT32_MAX) {
+    set_error("ldx=%lld does not fit 32 bits", (long long)ldx);
+    return GCN_ERANGE;
+  }
   if (ldx < F || ldy < F) {
     set_error("leading dimensions must be >= F (ldx=%lld ldy=%lld F=%lld)", (long long)ldx,
               (long long)ldy, (long long)F);
@@ -820,7 +857,7 @@ gcn_status aggregate(const gcn_graph* g, const Mat& m, const void* X, int64_t ld
     const bool vec4 = yvec && aligned(X, 16) && ldx % 4 == 0;
     return dispatch<SrcF32>(m, vec4, Fi, Y, ldy, s, [&](auto t) {
       t.x = (const float*)X;
-      t.ld = ldx;
+      t.ld = (uint32_t)ldx;
       t.F = Fi;
       return t;
     });
@@ -828,7 +865,7 @@ gcn_status aggregate(const gcn_graph* g, const Mat& m, const void* X, int64_t ld
   const bool vec4 = yvec && aligned(X, 8) && ldx % 4 == 0;
   return dispatch<SrcBF16>(m, vec4, Fi, Y, ldy, s, [&](auto t) {
     t.x = (const uint16_t*)X;
-    t.ld = ldx;
+    t.ld = (uint32_t)ldx;
     t.F = Fi;
     return t;
   });
@@ -842,7 +879,7 @@ gcn_status aggregate_f32(const Mat& m, const float* X, int64_t ldx, float* Y, in
   const bool vec4 = aligned(Y, 16) && ldy % 4 == 0 && aligned(X, 16) && ldx % 4 == 0;
   auto make = [&](auto t) {
     t.x = X;
-    t.ld = ldx;
+    t.ld = (uint32_t)ldx;
     t.F = Fi;
     return t;
   };
@@ -894,6 +931,10 @@ extern "C" gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_loc
     set_error("X_local must be non-NULL with ldx >= F when n_local_cols > 0");
     return GCN_EINVAL;
   }
+  if (ldx > (int64_t)UINT32_MAX || ldq > (int64_t)UINT32_MAX || ldp > (int64_t)UINT32_MAX) {
+    set_error("ldx, ldq and ldp must fit 32 bits");
+    return GCN_ERANGE;
+  }
   const bool two_bit = (flags & GCN_Q_CODES_2BIT) != 0;
   const int64_t qbytes = two_bit ? (F + 3) / 4 : F;
   if (n_local_cols < n_in && (!Q_halo || !halo_min || !halo_scale || ldq < qbytes || ldp < 1)) {
@@ -901,21 +942,19 @@ extern "C" gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_loc
               "ldp >= 1 when halo rows exist");
     return GCN_EINVAL;
   }
-  const bool paired = ldp == 2 && halo_scale == halo_min + 1 && aligned(halo_min, 8);
   const int Fi = (int)F;
   const bool vec4 = aligned(Y, 16) && ldy % 4 == 0 && (n_local_cols == 0 ||
                     (aligned(X_local, 16) && ldx % 4 == 0)) &&
                     (n_local_cols == n_in || two_bit || (aligned(Q_halo, 4) && ldq % 4 == 0));
   auto make = [&](auto t) {
     t.x = X_local;
-    t.ldx = ldx;
-    t.n_local = n_local_cols;
+    t.ldx = (uint32_t)ldx;
+    t.n_local = (uint32_t)n_local_cols;
     t.q = Q_halo;
-    t.ldq = ldq;
+    t.ldq = (uint32_t)ldq;
     t.zmin = halo_min;
     t.scale = halo_scale;
-    t.ldp = ldp;
-    t.paired = paired;
+    t.ldp = (uint32_t)ldp;
     t.F = Fi;
     return t;
   };
