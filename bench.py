@@ -38,7 +38,10 @@ if ROOT not in sys.path:
 
 METRIC = "aggregation GB/s (% of HBM peak) + edge-features/s, fwd Â·X and bwd Âᵀ·G"
 HBM_PEAK_GBS = 8000.0
-AGG_SOURCE = os.path.join(ROOT, "paper_2411_16025_amd", "csrc", "aggregate.hip")
+# the kernels and the plan that decides their work: counters taken on other
+# sources do not describe this build
+AGG_SOURCES = [os.path.join(ROOT, "paper_2411_16025_amd", "csrc", f)
+               for f in ("aggregate.hip", "build.hip")]
 COUNTERS = os.path.join(ROOT, "profiles", "agg_counters_rmat24_q8.txt")
 
 # kernel name -> row-length classes whose rows it processes
@@ -86,9 +89,12 @@ def model_bytes(rows, entries, halo_entries, F, bits=8):
             + 4 * F * rows)
 
 
-def file_sha256(path):
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+def sources_sha256(paths):
+    h = hashlib.sha256()
+    for path in paths:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def read_counters(kernel):
@@ -101,7 +107,7 @@ def read_counters(kernel):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    if kv.get("source_sha256") != file_sha256(AGG_SOURCE) or kv.get("kernel") != kernel:
+    if kv.get("source_sha256") != sources_sha256(AGG_SOURCES) or kv.get("kernel") != kernel:
         return None
     try:
         return float(kv["fetch_bytes_per_dispatch"]) + float(kv["write_bytes_per_dispatch"])

@@ -368,12 +368,12 @@ gcn_status gcn_graph_export(const gcn_graph* g, int which, int64_t* ptr, int32_t
  * halo_from >= 0.
  *
  * The plan's bounds can be set at build time through the environment:
- * GCN_MEDIUM_MAX (longest medium row, default 64 where rows are column-blocked,
- * else 256), GCN_CHUNK_LEN (entries
- * per chunk, 2048), GCN_BLOCKED_MIN (shortest column-blocked row, 65),
- * GCN_COL_BLOCKS (column blocks, 64; 1 blocks nothing), GCN_SEGMENT_MIN
- * (entries per segment a blocked row is cut for: about len / 32 segments, a
- * power of two up to GCN_COL_BLOCKS; 0 cuts at every block), GCN_PIECE_MAX
+ * GCN_MEDIUM_MAX (longest medium row, default 48 where rows are column-blocked,
+ * else 256), GCN_CHUNK_LEN (entries per chunk, 2048), GCN_BLOCKED_MIN
+ * (shortest column-blocked row, 49), GCN_COL_BLOCKS (column blocks, 64; 1
+ * blocks nothing), GCN_SEGMENT_MIN (entries per segment a blocked row is cut
+ * for, 24: about len / 24 segments, a power of two up to GCN_COL_BLOCKS; 0
+ * cuts at every block), GCN_PIECE_MAX
  * (entries per blocked piece, 256) and GCN_BLOCK_MIN_COLS (fewest columns
  * for which rows are blocked, 2^20). Out-of-range values are ignored. */
 gcn_status gcn_graph_bins(const gcn_graph* g, int which, int64_t halo_from, int64_t* records,

@@ -567,15 +567,15 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
   p.col_blocks = env_int("GCN_COL_BLOCKS", 64, 1, 256);
   const int64_t block_min_cols = env_int("GCN_BLOCK_MIN_COLS", 1 << 20, 0, 1ll << 40);
   const bool blocking = p.col_blocks > 1 && m.n_minor >= block_min_cols;
-  // with column blocking, rows past 64 entries gain from it; without, rows up
+  // with column blocking, rows past 48 entries gain from it; without, rows up
   // to 256 entries run fastest one per lane group
-  p.medium_max = env_int("GCN_MEDIUM_MAX", blocking ? 64 : 256, 32, 1 << 20);
+  p.medium_max = env_int("GCN_MEDIUM_MAX", blocking ? 48 : 256, 32, 1 << 20);
   p.chunk_len = env_int("GCN_CHUNK_LEN", 2048, 64, 1 << 24);
   if (p.chunk_len < p.medium_max) p.chunk_len = p.medium_max;
-  p.blocked_min = env_int("GCN_BLOCKED_MIN", 65, 1, (int64_t)kLenMask);
+  p.blocked_min = env_int("GCN_BLOCKED_MIN", 49, 1, (int64_t)kLenMask);
   if (p.blocked_min <= p.medium_max) p.blocked_min = p.medium_max + 1;
   p.piece_max = env_int("GCN_PIECE_MAX", 256, 16, 511);
-  p.seg_min = env_int("GCN_SEGMENT_MIN", 32, 0, 1 << 20);
+  p.seg_min = env_int("GCN_SEGMENT_MIN", 24, 0, 1 << 20);
   // a row cut into one segment would only pay for its partial row
   if (p.blocked_min < 2 * p.seg_min) p.blocked_min = 2 * p.seg_min;
   const int64_t n = m.n_major;

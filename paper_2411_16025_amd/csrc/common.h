@@ -44,7 +44,7 @@ struct Plan {
   int32_t* rlen = nullptr;
   int64_t class_off[kNumClasses + 1] = {};  // host copy of the class boundaries in `rows`
   int64_t class_nnz[kNumClasses] = {};      // host: stored entries per class
-  int64_t medium_max = 64;                  // longest row of the medium class (256 unblocked)
+  int64_t medium_max = 48;                  // longest row of the medium class (256 unblocked)
   int64_t chunk_len = 2048;                 // entries per chunk of a chunked row
   // chunk table for rows of the chunked class
   int64_t n_chunks = 0;
@@ -60,9 +60,9 @@ struct Plan {
   // are reused in cache; every piece writes a partial row (slots from
   // n_parts - n_pieces on, in entry order within each row).
   int64_t col_blocks = 64;
-  int64_t blocked_min = 65;
+  int64_t blocked_min = 49;
   int64_t piece_max = 256;
-  int64_t seg_min = 32;             // entries per segment aimed at (0: one per block)
+  int64_t seg_min = 24;             // entries per segment aimed at (0: one per block)
   int64_t block_width = 0;
   int64_t n_blocked = 0;
   int64_t blocked_nnz = 0;          // host: stored entries of the blocked rows
