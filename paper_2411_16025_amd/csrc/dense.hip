@@ -26,6 +26,7 @@ namespace gcn {
 namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef float f2 __attribute__((ext_vector_type(2)));
 
 constexpr int kThreads = 256;
 constexpr int kTile = 64;  // C tile is kTile x kTile
@@ -194,15 +195,20 @@ __global__ __launch_bounds__(kThreads, GCN_GEMM_MIN_BLOCKS) void k_gemm_tall_v(i
                                                           int64_t ldm, bool relu, bool cvec) {
   constexpr int NB = BN / 16;
   constexpr int BL = BN / 32;  // 16-byte B loads per thread per slice
+  // LDS strides chosen so that the operand reads of a half-wavefront (16
+  // rows or columns x 2 k values) hit 32 distinct banks: rows read along k
+  // (A, and B of NT) have a stride of 2 mod 32 floats and are written with
+  // 8-byte stores; rows read along n (B of NN) have a stride of 16 mod 32
+  constexpr int AS = kKc + 2;
   constexpr int BR = OP == kNN ? kKc : BN;
-  constexpr int BC = OP == kNN ? BN + 4 : kKc + 4;
+  constexpr int BC = OP == kNN ? BN + 16 : kKc + 2;
   // the output tile is staged through the same LDS, CW columns at a time
   constexpr int CW = BN < 128 ? BN : 128;
-  constexpr int kOperands = kTile * (kKc + 4) + BR * BC;
+  constexpr int kOperands = kTile * AS + BR * BC;
   constexpr int kStage = kTile * (CW + 4);
   __shared__ __align__(16) float smem[kOperands > kStage ? kOperands : kStage];
-  auto& As = *reinterpret_cast<float (*)[kTile][kKc + 4]>(smem);
-  auto& Bs = *reinterpret_cast<float (*)[BR][BC]>(smem + kTile * (kKc + 4));
+  auto& As = *reinterpret_cast<float (*)[kTile][AS]>(smem);
+  auto& Bs = *reinterpret_cast<float (*)[BR][BC]>(smem + kTile * AS);
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int64_t m0 = (int64_t)blockIdx.x * kTile;
   const int64_t n0 = (int64_t)blockIdx.y * BN;
@@ -232,14 +238,20 @@ __global__ __launch_bounds__(kThreads, GCN_GEMM_MIN_BLOCKS) void k_gemm_tall_v(i
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int idx = t + kThreads * j, r = idx >> 3, c = (idx & 7) * 4;
-      *reinterpret_cast<f4*>(&As[r][c]) = ra[j];
+      *reinterpret_cast<f2*>(&As[r][c]) = f2{ra[j].x, ra[j].y};
+      *reinterpret_cast<f2*>(&As[r][c + 2]) = f2{ra[j].z, ra[j].w};
     }
 #pragma unroll
     for (int j = 0; j < BL; ++j) {
       const int idx = t + kThreads * j;
-      const int r = OP == kNN ? idx / (BN / 4) : idx >> 3;
-      const int c = OP == kNN ? (idx % (BN / 4)) * 4 : (idx & 7) * 4;
-      *reinterpret_cast<f4*>(&Bs[r][c]) = rb[j];
+      if (OP == kNN) {
+        const int r = idx / (BN / 4), c = (idx % (BN / 4)) * 4;
+        *reinterpret_cast<f4*>(&Bs[r][c]) = rb[j];
+      } else {
+        const int r = idx >> 3, c = (idx & 7) * 4;
+        *reinterpret_cast<f2*>(&Bs[r][c]) = f2{rb[j].x, rb[j].y};
+        *reinterpret_cast<f2*>(&Bs[r][c + 2]) = f2{rb[j].z, rb[j].w};
+      }
     }
   };
   load_slice(0);
@@ -337,8 +349,10 @@ __global__ __launch_bounds__(WAVES * 64) void k_gemm_tn_v(int64_t M, int64_t N, 
                                                           const float* __restrict__ B, int64_t ldb,
                                                           float* __restrict__ part) {
   constexpr int BM = 16 * WAVES, NT = 64 * WAVES, NB = BN / 16;
-  __shared__ __align__(16) float As[kKc][BM + 4];
-  __shared__ __align__(16) float Bs[kKc][BN + 4];
+  // row strides of 16 mod 32 floats: a half-wavefront's reads (16 columns x
+  // 2 rows) hit 32 distinct banks
+  __shared__ __align__(16) float As[kKc][BM + 16];
+  __shared__ __align__(16) float Bs[kKc][BN + 16];
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int64_t m0 = (int64_t)blockIdx.x * BM;
   const int64_t n0 = (int64_t)blockIdx.y * BN;
