@@ -584,7 +584,9 @@ def main():
         roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": read_counters(dom) if bits == 8 else None,
+                    # the committed counters describe the default workload only
+                    "traffic": (read_counters(dom) if bits == 8 and args.workload == "rmat24_q8"
+                                else None),
                     "bytes_per_launch": int(per_launch_bytes), "avg_launch_ms": round(avg_ms, 4)}
 
     out = {
