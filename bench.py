@@ -45,7 +45,9 @@ AGG_SOURCES = [os.path.join(ROOT, "paper_2411_16025_amd", "csrc", f)
 COUNTERS = os.path.join(ROOT, "profiles", "agg_counters_rmat24_q8.txt")
 
 # kernel name -> row-length classes whose rows it processes
-KERNEL_CLASSES = {"agg_zero_rows": [0], "agg_tiny": [1, 2], "agg_short": [3, 4, 5, 6],
+# (the medium class runs in k_short, or in k_medium when the library is built
+# with GCN_MEDIUM_BY_SLOTS=0; only one of the two is ever timed)
+KERNEL_CLASSES = {"agg_zero_rows": [0], "agg_tiny": [1, 2], "agg_short": [3, 4, 5, 6, 7],
                   "agg_medium": [7], "agg_chunk": [8], "agg_pieces": [9]}
 
 
@@ -589,6 +591,21 @@ def main():
                                 else None),
                     "bytes_per_launch": int(per_launch_bytes), "avg_launch_ms": round(avg_ms, 4)}
 
+    # every aggregation kernel against the same model, per pass (one forward
+    # and one transposed pass per profiled step; k_tiny is two launches a pass)
+    kernel_rooflines = {}
+    n_pass = 2 * max(args.profile_steps, 1)
+    for k, (launches, tot_ms) in agg.items():
+        if not KERNEL_CLASSES.get(k) or launches == 0:
+            continue
+        kb = 0.5 * sum(model_bytes(b["rows"], b["entries"], b["halo_entries"], F, bits)
+                       for bins in (bins_f, bins_b) for c, b in enumerate(bins)
+                       if c in KERNEL_CLASSES[k])
+        ms = tot_ms / n_pass
+        kernel_rooflines[k] = {"ms_per_pass": round(ms, 4), "modeled_GB": round(kb / 1e9, 2),
+                               "GBps": round(kb / (ms * 1e-3) / 1e9, 1),
+                               "frac": round(kb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
@@ -613,6 +630,7 @@ def main():
                                 for k, v in prof.items()},
         "row_classes": [[b["first_len"], b["last_len"], b["rows"], b["entries"]] for b in bins_f],
         "roofline": roofline,
+        "kernel_rooflines": kernel_rooflines,
     }
 
     # ---- CPU baseline: the oracle on a bounded sample of the same workload ----
