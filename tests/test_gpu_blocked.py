@@ -16,7 +16,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import assert_close, dev, host, note
+from gpu_util import assert_close, bf16_bits, bf16_round, dev, host, note
 
 pytestmark = pytest.mark.gpu
 
@@ -165,3 +165,44 @@ def test_blocking_off_by_default_on_small_matrices(G):
     with plan_env(GCN_BLOCK_MIN_COLS=0, GCN_COL_BLOCKS=1):
         g1 = G.gcn_build_csr(n, n, dev(src), dev(dst), SYM | LOOPS)
     assert G.gcn_graph_bins(g1, 0)[9]["rows"] == 0
+
+
+def test_blocked_bf16_and_relu_paths(G):
+    # bf16 inputs (the other gather policy) and an odd F (the guarded tail
+    # policy) through the pieces
+    import torch
+    note("blocked bf16 / odd F")
+    n = 1 << 14
+    src, dst = synth.rmat_edges(390, n, 24 * n, perm_seed=391)
+    og = oracle.Graph(n, n, src, dst, SYM | LOOPS)
+    g = build(G, n, n, src, dst, SYM | LOOPS, GCN_COL_BLOCKS=32, GCN_SEGMENT_MIN=8)
+    assert check_bins(G, g)[9]["rows"] > 0
+    X = synth.uniform(392, n, 128)
+    Xb = torch.from_numpy(bf16_bits(X).view(np.int16)).view(torch.bfloat16).to("cuda:0")
+    assert_close(host(G.gcn_aggregate_fwd(g, Xb)), *og.fwd(bf16_round(X)), what="bf16 fwd")
+    assert_close(host(G.gcn_aggregate_bwd(g, Xb)), *og.bwd(bf16_round(X)), what="bf16 bwd")
+    for F in (47, 130):
+        X = synth.uniform(393 + F, n, F)
+        assert_close(host(G.gcn_aggregate_fwd(g, dev(X))), *og.fwd(X), what="F=%d" % F)
+
+
+def test_blocked_gcn_step(G):
+    # the 2-layer GCN step (ReLU fused into the partial-row reduction) on a
+    # column-blocked graph
+    from test_gpu_dense import _step_check
+    note("blocked gcn step")
+    n = 3000
+    src, dst = synth.rmat_edges(395, n, 12 * n, perm_seed=396)
+    w = synth.Workload("rmat3000", n, n, src, dst, SYM | LOOPS, 100)
+    with plan_env(GCN_BLOCK_MIN_COLS=0, GCN_COL_BLOCKS=16, GCN_SEGMENT_MIN=8):
+        _step_check(G, w, 100, 256, 47, 13)
+
+
+@pytest.mark.parametrize("lp", [False, True])
+def test_blocked_sage_step(G, lp):
+    # the GraphSAGE step (mean values, strided Z blocks, F = 100 and 64) on a
+    # column-blocked graph
+    from test_gpu_sage import check_step
+    note("blocked sage step lp=%s" % lp)
+    with plan_env(GCN_BLOCK_MIN_COLS=0, GCN_COL_BLOCKS=16, GCN_SEGMENT_MIN=8):
+        check_step(G, 3000, 36000, 100, 64, 10, 397, lp)
