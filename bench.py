@@ -39,7 +39,7 @@ if ROOT not in sys.path:
 METRIC = "aggregation GB/s (% of HBM peak) + edge-features/s, fwd Â·X and bwd Âᵀ·G"
 HBM_PEAK_GBS = 8000.0
 # the kernels and the plan that decides their work: counters taken on other
-# sources do not describe this build
+# sources do not describe the library being timed
 AGG_SOURCES = [os.path.join(ROOT, "paper_2411_16025_amd", "csrc", f)
                for f in ("aggregate.hip", "build.hip")]
 COUNTERS = os.path.join(ROOT, "profiles", "agg_counters_rmat24_q8.txt")
@@ -414,8 +414,8 @@ def run_producer(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: the aggregation path is built and timed on a "
-              "single MI355X (multi-GPU sharding is a design note, not part of this build); "
+        print("bench.py measures one GPU only: the aggregation path runs and is timed on a "
+              "single MI355X (sharding across GPUs is designed, not implemented); "
               "run with --gpus 1", file=sys.stderr)
         sys.exit(2)
     if args.workload == "gcn_step":

@@ -56,8 +56,8 @@ def lib():
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
-            raise RuntimeError("libgcnagg.so is not built (%s); run __graft_entry__.build()"
-                               % LIB_PATH)
+            raise RuntimeError("libgcnagg.so is not built (%s); run "
+                               "paper_2411_16025_amd.build.build()" % LIB_PATH)
         L = ctypes.CDLL(LIB_PATH)
         P, i64, u32, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint32, ctypes.c_int
         L.gcn_build_csr.argtypes = [i64, i64, i64, P, P, u32, P, ctypes.POINTER(P)]
