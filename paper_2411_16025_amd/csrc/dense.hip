@@ -180,6 +180,11 @@ __device__ inline f4 load4(const float* __restrict__ p, int64_t row, int64_t row
 #ifndef GCN_GEMM_MIN_BLOCKS
 #define GCN_GEMM_MIN_BLOCKS 2
 #endif
+// Workgroups per CU the 64- and 128-column tiles must fit (fewer registers,
+// more waves to overlap LDS and global latency).
+#ifndef GCN_GEMM_MIN_BLOCKS_NARROW
+#define GCN_GEMM_MIN_BLOCKS_NARROW 4
+#endif
 #ifndef GCN_GEMM_KK_UNROLL
 #define GCN_GEMM_KK_UNROLL 8
 #endif
@@ -187,7 +192,7 @@ __device__ inline f4 load4(const float* __restrict__ p, int64_t row, int64_t row
 #define GCN_GEMM_UNROLL(n) GCN_GEMM_PRAGMA(unroll n)
 
 template <int OP, int BN>
-__global__ __launch_bounds__(kThreads, GCN_GEMM_MIN_BLOCKS) void k_gemm_tall_v(int64_t M, int64_t N, int64_t K,
+__global__ __launch_bounds__(kThreads, BN == 256 ? GCN_GEMM_MIN_BLOCKS : GCN_GEMM_MIN_BLOCKS_NARROW) void k_gemm_tall_v(int64_t M, int64_t N, int64_t K,
                                                           const float* __restrict__ A, int64_t lda,
                                                           const float* __restrict__ B, int64_t ldb,
                                                           float* __restrict__ C, int64_t ldc,
@@ -520,13 +525,21 @@ namespace {
 bool aligned16(const void* p, int64_t ld) { return ((uintptr_t)p % 16) == 0 && ld % 4 == 0; }
 
 // widest tile of 64, 128 or 256 columns that is not mostly padding
+// Output tile widths. C = A B: 256 columns once N > 128 (A is read once per
+// tile column). C = A B^T: 128 or 256, whichever pads N less (256 on a tie).
+// C = A^T B: at most 128, for twice the workgroups per K chunk.
 int tile_n(int64_t N) { return N <= 64 ? 64 : (N <= 128 ? 128 : 256); }
+int tile_n_nt(int64_t N) {
+  if (N <= 128) return tile_n(N);
+  return ceil_div(N, (int64_t)128) * 128 < ceil_div(N, (int64_t)256) * 256 ? 128 : 256;
+}
+int tile_n_tn(int64_t N) { return N <= 64 ? 64 : 128; }
 
 template <int OP>
 void launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
                  int64_t ldb, float* C, int64_t ldc, const float* mask, int64_t ldm,
                  bool relu, hipStream_t stream) {
-  const int bn = tile_n(N);
+  const int bn = OP == kNN ? tile_n(N) : tile_n_nt(N);
   // staged 16-byte stores need 16-byte aligned rows of C (and of the mask)
   const bool cvec = aligned16(C, ldc) && (!mask || aligned16(mask, ldm));
   const dim3 grid((unsigned)ceil_div(M, kTile), (unsigned)ceil_div(N, bn));
@@ -544,16 +557,13 @@ void launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, c
 void launch_tn(int64_t M, int64_t N, int64_t K, int64_t split, int64_t n_chunks, const float* A,
                int64_t lda, const float* B, int64_t ldb, float* part, hipStream_t stream) {
   constexpr int kWaves = 8, kBm = 16 * kWaves;
-  const int bn = tile_n(N);
+  const int bn = tile_n_tn(N);
   const dim3 grid((unsigned)ceil_div(M, kBm), (unsigned)ceil_div(N, bn), (unsigned)n_chunks);
   if (bn == 64)
     hipLaunchKernelGGL((k_gemm_tn_v<kWaves, 64>), grid, dim3(64 * kWaves), 0, stream, M, N, K,
                        split, A, lda, B, ldb, part);
-  else if (bn == 128)
-    hipLaunchKernelGGL((k_gemm_tn_v<kWaves, 128>), grid, dim3(64 * kWaves), 0, stream, M, N, K,
-                       split, A, lda, B, ldb, part);
   else
-    hipLaunchKernelGGL((k_gemm_tn_v<kWaves, 256>), grid, dim3(64 * kWaves), 0, stream, M, N, K,
+    hipLaunchKernelGGL((k_gemm_tn_v<kWaves, 128>), grid, dim3(64 * kWaves), 0, stream, M, N, K,
                        split, A, lda, B, ldb, part);
 }
 
