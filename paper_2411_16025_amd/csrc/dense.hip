@@ -526,30 +526,26 @@ bool aligned16(const void* p, int64_t ld) { return ((uintptr_t)p % 16) == 0 && l
 
 // widest tile of 64, 128 or 256 columns that is not mostly padding
 // Output tile widths. C = A B: 256 columns once N > 128 (A is read once per
-// tile column). C = A B^T: 128 or 256, whichever pads N less (256 on a tie).
-// C = A^T B: at most 128, for twice the workgroups per K chunk.
+// tile column). C = A B^T and C = A^T B: at most 128 (more workgroups at 4
+// per CU, and less padding of odd widths, outweigh the extra reads of A).
 int tile_n(int64_t N) { return N <= 64 ? 64 : (N <= 128 ? 128 : 256); }
-int tile_n_nt(int64_t N) {
-  if (N <= 128) return tile_n(N);
-  return ceil_div(N, (int64_t)128) * 128 < ceil_div(N, (int64_t)256) * 256 ? 128 : 256;
-}
-int tile_n_tn(int64_t N) { return N <= 64 ? 64 : 128; }
+int tile_n_narrow(int64_t N) { return N <= 64 ? 64 : 128; }
 
 template <int OP>
 void launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
                  int64_t ldb, float* C, int64_t ldc, const float* mask, int64_t ldm,
                  bool relu, hipStream_t stream) {
-  const int bn = OP == kNN ? tile_n(N) : tile_n_nt(N);
+  const int bn = OP == kNN ? tile_n(N) : tile_n_narrow(N);
   // staged 16-byte stores need 16-byte aligned rows of C (and of the mask)
   const bool cvec = aligned16(C, ldc) && (!mask || aligned16(mask, ldm));
   const dim3 grid((unsigned)ceil_div(M, kTile), (unsigned)ceil_div(N, bn));
   if (bn == 64)
     hipLaunchKernelGGL((k_gemm_tall_v<OP, 64>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda, B,
                        ldb, C, ldc, mask, ldm, relu, cvec);
-  else if (bn == 128)
+  else if (OP != kNN || bn == 128)
     hipLaunchKernelGGL((k_gemm_tall_v<OP, 128>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda,
                        B, ldb, C, ldc, mask, ldm, relu, cvec);
-  else
+  else if constexpr (OP == kNN)
     hipLaunchKernelGGL((k_gemm_tall_v<OP, 256>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda,
                        B, ldb, C, ldc, mask, ldm, relu, cvec);
 }
@@ -557,7 +553,7 @@ void launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, c
 void launch_tn(int64_t M, int64_t N, int64_t K, int64_t split, int64_t n_chunks, const float* A,
                int64_t lda, const float* B, int64_t ldb, float* part, hipStream_t stream) {
   constexpr int kWaves = 8, kBm = 16 * kWaves;
-  const int bn = tile_n_tn(N);
+  const int bn = tile_n_narrow(N);
   const dim3 grid((unsigned)ceil_div(M, kBm), (unsigned)ceil_div(N, bn), (unsigned)n_chunks);
   if (bn == 64)
     hipLaunchKernelGGL((k_gemm_tn_v<kWaves, 64>), grid, dim3(64 * kWaves), 0, stream, M, N, K,
