@@ -564,6 +564,7 @@ gcn_status transpose_csr(const Mat& a, const int32_t* a_major, Mat& t, hipStream
 
 gcn_status build_plan(Mat& m, hipStream_t stream) {
   Plan& p = m.plan;
+  TempScope tmp(stream);
   p.col_blocks = env_int("GCN_COL_BLOCKS", 64, 1, 256);
   const int64_t block_min_cols = env_int("GCN_BLOCK_MIN_COLS", 1 << 20, 0, 1ll << 40);
   const bool blocking = p.col_blocks > 1 && m.n_minor >= block_min_cols;
@@ -581,9 +582,9 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
   const int64_t n = m.n_major;
   uint64_t *keys = nullptr, *sorted = nullptr;
   unsigned long long* counts = nullptr;
-  GCN_CHECK(talloc(&keys, n, stream, "class keys"));
-  GCN_CHECK(talloc(&sorted, n, stream, "class keys"));
-  GCN_CHECK(talloc(&counts, 2 * kNumClasses, stream, "class counts"));
+  GCN_CHECK(tmp.alloc(&keys, n, "class keys"));
+  GCN_CHECK(tmp.alloc(&sorted, n, "class keys"));
+  GCN_CHECK(tmp.alloc(&counts, 2 * kNumClasses, "class counts"));
   GCN_CHECK(dalloc(&p.rows, n, "class rows"));
   GCN_HIP(hipMemsetAsync(counts, 0, 2 * kNumClasses * sizeof(unsigned long long), stream));
   hipLaunchKernelGGL(k_class_keys, dim3(grid_for(n)), dim3(kThreads), 0, stream, m.ptr, n,
@@ -603,9 +604,6 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
   unsigned long long host_counts[2 * kNumClasses];
   GCN_HIP(hipMemcpyAsync(host_counts, counts, sizeof(host_counts), hipMemcpyDeviceToHost, stream));
   GCN_HIP(hipStreamSynchronize(stream));
-  tfree(counts, stream);
-  tfree(sorted, stream);
-  tfree(keys, stream);
   p.class_off[0] = 0;
   for (int c = 0; c < kNumClasses; ++c) {
     p.class_off[c + 1] = p.class_off[c] + (int64_t)host_counts[c];
@@ -634,15 +632,14 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
   const int B = (int)p.col_blocks;
   p.block_width = blocking ? ceil_div(m.n_minor, (int64_t)B) : 0;
   int64_t* scratch = nullptr;
-  GCN_CHECK(talloc(&scratch, scan_scratch_elems(nc_rows), stream, "scan scratch"));
+  GCN_CHECK(tmp.alloc(&scratch, scan_scratch_elems(nc_rows), "scan scratch"));
   if (blocking) {
     int64_t* flag_off = nullptr;
-    GCN_CHECK(talloc(&flag_off, nc_rows + 1, stream, "blocked-row scan"));
+    GCN_CHECK(tmp.alloc(&flag_off, nc_rows + 1, "blocked-row scan"));
     GCN_CHECK(scan_functor(BlockedCount{crow, m.ptr, p.blocked_min}, nc_rows, flag_off, scratch,
                            stream));
     GCN_HIP(hipMemcpyAsync(&p.n_blocked, flag_off + nc_rows, 8, hipMemcpyDeviceToHost, stream));
     GCN_HIP(hipStreamSynchronize(stream));
-    tfree(flag_off, stream);
   }
   const int64_t nb = p.n_blocked;
   const int32_t* chrow = crow + nb;  // rows of the chunk table
@@ -651,9 +648,9 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
   int64_t *bnd = nullptr, *piece_off = nullptr, *pscratch = nullptr, *len_off = nullptr;
   int64_t tot[5] = {0, 0, 0, 0, 0};
   if (nch > 0) {
-    GCN_CHECK(talloc(&chunk_off, nch + 1, stream, "chunk offsets"));
-    GCN_CHECK(talloc(&part_off, nch + 1, stream, "partial offsets"));
-    GCN_CHECK(talloc(&giant_idx, nch + 1, stream, "giant index"));
+    GCN_CHECK(tmp.alloc(&chunk_off, nch + 1, "chunk offsets"));
+    GCN_CHECK(tmp.alloc(&part_off, nch + 1, "partial offsets"));
+    GCN_CHECK(tmp.alloc(&giant_idx, nch + 1, "giant index"));
     GCN_CHECK(scan_functor(ChunkCount{chrow, m.ptr, p.chunk_len, 0}, nch, chunk_off, scratch,
                            stream));
     GCN_CHECK(scan_functor(ChunkCount{chrow, m.ptr, p.chunk_len, 1}, nch, part_off, scratch,
@@ -665,9 +662,9 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
     GCN_HIP(hipMemcpyAsync(&tot[2], giant_idx + nch, 8, hipMemcpyDeviceToHost, stream));
   }
   if (nb > 0) {
-    GCN_CHECK(talloc(&bnd, nb * (B + 1), stream, "block bounds"));
-    GCN_CHECK(talloc(&piece_off, nb * B + 1, stream, "piece offsets"));
-    GCN_CHECK(talloc(&pscratch, scan_scratch_elems(nb * B), stream, "scan scratch"));
+    GCN_CHECK(tmp.alloc(&bnd, nb * (B + 1), "block bounds"));
+    GCN_CHECK(tmp.alloc(&piece_off, nb * B + 1, "piece offsets"));
+    GCN_CHECK(tmp.alloc(&pscratch, scan_scratch_elems(nb * B), "scan scratch"));
     hipLaunchKernelGGL(k_block_bounds, dim3(grid_for(nb * (B + 1))), dim3(kThreads), 0, stream,
                        crow, nb, (const int64_t*)m.ptr, (const Ent*)m.ent, B, p.block_width, bnd);
     GCN_HIP(hipGetLastError());
@@ -675,7 +672,7 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
                            stream));
     GCN_HIP(hipMemcpyAsync(&tot[3], piece_off + nb * B, 8, hipMemcpyDeviceToHost, stream));
     // entries of the blocked rows
-    GCN_CHECK(talloc(&len_off, nb + 1, stream, "blocked entry scan"));
+    GCN_CHECK(tmp.alloc(&len_off, nb + 1, "blocked entry scan"));
     GCN_CHECK(scan_functor(RowLength{crow, m.ptr}, nb, len_off, pscratch, stream));
     GCN_HIP(hipMemcpyAsync(&tot[4], len_off + nb, 8, hipMemcpyDeviceToHost, stream));
   }
@@ -707,10 +704,10 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
     int64_t* tbeg = nullptr;
     int32_t* tlen = nullptr;
     uint64_t *keys = nullptr, *alt = nullptr;
-    GCN_CHECK(talloc(&tbeg, p.n_pieces, stream, "piece starts"));
-    GCN_CHECK(talloc(&tlen, p.n_pieces, stream, "piece lengths"));
-    GCN_CHECK(talloc(&keys, p.n_pieces, stream, "piece keys"));
-    GCN_CHECK(talloc(&alt, p.n_pieces, stream, "piece keys"));
+    GCN_CHECK(tmp.alloc(&tbeg, p.n_pieces, "piece starts"));
+    GCN_CHECK(tmp.alloc(&tlen, p.n_pieces, "piece lengths"));
+    GCN_CHECK(tmp.alloc(&keys, p.n_pieces, "piece keys"));
+    GCN_CHECK(tmp.alloc(&alt, p.n_pieces, "piece keys"));
     hipLaunchKernelGGL(k_make_pieces, dim3(grid_for(nb * B)), dim3(kThreads), 0, stream, crow,
                        nb, B, p.piece_max, p.seg_min, (const int64_t*)bnd,
                        (const int64_t*)piece_off,
@@ -728,19 +725,7 @@ gcn_status build_plan(Mat& m, hipStream_t stream) {
                        (const uint64_t*)alt, p.n_pieces, (const int64_t*)tbeg,
                        (const int32_t*)tlen, n_cparts, p.piece_beg, p.piece_len, p.piece_part);
     GCN_HIP(hipGetLastError());
-    tfree(alt, stream);
-    tfree(keys, stream);
-    tfree(tlen, stream);
-    tfree(tbeg, stream);
   }
-  tfree(len_off, stream);
-  tfree(pscratch, stream);
-  tfree(piece_off, stream);
-  tfree(bnd, stream);
-  tfree(giant_idx, stream);
-  tfree(part_off, stream);
-  tfree(chunk_off, stream);
-  tfree(scratch, stream);
   return GCN_OK;
 }
 
@@ -1063,10 +1048,11 @@ extern "C" gcn_status gcn_graph_export(const gcn_graph* g, int which, int64_t* p
     GCN_HIP(hipMemcpyAsync(ptr, m.ptr, (m.n_major + 1) * sizeof(int64_t), hipMemcpyDeviceToHost,
                            stream));
   if ((idx || val) && m.nnz > 0) {
+    TempScope tmp(stream);
     int32_t* didx = nullptr;
     float* dval = nullptr;
-    GCN_CHECK(talloc(&didx, m.nnz, stream, "export columns"));
-    GCN_CHECK(talloc(&dval, m.nnz, stream, "export values"));
+    GCN_CHECK(tmp.alloc(&didx, m.nnz, "export columns"));
+    GCN_CHECK(tmp.alloc(&dval, m.nnz, "export values"));
     hipLaunchKernelGGL(k_split, dim3(grid_for(m.nnz)), dim3(kThreads), 0, stream,
                        (const Ent*)m.ent, m.nnz, didx, dval);
     GCN_HIP(hipGetLastError());
@@ -1074,8 +1060,6 @@ extern "C" gcn_status gcn_graph_export(const gcn_graph* g, int which, int64_t* p
       GCN_HIP(hipMemcpyAsync(idx, didx, m.nnz * sizeof(int32_t), hipMemcpyDeviceToHost, stream));
     if (val)
       GCN_HIP(hipMemcpyAsync(val, dval, m.nnz * sizeof(float), hipMemcpyDeviceToHost, stream));
-    tfree(dval, stream);
-    tfree(didx, stream);
   }
   GCN_HIP(hipStreamSynchronize(stream));
   return GCN_OK;
@@ -1098,15 +1082,15 @@ extern "C" gcn_status gcn_graph_bins(const gcn_graph* g, int which, int64_t halo
   const int64_t bmin = p.n_blocked > 0 ? p.blocked_min : 0;
   if (halo_from >= 0 && m.n_major > 0) {
     hipStream_t stream = (hipStream_t)stream_;
+    TempScope tmp(stream);
     unsigned long long* d = nullptr;
-    GCN_CHECK(talloc(&d, kBins, stream, "halo counts"));
+    GCN_CHECK(tmp.alloc(&d, kBins, "halo counts"));
     GCN_HIP(hipMemsetAsync(d, 0, sizeof(halo), stream));
     hipLaunchKernelGGL(k_class_halo, dim3(grid_for(m.n_major)), dim3(kThreads), 0, stream,
                        (const int64_t*)m.ptr, (const Ent*)m.ent, m.n_major, p.medium_max, bmin,
                        halo_from, d);
     GCN_HIP(hipGetLastError());
     GCN_HIP(hipMemcpyAsync(halo, d, sizeof(halo), hipMemcpyDeviceToHost, stream));
-    tfree(d, stream);
     GCN_HIP(hipStreamSynchronize(stream));
   }
   static const int64_t lo[kNumClasses] = {0, 1, 2, 3, 5, 9, 17, 33, -1};

@@ -133,6 +133,30 @@ gcn_status talloc(T** p, int64_t count, hipStream_t stream, const char* what) {
 }
 void tfree(void* p, hipStream_t stream);
 
+// Stream-ordered temporaries released when the scope ends, on every return
+// path (error returns included).
+struct TempScope {
+  hipStream_t stream;
+  void* ptrs[32];
+  int n = 0;
+  explicit TempScope(hipStream_t s) : stream(s) {}
+  TempScope(const TempScope&) = delete;
+  TempScope& operator=(const TempScope&) = delete;
+  ~TempScope() {
+    for (int i = n - 1; i >= 0; --i) tfree(ptrs[i], stream);
+  }
+  template <class T>
+  gcn_status alloc(T** p, int64_t count, const char* what) {
+    if (n == 32) {
+      set_error("too many temporaries for %s", what);
+      return GCN_ENOMEM;
+    }
+    GCN_CHECK(talloc(p, count, stream, what));
+    ptrs[n++] = *p;
+    return GCN_OK;
+  }
+};
+
 gcn_status check_graph(const gcn_graph* g);
 
 // ---- per-kernel profiling (see gcn_profile_enable) --------------------------
