@@ -591,11 +591,10 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_chunk(const Ent* __re
 // the plan's launch order (column block by column block, decreasing length
 // within a block); each writes its partial row.
 template <int VEC, int G, class Src>
-__global__ __launch_bounds__(kBlock, GCN_PIECE_MIN_WAVES) void k_pieces(const int64_t* __restrict__ pbeg,
-                                                   const int32_t* __restrict__ plen,
-                                                   const int32_t* __restrict__ ppart, int64_t n,
-                                                   const Ent* __restrict__ ent, Src src,
-                                                   float* __restrict__ parts, int64_t ldp, int F) {
+__global__ __launch_bounds__(kBlock, GCN_PIECE_MIN_WAVES)
+void k_pieces(const int64_t* __restrict__ pbeg, const int32_t* __restrict__ plen,
+              const int32_t* __restrict__ ppart, int64_t n, const Ent* __restrict__ ent, Src src,
+              float* __restrict__ parts, int64_t ldp, int F) {
   constexpr int E = 64 / G;
   const int lane = threadIdx.x & 63;
   const int slot = lane / G, gl = lane % G;
@@ -763,7 +762,8 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
     }
     if (p.n_pieces > 0) {
       ProfScope ps("agg_pieces", stream);
-      hipLaunchKernelGGL((k_pieces<VEC, G, Src>), dim3(blocks_for_waves(ceil_div(p.n_pieces, E)), tiles),
+      hipLaunchKernelGGL((k_pieces<VEC, G, Src>),
+                         dim3(blocks_for_waves(ceil_div(p.n_pieces, E)), tiles),
                          dim3(kBlock), 0, stream, (const int64_t*)p.piece_beg,
                          (const int32_t*)p.piece_len, (const int32_t*)p.piece_part, p.n_pieces,
                          (const Ent*)m.ent, src, parts, ldp, F);

@@ -192,12 +192,11 @@ __device__ inline f4 load4(const float* __restrict__ p, int64_t row, int64_t row
 #define GCN_GEMM_UNROLL(n) GCN_GEMM_PRAGMA(unroll n)
 
 template <int OP, int BN>
-__global__ __launch_bounds__(kThreads, BN == 256 ? GCN_GEMM_MIN_BLOCKS : GCN_GEMM_MIN_BLOCKS_NARROW) void k_gemm_tall_v(int64_t M, int64_t N, int64_t K,
-                                                          const float* __restrict__ A, int64_t lda,
-                                                          const float* __restrict__ B, int64_t ldb,
-                                                          float* __restrict__ C, int64_t ldc,
-                                                          const float* __restrict__ mask,
-                                                          int64_t ldm, bool relu, bool cvec) {
+__global__ __launch_bounds__(kThreads,
+                             BN == 256 ? GCN_GEMM_MIN_BLOCKS : GCN_GEMM_MIN_BLOCKS_NARROW)
+void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A, int64_t lda,
+                   const float* __restrict__ B, int64_t ldb, float* __restrict__ C, int64_t ldc,
+                   const float* __restrict__ mask, int64_t ldm, bool relu, bool cvec) {
   constexpr int NB = BN / 16;
   constexpr int BL = BN / 32;  // 16-byte B loads per thread per slice
   // LDS strides chosen so that the operand reads of a half-wavefront (16
