@@ -790,11 +790,14 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
   return GCN_OK;
 }
 
-// Lanes per slot: smallest power of two covering min(F, 256) features with
-// 4-float lanes (at least 4 lanes); the scalar path always uses 64 lanes.
+// Lanes per slot: smallest power of two covering min(F, 128) features with
+// 4-float lanes (at least 4 lanes); wider rows run as 128-feature tiles
+// (blockIdx.y), which beats one slot of 64 lanes per wavefront (F = 256:
+// 5% on the product-shaped graph, 16 lanes for F = 128 lose 9%); the scalar
+// path always uses 64 lanes.
 int lanes_for(int F, bool vec4) {
   if (!vec4) return 64;
-  const int need = (std::min(F, 256) + 3) / 4;
+  const int need = (std::min(F, 128) + 3) / 4;
   int g = 4;
   while (g < need) g <<= 1;
   return g;
@@ -807,8 +810,7 @@ gcn_status launch_vec4(const Mat& m, const Src& src, float* y, int64_t ldy, int 
     case 4: return launch_all<4, 4, RELU>(m, src, y, ldy, F, stream);
     case 8: return launch_all<4, 8, RELU>(m, src, y, ldy, F, stream);
     case 16: return launch_all<4, 16, RELU>(m, src, y, ldy, F, stream);
-    case 32: return launch_all<4, 32, RELU>(m, src, y, ldy, F, stream);
-    default: return launch_all<4, 64, RELU>(m, src, y, ldy, F, stream);
+    default: return launch_all<4, 32, RELU>(m, src, y, ldy, F, stream);
   }
 }
 
