@@ -814,12 +814,18 @@ gcn_status launch_vec4(const Mat& m, const Src& src, float* y, int64_t ldy, int 
   }
 }
 
+// pad_ok: every input row may be read up to a multiple of 4 features (its
+// stride leaves room), so an odd F still takes the unguarded 16-byte loads;
+// the extra features are never stored.
 template <template <int, bool> class SrcT, bool RELU = false, class Make>
 gcn_status dispatch(const Mat& m, bool vec4, int F, float* y, int64_t ldy, hipStream_t stream,
-                    Make make) {
+                    Make make, bool pad_ok = false) {
   if (!vec4) return launch_all<1, 64, RELU>(m, make(SrcT<1, false>{}), y, ldy, F, stream);
-  if (F % 4 != 0) return launch_vec4<SrcT<4, true>, RELU>(m, make(SrcT<4, true>{}), y, ldy, F, stream);
-  return launch_vec4<SrcT<4, false>, RELU>(m, make(SrcT<4, false>{}), y, ldy, F, stream);
+  if (F % 4 != 0 && !pad_ok)
+    return launch_vec4<SrcT<4, true>, RELU>(m, make(SrcT<4, true>{}), y, ldy, F, stream);
+  auto src = make(SrcT<4, false>{});
+  src.F = (F + 3) & ~3;  // the width the loads may cover; F bounds the stores
+  return launch_vec4<SrcT<4, false>, RELU>(m, src, y, ldy, F, stream);
 }
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
@@ -885,8 +891,10 @@ gcn_status aggregate_f32(const Mat& m, const float* X, int64_t ldx, float* Y, in
     t.F = Fi;
     return t;
   };
-  return relu ? dispatch<SrcF32, true>(m, vec4, Fi, Y, ldy, stream, make)
-              : dispatch<SrcF32, false>(m, vec4, Fi, Y, ldy, stream, make);
+  // the training steps keep their feature rows at strides of a multiple of 4
+  const bool pad_ok = ldx >= ((F + 3) & ~int64_t(3));
+  return relu ? dispatch<SrcF32, true>(m, vec4, Fi, Y, ldy, stream, make, pad_ok)
+              : dispatch<SrcF32, false>(m, vec4, Fi, Y, ldy, stream, make, pad_ok);
 }
 
 }  // namespace gcn
