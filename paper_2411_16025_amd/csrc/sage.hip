@@ -88,6 +88,7 @@ __global__ __launch_bounds__(kThreadsS) void k_unpack_grads(int64_t f, int64_t z
 }
 
 // Masked label propagation, forward: Xp = X + E[y] on rows with mask = 1.
+// One row per wavefront, the lanes striding over its features.
 __global__ __launch_bounds__(kThreadsS) void k_embed_labels(int64_t n, int64_t f, int C,
                                                             const float* __restrict__ x,
                                                             int64_t ldx,
@@ -95,45 +96,39 @@ __global__ __launch_bounds__(kThreadsS) void k_embed_labels(int64_t n, int64_t f
                                                             const int32_t* __restrict__ y,
                                                             const float* __restrict__ e,
                                                             float* __restrict__ xp, int64_t ldp) {
-  const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
-  if (t >= n * f) return;
-  const int64_t i = t / f, c = t % f;
-  float v = x[i * ldx + c];
+  const int64_t i = (int64_t)blockIdx.x * (kThreadsS / 64) + (threadIdx.x >> 6);
+  if (i >= n) return;
+  const int lane = threadIdx.x & 63;
   const int32_t k = y[i];
-  if (mask[i] && k >= 0 && k < C) v += e[(int64_t)k * f + c];
-  xp[i * ldp + c] = v;
+  const bool on = mask[i] && k >= 0 && k < C;
+  for (int64_t c = lane; c < f; c += 64) {
+    float v = x[i * ldx + c];
+    if (on) v += e[(int64_t)k * f + c];
+    xp[i * ldp + c] = v;
+  }
 }
 
-// Masked label propagation, backward: dE[k] = sum of dXp rows with mask = 1
-// and label k. Workgroup b sums its range of rows in row order into an LDS
-// table (thread = feature, so no two threads touch one entry), then writes
-// the table as partial b; k_embed_grad_reduce adds the partials in order.
-constexpr int kEmbedRows = 2048;
-
-__global__ __launch_bounds__(kThreadsS) void k_embed_grad_partial(
-    int64_t n, int64_t f, int C, const float* __restrict__ dx, int64_t ldx,
-    const uint8_t* __restrict__ mask, const int32_t* __restrict__ y, float* __restrict__ part) {
-  __shared__ float acc[64][kThreadsS];
-  const int t = threadIdx.x;
-  const int64_t c = (int64_t)blockIdx.y * kThreadsS + t;
-  for (int k = 0; k < C; ++k) acc[k][t] = 0.f;
-  const int64_t i0 = (int64_t)blockIdx.x * kEmbedRows;
-  const int64_t i1 = std::min(n, i0 + kEmbedRows);
-  if (c < f)
-    for (int64_t i = i0; i < i1; ++i)
-      if (mask[i] && y[i] >= 0 && y[i] < C) acc[y[i]][t] += dx[i * ldx + c];
-  if (c < f)
-    for (int k = 0; k < C; ++k) part[((int64_t)blockIdx.x * C + k) * f + c] = acc[k][t];
-}
-
-__global__ __launch_bounds__(kThreadsS) void k_embed_grad_reduce(int64_t nb, int64_t f, int C,
-                                                                 const float* __restrict__ part,
-                                                                 float* __restrict__ de) {
+// Masked label propagation, backward: Xp = X + M E with M the one-hot matrix
+// of the embedded rows' labels (row i: 1 at column y[i] if mask[i]), so
+// dE = M^T dXp, a weight-gradient product. Thread t writes the 4 entries
+// [4 (t % q), 4 (t % q) + 4) of row t / q of M (q = ldo / 4).
+__global__ __launch_bounds__(kThreadsS) void k_onehot(int64_t n, int C, int64_t ldo,
+                                                      const uint8_t* __restrict__ mask,
+                                                      const int32_t* __restrict__ y,
+                                                      float* __restrict__ m) {
   const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
-  if (t >= (int64_t)C * f) return;
-  float s = 0.f;
-  for (int64_t b = 0; b < nb; ++b) s += part[b * C * f + t];
-  de[t] = s;
+  const int64_t q = ldo / 4;
+  if (t >= n * q) return;
+  const int64_t i = t / q;
+  const int c0 = (int)(t - i * q) * 4;
+  const int32_t k = y[i];
+  const int hot = mask[i] && k >= 0 && k < C ? k : -1;
+  float4 v;
+  v.x = hot == c0 ? 1.f : 0.f;
+  v.y = hot == c0 + 1 ? 1.f : 0.f;
+  v.z = hot == c0 + 2 ? 1.f : 0.f;
+  v.w = hot == c0 + 3 ? 1.f : 0.f;
+  *reinterpret_cast<float4*>(m + i * ldo + c0) = v;
 }
 
 // Column sums of dO (the bias gradient) in a fixed order: workgroup b adds
@@ -284,7 +279,7 @@ gcn_status sage_forward(const gcn_graph* g, const float* X, int64_t ldx, int64_t
   const float* h = X;
   int64_t ldh = ldx;
   if (lp_mask) {
-    hipLaunchKernelGGL(k_embed_labels, dim3(blocks(n * f_in)), dim3(kThreadsS), 0, s, n, f_in,
+    hipLaunchKernelGGL(k_embed_labels, dim3(blocks(n * 64)), dim3(kThreadsS), 0, s, n, f_in,
                        (int)n_classes, X, ldx, lp_mask, labels, E, m.xp, L[0].fp);
     GCN_HIP(hipGetLastError());
     h = m.xp;
@@ -374,21 +369,16 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
       // label propagation: dXp, then the embedding gradient
       st = layernorm_bwd(n, y.f, y.c, y.ldc, y.rstd, dc, y.ldc, t, y.fp, nullptr, 0, m.xp, y.fp,
                          s);
-      const int64_t nb = std::max<int64_t>(1, ceil_div(n, kEmbedRows));
-      if (st == GCN_OK) st = talloc(&part, nb * C * f_in, s, "embedding gradient partials");
+      const int64_t ldo = (C + 3) & ~int64_t(3);
+      if (st == GCN_OK) st = talloc(&part, n * ldo, s, "label one-hot rows");
       if (st == GCN_OK) {
-        hipLaunchKernelGGL(k_embed_grad_partial,
-                           dim3((unsigned)nb, (unsigned)ceil_div(f_in, kThreadsS)),
-                           dim3(kThreadsS), 0, s, n, f_in, C, (const float*)m.xp, y.fp, lp_mask,
-                           labels, part);
+        hipLaunchKernelGGL(k_onehot, dim3(blocks(n * (ldo / 4))), dim3(kThreadsS), 0, s, n,
+                           (int)C, ldo, lp_mask, labels, part);
         e = hipGetLastError();
-        if (e == hipSuccess) {
-          hipLaunchKernelGGL(k_embed_grad_reduce, dim3(blocks((int64_t)C * f_in)),
-                             dim3(kThreadsS), 0, s, nb, f_in, C, (const float*)part, dE);
-          e = hipGetLastError();
-        }
-        if (e != hipSuccess) st = hip_fail(e, "embedding gradient", __FILE__, __LINE__);
+        if (e != hipSuccess) st = hip_fail(e, "k_onehot", __FILE__, __LINE__);
       }
+      if (st == GCN_OK)
+        st = gemm_f32(GCN_GEMM_TN, C, f_in, n, part, ldo, m.xp, y.fp, dE, f_in, s);
     }
   }
   tfree(part, s);
