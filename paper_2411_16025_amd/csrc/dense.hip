@@ -33,6 +33,11 @@ constexpr int kTile = 64;  // C tile is kTile x kTile
 constexpr int kKc = 32;    // K slice staged in LDS
 constexpr int kPad = 1;    // LDS row padding against bank conflicts
 constexpr int64_t kSplitRows = 8192;  // K chunk of the A^T B kernel
+#ifndef GCN_TN_MIN_BLOCKS
+#define GCN_TN_MIN_BLOCKS 1024
+#endif
+constexpr int64_t kSplitRowsMin = 1024;
+constexpr int64_t kTnMinBlocks = GCN_TN_MIN_BLOCKS;  // workgroups the A^T B grid aims for
 
 enum Op { kNN = 0, kNT = 1 };
 
@@ -570,8 +575,13 @@ gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int
   if (M == 0 || N == 0) return GCN_OK;
   const bool vec = aligned16(A, lda) && aligned16(B, ldb);
   if (op == GCN_GEMM_TN) {
-    // chunk length: kSplitRows, grown so the chunk count fits the grid's z range
-    const int64_t split = std::max<int64_t>(kSplitRows, ceil_div(ceil_div(K, 65535), kKc) * kKc);
+    // chunk length: kSplitRows, shrunk (down to kSplitRowsMin) when the output
+    // has few tiles so the grid still fills the chip, and grown so the chunk
+    // count fits the grid's z range
+    const int64_t tiles = ceil_div(M, (int64_t)128) * ceil_div(N, (int64_t)tile_n_narrow(N));
+    int64_t split = kSplitRows;
+    while (split > kSplitRowsMin && tiles * ceil_div(K, split) < kTnMinBlocks) split /= 2;
+    split = std::max<int64_t>(split, ceil_div(ceil_div(K, 65535), kKc) * kKc);
     const int64_t n_chunks = std::max<int64_t>(1, ceil_div(K, split));
     float* part = nullptr;
     GCN_CHECK(talloc(&part, n_chunks * M * N, stream, "GEMM partials"));
