@@ -406,15 +406,38 @@ __global__ __launch_bounds__(WAVES * 64) void k_gemm_tn_v(int64_t M, int64_t N, 
   }
 }
 
-// C[m][n] = sum over chunks, in chunk order, of part[chunk][m][n].
+// C[m][n] = sum over chunks of part[chunk][m][n] in a fixed order: a
+// workgroup takes 64 consecutive elements; its wavefront g adds chunks g,
+// g + 4, g + 8, ... in turn (4 loads in flight), and the four sums are added
+// in wavefront order.
 __global__ __launch_bounds__(kThreads) void k_sum_partials(int64_t M, int64_t N, int64_t n_chunks,
                                                            const float* __restrict__ part,
                                                            float* __restrict__ C, int64_t ldc) {
-  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (e >= M * N) return;
+  __shared__ float red[kThreads / 64][64];
+  constexpr int kW = kThreads / 64, U = 4;
+  const int lane = threadIdx.x & 63, g = threadIdx.x >> 6;
+  const int64_t e = (int64_t)blockIdx.x * 64 + lane;
+  const int64_t MN = M * N;
   float s = 0.f;
-  for (int64_t c = 0; c < n_chunks; ++c) s += part[c * M * N + e];
-  C[(e / N) * ldc + (e % N)] = s;
+  if (e < MN) {
+    int64_t c = g;
+    for (; c + (U - 1) * kW < n_chunks; c += U * kW) {
+      float v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = part[(c + u * kW) * MN + e];
+#pragma unroll
+      for (int u = 0; u < U; ++u) s += v[u];
+    }
+    for (; c < n_chunks; c += kW) s += part[c * MN + e];
+  }
+  red[g][lane] = s;
+  __syncthreads();
+  if (g == 0 && e < MN) {
+    float t = red[0][lane];
+#pragma unroll
+    for (int w = 1; w < kW; ++w) t += red[w][lane];
+    C[(e / N) * ldc + (e % N)] = t;
+  }
 }
 
 // one wavefront per row
@@ -602,7 +625,7 @@ gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int
     }
     {
       ProfScope ps("gemm_sum_partials", stream);
-      hipLaunchKernelGGL(k_sum_partials, dim3((unsigned)ceil_div(M * N, kThreads)), dim3(kThreads),
+      hipLaunchKernelGGL(k_sum_partials, dim3((unsigned)ceil_div(M * N, (int64_t)64)), dim3(kThreads),
                          0, stream, M, N, n_chunks, (const float*)part, C, ldc);
       hipError_t e = hipGetLastError();
       tfree(part, stream);
