@@ -34,9 +34,12 @@ constexpr int kKc = 32;    // K slice staged in LDS
 constexpr int kPad = 1;    // LDS row padding against bank conflicts
 constexpr int64_t kSplitRows = 8192;  // K chunk of the A^T B kernel
 #ifndef GCN_TN_MIN_BLOCKS
-#define GCN_TN_MIN_BLOCKS 1024
+#define GCN_TN_MIN_BLOCKS 4096
 #endif
-constexpr int64_t kSplitRowsMin = 1024;
+#ifndef GCN_TN_MIN_SPLIT
+#define GCN_TN_MIN_SPLIT 1024
+#endif
+constexpr int64_t kSplitRowsMin = GCN_TN_MIN_SPLIT;
 constexpr int64_t kTnMinBlocks = GCN_TN_MIN_BLOCKS;  // workgroups the A^T B grid aims for
 
 enum Op { kNN = 0, kNT = 1 };
