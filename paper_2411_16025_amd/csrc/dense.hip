@@ -188,6 +188,10 @@ __device__ inline f4 load4(const float* __restrict__ p, int64_t row, int64_t row
 #ifndef GCN_GEMM_MIN_BLOCKS
 #define GCN_GEMM_MIN_BLOCKS 2
 #endif
+// From this depth on, the 256-column NN tile takes two 16-row blocks per
+// wavefront (128 x 256 per workgroup, each B fragment feeding two MFMAs):
+// 3% faster at K = 516, slower at K <= 204.
+constexpr int64_t kDeepK = 384;
 // Workgroups per CU the 64- and 128-column tiles must fit (fewer registers,
 // more waves to overlap LDS and global latency).
 #ifndef GCN_GEMM_MIN_BLOCKS_NARROW
@@ -199,14 +203,17 @@ __device__ inline f4 load4(const float* __restrict__ p, int64_t row, int64_t row
 #define GCN_GEMM_PRAGMA(x) _Pragma(#x)
 #define GCN_GEMM_UNROLL(n) GCN_GEMM_PRAGMA(unroll n)
 
-template <int OP, int BN>
+template <int OP, int BN, int RB>
 __global__ __launch_bounds__(kThreads,
                              BN == 256 ? GCN_GEMM_MIN_BLOCKS : GCN_GEMM_MIN_BLOCKS_NARROW)
 void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A, int64_t lda,
                    const float* __restrict__ B, int64_t ldb, float* __restrict__ C, int64_t ldc,
                    const float* __restrict__ mask, int64_t ldm, bool relu, bool cvec) {
+  // RB 16-row blocks per wavefront: a BM x BN tile per workgroup
+  constexpr int BM = kTile * RB;
   constexpr int NB = BN / 16;
   constexpr int BL = BN / 32;  // 16-byte B loads per thread per slice
+  constexpr int AL = 2 * RB;   // 16-byte A loads per thread per slice
   // LDS strides chosen so that the operand reads of a half-wavefront (16
   // rows or columns x 2 k values) hit 32 distinct banks: rows read along k
   // (A, and B of NT) have a stride of 2 mod 32 floats and are written with
@@ -216,21 +223,23 @@ void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A,
   constexpr int BC = OP == kNN ? BN + 16 : kKc + 2;
   // the output tile is staged through the same LDS, CW columns at a time
   constexpr int CW = BN < 128 ? BN : 128;
-  constexpr int kOperands = kTile * AS + BR * BC;
-  constexpr int kStage = kTile * (CW + 4);
+  constexpr int kOperands = BM * AS + BR * BC;
+  constexpr int kStage = BM * (CW + 4);
   __shared__ __align__(16) float smem[kOperands > kStage ? kOperands : kStage];
-  auto& As = *reinterpret_cast<float (*)[kTile][AS]>(smem);
-  auto& Bs = *reinterpret_cast<float (*)[BR][BC]>(smem + kTile * AS);
+  auto& As = *reinterpret_cast<float (*)[BM][AS]>(smem);
+  auto& Bs = *reinterpret_cast<float (*)[BR][BC]>(smem + BM * AS);
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int64_t m0 = (int64_t)blockIdx.x * kTile;
+  const int64_t m0 = (int64_t)blockIdx.x * BM;
   const int64_t n0 = (int64_t)blockIdx.y * BN;
-  f4 acc[NB];
+  f4 acc[RB][NB];
 #pragma unroll
-  for (int j = 0; j < NB; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
-  f4 ra[2], rb[BL];
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int j = 0; j < NB; ++j) acc[r][j] = f4{0.f, 0.f, 0.f, 0.f};
+  f4 ra[AL], rb[BL];
   auto load_slice = [&](int64_t k0) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {  // A: 64 x 32 = 512 float4
+    for (int j = 0; j < AL; ++j) {  // A: BM x 32 floats
       const int idx = t + kThreads * j, r = idx >> 3, c = (idx & 7) * 4;
       ra[j] = load4(A, m0 + r, M, lda, k0 + c, K);
     }
@@ -248,7 +257,7 @@ void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A,
   };
   auto store_slice = [&]() {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < AL; ++j) {
       const int idx = t + kThreads * j, r = idx >> 3, c = (idx & 7) * 4;
       *reinterpret_cast<f2*>(&As[r][c]) = f2{ra[j].x, ra[j].y};
       *reinterpret_cast<f2*>(&As[r][c + 2]) = f2{ra[j].z, ra[j].w};
@@ -274,12 +283,16 @@ void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A,
     if (more) load_slice(k0 + kKc);
     GCN_GEMM_UNROLL(GCN_GEMM_KK_UNROLL)
     for (int kk = 0; kk < kKc; kk += 4) {
-      const float a = As[16 * w + (lane & 15)][kk + (lane >> 4)];
+      float a[RB];
+#pragma unroll
+      for (int r = 0; r < RB; ++r) a[r] = As[16 * (RB * w + r) + (lane & 15)][kk + (lane >> 4)];
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
         const float b = OP == kNN ? Bs[kk + (lane >> 4)][16 * j + (lane & 15)]
                                   : Bs[16 * j + (lane & 15)][kk + (lane >> 4)];
-        acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[j], 0, 0, 0);
+#pragma unroll
+        for (int r = 0; r < RB; ++r)
+          acc[r][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[r], b, acc[r][j], 0, 0, 0);
       }
     }
     __syncthreads();
@@ -299,14 +312,16 @@ void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A,
     for (int c0 = 0; c0 < BN; c0 += CW) {
       __syncthreads();  // the operands (or the previous columns) are no longer read
 #pragma unroll
-      for (int j = c0 / 16; j < (c0 + CW) / 16; ++j)
+      for (int r = 0; r < RB; ++r)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          st[16 * w + 4 * (lane >> 4) + i][16 * j - c0 + (lane & 15)] = acc[j][i];
+        for (int j = c0 / 16; j < (c0 + CW) / 16; ++j)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            st[16 * (RB * w + r) + 4 * (lane >> 4) + i][16 * j - c0 + (lane & 15)] = acc[r][j][i];
       __syncthreads();
 #pragma unroll
-      for (int it = 0; it < 16 / RPI; ++it) {
-        const int rl = 16 * w + it * RPI + lane / LPR;
+      for (int it = 0; it < 16 * RB / RPI; ++it) {
+        const int rl = 16 * RB * w + it * RPI + lane / LPR;
         const int cl = 4 * (lane % LPR);
         const int64_t gm = m0 + rl, gn = n0 + c0 + cl;
         if (gm >= M || gn >= N) continue;
@@ -337,13 +352,15 @@ void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A,
     return;
   }
 #pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int64_t gn = n0 + 16 * j + (lane & 15);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int64_t gm = m0 + 16 * w + 4 * (lane >> 4) + i;
+      const int64_t gm = m0 + 16 * (RB * w + r) + 4 * (lane >> 4) + i;
       if (gm < M && gn < N) {
-        float v = (mask && !(mask[gm * ldm + gn] > 0.f)) ? 0.f : acc[j][i];
+        float v = (mask && !(mask[gm * ldm + gn] > 0.f)) ? 0.f : acc[r][j][i];
         if (relu) v = fmaxf(v, 0.f);
         C[gm * ldc + gn] = v;
       }
@@ -570,14 +587,21 @@ void launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, c
   const bool cvec = aligned16(C, ldc) && (!mask || aligned16(mask, ldm));
   const dim3 grid((unsigned)ceil_div(M, kTile), (unsigned)ceil_div(N, bn));
   if (bn == 64)
-    hipLaunchKernelGGL((k_gemm_tall_v<OP, 64>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda, B,
-                       ldb, C, ldc, mask, ldm, relu, cvec);
+    hipLaunchKernelGGL((k_gemm_tall_v<OP, 64, 1>), grid, dim3(kThreads), 0, stream, M, N, K, A,
+                       lda, B, ldb, C, ldc, mask, ldm, relu, cvec);
   else if (OP != kNN || bn == 128)
-    hipLaunchKernelGGL((k_gemm_tall_v<OP, 128>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda,
-                       B, ldb, C, ldc, mask, ldm, relu, cvec);
-  else if constexpr (OP == kNN)
-    hipLaunchKernelGGL((k_gemm_tall_v<OP, 256>), grid, dim3(kThreads), 0, stream, M, N, K, A, lda,
-                       B, ldb, C, ldc, mask, ldm, relu, cvec);
+    hipLaunchKernelGGL((k_gemm_tall_v<OP, 128, 1>), grid, dim3(kThreads), 0, stream, M, N, K, A,
+                       lda, B, ldb, C, ldc, mask, ldm, relu, cvec);
+  else if constexpr (OP == kNN) {
+    if (K >= kDeepK) {  // deep products: 128 x 256 tiles
+      const dim3 grid_w((unsigned)ceil_div(M, (int64_t)kTile * 2), (unsigned)ceil_div(N, bn));
+      hipLaunchKernelGGL((k_gemm_tall_v<OP, 256, 2>), grid_w, dim3(kThreads), 0, stream, M, N,
+                         K, A, lda, B, ldb, C, ldc, mask, ldm, relu, cvec);
+    } else {
+      hipLaunchKernelGGL((k_gemm_tall_v<OP, 256, 1>), grid, dim3(kThreads), 0, stream, M, N, K,
+                         A, lda, B, ldb, C, ldc, mask, ldm, relu, cvec);
+    }
+  }
 }
 
 void launch_tn(int64_t M, int64_t N, int64_t K, int64_t split, int64_t n_chunks, const float* A,
