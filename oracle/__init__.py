@@ -76,6 +76,7 @@ def _L():
         lib.orc_bipartite_cover.argtypes = [i64, i64, i64, P, P, P, P]
         lib.orc_bipartite_cover.restype = i64
         lib.orc_num_threads.restype = ctypes.c_int
+        lib.orc_set_num_threads.argtypes = [ctypes.c_int]
         _lib = lib
     return _lib
 
@@ -90,6 +91,11 @@ def _c(a, dtype):
 
 def num_threads() -> int:
     return _L().orc_num_threads()
+
+
+def set_num_threads(n: int) -> None:
+    """Thread count of the oracle's later parallel loops (results do not depend on it)."""
+    _L().orc_set_num_threads(int(n))
 
 
 _ERR = {-1: "capacity", -2: "id out of range", -3: "symmetrize needs a square shape",

@@ -480,4 +480,7 @@ int64_t orc_bipartite_cover(int64_t n_u, int64_t n_v, int64_t n_edges, const int
 
 int orc_num_threads(void) { return omp_get_max_threads(); }
 
+// Threads used by later parallel regions (n >= 1); timing only, no arithmetic.
+void orc_set_num_threads(int n) { omp_set_num_threads(n < 1 ? 1 : n); }
+
 }  // extern "C"
