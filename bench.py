@@ -102,21 +102,28 @@ def sources_sha256(paths):
 
 
 def read_counters(kernel):
-    """HBM bytes per dispatch from the committed rocprofv3 PMC summary, only
-    if it was taken on the current aggregation source."""
+    """(HBM bytes per dispatch, L2 hit rate) from the committed rocprofv3 PMC
+    summary, only if it was taken on the current aggregation source; else
+    (None, None)."""
     if not os.path.exists(COUNTERS):
-        return None
-    kv = {}
-    for line in open(COUNTERS):
+        return None, None
+    kv, lines = {}, open(COUNTERS).read().splitlines()
+    for line in lines:
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
     if kv.get("source_sha256") != sources_sha256(AGG_SOURCES) or kv.get("kernel") != kernel:
-        return None
+        return None, None
     try:
-        return float(kv["fetch_bytes_per_dispatch"]) + float(kv["write_bytes_per_dispatch"])
+        traffic = float(kv["fetch_bytes_per_dispatch"]) + float(kv["write_bytes_per_dispatch"])
     except (KeyError, ValueError):
-        return None
+        return None, None
+    hit = None
+    sym = "# " + kv.get("kernel_symbol", "\0")
+    for line in lines:  # the table row of the kernel: its last column is the L2 hit rate
+        if line.startswith(sym) and line.rstrip().endswith("%"):
+            hit = round(float(line.split()[-1].rstrip("%")) / 100.0, 4)
+    return traffic, hit
 
 
 FP32_MFMA_PEAK_TFLOPS = 157.3
@@ -585,13 +592,19 @@ def main():
             for bins in (bins_f, bins_b) for c, b in enumerate(bins) if c in KERNEL_CLASSES[dom])
         avg_ms = tot_ms / launches
         achieved = per_launch_bytes / (avg_ms * 1e-3) / 1e9
+        # the committed counters describe the default workload only
+        traffic, l2_hit = (read_counters(dom) if bits == 8 and args.workload == "rmat24_q8"
+                           else (None, None))
         roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    # the committed counters describe the default workload only
-                    "traffic": (read_counters(dom) if bits == 8 and args.workload == "rmat24_q8"
-                                else None),
+                    "traffic": traffic,
                     "bytes_per_launch": int(per_launch_bytes), "avg_launch_ms": round(avg_ms, 4)}
+        if traffic is not None:
+            # the counted bytes over the same launch time: the rate the memory system delivered
+            tr = traffic / (avg_ms * 1e-3) / 1e9
+            roofline.update({"traffic_GBps": round(tr, 1),
+                             "traffic_frac": round(tr / HBM_PEAK_GBS, 4), "l2_hit": l2_hit})
 
     # every aggregation kernel against the same model, per pass (one forward
     # and one transposed pass per profiled step; k_tiny is two launches a pass)
