@@ -281,8 +281,12 @@ void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A,
   for (int64_t k0 = 0; k0 < K; k0 += kKc) {
     const bool more = k0 + kKc < K;
     if (more) load_slice(k0 + kKc);
+    // the steps of a last, partial slice past K would only add zero products
+    // (kn is the same for the whole workgroup)
+    const int kn = more ? kKc : (int)(K - k0);
     GCN_GEMM_UNROLL(GCN_GEMM_KK_UNROLL)
     for (int kk = 0; kk < kKc; kk += 4) {
+      if (kk >= kn) break;
       float a[RB];
 #pragma unroll
       for (int r = 0; r < RB; ++r) a[r] = As[16 * (RB * w + r) + (lane & 15)][kk + (lane >> 4)];
