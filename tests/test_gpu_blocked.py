@@ -84,7 +84,7 @@ def test_rmat_blocked_fwd_bwd(G, blocks, piece, seg):
     bins = check_bins(G, g)
     assert bins[9]["rows"] > 20 and bins[9]["first_len"] == 300
     assert bins[8]["rows"] > 20 and (bins[8]["first_len"], bins[8]["last_len"]) == (41, 299)
-    for F in (4, 47, 128, 256):
+    for F in (4, 47, 128, 256, 1030):
         X = synth.uniform(303 + F, n, F)
         assert_close(host(G.gcn_aggregate_fwd(g, dev(X))), *og.fwd(X), what="fwd F=%d" % F)
     Gm = synth.uniform(310, n, 100)

@@ -116,7 +116,7 @@ def rmat14(G):
     return n, og, g
 
 
-@pytest.mark.parametrize("F", [1, 3, 4, 47, 64, 100, 128, 256, 300])
+@pytest.mark.parametrize("F", [1, 3, 4, 47, 64, 100, 128, 256, 300, 1030, 2049])
 def test_fwd_bwd_fp32_feature_sweep(G, rmat14, F):
     n, og, g = rmat14
     note("fwd/bwd fp32 rmat14 F=%d" % F)
