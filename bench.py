@@ -45,10 +45,8 @@ AGG_SOURCES = [os.path.join(ROOT, "paper_2411_16025_amd", "csrc", f)
 COUNTERS = os.path.join(ROOT, "profiles", "agg_counters_rmat24_q8.txt")
 
 # kernel name -> row-length classes whose rows it processes
-# (the medium class runs in k_short, or in k_medium when the library is built
-# with GCN_MEDIUM_BY_SLOTS=0; only one of the two is ever timed)
 KERNEL_CLASSES = {"agg_zero_rows": [0], "agg_tiny": [1, 2], "agg_short": [3, 4, 5, 6, 7],
-                  "agg_medium": [7], "agg_chunk": [8], "agg_pieces": [9]}
+                  "agg_chunk": [8], "agg_pieces": [9]}
 
 
 def log(msg):

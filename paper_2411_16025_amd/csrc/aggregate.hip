@@ -19,9 +19,7 @@
 //      1 or 2 entries       -> one row per slot, several row groups per
 //                              wavefront with all their loads issued first
 //      3..medium_max        -> one row per slot, E rows of about the same
-//                              length per wavefront (or, with
-//                              GCN_MEDIUM_BY_SLOTS=0, one wavefront per row
-//                              from 33 entries, slots interleaving entries)
+//                              length per wavefront
 //      longer rows          -> one 256-thread workgroup per chunk of entries,
 //                              slots reduced in fixed order through LDS; a row
 //                              with several chunks writes partial rows that a
@@ -225,15 +223,6 @@ __device__ inline void store_row(float* __restrict__ y, int f0, int F, const flo
 #ifndef GCN_GROUP_UNROLL
 #define GCN_GROUP_UNROLL 1
 #endif
-// Medium rows (33 .. medium_max entries) run one per lane group in k_short (1)
-// or one per wavefront in k_medium (0).
-#ifndef GCN_MEDIUM_BY_SLOTS
-#define GCN_MEDIUM_BY_SLOTS 1
-#endif
-// Gathers in flight per lane in the one-wavefront-per-row kernel.
-#ifndef GCN_MEDIUM_UNROLL
-#define GCN_MEDIUM_UNROLL GCN_AGG_UNROLL
-#endif
 // Row groups per wavefront of the one-entry and two-entry row kernels.
 #ifndef GCN_TINY_GROUPS1
 #define GCN_TINY_GROUPS1 4
@@ -393,8 +382,7 @@ __device__ inline void reduce_slots(float* acc) {
 }
 
 // Classes run one row per lane group by k_short: kFirstShort .. kMedium (the
-// one- and two-entry classes get no wavefronts there, and the medium class
-// only with GCN_MEDIUM_BY_SLOTS).
+// one- and two-entry classes get no wavefronts there).
 constexpr int kSlotClasses = kMedium - kFirstShort + 1;
 struct ShortArgs {
   int64_t row_off[kSlotClasses + 1];   // rows of class kFirstShort + k start at row_off[k]
@@ -514,29 +502,6 @@ __global__ __launch_bounds__(kBlock, GCN_MIN_WAVES) void k_short(const int64_t* 
   float acc[VEC];
   accumulate_slot<VEC, G, GCN_SLOT_UNROLL>(ent, b, len, src, f0, active, acc);
   if (active) store_row<VEC, RELU>(y + (int64_t)r * ldy, f0, F, acc);
-}
-
-// Rows with 33..medium_max entries: one wavefront per row.
-template <int VEC, int G, class Src, bool RELU>
-__global__ __launch_bounds__(kBlock) void k_medium(const int64_t* __restrict__ ptr,
-                                                   const Ent* __restrict__ ent,
-                                                   const int32_t* __restrict__ rows, int64_t n,
-                                                   Src src, float* __restrict__ y, int64_t ldy,
-                                                   int F) {
-  const int lane = threadIdx.x & 63;
-  const int64_t i = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-  if (i >= n) return;  // whole wavefront leaves together
-  const int slot = lane / G;
-  const int f0 = (int)blockIdx.y * G * VEC + (lane % G) * VEC;
-  const bool active = f0 < F;
-  const int32_t r = rows[i];
-  const int64_t b = ptr[r], e = ptr[r + 1];
-  float acc[VEC];
-#pragma unroll
-  for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
-  accumulate_blocks<VEC, G, GCN_MEDIUM_UNROLL>(ent, b, e, 0, 1, src, f0, active, acc);
-  reduce_slots<VEC, G>(acc);
-  if (slot == 0 && active) store_row<VEC, RELU>(y + (int64_t)r * ldy, f0, F, acc);
 }
 
 // One workgroup per chunk of a long row. Wavefront w of the workgroup takes
@@ -716,15 +681,14 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
       GCN_HIP(hipGetLastError());
     }
   }
-  // rows of 3 .. 32 entries, and of the medium class with GCN_MEDIUM_BY_SLOTS (the
-  // classes of one and two entries get no waves here)
-  constexpr int last_slot_class = GCN_MEDIUM_BY_SLOTS ? kMedium : kLastShort;
+  // rows of 3 .. medium_max entries (the classes of one and two entries get no
+  // waves here)
   ShortArgs sa;
   int64_t waves = 0;
   for (int c = kFirstShort; c <= kMedium + 1; ++c) {
     sa.row_off[c - kFirstShort] = p.class_off[c];
     sa.wave_off[c - kFirstShort] = waves;
-    if (c >= kFirstShort + 2 && c <= last_slot_class)
+    if (c >= kFirstShort + 2 && c <= kMedium)
       waves += ceil_div(p.class_off[c + 1] - p.class_off[c], E);
   }
   if (waves > 0) {
@@ -732,15 +696,6 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
     hipLaunchKernelGGL((k_short<VEC, G, Src, RELU>), dim3(blocks_for_waves(waves), tiles),
                        dim3(kBlock), 0, stream, (const int64_t*)p.rbeg, (const int32_t*)p.rlen,
                        (const Ent*)m.ent, (const int32_t*)p.rows, sa, src, y, ldy, F);
-    GCN_HIP(hipGetLastError());
-  }
-  // medium rows, one wavefront per row (unless they ran one per lane group above)
-  const int64_t n_med = GCN_MEDIUM_BY_SLOTS ? 0 : p.class_off[kMedium + 1] - p.class_off[kMedium];
-  if (n_med > 0) {
-    ProfScope ps("agg_medium", stream);
-    hipLaunchKernelGGL((k_medium<VEC, G, Src, RELU>), dim3(blocks_for_waves(n_med), tiles),
-                       dim3(kBlock), 0, stream, (const int64_t*)m.ptr, (const Ent*)m.ent,
-                       (const int32_t*)(p.rows + p.class_off[kMedium]), n_med, src, y, ldy, F);
     GCN_HIP(hipGetLastError());
   }
   // long rows: chunk table, then column-blocked pieces, then the partial sums
