@@ -216,7 +216,11 @@ gcn_status gcn_softmax_xent(int64_t n, int64_t C, const float* logits, int64_t l
  *  row-major), labels int32 [n] in [0, n_classes), n_classes <= 64.
  *  Outputs: dW1, dW2 (same shapes as W1, W2), *loss (device double).
  * No bias, dropout or normalization layer. Intermediates are allocated
- * stream-ordered for the duration of the call. */
+ * stream-ordered for the duration of the call. dW2 is computed on a second,
+ * library-owned stream of the current device (non-blocking, default priority),
+ * forked from `stream` by an event and joined back to it before the call
+ * returns, so all outputs are ordered on `stream` (the fork and join are
+ * captured with it in a graph capture). */
 gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t ldx, int64_t f_in,
                          const float* W1, int64_t hidden, const float* W2, int64_t n_classes,
                          const int32_t* labels, float* dW1, float* dW2, double* loss,
@@ -295,7 +299,10 @@ gcn_status gcn_sage3_forward(const gcn_graph* g, const float* X, int64_t ldx, in
  *           same shape) are required with it.
  *  eps      LayerNorm epsilon; loss: device double, the mean loss.
  *  1 <= n_classes <= 64. Asynchronous; temporaries are stream-ordered
- *  (about 4 n (2 f_in + 3 (2 hidden + 4) + 4 hidden) bytes). */
+ *  (about 4 n (2 f_in + 3 (2 hidden + 4) + 4 hidden) bytes). The weight
+ *  gradients of each layer run on a second, library-owned stream of the
+ *  current device, forked from `stream` by an event and joined back to it
+ *  before the call returns: all outputs are ordered on `stream`. */
 gcn_status gcn_sage3_step(const gcn_graph* g, const float* X, int64_t ldx, int64_t f_in,
                           int64_t hidden, int64_t n_classes, const float* const* params,
                           const int32_t* labels, const uint8_t* lp_mask, const float* E,

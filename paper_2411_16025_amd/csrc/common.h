@@ -133,6 +133,22 @@ gcn_status talloc(T** p, int64_t count, hipStream_t stream, const char* what) {
 }
 void tfree(void* p, hipStream_t stream);
 
+// Work that may overlap the caller's stream runs on a second stream of the
+// current device (non-blocking, default priority, created on first use and
+// kept until the process ends). fork() makes the side stream wait for all
+// work enqueued on `main` so far; join() makes `main` wait for all work
+// enqueued on the side stream. The destructor joins, so on every return path
+// the side work is ordered before whatever the caller enqueues next.
+struct SideWork {
+  hipStream_t main = nullptr, side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  bool pending = false;  // side work enqueued since the last join
+  gcn_status init(hipStream_t m);
+  gcn_status fork();
+  gcn_status join();
+  ~SideWork();
+};
+
 // Stream-ordered temporaries released when the scope ends, on every return
 // path (error returns included).
 struct TempScope {

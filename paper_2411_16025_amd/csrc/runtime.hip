@@ -86,6 +86,50 @@ void keep_pool_memory() {
 }
 }  // namespace
 
+namespace {
+std::mutex g_side_mu;
+hipStream_t g_side[64] = {};
+}  // namespace
+
+gcn_status SideWork::init(hipStream_t m) {
+  main = m;
+  int dev = 0;
+  GCN_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) {
+    set_error("device %d out of range for the side stream", dev);
+    return GCN_EINVAL;
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_side_mu);
+    if (!g_side[dev]) GCN_HIP(hipStreamCreateWithFlags(&g_side[dev], hipStreamNonBlocking));
+    side = g_side[dev];
+  }
+  GCN_HIP(hipEventCreateWithFlags(&ev_fork, hipEventDisableTiming));
+  GCN_HIP(hipEventCreateWithFlags(&ev_join, hipEventDisableTiming));
+  return GCN_OK;
+}
+
+gcn_status SideWork::fork() {
+  GCN_HIP(hipEventRecord(ev_fork, main));
+  GCN_HIP(hipStreamWaitEvent(side, ev_fork, 0));
+  pending = true;
+  return GCN_OK;
+}
+
+gcn_status SideWork::join() {
+  if (!pending) return GCN_OK;
+  pending = false;
+  GCN_HIP(hipEventRecord(ev_join, side));
+  GCN_HIP(hipStreamWaitEvent(main, ev_join, 0));
+  return GCN_OK;
+}
+
+SideWork::~SideWork() {
+  (void)join();
+  if (ev_fork) (void)hipEventDestroy(ev_fork);
+  if (ev_join) (void)hipEventDestroy(ev_join);
+}
+
 gcn_status tmalloc(void** p, size_t bytes, hipStream_t stream, const char* what) {
   *p = nullptr;
   keep_pool_memory();

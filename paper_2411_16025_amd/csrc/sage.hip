@@ -320,30 +320,46 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
     st = talloc(&colpart, n_colsum * std::max(L[1].fop, L[2].fop), s, "bias gradient partials");
   if (st == GCN_OK)
     st = softmax_xent(n, C, L[2].o, L[2].fop, labels, dlogits, L[2].fop, loss, s, lp_mask);
+  // The weight gradients of a layer (product, bias sums, unpacking) read only
+  // that layer's C and dO, so they run on the side stream. They are forked
+  // after the input-gradient product (also matrix-core bound), so that they
+  // overlap the memory-bound transposed aggregation and LayerNorm backward
+  // on s. dwp and colpart are used on the side stream only.
+  SideWork side;
+  if (st == GCN_OK) st = side.init(s);
+  const hipStream_t s2 = side.side;
   float* dO = dlogits;
   int64_t ld_do = L[2].fop;
   for (int l = 2; l >= 0 && st == GCN_OK; --l) {
     Layer& y = L[l];
+    const bool input_grad = l > 0 || lp_mask;
+    // dC = dO Wp^T; the input gradient of the layer is
+    // dY = dC[:, Y block] + A^T dC[:, Z block], then the LayerNorm backward
+    // dC over the Y and Z blocks only (the ones and padding columns are not read)
+    if (input_grad) st = gemm_f32(GCN_GEMM_NT, n, y.zo + y.f, y.fo, dO, ld_do, y.wp, y.fop, dc,
+                                  y.ldc, s);
+    if (st == GCN_OK) st = side.fork();  // dO of this layer and dC are complete on s
+    if (st != GCN_OK) break;
     // only the fo real columns of dO enter the products: the padding columns of
     // the logits gradient are never written. The product covers rows [0, oc)
     // of the packed gradient (the W blocks); the bias row oc is the column sum
     // of dO, computed on its own so that a 2f + 4 row count does not cost a
     // whole extra tile of the product.
-    st = gemm_f32(GCN_GEMM_TN, y.oc, y.fo, n, y.c, y.ldc, dO, ld_do, dwp, y.fop, s);
+    st = gemm_f32(GCN_GEMM_TN, y.oc, y.fo, n, y.c, y.ldc, dO, ld_do, dwp, y.fop, s2);
     if (st != GCN_OK) break;
     {
-      ProfScope ps("bias_grad", s);
+      ProfScope ps("bias_grad", s2);
       hipLaunchKernelGGL(k_colsum_partial,
                          dim3((unsigned)n_colsum, (unsigned)ceil_div(y.fo, kThreadsS)),
-                         dim3(kThreadsS), 0, s, n, y.fo, (const float*)dO, ld_do, colpart);
-      hipLaunchKernelGGL(k_colsum_reduce, dim3((unsigned)y.fo), dim3(kThreadsS), 0, s, n_colsum,
-                         y.fo, (const float*)colpart, dwp + y.oc * y.fop);
+                         dim3(kThreadsS), 0, s2, n, y.fo, (const float*)dO, ld_do, colpart);
+      hipLaunchKernelGGL(k_colsum_reduce, dim3((unsigned)y.fo), dim3(kThreadsS), 0, s2,
+                         n_colsum, y.fo, (const float*)colpart, dwp + y.oc * y.fop);
     }
     if (hipGetLastError() != hipSuccess) {
       st = hip_fail(hipErrorLaunchFailure, "bias gradient", __FILE__, __LINE__);
       break;
     }
-    hipLaunchKernelGGL(k_unpack_grads, dim3(blocks((2 * y.f + 1) * y.fo)), dim3(kThreadsS), 0, s,
+    hipLaunchKernelGGL(k_unpack_grads, dim3(blocks((2 * y.f + 1) * y.fo)), dim3(kThreadsS), 0, s2,
                        y.f, y.zo, y.oc, y.fo, y.fop, (const float*)dwp, grads[3 * l],
                        grads[3 * l + 1], grads[3 * l + 2]);
     hipError_t e = hipGetLastError();
@@ -351,12 +367,8 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
       st = hip_fail(e, "k_unpack_grads", __FILE__, __LINE__);
       break;
     }
-    if (l == 0 && !lp_mask) break;
-    // dC = dO Wp^T; the input gradient of the layer is
-    // dY = dC[:, Y block] + A^T dC[:, Z block], then the LayerNorm backward
-    // dC over the Y and Z blocks only (the ones and padding columns are not read)
-    st = gemm_f32(GCN_GEMM_NT, n, y.zo + y.f, y.fo, dO, ld_do, y.wp, y.fop, dc, y.ldc, s);
-    if (st == GCN_OK) st = aggregate_f32(g->csc, dc + y.zo, y.ldc, t, y.fp, y.f, false, s);
+    if (!input_grad) break;
+    st = aggregate_f32(g->csc, dc + y.zo, y.ldc, t, y.fp, y.f, false, s);
     if (st != GCN_OK) break;
     if (l > 0) {
       // the gradient of the layer below, masked by its ReLU, overwrites its output
@@ -381,6 +393,9 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
         st = gemm_f32(GCN_GEMM_TN, C, f_in, n, part, ldo, m.xp, y.fp, dE, f_in, s);
     }
   }
+  // the side work ends before its buffers are released on s
+  const gcn_status sj = side.join();
+  if (st == GCN_OK) st = sj;
   tfree(part, s);
   tfree(colpart, s);
   tfree(dwp, s);

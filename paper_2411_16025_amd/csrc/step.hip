@@ -1,7 +1,8 @@
 // One training step of a 2-layer GCN built from the library's kernels:
 // aggregation (Section 4 of SuperGCN, arXiv 2411.16025) interleaved with the
-// dense UPDATE of each layer (Section 2.1). Everything runs on the caller's
-// stream without host synchronization.
+// dense UPDATE of each layer (Section 2.1). Everything is ordered on the
+// caller's stream without host synchronization (one product runs on the side
+// stream, forked from and joined back to it).
 
 #include "common.h"
 
@@ -27,6 +28,7 @@ extern "C" gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t 
   const int64_t ldh = (hidden + 3) & ~int64_t(3);
   const int64_t ldc = (n_classes + 3) & ~int64_t(3);
   float *z1 = nullptr, *h1 = nullptr, *z2 = nullptr, *lg = nullptr, *dl = nullptr, *dz2 = nullptr;
+  float* dz1 = nullptr;
   float* w2p = nullptr;  // W2 with rows padded to a multiple of 4 floats (16-byte aligned rows)
   gcn_status st = talloc(&z1, n * ldh, s, "Z1");
   if (st == GCN_OK) st = talloc(&w2p, hidden * ldc, s, "W2 copy");
@@ -48,15 +50,24 @@ extern "C" gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t 
   if (st == GCN_OK) st = softmax_xent(n, (int)n_classes, lg, ldc, labels, dl, ldc, loss, s);
   // backward
   if (st == GCN_OK) st = aggregate_f32(g->csc, dl, ldc, dz2, ldc, n_classes, false, s);
-  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_TN, hidden, n_classes, n, h1, ldh, dz2, ldc, dW2,
-                                  n_classes, s);
   float* dh1 = z1;  // Z1 is dead after the first aggregation
   // dH1 = dZ2 W2^T with the ReLU mask (H1 > 0) applied as it is stored
   if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NT, n, hidden, n_classes, dz2, ldc, w2p, ldc, dh1, ldh,
                                   s, h1, ldh);
-  float* dz1 = h1;  // H1 is dead once the ReLU mask is applied
+  // dW2 = H1^T dZ2 reads only H1 and dZ2: on the side stream it overlaps the
+  // memory-bound transposed aggregation, which writes dZ1 to a buffer of its own
+  SideWork side;
+  if (st == GCN_OK) st = talloc(&dz1, n * ldh, s, "dZ1");
+  if (st == GCN_OK) st = side.init(s);
+  if (st == GCN_OK) st = side.fork();
+  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_TN, hidden, n_classes, n, h1, ldh, dz2, ldc, dW2,
+                                  n_classes, side.side);
   if (st == GCN_OK) st = aggregate_f32(g->csc, dh1, ldh, dz1, ldh, hidden, false, s);
   if (st == GCN_OK) st = gemm_f32(GCN_GEMM_TN, f_in, hidden, n, X, ldx, dz1, ldh, dW1, hidden, s);
+  // the side work ends before the buffers it reads are released on s
+  const gcn_status sj = side.join();
+  if (st == GCN_OK) st = sj;
+  tfree(dz1, s);
   tfree(dz2, s);
   tfree(dl, s);
   tfree(lg, s);

@@ -163,6 +163,14 @@ def check_step(G, n, m, f_in, hidden, C, seed, lp, flags=synth.SYMMETRIZE):
     for nm, a, b in pairs:
         err = np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300)
         assert err <= 1e-5, (nm, err)
+    # a repeated step gives identical bits (its weight gradients run on a
+    # second stream, forked from and joined to the caller's)
+    loss2, grads2, dE2 = G.gcn_sage3_step(g, dev(X), pd, *args)
+    assert float(host(loss2)) == got_loss
+    for nm, a, b in zip(names, grads, grads2):
+        assert np.array_equal(host(a).view(np.uint32), host(b).view(np.uint32)), nm
+    if lp:
+        assert np.array_equal(host(dE).view(np.uint32), host(dE2).view(np.uint32))
     return ref
 
 
@@ -202,6 +210,12 @@ def test_sage_step_product_full(G):
     loss, grads, dE = G.gcn_sage3_step(g, dev(X), pd, *args)
     got = [host(t) for t in grads] + [host(dE)]
     got_loss = float(host(loss))
+    del loss, grads, dE
+    loss2, grads2, dE2 = G.gcn_sage3_step(g, dev(X), pd, *args)  # identical bits again
+    assert float(host(loss2)) == got_loss
+    for a, b in zip(got, [host(t) for t in grads2] + [host(dE2)]):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    del loss2, grads2, dE2
     g.free()
     torch.cuda.empty_cache()
     og = oracle.Graph(n, n, w.src, w.dst, synth.SYMMETRIZE, mean=True)
