@@ -1,7 +1,9 @@
 // One training step of the 3-layer GraphSAGE model the paper evaluates
 // (Section 8.1, Table 2: LayerNorm before each layer, mean aggregation), with
 // optional masked label propagation (Section 6.1 step 1, Lemma 2), built from
-// the library's kernels on the caller's stream without host synchronization.
+// the library's kernels, ordered on the caller's stream without host
+// synchronization (the weight gradients run on the side stream, forked from
+// and joined back to it).
 //
 // Layer l reads H (n x f), and writes the row-major concatenation
 //   C = [ LayerNorm(H) | D^-1 A LayerNorm(H) | 1 | 0 0 0 ]
