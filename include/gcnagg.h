@@ -219,8 +219,7 @@ gcn_status gcn_softmax_xent(int64_t n, int64_t C, const float* logits, int64_t l
  * stream-ordered for the duration of the call. dW2 is computed on a second,
  * library-owned stream of the current device (non-blocking, default priority),
  * forked from `stream` by an event and joined back to it before the call
- * returns, so all outputs are ordered on `stream` (the fork and join are
- * captured with it in a graph capture). */
+ * returns, so all outputs are ordered on `stream`. */
 gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t ldx, int64_t f_in,
                          const float* W1, int64_t hidden, const float* W2, int64_t n_classes,
                          const int32_t* labels, float* dW1, float* dW2, double* loss,
