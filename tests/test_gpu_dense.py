@@ -27,8 +27,10 @@ def G():
     return pkg
 
 
+# (narrow outputs, N <= 64, take the register-streaming kernel: 1 to 4
+# column tiles, K tails within a 16-deep chunk, partial last wavefronts)
 SHAPES = [(1, 1, 1), (64, 64, 32), (1000, 47, 256), (777, 256, 100), (130, 100, 5),
-          (4099, 33, 47)]
+          (4099, 33, 47), (517, 20, 516), (3001, 48, 1030), (95, 16, 17)]
 
 
 @pytest.mark.parametrize("M,N,K", SHAPES)
