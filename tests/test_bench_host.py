@@ -66,6 +66,7 @@ def test_cpu_baseline_small_graph_repeats_and_threads():
         assert b["value"] > 0 and b["edge_features_per_s"] > 0
         # the whole graph is far below 0.3 s of work: it is run repeatedly
         assert "%d uniformly sampled rows" % n in b["sample"] and "repeated" in b["sample"]
+        assert "median of 3 such batches" in b["sample"]
         q = bench.cpu_baseline(w, X, 3 * n // 4, 16, 0.1, 8, threads=1)
         assert "8-bit halo dequantized" in q["sample"] and q["value"] > 0
     finally:
