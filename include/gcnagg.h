@@ -117,6 +117,10 @@ gcn_status gcn_normalize(gcn_graph* g, const int32_t* deg, void* stream);
  * receiver whose columns are its own nodes followed by received rows.
  *  deg_rows  int32 device array [n_rows], degrees without the self-loop, >= 0.
  *  deg_cols  int32 device array [n_cols], likewise.
+ * A^T receives the transposed values. A symmetric graph (GCN_SYMMETRIZE)
+ * stores one structure for both directions; when deg_rows and deg_cols are
+ * different arrays its A^T first gets entries of its own (8 bytes per entry),
+ * since its values are then not those of A.
  *  Negative degrees or NULL arrays -> GCN_EINVAL. Synchronizes `stream`. */
 gcn_status gcn_normalize_rc(gcn_graph* g, const int32_t* deg_rows, const int32_t* deg_cols,
                             void* stream);

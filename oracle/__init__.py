@@ -460,8 +460,7 @@ def layernorm64_bwd(Y, rstd, dY):
                             - Y * (dY * Y).mean(axis=1, keepdims=True))
 
 
-def sage_step(graph: Graph, X, params, labels, lp_mask=None, E=None, eps=1e-5, masks=None,
-              with_margins=True):
+def sage_step(graph: Graph, X, params, labels, lp_mask=None, E=None, eps=1e-5, masks=None):
     """Loss and gradients of one step of the 3-layer GraphSAGE-mean model.
 
     graph: mean-normalized (Graph(..., mean=True)); params: the list
@@ -474,9 +473,12 @@ def sage_step(graph: Graph, X, params, labels, lp_mask=None, E=None, eps=1e-5, m
     rows without lp_mask). masks (optional): the ReLU patterns of layers 1 and
     2 to use in place of O > 0 (a unit whose pre-activation lies within
     rounding of 0 may fall either way in another precision). Returns
-    dict(loss, grads (same order as params), dE or None, logits, margins: per
-    hidden layer |O| / (sum of the magnitudes of its terms), acts: the float64
-    patterns O > 0)."""
+    dict(loss, grads (same order as params), dE or None, logits, acts: the
+    float64 patterns O > 0 of the hidden layers, flip_margins: per hidden
+    layer, |O| / (sum of the magnitudes of its terms) at every unit where the
+    given mask differs from O > 0 (empty without masks), saved: per layer
+    (Y, rstd, Z, pattern used), douts: per layer the gradient of the loss
+    with respect to its output O)."""
     H = np.asarray(X, np.float64).copy()
     y = np.asarray(labels)
     n = H.shape[0]
@@ -491,18 +493,20 @@ def sage_step(graph: Graph, X, params, labels, lp_mask=None, E=None, eps=1e-5, m
     fwd = lambda T: _agg64(graph.csr_ptr, graph.csr_idx, graph.csr_val, T)
     bwd = lambda T: _agg64(graph.csc_ptr, graph.csc_idx, graph.csc_val, T)
     saved = []
-    margins, acts = [], []
+    flip_margins, acts = [], []
     for l in range(3):
         Ws, Wn, b = P[3 * l], P[3 * l + 1], P[3 * l + 2]
         Yl, rstd = layernorm64(H, eps)
         Zl = fwd(Yl)
         O = Yl @ Ws + Zl @ Wn + b
         if l < 2:
-            act = (O > 0) if masks is None else np.asarray(masks[l], bool)
-            if with_margins:
-                margins.append(np.abs(O) / (np.abs(Yl) @ np.abs(Ws) + np.abs(Zl) @ np.abs(Wn)
-                                            + np.abs(b)))
-            acts.append(O > 0)
+            own = O > 0
+            act = own if masks is None else np.asarray(masks[l], bool)
+            flip = act != own
+            rows = np.flatnonzero(flip.any(axis=1))
+            mag = (np.abs(Yl[rows]) @ np.abs(Ws) + np.abs(Zl[rows]) @ np.abs(Wn) + np.abs(b))
+            flip_margins.append((np.abs(O[rows]) / mag)[flip[rows]])
+            acts.append(own)
             H = O * act
         else:
             act = None
@@ -521,8 +525,10 @@ def sage_step(graph: Graph, X, params, labels, lp_mask=None, E=None, eps=1e-5, m
     dO /= max(n_loss, 1)
     grads = [None] * 9
     dE = None
+    douts = [None] * 3
     for l in (2, 1, 0):
         Yl, rstd, Zl, _ = saved[l]
+        douts[l] = dO
         grads[3 * l] = Yl.T @ dO
         grads[3 * l + 1] = Zl.T @ dO
         grads[3 * l + 2] = dO.sum(axis=0)
@@ -535,5 +541,6 @@ def sage_step(graph: Graph, X, params, labels, lp_mask=None, E=None, eps=1e-5, m
         else:
             dE = np.zeros_like(np.asarray(E, np.float64))
             np.add.at(dE, y[m], dH[m])
-    return dict(loss=loss, grads=grads, dE=dE, logits=logits, margins=margins, acts=acts)
+    return dict(loss=loss, grads=grads, dE=dE, logits=logits, acts=acts,
+                flip_margins=flip_margins, saved=saved, douts=douts)
 

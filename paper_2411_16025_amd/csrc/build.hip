@@ -943,9 +943,35 @@ gcn_status check_degrees(const int32_t* deg, int64_t n, hipStream_t stream) {
   return GCN_OK;
 }
 
-// values of A from row degrees and column degrees; A^T takes them swapped
+// A symmetric graph's transpose shares the structure and, until now, the
+// entries of A; give it entries of its own (8 bytes per entry) for values
+// that are not symmetric.
+gcn_status own_csc_entries(gcn_graph* g, hipStream_t stream) {
+  if (!g->csc_shared || g->csc_own_ent) return GCN_OK;
+  const int64_t nnz = g->csr.nnz;
+  Ent* e = nullptr;
+  GCN_CHECK(dalloc(&e, nnz, "transpose entries"));
+  hipError_t err = nnz > 0 ? hipMemcpyAsync(e, g->csr.ent, nnz * sizeof(Ent),
+                                            hipMemcpyDeviceToDevice, stream)
+                           : hipSuccess;
+  if (err != hipSuccess) {
+    dfree(e);
+    return hip_fail(err, "hipMemcpyAsync(transpose entries)", __FILE__, __LINE__);
+  }
+  g->csc.ent = e;
+  g->csc_own_ent = true;
+  return GCN_OK;
+}
+
+// values of A from row degrees and column degrees; A^T takes them swapped.
+// Entry (r, c) of A gets f(deg_rows[r], deg_cols[c]); entry (c, r) of A^T
+// the same value. With shared entries (a symmetric graph) entry (c, r) of
+// A^T is entry (c, r) of A, f(deg_rows[c], deg_cols[r]): equal for every
+// entry only when the two arrays are the same, so different arrays give the
+// transpose entries of its own first.
 gcn_status normalize_with(gcn_graph* g, const int32_t* deg_rows, const int32_t* deg_cols,
                           hipStream_t stream) {
+  if (deg_rows != deg_cols) GCN_CHECK(own_csc_entries(g, stream));
   for (int which = 0; which < 2; ++which) {
     if (which == 1 && g->csc_shared && !g->csc_own_ent) break;
     Mat& m = which ? g->csc : g->csr;
@@ -991,21 +1017,8 @@ extern "C" gcn_status gcn_normalize_mean(gcn_graph* g, void* stream_) {
   clear_error();
   GCN_CHECK(check_graph(g));
   hipStream_t stream = (hipStream_t)stream_;
-  const int64_t nnz = g->csr.nnz;
-  if (g->csc_shared && !g->csc_own_ent) {
-    // the transpose keeps the shared structure but needs values of its own
-    Ent* e = nullptr;
-    GCN_CHECK(dalloc(&e, nnz, "transpose entries"));
-    hipError_t err = nnz > 0 ? hipMemcpyAsync(e, g->csr.ent, nnz * sizeof(Ent),
-                                              hipMemcpyDeviceToDevice, stream)
-                             : hipSuccess;
-    if (err != hipSuccess) {
-      dfree(e);
-      return hip_fail(err, "hipMemcpyAsync(transpose entries)", __FILE__, __LINE__);
-    }
-    g->csc.ent = e;
-    g->csc_own_ent = true;
-  }
+  // the transpose keeps the shared structure but needs values of its own
+  GCN_CHECK(own_csc_entries(g, stream));
   for (int which = 0; which < 2; ++which) {
     Mat& m = which ? g->csc : g->csr;
     if (m.nnz == 0) continue;

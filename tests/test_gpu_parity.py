@@ -103,6 +103,42 @@ def test_normalization_bit_exact_over_wide_degrees(G):
     check_structure(G, g, og)
 
 
+@pytest.mark.parametrize("flags", [SYM | LOOPS, SYM])
+def test_normalize_rc_symmetric_graph_unequal_degrees(G, flags):
+    # A symmetric graph stores A once for both directions. Row and column
+    # degrees that differ make A_hat non-symmetric: entry (r, c) of A is
+    # f(dr[r], dc[c]) and entry (c, r) of A^T must carry the same value, so
+    # the transpose needs values of its own; the backward then computes
+    # A_hat^T G, not A_hat G.
+    note("normalize_rc symmetric flags=%d" % flags)
+    n = 3000
+    src, dst = synth.rmat_edges(141, n, 10 * n, perm_seed=142)
+    og = oracle.Graph(n, n, src, dst, flags, normalized=False)
+    dr = (synth.splitmix64(143, 0, n) % 500).astype(np.int32)
+    dc = (synth.splitmix64(144, 0, n) % 70).astype(np.int32)
+    csr_val = oracle.normalize_listed(og.csr_ptr, dr, dc[og.csr_idx])
+    csc_val = oracle.normalize_listed(og.csc_ptr, dc, dr[og.csc_idx])
+    assert not np.array_equal(csr_val, csc_val)
+    g = gpu_graph(G, n, n, src, dst, flags, normalize=False)
+    G.gcn_normalize_rc(g, dev(dr), dev(dc))
+    for which, (p, i, v) in ((0, (og.csr_ptr, og.csr_idx, csr_val)),
+                             (1, (og.csc_ptr, og.csc_idx, csc_val))):
+        ptr, idx, val = G.gcn_graph_export(g, which)
+        assert np.array_equal(ptr, p) and np.array_equal(idx, i)
+        assert np.array_equal(val.view(np.uint32), v.view(np.uint32)), "values of %d" % which
+    X = synth.uniform(145, n, 64)
+    assert_close(host(G.gcn_aggregate_fwd(g, dev(X))),
+                 *oracle.spmm(og.csr_ptr, og.csr_idx, csr_val, X), what="fwd")
+    assert_close(host(G.gcn_aggregate_bwd(g, dev(X))),
+                 *oracle.spmm(og.csc_ptr, og.csc_idx, csc_val, X), what="bwd")
+    # the same degree array for both: the symmetric normalization again
+    G.gcn_normalize(g)
+    og2 = oracle.Graph(n, n, src, dst, flags)
+    for which, v in ((0, og2.csr_val), (1, og2.csc_val)):
+        _, _, val = G.gcn_graph_export(g, which)
+        assert np.array_equal(val.view(np.uint32), v.view(np.uint32))
+
+
 # ---------------------------------------------------------------------------
 # Aggregation, fp32 and bf16.
 # ---------------------------------------------------------------------------
@@ -277,6 +313,33 @@ def test_star_giant_row(G):
     g = gpu_graph(G, k + 1, k + 1, src, dst, SYM | LOOPS)
     X = synth.uniform(74, k + 1, 128)
     assert_close(host(G.gcn_aggregate_fwd(g, dev(X))), *og.fwd(X), what="star")
+
+
+def test_star_2p20_leaves_default_plan(G):
+    # the single giant row of a power-law extreme: a star with 2^20 leaves,
+    # 2^20 + 1 columns, so the default plan cuts the hub row at column blocks
+    # (its 2^20 + 1 entries make the most segments and pieces a row gets);
+    # forward and transposed, against the oracle and the closed form
+    note("star 2^20 leaves, default plan")
+    k = 1 << 20
+    src = np.arange(1, k + 1, dtype=np.int32)
+    dst = np.zeros(k, np.int32)
+    og = oracle.Graph(k + 1, k + 1, src, dst, SYM | LOOPS)
+    g = gpu_graph(G, k + 1, k + 1, src, dst, SYM | LOOPS)
+    bins = G.gcn_graph_bins(g, 0)
+    assert bins[-1]["rows"] == 1 and bins[-1]["entries"] == k + 1, bins[-1]
+    X = synth.uniform(75, k + 1, 128)
+    Y = host(G.gcn_aggregate_fwd(g, dev(X)))
+    ref, S = og.fwd(X)
+    assert_close(Y, ref, S, what="star 2^20 fwd")
+    # the hub row in closed form: x_0 / (k + 1) + (sum of the leaves' rows) /
+    # sqrt(2 (k + 1)), up to the fp32 rounding of the two stored values
+    hub = (X[0].astype(np.float64) / (k + 1)
+           + X[1:].astype(np.float64).sum(axis=0) / np.sqrt(2.0 * (k + 1)))
+    assert np.allclose(Y[0], hub, rtol=0, atol=1e-5 * S[0].max())
+    Gm = synth.uniform(76, k + 1, 128)
+    assert_close(host(G.gcn_aggregate_bwd(g, dev(Gm))), *og.bwd(Gm), what="star 2^20 bwd")
+    g.free()
 
 
 def test_unnormalized_index_add(G):

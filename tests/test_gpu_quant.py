@@ -4,9 +4,11 @@
 Without LayerNorm the codes and parameters are bit-exact. With it, both
 sides compute the row statistics in double, whose summation order differs,
 then round once to fp32: the normalized values must agree to the last bit
-on at least 99.9% of rows and within one ulp everywhere, and on every row
-whose normalized values agree exactly the codes and parameters must agree
-bit for bit (they are then the same fp32 computation on the same numbers).
+on at least 99.9% of rows and within one ulp everywhere. The codes and
+parameters are then checked on every row, bit for bit: against the oracle's
+quantizer applied to the kernel's own normalized rows (the same fp32
+computation on the same numbers), and, on the rows whose normalized values
+agree exactly, against the oracle's whole LayerNorm + quantize chain.
 """
 
 import numpy as np
@@ -26,6 +28,15 @@ def G():
     import paper_2411_16025_amd as pkg
     pkg.lib()
     return pkg
+
+
+def check_codes_every_row(q, z, s, y, bits):
+    """Codes and (Z, S) of every row equal the oracle's quantizer applied to
+    the kernel's own normalized rows y, bit for bit."""
+    Qy, Zy, Sy = oracle.quantize_rows_bits(y, bits)
+    assert np.array_equal(q, Qy), "codes differ on %d rows" % np.any(q != Qy, axis=1).sum()
+    assert np.array_equal(z.view(np.uint32), Zy.view(np.uint32))
+    assert np.array_equal(s.view(np.uint32), Sy.view(np.uint32))
 
 
 @pytest.mark.parametrize("bits", [8, 2])
@@ -58,6 +69,7 @@ def test_layernorm_quantize(G, bits, F):
     assert ulp.max() <= 1
     same = np.all(ulp == 0, axis=1)
     assert same.mean() >= 0.999
+    check_codes_every_row(q, z, s, y, bits)
     assert np.array_equal(q[same], Qr[same])
     assert np.array_equal(z[same].view(np.uint32), Zr[same].view(np.uint32))
     assert np.array_equal(s[same].view(np.uint32), Sr[same].view(np.uint32))
@@ -127,7 +139,9 @@ def test_quantize_register_kernel_shapes(G, bits, F, ld):
     assert ulp.max() <= 1
     same = np.all(ulp == 0, axis=1)
     assert same.mean() >= 0.99
+    check_codes_every_row(q, z, s, y, bits)
     assert np.array_equal(q[same], Qr[same])
+    assert np.array_equal(z[same].view(np.uint32), Zr[same].view(np.uint32))
     assert np.array_equal(s[same].view(np.uint32), Sr[same].view(np.uint32))
     if bits == 8:  # the plain u8 entry point shares the kernels
         qu, zu, su = G.gcn_quantize_rows_u8(dev(Xp)[:, :F])

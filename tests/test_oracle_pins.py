@@ -383,6 +383,58 @@ def test_gcn_step_initial_loss_near_log_classes():
     assert abs(out["loss"] - math.log(ncls)) < 0.5
 
 
+def test_gcn_forward_brute_force_loops():
+    # The forward of the two-layer step written out with explicit loops from
+    # the edge list (Section 2.1: each layer aggregates the neighbours' rows
+    # of X W, then the activation; GCN's propagation matrix): neighbour sets
+    # of the symmetrized edge list without drawn self pairs, d~ = |N(i)| + 1,
+    # A_hat[i][j] = 1 / sqrt(d~_i d~_j) over N(i) and i itself;
+    # H1 = relu(A_hat (X W1)), logits = A_hat (H1 W2), loss = mean of
+    # log sum exp(logits) - logit of the label. A ReLU placed before the
+    # aggregation, a dropped self term or a transposed weight fails here.
+    n, fin, hid, ncls = 12, 3, 4, 3
+    src, dst = synth.rmat_edges(34, n, 30, perm_seed=35)
+    g = oracle.Graph(n, n, src, dst, SYM | LOOPS)
+    rng = np.random.default_rng(36)
+    X = rng.normal(size=(n, fin))
+    W1 = rng.normal(size=(fin, hid))
+    W2 = rng.normal(size=(hid, ncls))
+    y = rng.integers(0, ncls, n)
+    nbr = [set() for _ in range(n)]
+    for s, d in zip(src, dst):
+        if s != d:
+            nbr[d].add(int(s))
+            nbr[s].add(int(d))
+    dt = [len(nb) + 1 for nb in nbr]
+
+    def agg(H):
+        out = []
+        for i in range(n):
+            row = [H[i][f] / dt[i] for f in range(len(H[0]))]  # self term 1/sqrt(d~_i d~_i)
+            for j in nbr[i]:
+                w = 1.0 / math.sqrt(dt[i] * dt[j])
+                row = [row[f] + w * H[j][f] for f in range(len(H[0]))]
+            out.append(row)
+        return out
+
+    def matmul(H, W):
+        return [[sum(H[i][k] * W[k][c] for k in range(len(W))) for c in range(len(W[0]))]
+                for i in range(len(H))]
+
+    H1 = [[max(v, 0.0) for v in row] for row in agg(matmul(X.tolist(), W1.tolist()))]
+    logits = agg(matmul(H1, W2.tolist()))
+    loss = 0.0
+    for i in range(n):
+        m = max(logits[i])
+        loss += m + math.log(sum(math.exp(v - m) for v in logits[i])) - logits[i][y[i]]
+    loss /= n
+    out = oracle.gcn_step(g, X, W1, W2, y)
+    # the oracle aggregates with fp32-rounded A_hat values: within 2^-24 relative per entry
+    assert np.allclose(out["H1"], np.array(H1), rtol=1e-6, atol=1e-7)
+    assert np.allclose(out["logits"], np.array(logits), rtol=1e-6, atol=1e-7)
+    assert abs(out["loss"] - loss) <= 1e-6 * abs(loss)
+
+
 def test_double_input_aggregation_matches_dense():
     # the float64-input aggregation of the training step against dense A_hat H
     n = 150
