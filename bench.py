@@ -10,11 +10,16 @@ node, quadrant probabilities .57/.19/.19/.05, relabelled by a seeded
 permutation, symmetrized, deduplicated, one self-loop per node), F = 128,
 fp32 inputs drawn from N(0, 1).
 
-Reported: modeled HBM bytes per second (CSR bytes + gathered-row bytes +
-output bytes, the minimum traffic of the algorithm) for the whole step,
-its fraction of the 8 TB/s HBM peak, edge-features per second, the
-dominant kernel's roofline figures from per-launch HIP events, and the CPU
-oracle timed on a bounded row sample of the same workload.
+Reported: modeled bytes per second for the whole step under the traffic
+model (CSR bytes + gathered-row bytes + output bytes, where every stored
+entry brings its source row: the algorithm's traffic without cache reuse,
+so caches that serve repeated rows can put it above the 8 TB/s HBM peak),
+the bytes the L2 actually moved to and from the memory fabric (hardware
+counters committed under profiles/, scaled by a factor checked on a gather
+of known size), the compulsory traffic (every input row once), edge-features
+per second, the dominant kernel's roofline figures from per-launch HIP
+events, and the CPU oracle timed on a bounded row sample of the same
+workload.
 
 The graph build (sort, deduplication, transpose, binning) and the
 normalization run once per graph; they are timed separately and are not
@@ -42,7 +47,9 @@ HBM_PEAK_GBS = 8000.0
 # sources do not describe the library being timed
 AGG_SOURCES = [os.path.join(ROOT, "paper_2411_16025_amd", "csrc", f)
                for f in ("aggregate.hip", "build.hip")]
-COUNTERS = os.path.join(ROOT, "profiles", "agg_counters_rmat24_q8.txt")
+MODEL_NOTE = ("no-reuse gather model: every stored entry brings its source row, so cache hits "
+              "on repeated rows are priced as HBM traffic and frac can exceed 1; the counted "
+              "fabric bytes are the hardware figure")
 
 # kernel name -> row-length classes whose rows it processes
 KERNEL_CLASSES = {"agg_zero_rows": [0], "agg_tiny": [1, 2], "agg_short": [3, 4, 5, 6, 7],
@@ -60,7 +67,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="rmat24_q8",
                     choices=["rmat24_q8", "rmat24", "rmat20", "er4096", "product", "partition",
-                             "gcn_step", "sage_step", "prepost", "producer"])
+                             "perm22", "gcn_step", "sage_step", "prepost", "producer"])
     ap.add_argument("--halo-bits", type=int, default=8, choices=[8, 2],
                     help="code width of the halo rows (8: one byte per feature; 2: four per byte)")
     ap.add_argument("--senders", type=int, default=7,
@@ -99,29 +106,30 @@ def sources_sha256(paths):
     return h.hexdigest()
 
 
-def read_counters(kernel):
-    """(HBM bytes per dispatch, L2 hit rate) from the committed rocprofv3 PMC
-    summary, only if it was taken on the current aggregation source; else
-    (None, None)."""
-    if not os.path.exists(COUNTERS):
-        return None, None
-    kv, lines = {}, open(COUNTERS).read().splitlines()
-    for line in lines:
-        if ":" in line and not line.startswith("#"):
-            k, v = line.split(":", 1)
+def counters_path(workload, bits=8):
+    tag = workload + ("_int2" if bits == 2 else "")
+    return os.path.join(ROOT, "profiles", "agg_counters_%s.txt" % tag)
+
+
+def read_counters(path):
+    """Per (library kernel name, pass): counted L2-to-fabric bytes read and
+    written per pass and the L2 hit rate, from a committed rocprofv3 summary,
+    only if it was taken on the current aggregation source; else None."""
+    if not os.path.exists(path):
+        return None
+    kv, rows = {}, {}
+    for line in open(path).read().splitlines():
+        if line.startswith("#") or ":" not in line:
+            continue
+        k, v = line.split(":", 1)
+        if k.strip() == "counted":
+            name, op, fetch, write, hit = v.split()
+            rows[(name, op)] = (float(fetch), float(write), float(hit))
+        else:
             kv[k.strip()] = v.strip()
-    if kv.get("source_sha256") != sources_sha256(AGG_SOURCES) or kv.get("kernel") != kernel:
-        return None, None
-    try:
-        traffic = float(kv["fetch_bytes_per_dispatch"]) + float(kv["write_bytes_per_dispatch"])
-    except (KeyError, ValueError):
-        return None, None
-    hit = None
-    sym = "# " + kv.get("kernel_symbol", "\0")
-    for line in lines:  # the table row of the kernel: its last column is the L2 hit rate
-        if line.startswith(sym) and line.rstrip().endswith("%"):
-            hit = round(float(line.split()[-1].rstrip("%")) / 100.0, 4)
-    return traffic, hit
+    if kv.get("source_sha256") != sources_sha256(AGG_SOURCES) or not rows:
+        return None
+    return {"rows": rows, "fetch_scale": kv.get("fetch_scale"), "path": os.path.relpath(path, ROOT)}
 
 
 FP32_MFMA_PEAK_TFLOPS = 157.3
@@ -463,8 +471,10 @@ def main():
 
     t0 = time.time()
     w = {"rmat24_q8": synth.rmat24_q8, "rmat24": synth.rmat24, "rmat20": synth.rmat20, "er4096": synth.er_4096,
-         "product": synth.product_like, "partition": synth.partition_111m}[args.workload]()
-    k_seed = {"rmat24_q8": 5, "rmat24": 5, "rmat20": 2, "er4096": 1, "product": 3, "partition": 4}[args.workload]
+         "product": synth.product_like, "partition": synth.partition_111m,
+         "perm22": synth.perm22}[args.workload]()
+    k_seed = {"rmat24_q8": 5, "rmat24": 5, "rmat20": 2, "er4096": 1, "product": 3, "partition": 4,
+              "perm22": 6}[args.workload]
     log("generated %s: %d edges in %.1f s" % (w.name, len(w.src), time.time() - t0))
     F = w.F
     q8 = w.n_local_cols is not None
@@ -493,9 +503,8 @@ def main():
     X = torch.from_numpy(X_h).to(dev)
     G_h = gen(4000 + k_seed, w.n_rows, F)
     Gd = torch.from_numpy(G_h).to(dev)
-    del G_h
     if args.no_cpu_baseline:
-        X_h = None
+        X_h = G_h = None
     nlc = w.n_local_cols
     bits = args.halo_bits if q8 else 8
     if q8 and bits == 8:
@@ -584,6 +593,13 @@ def main():
     value = (Bf + Bb) / (step_ms * 1e-3) / 1e9
     ef_per_s = (nnz_f + nnz_b) * F / (step_ms * 1e-3)
 
+    # counted fabric bytes of every aggregation kernel (committed summary of
+    # this workload, taken on the current sources), per pass
+    counted = read_counters(counters_path(args.workload, bits))
+    counted_step = None
+    if counted is not None:
+        counted_step = sum(f + wr for f, wr, _ in counted["rows"].values())
+
     # dominant kernel and its roofline figures
     agg = {k: v for k, v in prof.items() if k in KERNEL_CLASSES}
     roofline = None
@@ -595,13 +611,16 @@ def main():
             for bins in (bins_f, bins_b) for c, b in enumerate(bins) if c in KERNEL_CLASSES[dom])
         avg_ms = tot_ms / launches
         achieved = per_launch_bytes / (avg_ms * 1e-3) / 1e9
-        # the committed counters describe the default workload only
-        traffic, l2_hit = (read_counters(dom) if bits == 8 and args.workload == "rmat24_q8"
-                           else (None, None))
+        traffic = l2_hit = None
+        if counted is not None:
+            per_op = [counted["rows"].get((dom, op)) for op in ("fwd", "bwd")]
+            if all(per_op):  # one launch per pass: the average of the two passes
+                traffic = 0.5 * sum(f + wr for f, wr, _ in per_op)
+                l2_hit = round(0.5 * sum(h for _, _, h in per_op), 4)
         roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": traffic,
+                    "traffic": traffic, "model": MODEL_NOTE,
                     "bytes_per_launch": int(per_launch_bytes), "avg_launch_ms": round(avg_ms, 4)}
         if traffic is not None:
             # the counted bytes over the same launch time: the rate the memory system delivered
@@ -635,13 +654,21 @@ def main():
                                     % ("u8" if bits == 8 else "2-bit packed")) if q8 else None,
                    "step": "fwd A_hat x + bwd A_hat^T g"
                            + (" with fused %d-bit halo dequant" % bits if q8 else "")},
-        "hbm_frac": round(value / HBM_PEAK_GBS, 4),
+        "modeled_frac": round(value / HBM_PEAK_GBS, 4), "model": MODEL_NOTE,
         "edge_features_per_s": float("%.4g" % ef_per_s),
         "fwd_ms": round(fwd_ms, 4), "bwd_ms": round(bwd_ms, 4),
         "step_ms_median": round(float(np.median(per_step)), 4),
         "step_ms_min": round(float(np.min(per_step)), 4),
-        # secondary: every input row read once (not reachable by a gather)
+        # the L2-to-fabric bytes the kernels moved (counters; Infinity Cache
+        # hits included, so an upper bound on HBM bytes) over the step time
+        "counted": None if counted_step is None else {
+            "GBps": round(counted_step / (step_ms * 1e-3) / 1e9, 1),
+            "frac": round(counted_step / (step_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "bytes_per_step": int(counted_step), "source": counted["path"],
+            "fetch_scale": counted["fetch_scale"]},
+        # every input row read once (a gather of repeated rows cannot reach it)
         "compulsory_GBps": round(compulsory / (step_ms * 1e-3) / 1e9, 1),
+        "compulsory_frac": round(compulsory / (step_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "modeled_bytes_per_step": int(Bf + Bb),
         "build_ms": round(build_ms, 1), "normalize_ms": round(norm_ms, 1),
         "kernels_ms_per_step": {k: round(v[1] / max(args.profile_steps, 1), 4)
@@ -653,54 +680,77 @@ def main():
 
     # ---- CPU baseline: the oracle on a bounded sample of the same workload ----
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, X_h, nlc, F, args.cpu_target_s, bits, args.cpu_threads)
+        out["cpu_baseline"] = cpu_baseline(w, X_h, nlc, F, args.cpu_target_s / 2, bits,
+                                           args.cpu_threads, G_h=G_h)
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(w, X_h, nlc, F, target_s, bits=8, threads=0):
+def cpu_baseline(w, X_h, nlc, F, target_s, bits=8, threads=0, G_h=None):
+    """The oracle (fp64 accumulation, OpenMP over rows) on a bounded sample of
+    the workload: the forward pass over rows of A and, with G_h, the
+    transposed pass over rows of A^T, about target_s seconds each. Small
+    graphs run whole, repeatedly (median of three batches)."""
     import oracle
     import synth
 
     if threads > 0:
         oracle.set_num_threads(threads)
-
-    order = synth.permutation(778, w.n_rows)  # rows in a seeded random order
     q8 = nlc is not None
-    if q8 and bits == 8:
-        Q, Z, S = oracle.quantize_rows(X_h[nlc:])
-    elif q8:
-        Q, Z, S = oracle.quantize_rows_bits(X_h[nlc:], bits)
 
-    def run(n_sel, reps=1):
-        sel = np.sort(order[:n_sel]).astype(np.int32)
-        ptr, idx = oracle.rows_of(w.n_rows, w.n_cols, w.src, w.dst, w.flags, sel)
-        val = np.ones(len(idx), np.float32)  # unit weights: the cost does not depend on them
-        t = time.time()
-        for _ in range(reps):
-            if q8 and bits == 8:
-                oracle.spmm_q8(ptr, idx, val, nlc, X_h[:nlc], Q, Z, S)
-            elif q8:
-                oracle.spmm_qbits(ptr, idx, val, nlc, X_h[:nlc], Q, Z, S, F, bits)
-            else:
-                oracle.spmm(ptr, idx, val, X_h)
-        dt = time.time() - t
-        halo = int(np.sum(idx >= nlc)) if q8 else 0
-        return dt, reps * len(sel), reps * len(idx), reps * halo
+    def quant(M):
+        if not q8:
+            return None
+        return oracle.quantize_rows(M[nlc:]) if bits == 8 else oracle.quantize_rows_bits(M[nlc:], bits)
 
-    n = min(w.n_rows, max(64, w.n_rows // 400))
-    dt, rows, ents, halo = run(n)
-    for _ in range(4):  # grow the sample until it is about target_s of oracle work
-        if dt >= 0.6 * target_s or n >= w.n_rows:
-            break
-        n = int(min(w.n_rows, n * min(8.0, target_s / max(dt, 1e-3))))
+    def one_pass(M, transpose):
+        n_major = w.n_cols if transpose else w.n_rows
+        order = synth.permutation(778 + int(transpose), n_major)  # rows in a seeded random order
+        Q = quant(M)
+
+        def run(n_sel, reps=1):
+            sel = np.sort(order[:n_sel]).astype(np.int32)
+            ptr, idx = oracle.rows_of(w.n_rows, w.n_cols, w.src, w.dst, w.flags, sel,
+                                      transpose=transpose)
+            val = np.ones(len(idx), np.float32)  # unit weights: the cost does not depend on them
+            t = time.time()
+            for _ in range(reps):
+                if q8 and bits == 8:
+                    oracle.spmm_q8(ptr, idx, val, nlc, M[:nlc], *Q)
+                elif q8:
+                    oracle.spmm_qbits(ptr, idx, val, nlc, M[:nlc], *Q, F, bits)
+                else:
+                    oracle.spmm(ptr, idx, val, M)
+            dt = time.time() - t
+            halo = int(np.sum(idx >= nlc)) if q8 else 0
+            return dt, reps * len(sel), reps * len(idx), reps * halo
+
+        n = min(n_major, max(64, n_major // 400))
         dt, rows, ents, halo = run(n)
-    reps, batches = 1, 1
-    if dt < 0.6 * target_s:  # the whole graph is quick: repeat it, median of three batches
-        reps = int(min(100000, max(2, target_s / 3 / max(dt, 1e-4))))
-        batches = 3
-        timed = [run(n, reps) for _ in range(batches)]
-        dt, rows, ents, halo = sorted(timed)[1]
-    B = model_bytes(rows, ents, halo, F, bits)
+        for _ in range(4):  # grow the sample until it is about target_s of oracle work
+            if dt >= 0.6 * target_s or n >= n_major:
+                break
+            n = int(min(n_major, n * min(8.0, target_s / max(dt, 1e-3))))
+            dt, rows, ents, halo = run(n)
+        reps, batches = 1, 1
+        if dt < 0.6 * target_s:  # the whole matrix is quick: repeat it, median of three batches
+            reps = int(min(100000, max(2, target_s / 3 / max(dt, 1e-4))))
+            batches = 3
+            timed = [run(n, reps) for _ in range(batches)]
+            dt, rows, ents, halo = sorted(timed)[1]
+        B = model_bytes(rows, ents, halo, F, bits)
+        return {"GBps": round(B / dt / 1e9, 3), "edge_features_per_s": float("%.4g" % (ents * F / dt)),
+                "seconds": round(dt, 2), "bytes": B, "entries": ents,
+                "sample": "%d %s (%d entries)%s" % (
+                    rows // reps, "rows of A^T" if transpose else "rows of A", ents // reps,
+                    ", repeated %d times (median of %d such batches)" % (reps, batches)
+                    if reps > 1 else "")}
+
+    fwd = one_pass(X_h, False)
+    bwd = one_pass(G_h, True) if G_h is not None else None
+    parts = [p for p in (fwd, bwd) if p is not None]
+    secs = sum(p["seconds"] for p in parts)
+    B = sum(p["bytes"] for p in parts)
+    ents = sum(p["entries"] for p in parts)
     cpu = "unknown"
     try:
         for line in open("/proc/cpuinfo"):
@@ -709,17 +759,18 @@ def cpu_baseline(w, X_h, nlc, F, target_s, bits=8, threads=0):
                 break
     except OSError:
         pass
-    return {"value": round(B / dt / 1e9, 3), "unit": "GB/s", "cores": oracle.num_threads(),
-            "cpu_model": cpu, "host_cpus": os.cpu_count(),
-            "kind": "oracle", "edge_features_per_s": float("%.4g" % (ents * F / dt)),
-            "seconds": round(dt, 2),
-            "sample": "forward aggregation (fp64 accumulation%s) over %d uniformly sampled rows "
-                      "(%d entries) of %s%s, unit weights; structure of the sampled rows built by "
-                      "the oracle from the edge list beforehand (untimed)"
-                      % (", %d-bit halo dequantized" % bits if q8 else "", rows // reps,
-                         ents // reps, w.name,
-                         ", repeated %d times (median of %d such batches)" % (reps, batches)
-                         if reps > 1 else "")}
+    for p in parts:
+        del p["bytes"], p["entries"]
+    out = {"value": round(B / secs / 1e9, 3), "unit": "GB/s", "cores": oracle.num_threads(),
+           "cpu_model": cpu, "host_cpus": os.cpu_count(), "kind": "oracle",
+           "edge_features_per_s": float("%.4g" % (ents * F / secs)), "seconds": round(secs, 2),
+           "fwd": fwd, "bwd": bwd,
+           "sample": "fp64-accumulating aggregation%s of %s over uniformly sampled rows: forward %s%s;"
+                     " unit weights; structure of the sampled rows built by the oracle from the edge "
+                     "list beforehand (untimed)"
+                     % (", %d-bit halo dequantized" % bits if q8 else "", w.name, fwd["sample"],
+                        "; transposed %s" % bwd["sample"] if bwd else "")}
+    return out
 
 
 if __name__ == "__main__":

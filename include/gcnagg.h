@@ -352,6 +352,25 @@ gcn_status gcn_prepost_split(int64_t n_src, int64_t n_dst, int64_t n_edges, cons
 gcn_status gcn_add_rows(int64_t n, int64_t F, const float* P, int64_t ldp, const int32_t* idx,
                         int64_t n_y, float* Y, int64_t ldy, void* stream);
 
+/* gcn_add_rows for partial sums that were quantized by their sender
+ * (Section 6.1 steps 2-3 applied to the pre-aggregated rows of Section 5.2:
+ * the sender quantizes them like any boundary row, e.g. with
+ * gcn_layernorm_quantize without GCN_LAYERNORM):
+ *   Y[idx[j], f] += fmaf((float)q[j, f], scale[j * ldp], zmin[j * ldp])
+ * in fp32 (the dequantized value rounded once, then the add), j < n.
+ *  bits  8: Q [n x ldq] uint8 codes, ldq >= F; 2: codes packed four per byte
+ *        along the features (feature f in bits [2 (f % 4), 2 (f % 4) + 2) of
+ *        byte f / 4), ldq >= (F + 3) / 4.
+ *  zmin, scale  fp32 zero point and scale of row j at element j * ldp
+ *        (ldp >= 1; ldp = 2 with scale == zmin + 1 reads the pairs
+ *        gcn_layernorm_quantize writes).
+ *  idx, n_y, Y, ldy  as for gcn_add_rows (distinct ids; ids outside
+ *        [0, n_y) are skipped).
+ * Other bit widths -> GCN_EINVAL. Asynchronous on `stream`. */
+gcn_status gcn_add_rows_q(int64_t n, int64_t F, int bits, const uint8_t* Q, int64_t ldq,
+                          const float* zmin, const float* scale, int64_t ldp, const int32_t* idx,
+                          int64_t n_y, float* Y, int64_t ldy, void* stream);
+
 /* ---- support calls ---------------------------------------------------- */
 
 /* Release every device array of the graph (after synchronizing the device

@@ -314,10 +314,82 @@ __global__ __launch_bounds__(64 * kAddWaves) void k_add_rows(int64_t n, int64_t 
   }
 }
 
+// The same combine for partial sums that arrive quantized (Section 6.1 step
+// 3 applied to the pre-aggregated rows): Y[idx[j], f] += fmaf(q[j, f], S[j],
+// Z[j]), codes of BITS bits (8: a byte per feature; 2: four per byte, feature
+// f in bits 2 (f % 4) of byte f / 4). One wavefront per received row; with
+// vec4 a lane takes four features (one 4-byte or one 1-byte code load).
+template <int BITS>
+__global__ __launch_bounds__(64 * kAddWaves) void k_add_rows_q(
+    int64_t n, int64_t F, const uint8_t* __restrict__ Q, int64_t ldq,
+    const float* __restrict__ zmin, const float* __restrict__ scale, int64_t ldp,
+    const int32_t* __restrict__ idx, int64_t n_y, float* __restrict__ Y, int64_t ldy,
+    bool vec4) {
+  const int64_t j = (int64_t)blockIdx.x * kAddWaves + threadIdx.x / 64;
+  if (j >= n) return;
+  const int64_t r = idx[j];
+  if (r < 0 || r >= n_y) return;
+  const uint8_t* q = Q + j * ldq;
+  const float z = zmin[j * ldp], sc = scale[j * ldp];
+  float* y = Y + r * ldy;
+  const int lane = threadIdx.x & 63;
+  constexpr uint32_t mask = (1u << BITS) - 1u;
+  if (vec4) {
+    for (int64_t f = 4 * lane; f < F; f += 256) {
+      const uint32_t c = BITS == 8 ? *reinterpret_cast<const uint32_t*>(q + f) : (uint32_t)q[f >> 2];
+      float4 b = *reinterpret_cast<const float4*>(y + f);
+      b.x += __builtin_fmaf((float)(c & mask), sc, z);
+      b.y += __builtin_fmaf((float)((c >> BITS) & mask), sc, z);
+      b.z += __builtin_fmaf((float)((c >> (2 * BITS)) & mask), sc, z);
+      b.w += __builtin_fmaf((float)((c >> (3 * BITS)) & mask), sc, z);
+      *reinterpret_cast<float4*>(y + f) = b;
+    }
+  } else {
+    for (int64_t f = lane; f < F; f += 64) {
+      const uint32_t c = BITS == 8 ? (uint32_t)q[f] : ((uint32_t)q[f >> 2] >> (2 * (f & 3))) & mask;
+      y[f] += __builtin_fmaf((float)c, sc, z);
+    }
+  }
+}
+
 }  // namespace
 }  // namespace gcn
 
 using namespace gcn;
+
+extern "C" gcn_status gcn_add_rows_q(int64_t n, int64_t F, int bits, const uint8_t* Q, int64_t ldq,
+                                     const float* zmin, const float* scale, int64_t ldp,
+                                     const int32_t* idx, int64_t n_y, float* Y, int64_t ldy,
+                                     void* stream_) {
+  clear_error();
+  if (bits != 8 && bits != 2) {
+    set_error("bits must be 8 or 2 (got %d)", bits);
+    return GCN_EINVAL;
+  }
+  const int64_t qbytes = bits == 8 ? F : (F + 3) / 4;
+  if (n < 0 || F < 1 || n_y < 0 || ldq < qbytes || ldp < 1 || ldy < F) {
+    set_error("need n >= 0, n_y >= 0, F >= 1, ldq >= code bytes per row, ldp >= 1 and ldy >= F");
+    return GCN_EINVAL;
+  }
+  if (n == 0) return GCN_OK;
+  if (!Q || !zmin || !scale || !idx || !Y) {
+    set_error("Q, zmin, scale, idx and Y must not be NULL");
+    return GCN_EINVAL;
+  }
+  hipStream_t stream = (hipStream_t)stream_;
+  const bool vec4 = F % 4 == 0 && ldy % 4 == 0 && reinterpret_cast<uintptr_t>(Y) % 16 == 0 &&
+                    (bits == 2 || (ldq % 4 == 0 && reinterpret_cast<uintptr_t>(Q) % 4 == 0));
+  ProfScope ps("add_rows_q", stream);
+  const dim3 grid((unsigned)((n + kAddWaves - 1) / kAddWaves)), block(64 * kAddWaves);
+  if (bits == 8)
+    hipLaunchKernelGGL(k_add_rows_q<8>, grid, block, 0, stream, n, F, Q, ldq, zmin, scale, ldp,
+                       idx, n_y, Y, ldy, vec4);
+  else
+    hipLaunchKernelGGL(k_add_rows_q<2>, grid, block, 0, stream, n, F, Q, ldq, zmin, scale, ldp,
+                       idx, n_y, Y, ldy, vec4);
+  GCN_HIP(hipGetLastError());
+  return GCN_OK;
+}
 
 extern "C" gcn_status gcn_add_rows(int64_t n, int64_t F, const float* P, int64_t ldp,
                                    const int32_t* idx, int64_t n_y, float* Y, int64_t ldy,

@@ -33,7 +33,7 @@ GCN_GEMM_NN, GCN_GEMM_NT, GCN_GEMM_TN = 0, 1, 2
 EXPORTS = ("gcn_build_csr", "gcn_normalize", "gcn_normalize_rc", "gcn_normalize_mean",
            "gcn_layernorm_fwd", "gcn_layernorm_bwd", "gcn_sage3_forward", "gcn_sage3_step",
            "gcn_prepost_split",
-           "gcn_add_rows", "gcn_aggregate_fwd", "gcn_aggregate_bwd",
+           "gcn_add_rows", "gcn_add_rows_q", "gcn_aggregate_fwd", "gcn_aggregate_bwd",
            "gcn_aggregate_fwd_q8halo", "gcn_quantize_rows_u8", "gcn_layernorm_quantize",
            "gcn_gemm_f32", "gcn_relu",
            "gcn_relu_bwd", "gcn_softmax_xent", "gcn_gcn2_step", "gcn_graph_free",
@@ -65,6 +65,7 @@ def lib():
         L.gcn_normalize_rc.argtypes = [P, P, P, P]
         L.gcn_prepost_split.argtypes = [i64, i64, i64, P, P, P, P, P, P]
         L.gcn_add_rows.argtypes = [i64, i64, P, i64, P, i64, P, i64, P]
+        L.gcn_add_rows_q.argtypes = [i64, i64, i32, P, i64, P, P, i64, P, i64, P, i64, P]
         L.gcn_aggregate_fwd.argtypes = [P, P, i64, i32, P, i64, i64, P]
         L.gcn_aggregate_bwd.argtypes = [P, P, i64, i32, P, i64, i64, P]
         L.gcn_aggregate_fwd_q8halo.argtypes = [P, i64, P, i64, P, i64, P, P, i64, P, i64, i64, u32,
@@ -214,6 +215,33 @@ def gcn_add_rows(P: torch.Tensor, idx: torch.Tensor, Y: torch.Tensor, stream=Non
     _check(lib().gcn_add_rows(P.shape[0], P.shape[1], P.data_ptr(), _rowmajor(P, "P"),
                               idx.data_ptr(), Y.shape[0], Y.data_ptr(), _rowmajor(Y, "Y"),
                               _stream(stream)))
+    return Y
+
+
+def gcn_add_rows_q(Q: torch.Tensor, zmin: torch.Tensor, scale: torch.Tensor, idx: torch.Tensor,
+                   Y: torch.Tensor, bits: int = 8, F: int | None = None, stream=None):
+    """Y[idx[j], f] += fmaf(q[j, f], scale[j], zmin[j]) in place (distinct idx);
+    zmin / scale are 1-D with a common stride (the columns of an [n, 2] tensor
+    give the paired layout)."""
+    _dev(Q, torch.uint8, "Q")
+    _dev(Y, torch.float32, "Y")
+    _dev(idx, torch.int32, "idx")
+    F = Y.shape[1] if F is None else F
+    n = Q.shape[0]
+    if Q.dim() != 2 or Y.dim() != 2 or Y.shape[1] != F or idx.numel() != n:
+        raise ValueError("need Q [n x code bytes], idx [n], Y [m x F]")
+    if not idx.is_contiguous():
+        raise ValueError("idx must be contiguous")
+    for t, nm in ((zmin, "zmin"), (scale, "scale")):
+        _dev(t, torch.float32, nm)
+        if t.dim() != 1 or t.numel() < n:
+            raise ValueError("%s must be 1-D with at least %d entries" % (nm, n))
+    ldp = zmin.stride(0)
+    if scale.stride(0) != ldp or ldp < 1:
+        raise ValueError("zmin and scale need the same positive stride")
+    _check(lib().gcn_add_rows_q(n, F, bits, Q.data_ptr(), _rowmajor(Q, "Q"), zmin.data_ptr(),
+                                scale.data_ptr(), ldp, idx.data_ptr(), Y.shape[0], Y.data_ptr(),
+                                _rowmajor(Y, "Y"), _stream(stream)))
     return Y
 
 

@@ -49,8 +49,14 @@ def _L():
         lib.synth_permutation.argtypes = [u64, i64, P]
         lib.synth_er_edges.argtypes = [u64, i64, i64, P, P]
         lib.synth_rmat_edges.argtypes = [u64, i64, i64, d, d, d, P, P, P]
-        lib.synth_partition_edges.argtypes = [u64, i64, i64, i64, d, d, d, P, P, P, P]
-        lib.synth_partition_edges.restype = i64
+        lib.synth_first_draws.argtypes = [i64, P, P, i64, P]
+        lib.synth_first_draws.restype = i64
+        lib.synth_nth_set.argtypes = [i64, P, i64]
+        lib.synth_nth_set.restype = i64
+        lib.synth_partition_select.argtypes = [i64, P, P, P, i64, i64, P]
+        lib.synth_partition_select.restype = i64
+        lib.synth_partition_emit.argtypes = [i64, P, P, P, i64, i64, P, P, P]
+        lib.synth_partition_emit.restype = i64
         lib.synth_uniform.argtypes = [u64, i64, i64, i64, P]
         lib.synth_normal.argtypes = [u64, i64, i64, i64, P]
         lib.synth_glorot.argtypes = [u64, i64, i64, P]
@@ -98,18 +104,52 @@ def rmat_edges(seed: int, n: int, m: int, perm_seed: int | None = None, abc=RMAT
     return src, dst
 
 
-def partition_edges(seed: int, perm_seed: int, n_total: int, n_local: int, m: int, abc=RMAT_ABC):
-    """One worker's share of an undirected RMAT graph (see synth.cpp).
+def first_draws(a: np.ndarray, b: np.ndarray, n: int):
+    """(first, distinct): first[e] is True for the first draw of each unordered
+    pair {a[e], b[e]} with a[e] != b[e]; distinct = number of such pairs."""
+    a = np.ascontiguousarray(a, np.int32)
+    b = np.ascontiguousarray(b, np.int32)
+    first = np.empty(len(a), np.uint8)
+    distinct = _L().synth_first_draws(len(a), _p(a), _p(b), n, _p(first))
+    return first.view(bool), int(distinct)
 
-    Returns (src, dst, raw_count): entries "src contributes to row dst" with
-    dst < n_local, and the per-vertex count of non-self draws.
+
+def nth_set(flags: np.ndarray, k: int) -> int:
+    """Index of the k-th (1-based) True entry, or -1."""
+    flags = np.ascontiguousarray(flags).view(np.uint8)
+    return int(_L().synth_nth_set(len(flags), _p(flags), k))
+
+
+def partition_edges(seed: int, perm_seed: int, n_total: int, n_local: int, m: int,
+                    target: int | None = None, abc=RMAT_ABC):
+    """One worker's share of an undirected RMAT graph over [0, n_total): the
+    draws {u, v} of rmat_edges(seed, n_total, m, perm_seed), in draw order;
+    each emits "v contributes to row u" when u < n_local and "u contributes to
+    row v" when v < n_local (a local-local pair emits both, so the local block
+    stays symmetric); self pairs emit nothing (see synth.cpp).
+
+    target (optional): stop once the distinct entries emitted reach exactly
+    `target`; a draw whose new entries would pass it is left out.
+    Returns (src, dst, raw_count): the entries, "src contributes to row dst",
+    in draw order (duplicates included), and per vertex the number of draws
+    taken that touch it.
     """
-    perm = permutation(perm_seed, n_total)
-    src = np.empty(2 * m, np.int32)
-    dst = np.empty(2 * m, np.int32)
+    src_d, dst_d = rmat_edges(seed, n_total, m, perm_seed=perm_seed, abc=abc)
+    u, v = dst_d, src_d
+    take = np.empty(m, np.uint8)
+    if target is None:
+        first = np.ones(m, np.uint8)
+    else:
+        first, _ = first_draws(u, v, n_total)
+    used = _L().synth_partition_select(m, _p(u), _p(v), _p(first.view(np.uint8)), n_local,
+                                       -1 if target is None else target, _p(take))
+    if used < 0:
+        raise ValueError("%d draws do not reach %d distinct entries" % (m, target))
+    src = np.empty(2 * used, np.int32)
+    dst = np.empty(2 * used, np.int32)
     raw = np.empty(n_total, np.int64)
-    cnt = _L().synth_partition_edges(seed, n_total, n_local, m, abc[0], abc[1], abc[2],
-                                     _p(perm), _p(src), _p(dst), _p(raw))
+    cnt = _L().synth_partition_emit(used, _p(u), _p(v), _p(take), n_local, n_total, _p(src),
+                                    _p(dst), _p(raw))
     return src[:cnt].copy(), dst[:cnt].copy(), raw
 
 
@@ -201,25 +241,46 @@ def rmat24_q8() -> Workload:
     return rmat(24, 32, 128, 5, name="rmat24_ef32_f128_q8halo", halo_fraction=0.25)
 
 
+def perm22(F: int = 128, k: int = 6) -> Workload:
+    """Permutation graph over 2^22 nodes: row i holds the single entry
+    (i, perm[i]), no self-loops. Every pass gathers each input row exactly
+    once, so its traffic is known exactly: the workload on which hardware
+    byte counters of a gather are checked."""
+    n = 1 << 22
+    perm = permutation(2000 + k, n)
+    return Workload("perm22_f%d" % F, n, n, perm.copy(), np.arange(n, dtype=np.int32), 0, F)
+
+
 def rmat24() -> Workload:
     """RMAT scale 24, edge factor 32, F = 128, every input row fp32."""
     return rmat(24, 32, 128, 5)
 
 
-def product_like(n: int = 2_449_029, draws: int = 65_700_000, k: int = 3) -> Workload:
+def product_like(n: int = 2_449_029, pairs: int = 61_859_140, k: int = 3,
+                 max_draws: int = 68_000_000) -> Workload:
     """Product-graph-shaped RMAT: n nodes by rejection from the next power of
-    two, permuted, symmetrized, +I. The default draw count targets about
-    61.9M distinct undirected non-loop edges."""
-    src, dst = rmat_edges(1000 + k, n, draws, perm_seed=2000 + k)
-    return Workload(f"product_like_n{n}", n, n, src, dst, SYMMETRIZE | ADD_SELF_LOOPS, 256)
+    two, permuted; draws are taken in order until they hold exactly `pairs`
+    distinct undirected non-loop pairs; symmetrized, +I, so the graph stores
+    2 * pairs + n entries (126,167,309 by default)."""
+    src, dst = rmat_edges(1000 + k, n, max_draws, perm_seed=2000 + k)
+    first, distinct = first_draws(src, dst, n)
+    if distinct < pairs:
+        raise ValueError("%d draws hold only %d distinct pairs" % (max_draws, distinct))
+    m = nth_set(first, pairs) + 1
+    return Workload(f"product_like_n{n}", n, n, src[:m].copy(), dst[:m].copy(),
+                    SYMMETRIZE | ADD_SELF_LOOPS, 256, extra={"draws": m})
 
 
 def partition_111m(n_local: int = 14_000_000, n_total: int = 20_000_000,
-                   draws: int = 142_000_000, k: int = 4) -> Workload:
+                   stored: int = 200_000_000, k: int = 4,
+                   max_draws: int = 142_000_000) -> Workload:
     """One worker's partition of a large RMAT graph: n_local rows, columns
-    over [0, n_total) (ids >= n_local are halo), self-loops on local rows,
-    normalization by a supplied global degree deg = floor(2.2 * raw_count)."""
-    src, dst, raw = partition_edges(1000 + k, 2000 + k, n_total, n_local, draws)
+    over [0, n_total) (ids >= n_local are halo), self-loops on local rows, draws
+    taken in order until the rows store exactly `stored` entries (self-loops
+    included), normalization by a supplied global degree
+    deg = floor(2.2 * raw_count)."""
+    src, dst, raw = partition_edges(1000 + k, 2000 + k, n_total, n_local, max_draws,
+                                    target=stored - n_local)
     deg = ((raw * 11) // 5).astype(np.int32)
     return Workload(f"partition_{n_local}x{n_total}", n_local, n_total, src, dst, ADD_SELF_LOOPS,
                     128, deg=deg)

@@ -12,9 +12,11 @@
 // OOPSLA 2014). Every output depends only on (seed, counter), so the results
 // do not depend on the number of threads.
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <utility>
 #include <vector>
 
 #include <omp.h>
@@ -150,37 +152,129 @@ void synth_rmat_edges(uint64_t seed, int64_t n, int64_t m, double a, double b, d
   }
 }
 
-// One worker's partition of an undirected RMAT graph over [0, n_total).
-// Each draw {u, v} (after relabelling through perm) emits the directed entry
-// "v contributes to row u" when u < n_local and "u contributes to row v"
-// when v < n_local, so the local-local block stays symmetric and local rows
-// see their halo neighbours as columns >= n_local. Self pairs emit nothing.
-// Entries are written in draw order; the return value is their count
-// (at most 2*m). raw_count[v] (length n_total, zeroed here) receives the
-// number of non-self draws touching v, a stand-in for the vertex's degree in
+// Marks the first draw of every unordered pair: first[e] = 1 when the pair
+// {a[e], b[e]} (a[e] != b[e], ids in [0, n)) occurs in no earlier draw, else
+// 0 (self pairs get 0). Returns the number of distinct pairs. Used by recipes
+// that fix a count of distinct pairs rather than a count of draws: they take
+// draws in order until that count is reached. The draws are dealt into
+// buckets by a hash of the pair (keeping draw order within a bucket), and
+// each bucket is scanned in order against a hash set of its own.
+int64_t synth_first_draws(int64_t m, const int32_t* a, const int32_t* b, int64_t n,
+                          uint8_t* first) {
+  constexpr int kBucketBits = 10;
+  constexpr int kBuckets = 1 << kBucketBits;
+  const int nt = omp_get_max_threads();
+  std::vector<int64_t> cnt((size_t)nt * kBuckets + 1, 0);
+  auto key_of = [&](int64_t e) -> uint64_t {
+    const uint64_t lo = (uint64_t)std::min(a[e], b[e]), hi = (uint64_t)std::max(a[e], b[e]);
+    return lo * (uint64_t)n + hi;
+  };
+  auto bucket_of = [](uint64_t key) { return (int)(mix64(key) >> (64 - kBucketBits)); };
+#pragma omp parallel num_threads(nt)
+  {
+    const int t = omp_get_thread_num();
+    const int64_t lo = m * t / nt, hi = m * (t + 1) / nt;
+    for (int64_t e = lo; e < hi; ++e) {
+      first[e] = 0;
+      if (a[e] != b[e]) ++cnt[(size_t)bucket_of(key_of(e)) * nt + t];
+    }
+  }
+  // offsets: bucket-major, thread order within a bucket (draw order kept)
+  int64_t run = 0;
+  for (size_t i = 0; i < (size_t)nt * kBuckets; ++i) {
+    const int64_t c = cnt[i];
+    cnt[i] = run;
+    run += c;
+  }
+  cnt[(size_t)nt * kBuckets] = run;
+  std::vector<uint64_t> keys((size_t)run);
+  std::vector<int64_t> draw((size_t)run);
+#pragma omp parallel num_threads(nt)
+  {
+    const int t = omp_get_thread_num();
+    const int64_t lo = m * t / nt, hi = m * (t + 1) / nt;
+    for (int64_t e = lo; e < hi; ++e) {
+      if (a[e] == b[e]) continue;
+      const uint64_t k = key_of(e);
+      const int64_t o = cnt[(size_t)bucket_of(k) * nt + t]++;
+      keys[o] = k;
+      draw[o] = e;
+    }
+  }
+  // after the scatter, cnt[b * nt + t] is where slot (b, t + 1) starts; the
+  // start of bucket b is cnt[b * nt - 1] (0 for b = 0)
+  int64_t distinct = 0;
+#pragma omp parallel for schedule(dynamic, 4) reduction(+ : distinct)
+  for (int bk = 0; bk < kBuckets; ++bk) {
+    const int64_t beg = bk == 0 ? 0 : cnt[(size_t)bk * nt - 1];
+    const int64_t end = cnt[(size_t)(bk + 1) * nt - 1];
+    size_t cap = 16;
+    while (cap < (size_t)(2 * (end - beg))) cap <<= 1;
+    std::vector<uint64_t> set(cap, UINT64_MAX);
+    for (int64_t i = beg; i < end; ++i) {
+      size_t h = (size_t)mix64(keys[i] ^ 0x5bd1e995ULL) & (cap - 1);
+      while (set[h] != UINT64_MAX && set[h] != keys[i]) h = (h + 1) & (cap - 1);
+      if (set[h] == UINT64_MAX) {
+        set[h] = keys[i];
+        first[draw[i]] = 1;
+        ++distinct;
+      }
+    }
+  }
+  return distinct;
+}
+
+// Index of the k-th (1-based) nonzero flag, or -1 when there are fewer.
+int64_t synth_nth_set(int64_t m, const uint8_t* flags, int64_t k) {
+  int64_t seen = 0;
+  for (int64_t e = 0; e < m; ++e)
+    if (flags[e] && ++seen == k) return e;
+  return -1;
+}
+
+// One worker's partition of an undirected RMAT graph over [0, n_total), from
+// its draws {u[e], v[e]} in draw order (first: synth_first_draws of them).
+// A draw emits "v contributes to row u" when u < n_local and "u contributes
+// to row v" when v < n_local, so the local-local block stays symmetric; self
+// pairs emit nothing. A first draw adds as many distinct entries as it has
+// local endpoints. With target >= 0, draws are taken until the distinct
+// entries reach exactly `target`, a draw that would pass it being left out;
+// take[e] (length m) marks the draws taken. Returns the number of draws
+// consumed (one past the last taken), or -1 if the draws cannot reach the
+// target.
+int64_t synth_partition_select(int64_t m, const int32_t* u, const int32_t* v,
+                               const uint8_t* first, int64_t n_local, int64_t target,
+                               uint8_t* take) {
+  int64_t total = 0;
+  for (int64_t e = 0; e < m; ++e) {
+    const int64_t add = first[e] ? (int64_t)(u[e] < n_local) + (v[e] < n_local) : 0;
+    take[e] = 0;
+    if (target >= 0 && total + add > target) continue;
+    take[e] = u[e] != v[e];
+    total += add;
+    if (target >= 0 && total == target) return e + 1;
+  }
+  return target < 0 ? m : -1;
+}
+
+// The entries of the taken draws (see synth_partition_select), "src
+// contributes to row dst", in draw order (duplicates included); returns their
+// count (at most 2 m). raw_count[x] (length n_total, zeroed here) receives
+// the number of taken draws touching x, a stand-in for the vertex's degree in
 // the whole (unpartitioned) graph.
-int64_t synth_partition_edges(uint64_t seed, int64_t n_total, int64_t n_local, int64_t m,
-                              double a, double b, double c, const int32_t* perm, int32_t* src,
-                              int32_t* dst, int64_t* raw_count) {
-  const int scale = scale_for((uint64_t)n_total);
-  const RmatThresholds th = thresholds(a, b, c);
+int64_t synth_partition_emit(int64_t m, const int32_t* u, const int32_t* v, const uint8_t* take,
+                             int64_t n_local, int64_t n_total, int32_t* src, int32_t* dst,
+                             int64_t* raw_count) {
   const int nt = omp_get_max_threads();
   std::vector<int64_t> counts((size_t)nt + 1, 0);
-  std::vector<int32_t> pu((size_t)m), pv((size_t)m);
 #pragma omp parallel num_threads(nt)
   {
     const int tid = omp_get_thread_num();
     const int64_t lo = m * tid / nt, hi = m * (tid + 1) / nt;
-    int64_t cnt = 0;
-    for (int64_t e = lo; e < hi; ++e) {
-      uint64_t u, v;
-      rmat_draw(seed, (uint64_t)e, scale, (uint64_t)n_total, th, &u, &v);
-      const int32_t su = perm[u], sv = perm[v];
-      pu[e] = su;
-      pv[e] = sv;
-      if (su != sv) cnt += (su < n_local) + (sv < n_local);
-    }
-    counts[tid + 1] = cnt;
+    int64_t c = 0;
+    for (int64_t e = lo; e < hi; ++e)
+      if (take[e]) c += (u[e] < n_local) + (v[e] < n_local);
+    counts[tid + 1] = c;
   }
   for (int t = 0; t < nt; ++t) counts[t + 1] += counts[t];
 #pragma omp parallel num_threads(nt)
@@ -189,17 +283,16 @@ int64_t synth_partition_edges(uint64_t seed, int64_t n_total, int64_t n_local, i
     const int64_t lo = m * tid / nt, hi = m * (tid + 1) / nt;
     int64_t o = counts[tid];
     for (int64_t e = lo; e < hi; ++e) {
-      const int32_t su = pu[e], sv = pv[e];
-      if (su == sv) continue;
-      if (su < n_local) { src[o] = sv; dst[o] = su; ++o; }
-      if (sv < n_local) { src[o] = su; dst[o] = sv; ++o; }
+      if (!take[e]) continue;
+      if (u[e] < n_local) { src[o] = v[e]; dst[o] = u[e]; ++o; }
+      if (v[e] < n_local) { src[o] = u[e]; dst[o] = v[e]; ++o; }
     }
   }
   std::memset(raw_count, 0, sizeof(int64_t) * (size_t)n_total);
   for (int64_t e = 0; e < m; ++e) {
-    if (pu[e] == pv[e]) continue;
-    raw_count[pu[e]] += 1;
-    raw_count[pv[e]] += 1;
+    if (!take[e]) continue;
+    raw_count[u[e]] += 1;
+    raw_count[v[e]] += 1;
   }
   return counts[nt];
 }

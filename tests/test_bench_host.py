@@ -24,13 +24,13 @@ def test_traffic_model_by_hand():
     assert bench.model_bytes(3, 10, 0, 6) == 24 + 80 + 240 + 72
 
 
-def _counters_file(path, sha, kernel="agg_pieces", sym="k_pieces<4, 32, SrcQ<4, 8, false> >"):
+def _counters_file(path, sha):
     with open(path, "w") as f:
         f.write("# table\n")
-        f.write("# %-40s %16s %16s %14s %14s %8s\n" % ("kernel", "F", "W", "f", "w", "L2_hit"))
-        f.write("# %-40s %16.6g %16.6g %14.2f %14.2f %7.1f%%\n" % (sym, 1.0, 1.0, 1.0, 1.0, 61.5))
-        f.write("kernel: %s\nkernel_symbol: %s\nsource_sha256: %s\n" % (kernel, sym, sha))
-        f.write("fetch_bytes_per_dispatch: 1000\nwrite_bytes_per_dispatch: 234\n")
+        f.write("source_sha256: %s\nfetch_scale: 2.0\n" % sha)
+        f.write("counted: agg_pieces fwd 1000 234 0.615\n")
+        f.write("counted: agg_pieces bwd 1100 300 0.6\n")
+        f.write("counted: agg_short fwd 50 5 0.2\n")
 
 
 def test_counters_gate_on_source_hash(tmp_path, monkeypatch):
@@ -38,13 +38,20 @@ def test_counters_gate_on_source_hash(tmp_path, monkeypatch):
     src.write_text("// kernels\n")
     monkeypatch.setattr(bench, "AGG_SOURCES", [str(src)])
     cfile = tmp_path / "counters.txt"
-    monkeypatch.setattr(bench, "COUNTERS", str(cfile))
-    assert bench.read_counters("agg_pieces") == (None, None)  # no file
+    assert bench.read_counters(str(cfile)) is None  # no file
     _counters_file(cfile, bench.sources_sha256([str(src)]))
-    assert bench.read_counters("agg_pieces") == (1234.0, 0.615)
-    assert bench.read_counters("agg_short") == (None, None)  # another kernel
+    c = bench.read_counters(str(cfile))
+    assert c["rows"][("agg_pieces", "fwd")] == (1000.0, 234.0, 0.615)
+    assert c["rows"][("agg_pieces", "bwd")] == (1100.0, 300.0, 0.6)
+    assert c["rows"][("agg_short", "fwd")] == (50.0, 5.0, 0.2)
+    assert c["fetch_scale"] == "2.0"
     src.write_text("// kernels, edited\n")  # counters taken on other sources
-    assert bench.read_counters("agg_pieces") == (None, None)
+    assert bench.read_counters(str(cfile)) is None
+
+
+def test_counters_path_per_workload():
+    assert bench.counters_path("rmat24_q8").endswith("profiles/agg_counters_rmat24_q8.txt")
+    assert bench.counters_path("rmat24_q8", 2).endswith("profiles/agg_counters_rmat24_q8_int2.txt")
 
 
 def test_several_gpus_are_refused():
@@ -61,11 +68,13 @@ def test_cpu_baseline_small_graph_repeats_and_threads():
     X = synth.normal(73, n, 16)
     before = oracle.num_threads()
     try:
-        b = bench.cpu_baseline(w, X, None, 16, 0.3, 8, threads=1)
+        b = bench.cpu_baseline(w, X, None, 16, 0.3, 8, threads=1, G_h=X)
         assert b["cores"] == 1 and b["kind"] == "oracle" and b["unit"] == "GB/s"
         assert b["value"] > 0 and b["edge_features_per_s"] > 0
+        assert b["fwd"]["GBps"] > 0 and b["bwd"]["GBps"] > 0
         # the whole graph is far below 0.3 s of work: it is run repeatedly
-        assert "%d uniformly sampled rows" % n in b["sample"] and "repeated" in b["sample"]
+        assert "%d rows of A " % n in b["sample"] and "repeated" in b["sample"]
+        assert "%d rows of A^T" % n in b["sample"]
         assert "median of 3 such batches" in b["sample"]
         q = bench.cpu_baseline(w, X, 3 * n // 4, 16, 0.1, 8, threads=1)
         assert "8-bit halo dequantized" in q["sample"] and q["value"] > 0

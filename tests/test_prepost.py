@@ -130,17 +130,26 @@ def global_graph(seed, n, m):
     return rows, cols, np.bincount(rows, minlength=n).astype(np.int32)
 
 
-def hybrid_receiver(G, bounds, rows, cols, deg, X, check_values=None):
+def hybrid_receiver(G, bounds, rows, cols, deg, X, check_values=None, bits=None):
     """Worker 0 = nodes [0, bounds[1]); worker w = [bounds[w], bounds[w+1]).
     Returns the receiver's output and, per sender, (cut edges, distinct
-    destinations, distinct sources, rows sent)."""
+    destinations, distinct sources, rows sent), and a dict of what was sent.
+
+    bits (8 or 2): the senders quantize what they send, the covered source
+    rows and their partial sums, per row with gcn_layernorm_quantize (no
+    LayerNorm); the receiver aggregates the source rows through the fused
+    dequantizing kernel (columns >= its own nodes are the received rows) and
+    adds the partial sums with gcn_add_rows_q."""
     import torch
-    from gpu_util import dev
+    from gpu_util import dev, host
     n0 = bounds[1]
+    F = X.shape[1]
     degd = dev(deg)
     local = (rows < n0) & (cols < n0)
     post_src, post_dst, partials, volumes = [], [], [], []
     recv_X, col_ids = [dev(X[:n0])], [np.arange(n0)]
+    recv_q = []
+    sent = dict(pre=[], P=[], Pq=[])
     n_cols = n0
     for w in range(1, len(bounds) - 1):
         lo, hi = bounds[w], bounds[w + 1]
@@ -159,9 +168,21 @@ def hybrid_receiver(G, bounds, rows, cols, deg, X, check_values=None):
             G.gcn_normalize_rc(gp, dev(deg[cov_dst]), degd[lo:hi].contiguous())
             if check_values is not None:
                 check_values(gp, cov_dst, lo + np.arange(hi - lo))
-            partials.append((G.gcn_aggregate_fwd(gp, dev(X[lo:hi])), dev(cov_dst)))
+            P = G.gcn_aggregate_fwd(gp, dev(X[lo:hi]))
+            if bits is None:
+                partials.append((P, dev(cov_dst)))
+            else:
+                q = G.gcn_layernorm_quantize(P, bits=bits, layernorm=False)
+                partials.append((q, dev(cov_dst)))
+                sent["pre"].append((lo, hi, s_loc[pre], dst_slot[d_rec[pre]], cov_dst))
+                sent["P"].append(host(P))
+                sent["Pq"].append(tuple(host(t) for t in q))
         # sent: the covered source rows and the partial sums
-        recv_X.append(dev(X[lo + cov_src]))
+        if bits is None:
+            recv_X.append(dev(X[lo + cov_src]))
+        elif len(cov_src):
+            recv_q.append(G.gcn_layernorm_quantize(dev(X[lo + cov_src]), bits=bits,
+                                                   layernorm=False))
         col_ids.append(lo + cov_src)
         post_src.append(n_cols + src_slot[s_loc[is_post]])
         post_dst.append(d_rec[is_post])
@@ -173,11 +194,70 @@ def hybrid_receiver(G, bounds, rows, cols, deg, X, check_values=None):
     G.gcn_normalize_rc(gr, degd[:n0].contiguous(), dev(deg[col_ids]))
     if check_values is not None:
         check_values(gr, np.arange(n0), col_ids)
-    Y = G.gcn_aggregate_fwd(gr, torch.cat(recv_X))
-    for P, idx in partials:
-        G.gcn_add_rows(P, idx, Y)
+    if bits is None:
+        Y = G.gcn_aggregate_fwd(gr, torch.cat(recv_X))
+        for P, idx in partials:
+            G.gcn_add_rows(P, idx, Y)
+    else:
+        Qh = torch.cat([q[0] for q in recv_q])
+        Zh = torch.cat([q[1] for q in recv_q]).contiguous()
+        Sh = torch.cat([q[2] for q in recv_q]).contiguous()
+        Y = G.gcn_aggregate_fwd_q8halo(gr, n0, recv_X[0], Qh, Zh, Sh, F=F, bits=bits)
+        for (Q, Z, S), idx in partials:
+            G.gcn_add_rows_q(Q, Z, S, idx, Y, bits=bits, F=F)
+        sent.update(Qh=host(Qh), Zh=host(Zh), Sh=host(Sh), src_all=src_all, dst_all=dst_all,
+                    col_ids=col_ids, n_cols=n_cols)
     torch.cuda.synchronize()
-    return Y, volumes
+    return Y, volumes, sent
+
+
+def quantized_receiver_reference(n0, X, deg, bits, sent, sel=None):
+    """The oracle's output for the receiver rows sel (default: all) of a
+    quantized hybrid exchange: its own operator over [own rows | received
+    source rows dequantized], plus the dequantized partial sums. The codes
+    are checked first: the source rows' against the oracle's quantizer on
+    the same inputs, the partial sums' against the oracle's quantizer on the
+    GPU's fp32 partial sums (themselves checked against the oracle's
+    pre-aggregation within 1e-5 * S), both bit for bit. Returns (Y, S, B):
+    B[r] bounds the quantization error of row r against the exchange in fp32
+    (half a code step of every dequantized term it receives, times its
+    weight, plus 4 units of fp32 rounding of the row's largest value)."""
+    from gpu_util import assert_close
+    F = X.shape[1]
+    col_ids = sent["col_ids"]
+    Qr, Zr, Sr = oracle.quantize_rows_bits(X[col_ids[n0:]], bits)
+    assert np.array_equal(sent["Qh"], Qr), "source-row codes"
+    assert np.array_equal(sent["Zh"].view(np.uint32), Zr.view(np.uint32))
+    assert np.array_equal(sent["Sh"].view(np.uint32), Sr.view(np.uint32))
+    if sel is None:
+        sel = np.arange(n0, dtype=np.int32)
+    ptr, idx = oracle.rows_of(n0, sent["n_cols"], sent["src_all"], sent["dst_all"],
+                              synth.ADD_SELF_LOOPS, sel)
+    val = oracle.normalize_listed(ptr, deg[sel], deg[col_ids][idx])
+    Y, S = oracle.spmm_qbits(ptr, idx, val, n0, X[:n0], Qr, Zr, Sr, F, bits)
+    half = np.zeros((sent["n_cols"], 1), np.float32)
+    # the quantizer picks the nearest code in fp32 arithmetic: within half a
+    # step, plus a few units of fp32 rounding of the row's largest value
+    half[n0:, 0] = Sr / 2 + np.abs(oracle.dequant_rows_bits(Qr, Zr, Sr, F, bits)).max(axis=1) * 2.0 ** -21
+    B, _ = oracle.spmm(ptr, idx, val, half)
+    B = B[:, 0].copy()
+    pos = {int(r): i for i, r in enumerate(sel)}
+    for (lo, hi, s_pre, d_pre, cov_dst), P, (Q, Z, Sc) in zip(sent["pre"], sent["P"], sent["Pq"]):
+        gp_ptr, gp_idx = oracle.structure(len(cov_dst), hi - lo, s_pre, d_pre, 0)
+        gp_val = oracle.normalize_listed(gp_ptr, deg[cov_dst], deg[lo + gp_idx])
+        assert_close(P, *oracle.spmm(gp_ptr, gp_idx, gp_val, X[lo:hi]), what="partial sums")
+        Qo, Zo, So = oracle.quantize_rows_bits(P, bits)
+        assert np.array_equal(Q, Qo), "partial-sum codes"
+        assert np.array_equal(Z.view(np.uint32), Zo.view(np.uint32))
+        assert np.array_equal(Sc.view(np.uint32), So.view(np.uint32))
+        D = oracle.dequant_rows_bits(Qo, Zo, So, F, bits).astype(np.float64)
+        for j, r in enumerate(cov_dst):
+            i = pos.get(int(r))
+            if i is not None:
+                Y[i] += D[j]
+                S[i] += np.abs(D[j])
+                B[i] += So[j] / 2 + np.abs(D[j]).max() * 2.0 ** -21
+    return Y, S, B
 
 
 def value_checker(G, og, n):
@@ -209,8 +289,8 @@ def test_hybrid_equals_full_aggregation(G, n, m, bounds, F):
     rows, cols, deg = global_graph(11 + n, n, m)
     X = synth.normal(12 + n, n, F)
     og = oracle.Graph(n, n, cols.astype(np.int32), rows.astype(np.int32), synth.ADD_SELF_LOOPS)
-    Y, volumes = hybrid_receiver(G, bounds, rows, cols, deg, X,
-                                 check_values=value_checker(G, og, n))
+    Y, volumes, _ = hybrid_receiver(G, bounds, rows, cols, deg, X,
+                                    check_values=value_checker(G, og, n))
     ref, S = og.fwd(X)
     n0 = bounds[1]
     assert_close(host(Y), ref[:n0], S[:n0], what="hybrid receiver rows")
@@ -225,7 +305,7 @@ def test_hybrid_rmat20_two_workers(G):
     note("prepost rmat20 two workers F=64")
     rows, cols, deg = global_graph(21, n, 16 * n)
     X = synth.uniform(22, n, 64)
-    Y, volumes = hybrid_receiver(G, (0, n // 2, n), rows, cols, deg, X)
+    Y, volumes, _ = hybrid_receiver(G, (0, n // 2, n), rows, cols, deg, X)
     og = oracle.Graph(n, n, cols.astype(np.int32), rows.astype(np.int32), synth.ADD_SELF_LOOPS)
     ref, S = og.fwd(X)
     assert_close(host(Y), ref[: n // 2], S[: n // 2], what="rmat20 hybrid receiver rows")
@@ -250,6 +330,91 @@ def test_add_rows_exact(G):
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("bits", [8, 2])
+def test_add_rows_q_exact(G, bits):
+    # Y[idx] += fmaf(q, S, Z) in fp32: the oracle's dequantized value (one
+    # rounding) added in fp32, bit for bit; paired and separate (Z, S)
+    import torch
+    from gpu_util import dev, host, note
+    for F, ld, paired in ((64, 64, True), (47, 50, False), (5, 5, True), (256, 256, False)):
+        note("add_rows_q bits=%d F=%d" % (bits, F))
+        Y0 = synth.normal(33, 300, ld)
+        P = synth.normal(34, 40, F) * 3
+        P[7] = 1.25  # a constant row: S = 0, every code 0, dequantized value Z
+        Q, Z, S = oracle.quantize_rows_bits(P, bits)
+        idx = np.random.default_rng(F + bits).choice(300, 40, replace=False).astype(np.int32)
+        Yd = dev(Y0)
+        if paired:
+            zs = dev(np.stack([Z, S], axis=1))
+            z, sc = zs[:, 0], zs[:, 1]
+        else:
+            z, sc = dev(Z), dev(S)
+        G.gcn_add_rows_q(dev(Q), z, sc, dev(idx), Yd[:, :F], bits=bits, F=F)
+        torch.cuda.synchronize()
+        want = Y0.copy()
+        want[idx, :F] = (want[idx, :F] + oracle.dequant_rows_bits(Q, Z, S, F, bits)).astype(np.float32)
+        assert np.array_equal(host(Yd).view(np.uint32), want.view(np.uint32))
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("bits", [8, 2])
+@pytest.mark.parametrize("n,m,bounds,F", [
+    (3000, 12000, (0, 1500, 3000), 32),
+    (5000, 30000, (0, 1000, 2500, 5000), 47),
+])
+def test_hybrid_quantized_exchange(G, bits, n, m, bounds, F):
+    # Sections 5.2 and 6.1 together on one GPU: the senders quantize the
+    # covered source rows and their partial sums; the receiver dequantizes
+    # the source rows inside the aggregation and the partial sums in the
+    # combine. Every receiver row against the oracle on the same codes
+    # (1e-5 * S), and against the full fp32 aggregation within the
+    # quantization error of what it received.
+    from gpu_util import assert_close, host, note
+    note("prepost quantized bits=%d n=%d bounds=%s F=%d" % (bits, n, bounds, F))
+    rows, cols, deg = global_graph(11 + n, n, m)
+    X = synth.normal(12 + n, n, F)
+    Y, volumes, sent = hybrid_receiver(G, bounds, rows, cols, deg, X, bits=bits)
+    n0 = bounds[1]
+    ref, S, B = quantized_receiver_reference(n0, X, deg, bits, sent)
+    Yh = host(Y)
+    assert_close(Yh, ref, S, what="quantized hybrid receiver vs oracle")
+    og = oracle.Graph(n, n, cols.astype(np.int32), rows.astype(np.int32), synth.ADD_SELF_LOOPS)
+    full, Sf = og.fwd(X)
+    err = np.abs(Yh - full[:n0])
+    assert np.all(err <= B[:, None] + 1e-5 * Sf[:n0] + 1e-30), "beyond the quantization error"
+    note("largest deviation from fp32 exchange: %.3e of its bound"
+         % float((err / (B[:, None] + 1e-5 * Sf[:n0] + 1e-30)).max()))
+
+
+@pytest.mark.gpu
+def test_hybrid_partition_quantized_sampled(G):
+    """The 14M x 20M partition, 7 senders, 8-bit exchange: stratified rows of
+    the receiver (every length class, the longest rows, rows with and
+    without received columns) against the oracle on the same codes."""
+    import gc
+    import torch
+    from gpu_util import assert_close, host, note
+    note("prepost partition 14M x 20M, 7 senders, 8-bit exchange, sampled")
+    w = synth.partition_111m()
+    nl, nh = w.n_rows, w.n_cols - w.n_rows
+    bounds = [0, nl] + [nl - (-(o * nh) // 7) for o in range(1, 8)]
+    X = synth.normal(3014, w.n_cols, w.F)
+    Y, volumes, sent = hybrid_receiver(G, bounds, w.dst, w.src, w.deg, X, bits=8)
+    from test_gpu_configs import stratified_rows
+    ptr_r, idx_r = oracle.rows_of(nl, sent["n_cols"], sent["src_all"], sent["dst_all"],
+                                  synth.ADD_SELF_LOOPS, np.arange(nl, dtype=np.int32))
+    sel, strata, _ = stratified_rows(ptr_r, idx_r, halo_from=nl, per_class=100, per_octave=100)
+    del ptr_r, idx_r
+    ref, S, _ = quantized_receiver_reference(nl, X, w.deg, 8, sent, sel=sel)
+    got = host(Y[torch.from_numpy(sel.astype(np.int64)).to(Y.device)])
+    note("sampled %d receiver rows: %s" % (len(sel), ", ".join("%s %d" % (k, len(v)) for k, v in strata)))
+    assert_close(got, ref, S, what="partition quantized hybrid sampled rows")
+    del Y
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.gpu
 def test_hybrid_partition_sampled(G):
     """The 14M x 20M partition with its halo nodes owned by 7 senders
     (contiguous id ranges): sampled receiver rows against the oracle."""
@@ -262,7 +427,7 @@ def test_hybrid_partition_sampled(G):
     bounds = [0, nl] + [nl - (-(o * nh) // 7) for o in range(1, 8)]
     assert bounds[-1] == w.n_cols
     X = synth.normal(3014, w.n_cols, w.F)
-    Y, volumes = hybrid_receiver(G, bounds, w.dst, w.src, w.deg, X)
+    Y, volumes, _ = hybrid_receiver(G, bounds, w.dst, w.src, w.deg, X)
     assert sum(v[3] for v in volumes) < sum(v[2] for v in volumes)
     rng = np.random.default_rng(7)
     cnt = np.bincount(w.dst, minlength=nl)

@@ -6,6 +6,7 @@ import subprocess
 import sys
 
 import numpy as np
+import pytest
 
 import synth
 
@@ -18,8 +19,10 @@ def _digest_in_subprocess(threads):
         "s, d = synth.rmat_edges(7, 3000, 50000, perm_seed=8)\n"
         "x = synth.normal(9, 300, 33)\n"
         "p, q, r = synth.partition_edges(10, 11, 5000, 3500, 20000)\n"
+        "f, _ = synth.first_draws(s, d, 3000)\n"
+        "t, u, v = synth.partition_edges(10, 11, 5000, 3500, 20000, target=12345)\n"
         "h = hashlib.sha256()\n"
-        "[h.update(a.tobytes()) for a in (s, d, x, p, q, r)]\n"
+        "[h.update(a.tobytes()) for a in (s, d, x, p, q, r, f, t, u, v)]\n"
         "print(h.hexdigest())\n")
     env = dict(os.environ, OMP_NUM_THREADS=str(threads), PYTHONPATH=ROOT)
     return subprocess.check_output([sys.executable, "-c", code], env=env, cwd=ROOT).strip()
@@ -69,3 +72,33 @@ def test_partition_shape():
     assert np.all(src != dst)
     assert raw.sum() <= 2 * 100000
     assert np.mean(src >= 14000) > 0.2  # halo columns are referenced
+
+
+def test_first_draws_brute_force():
+    rng = np.random.default_rng(5)
+    a = rng.integers(0, 40, 3000).astype(np.int32)
+    b = rng.integers(0, 40, 3000).astype(np.int32)
+    first, distinct = synth.first_draws(a, b, 40)
+    seen, want = set(), []
+    for x, y in zip(a.tolist(), b.tolist()):
+        k = (min(x, y), max(x, y))
+        want.append(x != y and k not in seen)
+        if x != y:
+            seen.add(k)
+    assert first.tolist() == want and distinct == len(seen)
+    assert synth.nth_set(first, distinct) == max(i for i, w in enumerate(want) if w)
+    assert synth.nth_set(first, distinct + 1) == -1
+
+
+@pytest.mark.parametrize("target", [20000, 20001, 30123])
+def test_partition_exact_entry_count(target):
+    # distinct (row, col) entries of the emitted list reach exactly the target
+    src, dst, raw = synth.partition_edges(14, 15, 20000, 14000, 100000, target=target)
+    keys = np.unique(dst.astype(np.int64) * 20000 + src)
+    assert len(keys) == target
+    assert np.all(src != dst) and dst.max() < 14000
+    # a taken draw adds 2 to the counts and emits at most 2 entries
+    assert raw.sum() >= len(src)
+    full, _, _ = synth.partition_edges(14, 15, 20000, 14000, 100000)
+    # the taken draws are a prefix of the draws, save those left out
+    assert len(src) <= len(full)
