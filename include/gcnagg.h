@@ -145,6 +145,22 @@ gcn_status gcn_aggregate_fwd(const gcn_graph* g, const void* X, int64_t ldx, int
 gcn_status gcn_aggregate_bwd(const gcn_graph* g, const void* G, int64_t ldg, int dtype, float* dX,
                              int64_t lddx, int64_t F, void* stream);
 
+/* gcn_aggregate_fwd for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): same arguments, same kernels and identical results, but the
+ * partial rows of long rows live in a fixed array of the library, 2^24 floats
+ * (64 MiB) per device, held by every device the library runs on until the
+ * process ends. The call allocates nothing and frees nothing.
+ *  Returns GCN_ERANGE, before any work is enqueued, when the graph's plan
+ *  needs more: (rows cut into chunks or column-blocked pieces, counted as
+ *  partial rows) * round_up(F, 4) floats > 2^24.
+ * Every call on one device shares that array and leaves its contents behind
+ * (each call writes every partial row it reads, so nothing needs clearing):
+ * calls that may overlap on one device -- on different streams, or from
+ * different threads -- race and must be serialized by the caller. */
+gcn_status gcn_aggregate_fwd_noalloc(const gcn_graph* g, const void* X, int64_t ldx, int dtype,
+                                     float* Y, int64_t ldy, int64_t F, void* stream);
+
 /* Forward aggregation whose input rows >= n_local_cols are halo rows held as
  * uint8 codes (Section 6.1 step 3; quantization of Section 2.4 with b = 8):
  *   x[j, f] = X_local[j, f]                                   j <  n_local_cols

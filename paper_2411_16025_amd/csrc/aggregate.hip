@@ -31,6 +31,7 @@
 //    L2 and the Infinity Cache keep the gathered rows.
 
 #include <algorithm>
+#include <mutex>
 
 #include "common.h"
 
@@ -643,9 +644,11 @@ inline unsigned blocks_for_waves(int64_t waves) {
   return (unsigned)std::max<int64_t>(1, ceil_div(waves, kWavesPerBlock));
 }
 
+// ws: caller-provided room for the partial rows (at least parts_floats(m, F)
+// floats), or NULL to allocate them stream-ordered for the call.
 template <int VEC, int G, bool RELU, class Src>
 gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F,
-                      hipStream_t stream) {
+                      hipStream_t stream, float* ws) {
   constexpr int E = 64 / G;
   const Plan& p = m.plan;
   const unsigned tiles = (unsigned)ceil_div(F, G * VEC);
@@ -700,9 +703,13 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
   }
   // long rows: chunk table, then column-blocked pieces, then the partial sums
   if (p.n_chunks > 0 || p.n_pieces > 0) {
-    float* parts = nullptr;
+    float* parts = ws;
     const int64_t ldp = (F + 3) & ~3;
-    if (p.n_parts > 0) GCN_CHECK(talloc(&parts, p.n_parts * ldp, stream, "partial rows"));
+    if (p.n_parts > 0 && !ws) GCN_CHECK(talloc(&parts, p.n_parts * ldp, stream, "partial rows"));
+    // a workspace the caller owns is never released here
+    auto release = [&]() {
+      if (!ws) tfree(parts, stream);
+    };
     if (p.n_chunks > 0) {
       ProfScope ps("agg_chunk", stream);
       hipLaunchKernelGGL((k_chunk<VEC, G, Src, RELU>), dim3((unsigned)p.n_chunks, tiles),
@@ -711,7 +718,7 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
                          (const int32_t*)p.chunk_part, src, y, ldy, parts, ldp, F);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) {
-        tfree(parts, stream);
+        release();
         return hip_fail(e, "k_chunk", __FILE__, __LINE__);
       }
     }
@@ -724,7 +731,7 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
                          (const Ent*)m.ent, src, parts, ldp, F);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) {
-        tfree(parts, stream);
+        release();
         return hip_fail(e, "k_pieces", __FILE__, __LINE__);
       }
     }
@@ -736,14 +743,17 @@ gcn_status launch_all(const Mat& m, const Src& src, float* y, int64_t ldy, int F
                          ldy, F);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) {
-        tfree(parts, stream);
+        release();
         return hip_fail(e, "k_reduce_parts", __FILE__, __LINE__);
       }
     }
-    tfree(parts, stream);
+    release();
   }
   return GCN_OK;
 }
+
+// Floats of partial rows one aggregation with the plan of m needs at width F.
+int64_t parts_floats(const Mat& m, int64_t F) { return m.plan.n_parts * ((F + 3) & ~int64_t(3)); }
 
 // Lanes per slot: smallest power of two covering min(F, 128) features with
 // 4-float lanes (at least 4 lanes); wider rows run as 128-feature tiles
@@ -760,12 +770,12 @@ int lanes_for(int F, bool vec4) {
 
 template <class Src, bool RELU>
 gcn_status launch_vec4(const Mat& m, const Src& src, float* y, int64_t ldy, int F,
-                       hipStream_t stream) {
+                       hipStream_t stream, float* ws) {
   switch (lanes_for(F, true)) {
-    case 4: return launch_all<4, 4, RELU>(m, src, y, ldy, F, stream);
-    case 8: return launch_all<4, 8, RELU>(m, src, y, ldy, F, stream);
-    case 16: return launch_all<4, 16, RELU>(m, src, y, ldy, F, stream);
-    default: return launch_all<4, 32, RELU>(m, src, y, ldy, F, stream);
+    case 4: return launch_all<4, 4, RELU>(m, src, y, ldy, F, stream, ws);
+    case 8: return launch_all<4, 8, RELU>(m, src, y, ldy, F, stream, ws);
+    case 16: return launch_all<4, 16, RELU>(m, src, y, ldy, F, stream, ws);
+    default: return launch_all<4, 32, RELU>(m, src, y, ldy, F, stream, ws);
   }
 }
 
@@ -774,13 +784,13 @@ gcn_status launch_vec4(const Mat& m, const Src& src, float* y, int64_t ldy, int 
 // the extra features are never stored.
 template <template <int, bool> class SrcT, bool RELU = false, class Make>
 gcn_status dispatch(const Mat& m, bool vec4, int F, float* y, int64_t ldy, hipStream_t stream,
-                    Make make, bool pad_ok = false) {
-  if (!vec4) return launch_all<1, 64, RELU>(m, make(SrcT<1, false>{}), y, ldy, F, stream);
+                    Make make, bool pad_ok = false, float* ws = nullptr) {
+  if (!vec4) return launch_all<1, 64, RELU>(m, make(SrcT<1, false>{}), y, ldy, F, stream, ws);
   if (F % 4 != 0 && !pad_ok)
-    return launch_vec4<SrcT<4, true>, RELU>(m, make(SrcT<4, true>{}), y, ldy, F, stream);
+    return launch_vec4<SrcT<4, true>, RELU>(m, make(SrcT<4, true>{}), y, ldy, F, stream, ws);
   auto src = make(SrcT<4, false>{});
   src.F = (F + 3) & ~3;  // the width the loads may cover; F bounds the stores
-  return launch_vec4<SrcT<4, false>, RELU>(m, src, y, ldy, F, stream);
+  return launch_vec4<SrcT<4, false>, RELU>(m, src, y, ldy, F, stream, ws);
 }
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
@@ -794,8 +804,9 @@ gcn_status check_common(const gcn_graph* g, int64_t F) {
   return GCN_OK;
 }
 
-gcn_status aggregate(const gcn_graph* g, const Mat& m, const void* X, int64_t ldx, int dtype,
-                     float* Y, int64_t ldy, int64_t F, void* stream) {
+// Argument checks of the plain aggregation calls (before any work is enqueued).
+gcn_status check_plain(const void* X, int64_t ldx, int dtype, const float* Y, int64_t ldy,
+                       int64_t F) {
   if (!X || !Y) {
     set_error("input and output pointers must be non-NULL");
     return GCN_EINVAL;
@@ -813,6 +824,12 @@ gcn_status aggregate(const gcn_graph* g, const Mat& m, const void* X, int64_t ld
     set_error("unknown dtype %d", dtype);
     return GCN_EINVAL;
   }
+  return GCN_OK;
+}
+
+gcn_status aggregate(const Mat& m, const void* X, int64_t ldx, int dtype, float* Y, int64_t ldy,
+                     int64_t F, void* stream, float* ws = nullptr) {
+  GCN_CHECK(check_plain(X, ldx, dtype, Y, ldy, F));
   const int Fi = (int)F;
   hipStream_t s = (hipStream_t)stream;
   const bool yvec = aligned(Y, 16) && ldy % 4 == 0;
@@ -823,7 +840,7 @@ gcn_status aggregate(const gcn_graph* g, const Mat& m, const void* X, int64_t ld
       t.ld = (uint32_t)ldx;
       t.F = Fi;
       return t;
-    });
+    }, false, ws);
   }
   const bool vec4 = yvec && aligned(X, 8) && ldx % 4 == 0;
   return dispatch<SrcBF16>(m, vec4, Fi, Y, ldy, s, [&](auto t) {
@@ -831,7 +848,7 @@ gcn_status aggregate(const gcn_graph* g, const Mat& m, const void* X, int64_t ld
     t.ld = (uint32_t)ldx;
     t.F = Fi;
     return t;
-  });
+  }, false, ws);
 }
 
 }  // namespace
@@ -860,14 +877,14 @@ extern "C" gcn_status gcn_aggregate_fwd(const gcn_graph* g, const void* X, int64
                                         float* Y, int64_t ldy, int64_t F, void* stream) {
   clear_error();
   GCN_CHECK(check_common(g, F));
-  return aggregate(g, g->csr, X, ldx, dtype, Y, ldy, F, stream);
+  return aggregate(g->csr, X, ldx, dtype, Y, ldy, F, stream);
 }
 
 extern "C" gcn_status gcn_aggregate_bwd(const gcn_graph* g, const void* G, int64_t ldg, int dtype,
                                         float* dX, int64_t lddx, int64_t F, void* stream) {
   clear_error();
   GCN_CHECK(check_common(g, F));
-  return aggregate(g, g->csc, G, ldg, dtype, dX, lddx, F, stream);
+  return aggregate(g->csc, G, ldg, dtype, dX, lddx, F, stream);
 }
 
 extern "C" gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_local_cols,
@@ -925,4 +942,62 @@ extern "C" gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_loc
   };
   if (two_bit) return dispatch<SrcQ2>(m, vec4, Fi, Y, ldy, (hipStream_t)stream, make);
   return dispatch<SrcQ8>(m, vec4, Fi, Y, ldy, (hipStream_t)stream, make);
+}
+
+// ---- the aggregation without allocation -------------------------------------
+
+namespace gcn {
+namespace {
+
+// Room for the partial rows of gcn_aggregate_fwd_noalloc: 64 MiB per device,
+// held by every device the library runs on until the process ends. In host
+// code the name stands for no device address; the address comes from
+// hipGetSymbolAddress, once per device.
+constexpr int64_t kScratchFloats = int64_t(1) << 24;
+__device__ __align__(256) float scratch[kScratchFloats];
+
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[64] = {};
+
+// Device address of this device's scratch array (looked up on the first call
+// on the device, with the device current).
+gcn_status scratch_for_current_device(float** out) {
+  int dev = 0;
+  GCN_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) {
+    set_error("device %d out of range for the scratch table", dev);
+    return GCN_EINVAL;
+  }
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol,
+                      "hipGetSymbolAddress(scratch)", __FILE__, __LINE__);
+    g_scratch_ptr[dev] = static_cast<float*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return GCN_OK;
+}
+
+}  // namespace
+}  // namespace gcn
+
+extern "C" gcn_status gcn_aggregate_fwd_noalloc(const gcn_graph* g, const void* X, int64_t ldx,
+                                                int dtype, float* Y, int64_t ldy, int64_t F,
+                                                void* stream) {
+  clear_error();
+  GCN_CHECK(check_common(g, F));
+  GCN_CHECK(check_plain(X, ldx, dtype, Y, ldy, F));
+  const int64_t need = parts_floats(g->csr, F);
+  if (need > kScratchFloats) {
+    set_error("the graph's plan needs %lld floats of partial rows at F=%lld; the no-allocation "
+              "call holds %lld (use gcn_aggregate_fwd)", (long long)need, (long long)F,
+              (long long)kScratchFloats);
+    return GCN_ERANGE;
+  }
+  float* ws = nullptr;
+  GCN_CHECK(scratch_for_current_device(&ws));
+  return aggregate(g->csr, X, ldx, dtype, Y, ldy, F, stream, ws);
 }

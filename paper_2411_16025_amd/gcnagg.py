@@ -33,7 +33,7 @@ GCN_GEMM_NN, GCN_GEMM_NT, GCN_GEMM_TN = 0, 1, 2
 EXPORTS = ("gcn_build_csr", "gcn_normalize", "gcn_normalize_rc", "gcn_normalize_mean",
            "gcn_layernorm_fwd", "gcn_layernorm_bwd", "gcn_sage3_forward", "gcn_sage3_step",
            "gcn_prepost_split",
-           "gcn_add_rows", "gcn_add_rows_q", "gcn_aggregate_fwd", "gcn_aggregate_bwd",
+           "gcn_add_rows", "gcn_add_rows_q", "gcn_aggregate_fwd", "gcn_aggregate_bwd", "gcn_aggregate_fwd_noalloc",
            "gcn_aggregate_fwd_q8halo", "gcn_quantize_rows_u8", "gcn_layernorm_quantize",
            "gcn_gemm_f32", "gcn_relu",
            "gcn_relu_bwd", "gcn_softmax_xent", "gcn_gcn2_step", "gcn_graph_free",
@@ -68,6 +68,7 @@ def lib():
         L.gcn_add_rows_q.argtypes = [i64, i64, i32, P, i64, P, P, i64, P, i64, P, i64, P]
         L.gcn_aggregate_fwd.argtypes = [P, P, i64, i32, P, i64, i64, P]
         L.gcn_aggregate_bwd.argtypes = [P, P, i64, i32, P, i64, i64, P]
+        L.gcn_aggregate_fwd_noalloc.argtypes = [P, P, i64, i32, P, i64, i64, P]
         L.gcn_aggregate_fwd_q8halo.argtypes = [P, i64, P, i64, P, i64, P, P, i64, P, i64, i64, u32,
                                                P]
         L.gcn_quantize_rows_u8.argtypes = [i64, i64, P, i64, P, i64, P, P, i64, P]
@@ -268,6 +269,23 @@ def gcn_aggregate_fwd(g: Graph, X: torch.Tensor, Y: torch.Tensor | None = None, 
         raise ValueError("Y must be n_rows x F")
     _check(lib().gcn_aggregate_fwd(g.handle, X.data_ptr(), ldx, _dtype_code(X), Y.data_ptr(), ldy,
                                    F, _stream(stream)))
+    return Y
+
+
+def gcn_aggregate_fwd_noalloc(g: Graph, X: torch.Tensor, Y: torch.Tensor, stream=None):
+    """Y = A_hat X with the library's fixed partial-row array instead of an
+    allocation (Y must be given; see include/gcnagg.h for the size limit)."""
+    _dev(X, None, "X")
+    ldx = _rowmajor(X, "X")
+    if X.shape[0] != g.n_cols:
+        raise ValueError("X must have n_cols = %d rows" % g.n_cols)
+    F = X.shape[1]
+    _dev(Y, torch.float32, "Y")
+    ldy = _rowmajor(Y, "Y")
+    if tuple(Y.shape) != (g.n_rows, F):
+        raise ValueError("Y must be n_rows x F")
+    _check(lib().gcn_aggregate_fwd_noalloc(g.handle, X.data_ptr(), ldx, _dtype_code(X),
+                                           Y.data_ptr(), ldy, F, _stream(stream)))
     return Y
 
 
