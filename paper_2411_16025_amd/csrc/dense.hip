@@ -203,6 +203,10 @@ constexpr int64_t kDeepK = 384;
 #define GCN_GEMM_PRAGMA(x) _Pragma(#x)
 #define GCN_GEMM_UNROLL(n) GCN_GEMM_PRAGMA(unroll n)
 
+// LDS row stride for rows read along n: 16 mod 32 floats, so the operand
+// reads of a half-wavefront (16 columns x 2 rows) hit 32 distinct banks.
+constexpr int stride_n(int bn) { return bn + (48 - bn % 32) % 32; }
+
 template <int OP, int BN, int RB>
 __global__ __launch_bounds__(kThreads,
                              BN == 256 ? GCN_GEMM_MIN_BLOCKS : GCN_GEMM_MIN_BLOCKS_NARROW)
@@ -212,15 +216,16 @@ void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A,
   // RB 16-row blocks per wavefront: a BM x BN tile per workgroup
   constexpr int BM = kTile * RB;
   constexpr int NB = BN / 16;
-  constexpr int BL = BN / 32;  // 16-byte B loads per thread per slice
-  constexpr int AL = 2 * RB;   // 16-byte A loads per thread per slice
+  constexpr int BQ = 8 * BN;                          // 16-byte pieces of a B slice
+  constexpr int BL = (BQ + kThreads - 1) / kThreads;  // per thread (the last may be idle)
+  constexpr int AL = 2 * RB;                          // 16-byte A loads per thread per slice
   // LDS strides chosen so that the operand reads of a half-wavefront (16
   // rows or columns x 2 k values) hit 32 distinct banks: rows read along k
   // (A, and B of NT) have a stride of 2 mod 32 floats and are written with
   // 8-byte stores; rows read along n (B of NN) have a stride of 16 mod 32
   constexpr int AS = kKc + 2;
   constexpr int BR = OP == kNN ? kKc : BN;
-  constexpr int BC = OP == kNN ? BN + 16 : kKc + 2;
+  constexpr int BC = OP == kNN ? stride_n(BN) : kKc + 2;
   // the output tile is staged through the same LDS, CW columns at a time
   constexpr int CW = BN < 128 ? BN : 128;
   constexpr int kOperands = BM * AS + BR * BC;
@@ -246,6 +251,7 @@ void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A,
 #pragma unroll
     for (int j = 0; j < BL; ++j) {
       const int idx = t + kThreads * j;
+      if (BQ % kThreads != 0 && idx >= BQ) continue;
       if (OP == kNN) {  // B rows k0 .. k0 + 31, columns n0 .. n0 + BN - 1
         const int r = idx / (BN / 4), c = (idx % (BN / 4)) * 4;
         rb[j] = load4(B, k0 + r, K, ldb, n0 + c, N);
@@ -265,6 +271,7 @@ void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A,
 #pragma unroll
     for (int j = 0; j < BL; ++j) {
       const int idx = t + kThreads * j;
+      if (BQ % kThreads != 0 && idx >= BQ) continue;
       if (OP == kNN) {
         const int r = idx / (BN / 4), c = (idx % (BN / 4)) * 4;
         *reinterpret_cast<f4*>(&Bs[r][c]) = rb[j];
@@ -310,10 +317,24 @@ void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A,
     // matrix-core layout, then stores it row by row with 16-byte accesses (the
     // mask is read the same way)
     float (*st)[CW + 4] = reinterpret_cast<float (*)[CW + 4]>(smem);
-    constexpr int LPR = CW / 4;    // lanes per row
-    constexpr int RPI = 64 / LPR;  // rows per store instruction
+    constexpr int LPR = CW / 4;                     // lanes per row
+    constexpr int RPI = 64 / LPR;                   // rows per store instruction
+    constexpr int NIT = (16 * RB + RPI - 1) / RPI;  // store instructions per column block
 #pragma unroll
     for (int c0 = 0; c0 < BN; c0 += CW) {
+      // the mask values this lane applies, loaded before the staging so
+      // their latency overlaps it (one 16-byte load per store)
+      f4 mk[NIT];
+      if (mask) {
+#pragma unroll
+        for (int it = 0; it < NIT; ++it) {
+          mk[it] = f4{1.f, 1.f, 1.f, 1.f};
+          if (64 % LPR != 0 && (lane / LPR >= RPI || it * RPI + lane / LPR >= 16 * RB)) continue;
+          const int64_t gm = m0 + 16 * RB * w + it * RPI + lane / LPR;
+          const int64_t gn = n0 + c0 + 4 * (lane % LPR);
+          if (gm < M && gn + 4 <= N) mk[it] = *reinterpret_cast<const f4*>(mask + gm * ldm + gn);
+        }
+      }
       __syncthreads();  // the operands (or the previous columns) are no longer read
 #pragma unroll
       for (int r = 0; r < RB; ++r)
@@ -324,7 +345,9 @@ void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A,
             st[16 * (RB * w + r) + 4 * (lane >> 4) + i][16 * j - c0 + (lane & 15)] = acc[r][j][i];
       __syncthreads();
 #pragma unroll
-      for (int it = 0; it < 16 * RB / RPI; ++it) {
+      for (int it = 0; it < NIT; ++it) {
+        // with 48 columns (12 lanes a row) lanes 60 .. 63 have no row
+        if (64 % LPR != 0 && (lane / LPR >= RPI || it * RPI + lane / LPR >= 16 * RB)) continue;
         const int rl = 16 * RB * w + it * RPI + lane / LPR;
         const int cl = 4 * (lane % LPR);
         const int64_t gm = m0 + rl, gn = n0 + c0 + cl;
@@ -332,10 +355,9 @@ void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A,
         f4 v = *reinterpret_cast<const f4*>(&st[rl][cl]);
         if (gn + 4 <= N) {
           if (mask) {
-            const f4 mk = *reinterpret_cast<const f4*>(mask + gm * ldm + gn);
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-              if (!(mk[e] > 0.f)) v[e] = 0.f;
+              if (!(mk[it][e] > 0.f)) v[e] = 0.f;
           }
           if (relu) {
 #pragma unroll
@@ -384,8 +406,8 @@ __global__ __launch_bounds__(WAVES * 64) void k_gemm_tn_v(int64_t M, int64_t N, 
   constexpr int BM = 16 * WAVES, NT = 64 * WAVES, NB = BN / 16;
   // row strides of 16 mod 32 floats: a half-wavefront's reads (16 columns x
   // 2 rows) hit 32 distinct banks
-  __shared__ __align__(16) float As[kKc][BM + 16];
-  __shared__ __align__(16) float Bs[kKc][BN + 16];
+  __shared__ __align__(16) float As[kKc][stride_n(BM)];
+  __shared__ __align__(16) float Bs[kKc][stride_n(BN)];
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int64_t m0 = (int64_t)blockIdx.x * BM;
   const int64_t n0 = (int64_t)blockIdx.y * BN;
@@ -401,9 +423,11 @@ __global__ __launch_bounds__(WAVES * 64) void k_gemm_tn_v(int64_t M, int64_t N, 
       const int idx = t + NT * j, r = idx / (BM / 4), c = (idx % (BM / 4)) * 4;
       *reinterpret_cast<f4*>(&As[r][c]) = load4(A, k0 + r, ke, lda, m0 + c, M);
     }
+    constexpr int BQ = kKc * BN / 4;  // 16-byte pieces of a B slice
 #pragma unroll
-    for (int j = 0; j < kKc * BN / 4 / NT; ++j) {
+    for (int j = 0; j < (BQ + NT - 1) / NT; ++j) {
       const int idx = t + NT * j, r = idx / (BN / 4), c = (idx % (BN / 4)) * 4;
+      if (BQ % NT != 0 && idx >= BQ) continue;
       *reinterpret_cast<f4*>(&Bs[r][c]) = load4(B, k0 + r, ke, ldb, n0 + c, N);
     }
     __syncthreads();
@@ -579,8 +603,10 @@ bool aligned16(const void* p, int64_t ld) { return ((uintptr_t)p % 16) == 0 && l
 // Output tile widths. C = A B: 256 columns once N > 128 (A is read once per
 // tile column). C = A B^T and C = A^T B: at most 128 (more workgroups at 4
 // per CU, and less padding of odd widths, outweigh the extra reads of A).
-int tile_n(int64_t N) { return N <= 64 ? 64 : (N <= 128 ? 128 : 256); }
-int tile_n_narrow(int64_t N) { return N <= 64 ? 64 : 128; }
+// Outputs of at most 48 columns (the class count of the training steps, 47)
+// take a 48-column tile: 3 instead of 4 matrix-core blocks per 16 rows.
+int tile_n(int64_t N) { return N <= 48 ? 48 : (N <= 64 ? 64 : (N <= 128 ? 128 : 256)); }
+int tile_n_narrow(int64_t N) { return N <= 48 ? 48 : (N <= 64 ? 64 : 128); }
 
 template <int OP>
 void launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
@@ -590,7 +616,10 @@ void launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, c
   // staged 16-byte stores need 16-byte aligned rows of C (and of the mask)
   const bool cvec = aligned16(C, ldc) && (!mask || aligned16(mask, ldm));
   const dim3 grid((unsigned)ceil_div(M, kTile), (unsigned)ceil_div(N, bn));
-  if (bn == 64)
+  if (bn == 48)
+    hipLaunchKernelGGL((k_gemm_tall_v<OP, 48, 1>), grid, dim3(kThreads), 0, stream, M, N, K, A,
+                       lda, B, ldb, C, ldc, mask, ldm, relu, cvec);
+  else if (bn == 64)
     hipLaunchKernelGGL((k_gemm_tall_v<OP, 64, 1>), grid, dim3(kThreads), 0, stream, M, N, K, A,
                        lda, B, ldb, C, ldc, mask, ldm, relu, cvec);
   else if (OP != kNN || bn == 128)
@@ -613,7 +642,10 @@ void launch_tn(int64_t M, int64_t N, int64_t K, int64_t split, int64_t n_chunks,
   constexpr int kWaves = 8, kBm = 16 * kWaves;
   const int bn = tile_n_narrow(N);
   const dim3 grid((unsigned)ceil_div(M, kBm), (unsigned)ceil_div(N, bn), (unsigned)n_chunks);
-  if (bn == 64)
+  if (bn == 48)
+    hipLaunchKernelGGL((k_gemm_tn_v<kWaves, 48>), grid, dim3(64 * kWaves), 0, stream, M, N, K,
+                       split, A, lda, B, ldb, part);
+  else if (bn == 64)
     hipLaunchKernelGGL((k_gemm_tn_v<kWaves, 64>), grid, dim3(64 * kWaves), 0, stream, M, N, K,
                        split, A, lda, B, ldb, part);
   else
