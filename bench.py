@@ -67,7 +67,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="rmat24_q8",
                     choices=["rmat24_q8", "rmat24", "rmat20", "er4096", "product", "partition",
-                             "perm22", "gcn_step", "sage_step", "prepost", "producer"])
+                             "perm22", "gcn_step", "sage_step", "prepost", "producer", "gemm"])
     ap.add_argument("--halo-bits", type=int, default=8, choices=[8, 2],
                     help="code width of the halo rows (8: one byte per feature; 2: four per byte)")
     ap.add_argument("--senders", type=int, default=7,
@@ -431,6 +431,90 @@ def run_producer(args):
     print(json.dumps(out), flush=True)
 
 
+def run_gemm(args):
+    """Each fp32 product of the training steps alone, at the product-shaped
+    graph's 2,449,029 rows, in the layouts the steps use (rows padded to a
+    multiple of 4 floats), timed with HIP events on the stream the library
+    launches on. Per product: the algorithmic bytes (each operand and the
+    result once) and flops, the roofline time max(flops / 157.3 TFLOP/s,
+    bytes / 8 TB/s), and its fraction of the measured time."""
+    import torch
+    import synth
+    import paper_2411_16025_amd as G
+
+    dev = torch.device("cuda:0")
+    n, f_in, hid, C = 2_449_029, 100, 256, 47
+    K3 = 2 * hid + 4  # GraphSAGE: [Y | Z | 1 0 0 0] of a hidden layer
+    rnd = lambda seed, r, c: torch.from_numpy(synth.uniform(seed, r, c)).to(dev)  # noqa: E731
+    X = rnd(3100, n, f_in)
+    H1 = rnd(3101, n, hid)
+    W1 = rnd(3102, f_in, hid)
+    W2p = rnd(3103, hid, 48)
+    dZ2p = rnd(3104, n, 48)
+    dZ1 = rnd(3105, n, hid)
+    Cs = rnd(3106, n, K3)
+    Ws = rnd(3107, K3, hid)
+    W3p = rnd(3108, K3, 48)
+    out_nh = torch.empty((n, hid), device=dev)
+    out_nc = torch.empty((n, 48), device=dev)
+    NN, NT, TN = G.GCN_GEMM_NN, G.GCN_GEMM_NT, G.GCN_GEMM_TN
+    cases = [
+        ("gcn Z1 = X W1", NN, X, W1, out_nh, (n, hid, f_in)),
+        ("gcn Z2 = H1 W2", NN, H1, W2p[:, :C], out_nc[:, :C], (n, C, hid)),
+        ("gcn dH1 = dZ2 W2^T", NT, dZ2p[:, :C], W2p[:, :C], out_nh, (n, hid, C)),
+        ("gcn dW2 = H1^T dZ2", TN, H1, dZ2p[:, :C], None, (hid, C, n)),
+        ("gcn dW1 = X^T dZ1", TN, X, dZ1, None, (f_in, hid, n)),
+        ("sage O2 = C2 W (K=516)", NN, Cs, Ws, out_nh, (n, hid, K3)),
+        ("sage O3 = C3 W3 (K=516)", NN, Cs, W3p[:, :C], out_nc[:, :C], (n, C, K3)),
+        ("sage dW2 = C2^T dO2", TN, Cs, dZ1, None, (K3, hid, n)),
+    ]
+    res = {}
+    tot_roof = tot_ms = 0.0
+    for name, op, A, B, Cout, (M, N, K) in cases:
+        fn = lambda: G.gcn_gemm_f32(op, A, B, C=Cout)  # noqa: E731
+        for _ in range(max(args.warmup, 1)):
+            fn()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(args.steps):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            ev[0].record()
+            fn()
+            ev[1].record()
+            ev[1].synchronize()
+            times.append(ev[0].elapsed_time(ev[1]))
+        ms = float(np.median(times))
+        flops = 2.0 * M * N * K
+        nbytes = 4.0 * (M * K + K * N + M * N)
+        t_roof = max(flops / (FP32_MFMA_PEAK_TFLOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9)) * 1e3
+        res[name] = {"M": M, "N": N, "K": K, "ms": round(ms, 4),
+                     "TFLOPs": round(flops / (ms * 1e-3) / 1e12, 1),
+                     "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                     "bound": "mfma" if flops / (FP32_MFMA_PEAK_TFLOPS * 1e12) >= nbytes / (HBM_PEAK_GBS * 1e9) else "hbm",
+                     "roofline_ms": round(t_roof, 4), "frac": round(t_roof / ms, 4)}
+        tot_roof += t_roof
+        tot_ms += ms
+        log("%-26s %8.3f ms  roofline %.3f ms  %.0f%%" % (name, ms, t_roof, 100 * t_roof / ms))
+    dom = max(res, key=lambda k: res[k]["ms"])
+    d = res[dom]
+    out = {
+        "metric": "fp32 GEMMs of the training steps: roofline time / measured time",
+        "value": round(tot_roof / tot_ms, 4), "unit": "fraction", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(tot_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "training-step products at 2,449,029 rows (F_in 100, hidden 256, "
+                               "47 classes)"},
+        "products": res,
+        "roofline": {"bound": d["bound"], "kernel": dom,
+                     "achieved": d["TFLOPs"] if d["bound"] == "mfma" else d["GBps"],
+                     "peak": FP32_MFMA_PEAK_TFLOPS if d["bound"] == "mfma" else HBM_PEAK_GBS,
+                     "unit": "TFLOP/s" if d["bound"] == "mfma" else "GB/s", "frac": d["frac"],
+                     "traffic": None},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -449,6 +533,9 @@ def main():
         return
     if args.workload == "producer":
         run_producer(args)
+        return
+    if args.workload == "gemm":
+        run_gemm(args)
         return
 
     import torch

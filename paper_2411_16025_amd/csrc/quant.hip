@@ -5,6 +5,8 @@
 // stochastic rounding), optionally after a row LayerNorm (Section 6.1 step 2);
 // and the LayerNorm forward and backward of the GraphSAGE model (Table 2).
 
+#include <algorithm>
+
 #include "common.h"
 
 namespace gcn {
@@ -169,6 +171,20 @@ __device__ inline uint32_t code_of(float a, float s, float levels) {
   return (uint32_t)fminf(levels, fmaxf(0.0f, __builtin_rintf(a / s)));
 }
 
+// The same code from the row's correctly rounded reciprocal rs = RN(1 / S):
+// q = RN(a rs) is within one ulp of a / S, the residual a - q S is exact in
+// an fma, and RN(q + (a - q S) rs) is the correctly rounded quotient RN(a / S)
+// (Markstein's theorem for round-to-nearest division), so the code equals
+// code_of's. Valid while the residual cannot underflow where it matters:
+// S in [2^-100, 2^100] (quotients below 1/4 round to code 0 either way).
+__device__ inline uint32_t code_of_rcp(float a, float s, float rs, float levels) {
+  const float q = a * rs;
+  const float e = __builtin_fmaf(-q, s, a);
+  return (uint32_t)fminf(levels, fmaxf(0.0f, __builtin_rintf(__builtin_fmaf(e, rs, q))));
+}
+
+__device__ inline bool rcp_ok(float s) { return s >= 0x1p-100f && s <= 0x1p100f; }
+
 struct QuantArgs {
   int64_t n;
   int F;
@@ -189,138 +205,209 @@ struct QuantArgs {
   float* rstd;          // optional 1 / sqrt(var + eps) per row (bits == 0 only)
 };
 
-template <int G, int NV, int R, bool AFFINE>
+// LN: LayerNorm first; BITS: 8 or 2 (codes), 0 (LayerNorm output only);
+// FULL: every lane's features lie inside the row (F = 4 G NV) and the stores
+// are aligned (Q rows 4-byte aligned for 8-bit codes, Y rows 16-byte), so no
+// feature is guarded. Each variant is its own kernel: the run-time choices
+// cost more issue slots than the memory traffic leaves room for.
+template <int G, int NV, int R, bool AFFINE, bool LN, int BITS, bool FULL>
 __global__ __launch_bounds__(kBlock) void k_ln_quantize_v(QuantArgs a) {
   constexpr int E = 64 / G;
   const int lane = threadIdx.x & 63;
   const int sl = lane % G;
-  const int64_t base = ((int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6)) * (E * R) + lane / G;
-  float v[R][NV][4];
-  // every load of every group first
+  // the wavefront walks its row groups (E * R rows each) with a stride of
+  // the grid's wavefronts, loading the next group while it works on this one
+  const int64_t n_iter = (a.n + E * R - 1) / (E * R);
+  const int64_t stride = (int64_t)gridDim.x * (kBlock / 64);
+  int64_t it = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  const int F = FULL ? 4 * G * NV : a.F;
+  auto inside = [&](int f) { return FULL || f < F; };
+  auto load = [&](int64_t iter, float (&v)[R][NV][4]) {
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int64_t i = base + (int64_t)r * E;
-#pragma unroll
-    for (int j = 0; j < NV; ++j) {
-      const int f = 4 * (sl + j * G);
-      if (i < a.n && f + 4 <= a.F) {
-        const float4 t = *reinterpret_cast<const float4*>(a.x + i * a.ldx + f);
-        v[r][j][0] = t.x;
-        v[r][j][1] = t.y;
-        v[r][j][2] = t.z;
-        v[r][j][3] = t.w;
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          v[r][j][e] = (i < a.n && f + e < a.F) ? a.x[i * a.ldx + f + e] : 0.0f;
-      }
-    }
-  }
-  const float levels = (float)((1 << a.bits) - 1);
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int64_t i = base + (int64_t)r * E;
-    const bool live = i < a.n;
-    if (a.ln) {
-      double s = 0.0;
-#pragma unroll
-      for (int j = 0; j < NV; ++j)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) s += (double)v[r][j][e];  // masked entries are 0
-      const double mean = slot_sum<G>(s) / (double)a.F;
-      double var = 0.0;
-#pragma unroll
-      for (int j = 0; j < NV; ++j)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const double d = (double)v[r][j][e] - mean;
-          if (4 * (sl + j * G) + e < a.F) var += d * d;
-        }
-      const double inv = 1.0 / sqrt(slot_sum<G>(var) / (double)a.F + a.eps);
-      if (a.rstd && live && sl == 0) a.rstd[i] = (float)inv;
-#pragma unroll
-      for (int j = 0; j < NV; ++j)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int f = 4 * (sl + j * G) + e;
-          if (f < a.F) {
-            const double d = ((double)v[r][j][e] - mean) * inv;
-            if (AFFINE) {
-              const double g = a.gamma ? (double)a.gamma[f] : 1.0;
-              const double b = a.beta ? (double)a.beta[f] : 0.0;
-              v[r][j][e] = (float)(d * g + b);
-            } else {
-              v[r][j][e] = (float)(d + 0.0);  // times 1 is exact; + 0 turns -0 into +0
-            }
-          }
-        }
-    }
-    if (a.bits == 0) {  // LayerNorm only
-      if (!live) continue;
-      float* yr = a.y + i * a.ldy;
+    for (int r = 0; r < R; ++r) {
+      const int64_t i = iter * (E * R) + (int64_t)r * E + lane / G;
 #pragma unroll
       for (int j = 0; j < NV; ++j) {
         const int f = 4 * (sl + j * G);
-        if (f >= a.F) continue;
-        if (f + 4 <= a.F && a.y_vec)
-          *reinterpret_cast<float4*>(yr + f) = make_float4(v[r][j][0], v[r][j][1], v[r][j][2], v[r][j][3]);
-        else
-          for (int e = 0; e < 4 && f + e < a.F; ++e) yr[f + e] = v[r][j][e];
-      }
-      continue;
-    }
-    float mn = __builtin_inff(), mx = -__builtin_inff();
+        if (i < a.n && (FULL || f + 4 <= F)) {
+          const float4 t = *reinterpret_cast<const float4*>(a.x + i * a.ldx + f);
+          v[r][j][0] = t.x;
+          v[r][j][1] = t.y;
+          v[r][j][2] = t.z;
+          v[r][j][3] = t.w;
+        } else {
 #pragma unroll
-    for (int j = 0; j < NV; ++j)
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (4 * (sl + j * G) + e < a.F) {
-          mn = fminf(mn, v[r][j][e]);
-          mx = fmaxf(mx, v[r][j][e]);
+          for (int e = 0; e < 4; ++e)
+            v[r][j][e] = (i < a.n && f + e < F) ? a.x[i * a.ldx + f + e] : 0.0f;
         }
-    slot_minmax<G>(mn, mx);
-    if (!live) continue;
-    const float s = (mx - mn) / levels;
-    if (sl == 0) {
-      a.zmin[i * a.ldp] = mn;
-      a.scale[i * a.ldp] = s;
-    }
-#pragma unroll
-    for (int j = 0; j < NV; ++j) {
-      const int f = 4 * (sl + j * G);
-      if (f >= a.F) continue;
-      uint32_t c[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        c[e] = (f + e < a.F && s != 0.0f) ? code_of(v[r][j][e] - mn, s, levels) : 0u;
-      uint8_t* qr = a.q + i * a.ldq;
-      const bool whole = f + 4 <= a.F;
-      if (a.bits == 2) {
-        qr[f / 4] = (uint8_t)(c[0] | (c[1] << 2) | (c[2] << 4) | (c[3] << 6));
-      } else if (whole && a.q_dword) {
-        *reinterpret_cast<uint32_t*>(qr + f) = c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24);
-      } else {
-        for (int e = 0; e < 4 && f + e < a.F; ++e) qr[f + e] = (uint8_t)c[e];
       }
-      if (a.y) {
+    }
+  };
+  if (it >= n_iter) return;  // whole wavefronts leave together
+  float nxt[R][NV][4];
+  load(it, nxt);
+  constexpr float levels = (float)((1 << (BITS > 0 ? BITS : 1)) - 1);
+  for (; it < n_iter; it += stride) {
+    float v[R][NV][4];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int j = 0; j < NV; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[r][j][e] = nxt[r][j][e];
+    if (it + stride < n_iter) load(it + stride, nxt);
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int64_t i = it * (E * R) + (int64_t)r * E + lane / G;
+      const bool live = i < a.n;
+      if constexpr (LN) {
+        double s = 0.0;
+#pragma unroll
+        for (int j = 0; j < NV; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) s += (double)v[r][j][e];  // masked entries are 0
+        const double mean = slot_sum<G>(s) / (double)F;
+        double d[NV][4];
+        double var = 0.0;
+#pragma unroll
+        for (int j = 0; j < NV; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            d[j][e] = (double)v[r][j][e] - mean;
+            if (inside(4 * (sl + j * G) + e)) var = __builtin_fma(d[j][e], d[j][e], var);
+          }
+        const double inv = 1.0 / sqrt(slot_sum<G>(var) / (double)F + a.eps);
+        if (BITS == 0 && a.rstd && live && sl == 0) a.rstd[i] = (float)inv;
+#pragma unroll
+        for (int j = 0; j < NV; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int f = 4 * (sl + j * G) + e;
+            if (inside(f)) {
+              if (AFFINE) {
+                const double g = a.gamma ? (double)a.gamma[f] : 1.0;
+                const double b = a.beta ? (double)a.beta[f] : 0.0;
+                v[r][j][e] = (float)(d[j][e] * inv * g + b);
+              } else {
+                v[r][j][e] = (float)(d[j][e] * inv + 0.0);  // + 0 turns -0 into +0
+              }
+            }
+          }
+      }
+      if constexpr (BITS == 0) {  // LayerNorm only
+        if (!live) continue;
         float* yr = a.y + i * a.ldy;
-        if (whole && a.y_vec)
-          *reinterpret_cast<float4*>(yr + f) = make_float4(v[r][j][0], v[r][j][1], v[r][j][2], v[r][j][3]);
-        else
-          for (int e = 0; e < 4 && f + e < a.F; ++e) yr[f + e] = v[r][j][e];
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+          const int f = 4 * (sl + j * G);
+          if (!FULL && f >= F) continue;
+          if (FULL || (f + 4 <= F && a.y_vec))
+            *reinterpret_cast<float4*>(yr + f) = make_float4(v[r][j][0], v[r][j][1], v[r][j][2], v[r][j][3]);
+          else
+            for (int e = 0; e < 4 && f + e < F; ++e) yr[f + e] = v[r][j][e];
+        }
+        continue;
+      } else {
+        float mn = __builtin_inff(), mx = -__builtin_inff();
+#pragma unroll
+        for (int j = 0; j < NV; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (inside(4 * (sl + j * G) + e)) {
+              mn = fminf(mn, v[r][j][e]);
+              mx = fmaxf(mx, v[r][j][e]);
+            }
+        slot_minmax<G>(mn, mx);
+        const float s = (mx - mn) / levels;
+        const float rs = 1.0f / s;
+        // one path per wavefront: the reciprocal form while every live row's
+        // scale allows it (almost always), IEEE division otherwise
+        const bool fast = __all(!live || s == 0.0f || rcp_ok(s));
+        if (!live) continue;
+        if (sl == 0) {
+          a.zmin[i * a.ldp] = mn;
+          a.scale[i * a.ldp] = s;
+        }
+        uint8_t* qr = a.q + i * a.ldq;
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+          const int f = 4 * (sl + j * G);
+          if (!FULL && f >= F) continue;
+          uint32_t c[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float t = v[r][j][e] - mn;
+            const uint32_t cc = fast ? code_of_rcp(t, s, rs, levels) : code_of(t, s, levels);
+            c[e] = (inside(f + e) && s != 0.0f) ? cc : 0u;
+          }
+          const bool whole = FULL || f + 4 <= F;
+          if constexpr (BITS == 2) {
+            qr[f / 4] = (uint8_t)(c[0] | (c[1] << 2) | (c[2] << 4) | (c[3] << 6));
+          } else {
+            if (whole && (FULL || a.q_dword))
+              *reinterpret_cast<uint32_t*>(qr + f) = c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24);
+            else
+              for (int e = 0; e < 4 && f + e < F; ++e) qr[f + e] = (uint8_t)c[e];
+          }
+          if (a.y) {
+            float* yr = a.y + i * a.ldy;
+            if (whole && (FULL || a.y_vec))
+              *reinterpret_cast<float4*>(yr + f) = make_float4(v[r][j][0], v[r][j][1], v[r][j][2], v[r][j][3]);
+            else
+              for (int e = 0; e < 4 && f + e < F; ++e) yr[f + e] = v[r][j][e];
+          }
+        }
       }
     }
   }
 }
 
+template <int G, int NV, int R, bool AFFINE, bool LN, int BITS>
+void launch_v_full(const QuantArgs& a, hipStream_t s, dim3 grid) {
+  const bool full = a.F == 4 * G * NV && (BITS != 8 || a.q_dword) && (!a.y || a.y_vec);
+  if (full)
+    hipLaunchKernelGGL((k_ln_quantize_v<G, NV, R, AFFINE, LN, BITS, true>), grid, dim3(kBlock), 0,
+                       s, a);
+  else
+    hipLaunchKernelGGL((k_ln_quantize_v<G, NV, R, AFFINE, LN, BITS, false>), grid, dim3(kBlock), 0,
+                       s, a);
+}
+
+// With LayerNorm a wavefront works on a row group long enough that the next
+// group's loads are best issued meanwhile: the grid is capped at 32
+// workgroups per CU and every wavefront walks several groups, prefetching
+// (measured on 4M x 128 rows, LayerNorm + Int2: 0.62 ms one group per
+// wavefront, 0.60 / 0.59 / 0.56 / 0.55 ms at 4 / 8 / 16 / 32 workgroups per
+// CU). Without it the one-pass grid with two groups loaded up front is faster
+// (Int2: 0.42 against 0.46 ms).
+constexpr int64_t kQuantBlocksLN = 256 * 32;
+
 template <int G, int NV, int R>
 gcn_status launch_v(const QuantArgs& a, hipStream_t s) {
   const int64_t rows_per_block = (int64_t)(kBlock / 64) * (64 / G) * R;
-  const dim3 grid((unsigned)ceil_div(a.n, rows_per_block));
-  if (a.ln && (a.gamma || a.beta))
-    hipLaunchKernelGGL((k_ln_quantize_v<G, NV, R, true>), grid, dim3(kBlock), 0, s, a);
-  else
-    hipLaunchKernelGGL((k_ln_quantize_v<G, NV, R, false>), grid, dim3(kBlock), 0, s, a);
+  const int64_t need = ceil_div(a.n, rows_per_block);
+  const dim3 grid((unsigned)(a.ln ? std::min<int64_t>(need, kQuantBlocksLN) : need));
+  const bool affine = a.ln && (a.gamma || a.beta);
+  if (a.bits == 0) {  // LayerNorm only
+    if (affine)
+      launch_v_full<G, NV, R, true, true, 0>(a, s, grid);
+    else
+      launch_v_full<G, NV, R, false, true, 0>(a, s, grid);
+  } else if (a.bits == 8) {
+    if (!a.ln)
+      launch_v_full<G, NV, R, false, false, 8>(a, s, grid);
+    else if (affine)
+      launch_v_full<G, NV, R, true, true, 8>(a, s, grid);
+    else
+      launch_v_full<G, NV, R, false, true, 8>(a, s, grid);
+  } else {
+    if (!a.ln)
+      launch_v_full<G, NV, R, false, false, 2>(a, s, grid);
+    else if (affine)
+      launch_v_full<G, NV, R, true, true, 2>(a, s, grid);
+    else
+      launch_v_full<G, NV, R, false, true, 2>(a, s, grid);
+  }
   GCN_HIP(hipGetLastError());
   return GCN_OK;
 }
@@ -334,6 +421,8 @@ bool try_vector(const QuantArgs& a, hipStream_t s, gcn_status* st) {
     *st = launch_v<8, 1, 2>(a, s);
   else if (a.F <= 64)
     *st = launch_v<8, 2, 2>(a, s);
+  else if (a.F <= 128 && a.ln)
+    *st = launch_v<8, 4, 1>(a, s);
   else if (a.F <= 128)
     *st = launch_v<8, 4, 2>(a, s);
   else if (a.F <= 256)

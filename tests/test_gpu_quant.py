@@ -75,6 +75,44 @@ def test_layernorm_quantize(G, bits, F):
     assert np.array_equal(s[same].view(np.uint32), Sr[same].view(np.uint32))
 
 
+def near_half_step_rows(seed, n, F, bits, scale_exp):
+    """Rows whose values sit on and around the midpoints between codes: the
+    row's minimum is 0 and its maximum (2^bits - 1) * S0, the others are
+    (k + 1/2) * S nudged by -2 .. +2 ulps, where S is the scale the quantizer
+    will compute from the row; S0 is drawn around 2^scale_exp."""
+    rng = np.random.default_rng(seed)
+    levels = (1 << bits) - 1
+    X = np.zeros((n, F), np.float32)
+    for i in range(n):
+        s0 = np.float32(np.ldexp(1.0 + rng.random(), scale_exp))
+        mx = np.float32(levels * s0)
+        s = np.float32(mx / np.float32(levels))  # the quantizer's S, in fp32
+        k = rng.integers(0, levels, F).astype(np.float64)
+        v = ((k + 0.5) * np.float64(s)).astype(np.float32)
+        nudge = rng.integers(-2, 3, F).astype(np.int32)
+        v = (v.view(np.int32) + nudge).view(np.float32)
+        v = np.clip(v, np.float32(0), mx)
+        v[0], v[1] = 0.0, mx
+        X[i] = v
+    return X
+
+
+@pytest.mark.parametrize("bits", [8, 2])
+@pytest.mark.parametrize("scale_exp", [0, -20, 30, -99, 99, -110, 110])
+def test_quantize_codes_near_half_steps(G, bits, scale_exp):
+    # codes where rounding the quotient (x - Z) / S decides between two codes:
+    # bit-exact with the oracle's IEEE division, at scales inside and outside
+    # the range where the kernel divides by multiplying with 1 / S
+    note("quantize near half steps bits=%d 2^%d" % (bits, scale_exp))
+    for F in (128, 100):
+        X = near_half_step_rows(500 + scale_exp + bits, 600, F, bits, scale_exp)
+        Q, Z, S = oracle.quantize_rows_bits(X, bits)
+        q, z, s = G.gcn_layernorm_quantize(dev(X), bits=bits, layernorm=False)
+        assert np.array_equal(host(s).view(np.uint32), S.view(np.uint32))
+        assert np.array_equal(host(z).view(np.uint32), Z.view(np.uint32))
+        assert np.array_equal(host(q), Q), "codes differ on %d rows" % np.any(host(q) != Q, axis=1).sum()
+
+
 @pytest.mark.parametrize("F", [128, 64, 47])
 def test_int2_halo_fwd_and_bwd(G, F):
     note("int2 halo F=%d" % F)
