@@ -444,7 +444,7 @@ def run_gemm(args):
 
     dev = torch.device("cuda:0")
     n, f_in, hid, C = 2_449_029, 100, 256, 47
-    K3 = 2 * hid + 4  # GraphSAGE: [Y | Z | 1 0 0 0] of a hidden layer
+    K3 = 2 * hid + 4  # GraphSAGE: [Y | Z | 1 0 0 0] of a hidden layer, rows of 544 floats
     rnd = lambda seed, r, c: torch.from_numpy(synth.uniform(seed, r, c)).to(dev)  # noqa: E731
     X = rnd(3100, n, f_in)
     H1 = rnd(3101, n, hid)
@@ -452,7 +452,7 @@ def run_gemm(args):
     W2p = rnd(3103, hid, 48)
     dZ2p = rnd(3104, n, 48)
     dZ1 = rnd(3105, n, hid)
-    Cs = rnd(3106, n, K3)
+    Cs = rnd(3106, n, (K3 + 31) // 32 * 32)[:, :K3]
     Ws = rnd(3107, K3, hid)
     W3p = rnd(3108, K3, 48)
     out_nh = torch.empty((n, hid), device=dev)
@@ -522,6 +522,16 @@ def main():
               "single MI355X (sharding across GPUs is designed, not implemented); "
               "run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.calibrate_copy_mib > 0:
+        import torch
+        a = torch.empty(args.calibrate_copy_mib << 18, dtype=torch.float32, device="cuda:0")
+        a.fill_(1.0)
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        torch.mul(a, 1.0, out=b)  # one elementwise kernel: reads and writes exactly this size
+        torch.cuda.synchronize()
+        del a, b
+        log("copy calibration: %d MiB" % args.calibrate_copy_mib)
     if args.workload == "gcn_step":
         run_gcn_step(args)
         return
@@ -546,15 +556,6 @@ def main():
     G.lib()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-
-    if args.calibrate_copy_mib > 0:
-        a = torch.empty(args.calibrate_copy_mib << 18, dtype=torch.float32, device=dev).fill_(1.0)
-        b = torch.empty_like(a)
-        torch.cuda.synchronize()
-        torch.mul(a, 1.0, out=b)  # one elementwise kernel: reads and writes exactly this size
-        torch.cuda.synchronize()
-        del a, b
-        log("copy calibration: %d MiB" % args.calibrate_copy_mib)
 
     t0 = time.time()
     w = {"rmat24_q8": synth.rmat24_q8, "rmat24": synth.rmat24, "rmat20": synth.rmat20, "er4096": synth.er_4096,

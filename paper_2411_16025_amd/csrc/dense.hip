@@ -616,9 +616,11 @@ void launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, c
   // staged 16-byte stores need 16-byte aligned rows of C (and of the mask)
   const bool cvec = aligned16(C, ldc) && (!mask || aligned16(mask, ldm));
   const dim3 grid((unsigned)ceil_div(M, kTile), (unsigned)ceil_div(N, bn));
-  if (bn == 48)
-    hipLaunchKernelGGL((k_gemm_tall_v<OP, 48, 1>), grid, dim3(kThreads), 0, stream, M, N, K, A,
+  if (bn == 48) {  // two 16-row blocks per wavefront (each B fragment feeds two MFMAs)
+    const dim3 grid2((unsigned)ceil_div(M, (int64_t)kTile * 2), (unsigned)ceil_div(N, bn));
+    hipLaunchKernelGGL((k_gemm_tall_v<OP, 48, 2>), grid2, dim3(kThreads), 0, stream, M, N, K, A,
                        lda, B, ldb, C, ldc, mask, ldm, relu, cvec);
+  }
   else if (bn == 64)
     hipLaunchKernelGGL((k_gemm_tall_v<OP, 64, 1>), grid, dim3(kThreads), 0, stream, M, N, K, A,
                        lda, B, ldb, C, ldc, mask, ldm, relu, cvec);
