@@ -745,6 +745,15 @@ def main():
         "modeled_frac": round(value / HBM_PEAK_GBS, 4), "model": MODEL_NOTE,
         "edge_features_per_s": float("%.4g" % ef_per_s),
         "fwd_ms": round(fwd_ms, 4), "bwd_ms": round(bwd_ms, 4),
+        # per pass: modeled and counted rates over the event-timed pass
+        "per_op": {op: {
+            "ms": round(ms, 4), "modeled_GBps": round(B / (ms * 1e-3) / 1e9, 1),
+            "modeled_frac": round(B / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "edge_features_per_s": float("%.4g" % (nz * F / (ms * 1e-3))),
+            "counted_GBps": None if counted is None else round(
+                sum(f + wr for (k, o), (f, wr, _) in counted["rows"].items() if o == op)
+                / (ms * 1e-3) / 1e9, 1)}
+            for op, ms, B, nz in (("fwd", fwd_ms, Bf, nnz_f), ("bwd", bwd_ms, Bb, nnz_b))},
         "step_ms_median": round(float(np.median(per_step)), 4),
         "step_ms_min": round(float(np.min(per_step)), 4),
         # the L2-to-fabric bytes the kernels moved (counters; Infinity Cache

@@ -175,7 +175,8 @@ gcn_status gcn_aggregate_fwd_noalloc(const gcn_graph* g, const void* X, int64_t 
  *  halo_min, halo_scale   fp32 zero point Z and scale S of halo row h at
  *              element h * ldp (ldp >= 1). ldp = 1: two plain arrays;
  *              ldp = 2 with halo_scale == halo_min + 1: (Z, S) pairs side by
- *              side (8-byte aligned), read with one 8-byte load per gather.
+ *              side, so a gather's two 4-byte parameter loads touch one cache
+ *              line.
  *  Y           fp32 output (ldy). */
 gcn_status gcn_aggregate_fwd_q8halo(const gcn_graph* g, int64_t n_local_cols, const float* X_local,
                                     int64_t ldx, const uint8_t* Q_halo, int64_t ldq,

@@ -19,11 +19,21 @@
 //      1 or 2 entries       -> one row per slot, several row groups per
 //                              wavefront with all their loads issued first
 //      3..medium_max        -> one row per slot, E rows of about the same
-//                              length per wavefront
-//      longer rows          -> one 256-thread workgroup per chunk of entries,
+//                              length per wavefront (k_short)
+//      longer rows, on matrices of 2^20 or more columns
+//                           -> cut where their columns cross one of 64 column
+//                              blocks and into pieces of at most 256 entries;
+//                              one piece per slot, launched block by block so
+//                              the wavefronts in flight gather from one column
+//                              range (k_pieces); every piece writes a partial
+//                              row
+//      longer rows, on smaller matrices
+//                           -> one 256-thread workgroup per chunk of entries,
 //                              slots reduced in fixed order through LDS; a row
-//                              with several chunks writes partial rows that a
-//                              last kernel sums in chunk order.
+//                              with several chunks writes partial rows
+//                              (k_chunk)
+//    A last kernel sums each cut row's partial rows in a fixed order
+//    (k_reduce_parts).
 //  * Every output element is summed in an order fixed by the graph and F:
 //    no atomics, identical bits on every run.
 //  * Source rows are gathered with 16-byte loads; the (column, value) pair

@@ -28,6 +28,8 @@ def assert_close(y, ref, S, rel=1e-5, what=""):
     err = np.abs(y - ref)
     bound = rel * S + 1e-30
     bad = err > bound
+    if what and err.size:
+        note("%s: max err/S %.2e over %d elements" % (what, float((err / np.maximum(S, 1e-300)).max()), err.size))
     if bad.any():
         idx = np.argwhere(bad)
         ratio = (err / np.maximum(S, 1e-300)).max()
