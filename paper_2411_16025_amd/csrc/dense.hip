@@ -10,6 +10,9 @@
 //    each wavefront owns 16 rows and issues v_mfma_f32_16x16x4_f32 on BN / 16
 //    blocks of 16 x 16. The tile leaves through LDS as row-contiguous
 //    16-byte stores, with an optional ReLU or ReLU-backward mask.
+//  * Outputs of at most 48 columns with B in LDS (the class layer) take a
+//    resident-B kernel: B is staged once per CU and every wavefront streams
+//    its own rows of A into the matrix-core registers, several chunks ahead.
 //  * C = A^T B with K = nodes (the weight gradients): K is split into fixed
 //    chunks; every chunk writes a partial C tile and a second kernel adds the
 //    partials in chunk order, so the result is the same on every run.
@@ -19,6 +22,7 @@
 // i holds C[4 * (l / 16) + i][l % 16].
 
 #include <algorithm>
+#include <mutex>
 
 #include "common.h"
 
@@ -394,6 +398,277 @@ void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A,
   }
 }
 
+// Resident-B C = A op(B) for products whose B (a weight matrix) fits in LDS:
+// each workgroup (one per CU) stages its BN-column slice of B in LDS once and
+// then stays on its CU; every wavefront walks its own 16 * RB-row tiles of C
+// with no further barriers. A is streamed straight from memory into the
+// matrix-core operand registers, D slots of CPS 16-deep K chunks ahead
+// (across tile boundaries), so the loads of one wavefront overlap the MFMAs
+// of the others. Narrow outputs (the 47 classes) are bound by the stream of
+// A, which the staged-tile kernel reads one 32-deep slice per barrier pair.
+//
+// Operand order inside a chunk: for a full chunk of 16 k, lane (g = l / 16,
+// r = l % 16) holds A[r][16 j + 4 g .. + 3] as one 16-byte load and matrix-core
+// step i takes element i, so step i contracts over k = 16 j + 4 g + i for the
+// four lane groups g; the last, partial chunk (K % 16 != 0) takes
+// k = 16 j + 4 i + g instead, element by element, so that its steps stop at
+// ceil((K - 16 j) / 4). B is stored in LDS in the same order, one float4 per
+// (chunk, 16-column block, lane), and read with one 16-byte LDS load per block
+// and chunk. The sum over k is the same; only its order differs from the
+// staged-tile kernel.
+//
+// Stores: the four results of a lane (rows 4 g .. 4 g + 3 of one column) are
+// transposed within each quad of lanes with DPP moves, so that every lane
+// writes 4 consecutive columns of one row as one 16-byte store.
+
+__device__ inline float dpp_quad(float v, int ctrl_sel) {
+  // 0x4E: quad_perm [2, 3, 0, 1]; 0xB1: quad_perm [1, 0, 3, 2]
+  const int x = __float_as_int(v);
+  const int y = ctrl_sel == 0 ? __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false)
+                              : __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false);
+  return __int_as_float(y);
+}
+
+// In each quad of lanes (q = lane & 3) element i of lane q is M[i][q] on
+// entry and M[q][i] on return: the 2 x 2 blocks are swapped across lanes two
+// apart, then each 2 x 2 block is transposed across neighbouring lanes.
+__device__ inline f4 quad_transpose(f4 v, int q) {
+  const bool lo = q < 2;
+  float x = lo ? v[2] : v[0], y = lo ? v[3] : v[1];
+  x = dpp_quad(x, 0);
+  y = dpp_quad(y, 0);
+  if (lo) { v[2] = x; v[3] = y; } else { v[0] = x; v[1] = y; }
+  const bool ev = (q & 1) == 0;
+  x = ev ? v[1] : v[0];
+  y = ev ? v[3] : v[2];
+  x = dpp_quad(x, 1);
+  y = dpp_quad(y, 1);
+  if (ev) { v[1] = x; v[3] = y; } else { v[0] = x; v[2] = y; }
+  return v;
+}
+
+template <int OP, int NBLK, int RB, int D, int CPS, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void k_gemm_bres(
+    int64_t M, int64_t N, int64_t K, const float* __restrict__ A, int64_t lda,
+    const float* __restrict__ B, int64_t ldb, float* __restrict__ C, int64_t ldc,
+    const float* __restrict__ mask, int64_t ldm, bool relu, bool cvec) {
+  extern __shared__ __align__(16) float bres_lds[];
+  const f4* Bs = reinterpret_cast<const f4*>(bres_lds);
+  constexpr int BN = 16 * NBLK;
+  const int64_t NC = K / 16;          // full chunks (a multiple of D * CPS)
+  const int kt = (int)(K - 16 * NC);  // k of the partial chunk (0: none)
+  const int64_t n0 = (int64_t)blockIdx.y * BN;
+  const int t = threadIdx.x, lane = t & 63;
+  // stage B: slot (chunk j, block nb, lane l, element i) holds
+  // B[k][n0 + 16 nb + l % 16] with k as described above (zero past K or N);
+  // n runs fastest over the threads so the reads of an NN B row are
+  // contiguous; 8 loads are in flight per thread
+  {
+    const int64_t total = (NC + (kt > 0)) * NBLK * 256;
+    constexpr int U = 8, kThr = 64 * WAVES;
+    for (int64_t base = 0; base < total; base += (int64_t)U * kThr) {
+      float v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t idx = base + (int64_t)u * kThr + t;
+        const int n = (int)(idx & 15);
+        const int i = (int)((idx >> 4) & 3);
+        const int g = (int)((idx >> 6) & 3);
+        const int64_t jb = idx >> 8;  // j * NBLK + nb
+        const int nb = (int)(jb % NBLK);
+        const int64_t j = jb / NBLK;
+        const int64_t k = j < NC ? 16 * j + 4 * g + i : 16 * j + 4 * i + g;
+        const int64_t col = n0 + 16 * nb + n;
+        v[u] = 0.f;
+        if (idx < total && k < K && col < N) v[u] = OP == kNN ? B[k * ldb + col] : B[col * ldb + k];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t idx = base + (int64_t)u * kThr + t;
+        if (idx < total) {
+          const int n = (int)(idx & 15);
+          const int i = (int)((idx >> 4) & 3);
+          const int g = (int)((idx >> 6) & 3);
+          bres_lds[((idx >> 8) * 64 + 16 * g + n) * 4 + i] = v[u];
+        }
+      }
+    }
+  }
+  __syncthreads();
+  constexpr int TR = 16 * RB;  // rows per tile
+  const int64_t T = (M + TR - 1) / TR;
+  const int64_t TW = (int64_t)gridDim.x * WAVES;
+  const int64_t first = (int64_t)blockIdx.x * WAVES +
+                        __builtin_amdgcn_readfirstlane(t >> 6);
+  if (first >= T) return;
+  const int g = lane >> 4, r = lane & 15, q = lane & 3;
+  // This lane's A elements of a tile: row tile * TR + 16 rb + r (rows past M
+  // read row M - 1, never stored), from column 4 g on.
+  auto rowptr = [&](int64_t tile, int rb) {
+    return A + min(min(tile, T - 1) * TR + 16 * rb + r, M - 1) * lda + 4 * g;
+  };
+  auto load_b = [&](int64_t j, f4 (&b)[NBLK]) {
+    const f4* bp = Bs + j * NBLK * 64 + lane;
+#pragma unroll
+    for (int nb = 0; nb < NBLK; ++nb) b[nb] = bp[nb * 64];
+  };
+  f4 acc[RB][NBLK];
+  auto mma = [&](const f4 (&a)[RB], const f4 (&b)[NBLK], int steps) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (i >= steps) break;
+#pragma unroll
+      for (int nb = 0; nb < NBLK; ++nb)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          acc[rb][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[rb][i], b[nb][i], acc[rb][nb], 0, 0, 0);
+    }
+  };
+  // the partial chunk: element i of lane group g is k = 16 NC + 4 i + g
+  // (clamped to K - 1 here, zeroed after the load has landed)
+  auto issue_tail = [&](const float* const (&p)[RB], f4 (&dst)[RB]) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const float* row = p[rb] - 4 * g + 16 * NC;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dst[rb][i] = row[min(4 * i + g, kt - 1)];
+    }
+  };
+  // The chunk stream of a wavefront: its tiles first, first + TW, ..., NC
+  // chunks each. A ring slot holds CPS consecutive chunks (their loads go
+  // out back to back: 64 CPS contiguous bytes of each row), D slots are in
+  // flight, and D * CPS divides NC. Each slot is refilled right after its
+  // MFMAs with the slot D ahead (of this tile or, in the last group, of the
+  // next one; past the last tile a valid row is reloaded and never used), so
+  // every group issues the same loads and a wait covers one slot. The next
+  // chunk's B fragments are read from LDS before the current chunk's MFMAs.
+  // The first group of a tile is peeled: the stores of the previous tile
+  // make its first wait a full one (loads and stores share one counter); the
+  // groups after it wait for one slot at a time.
+  constexpr int SPG = D * CPS;  // chunks per group
+  const int64_t NG = NC / SPG;
+  const float* pc[RB];  // rows of the current tile
+  const float* pn[RB];  // rows of the next tile
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    pc[rb] = rowptr(first, rb);
+    pn[rb] = rowptr(first + TW, rb);
+  }
+  f4 buf[D][RB][CPS], tb[RB], tbn[RB];
+#pragma unroll
+  for (int d = 0; d < D; ++d)
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int c = 0; c < CPS; ++c)
+        buf[d][rb][c] = *reinterpret_cast<const f4*>(pc[rb] + 16 * (d * CPS + c));
+  if (kt > 0) issue_tail(pc, tb);
+  auto group = [&](int64_t gi) {
+    const bool last = gi + 1 == NG;
+    const float* src[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) src[rb] = last ? pn[rb] : pc[rb] + 16 * SPG * (gi + 1);
+    f4 b[2][NBLK];
+    load_b(gi * SPG, b[0]);
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+#pragma unroll
+      for (int c = 0; c < CPS; ++c) {
+        const int jj = d * CPS + c;
+        if (jj + 1 < SPG) load_b(gi * SPG + jj + 1, b[(jj + 1) & 1]);
+        f4 a[RB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) a[rb] = buf[d][rb][c];
+        mma(a, b[jj & 1], 4);
+      }
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int c = 0; c < CPS; ++c)
+          buf[d][rb][c] = *reinterpret_cast<const f4*>(src[rb] + 16 * (d * CPS + c));
+      // keep the slots in order: without this the scheduler hoists every
+      // slot's LDS reads to the top of the group and sinks the refills to
+      // its end, which costs registers and the staggering of the loads
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  for (int64_t tile = first; tile < T; tile += TW) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int nb = 0; nb < NBLK; ++nb) acc[rb][nb] = f4{0.f, 0.f, 0.f, 0.f};
+    group(0);
+    // the next tile's partial chunk goes out after the first (full) wait
+    if (kt > 0) issue_tail(pn, tbn);
+    for (int64_t gi = 1; gi < NG; ++gi) group(gi);
+    if (kt > 0) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (4 * i + g >= kt) tb[rb][i] = 0.f;
+      f4 b[NBLK];
+      load_b(NC, b);
+      mma(tb, b, (kt + 3) / 4);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) tb[rb] = tbn[rb];
+    }
+    // the tile leaves: C (with the ReLU-backward mask or the ReLU applied)
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int64_t rbase = tile * TR + 16 * rb;
+#pragma unroll
+      for (int nb = 0; nb < NBLK; ++nb) {
+        if (cvec) {
+          // after the transpose: row 4 g + q, columns 4 ((lane >> 2) & 3) .. + 3
+          f4 v = quad_transpose(acc[rb][nb], q);
+          const int64_t gm = rbase + 4 * g + q;
+          const int64_t gn = n0 + 16 * nb + 4 * ((lane >> 2) & 3);
+          if (gm < M && gn < N) {
+            if (gn + 4 <= N) {
+              if (mask) {
+                const f4 mk = *reinterpret_cast<const f4*>(mask + gm * ldm + gn);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  if (!(mk[e] > 0.f)) v[e] = 0.f;
+              }
+              if (relu) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = fmaxf(v[e], 0.f);
+              }
+              __builtin_nontemporal_store(v, reinterpret_cast<f4*>(C + gm * ldc + gn));
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                if (gn + e >= N) break;
+                float x = (mask && !(mask[gm * ldm + gn + e] > 0.f)) ? 0.f : v[e];
+                if (relu) x = fmaxf(x, 0.f);
+                C[gm * ldc + gn + e] = x;
+              }
+            }
+          }
+        } else {
+          const int64_t gn = n0 + 16 * nb + r;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int64_t gm = rbase + 4 * g + i;
+            if (gm < M && gn < N) {
+              float x = (mask && !(mask[gm * ldm + gn] > 0.f)) ? 0.f : acc[rb][nb][i];
+              if (relu) x = fmaxf(x, 0.f);
+              C[gm * ldc + gn] = x;
+            }
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      pc[rb] = pn[rb];
+      pn[rb] = rowptr(tile + 2 * TW, rb);
+    }
+  }
+}
+
 // Wide-tile partial C = A^T B over one K chunk for 16-byte aligned operands:
 // a (16 * WAVES) x BN tile per workgroup, so for C up to 128 x 256 each row
 // of A and B is read once per chunk.
@@ -608,13 +883,79 @@ bool aligned16(const void* p, int64_t ld) { return ((uintptr_t)p % 16) == 0 && l
 int tile_n(int64_t N) { return N <= 48 ? 48 : (N <= 64 ? 64 : (N <= 128 ? 128 : 256)); }
 int tile_n_narrow(int64_t N) { return N <= 48 ? 48 : (N <= 64 ? 64 : 128); }
 
+// Compute units of the current device (cached per device).
+int cu_count() {
+  static std::mutex mu;
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  std::lock_guard<std::mutex> lk(mu);
+  if (cached[dev] == 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        v <= 0)
+      v = 256;
+    cached[dev] = v;
+  }
+  return cached[dev];
+}
+
+#ifndef GCN_GEMM_RESIDENT
+#define GCN_GEMM_RESIDENT 1
+#endif
+constexpr int64_t kResMinRows = 65536;       // below this the staged tile is used
+constexpr int64_t kResMaxLds = 120 * 1024;   // LDS bytes for the resident B slice
+
+template <int OP, int NBLK, int RB, int D, int CPS, int WAVES>
+hipError_t launch_bres(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                       const float* B, int64_t ldb, float* C, int64_t ldc, const float* mask,
+                       int64_t ldm, bool relu, bool cvec, hipStream_t stream) {
+  const size_t lds = (size_t)((K + 15) / 16) * 16 * (16 * NBLK) * sizeof(float);
+  auto kern = k_gemm_bres<OP, NBLK, RB, D, CPS, WAVES>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  // one workgroup per CU (the B slice takes most of the LDS), at most one
+  // tile per wavefront
+  const int64_t tiles = ceil_div(M, (int64_t)16 * RB);
+  const int64_t wg = std::min<int64_t>(cu_count(), ceil_div(tiles, (int64_t)WAVES));
+  const dim3 grid((unsigned)wg, (unsigned)ceil_div(N, (int64_t)16 * NBLK));
+  hipLaunchKernelGGL(kern, grid, dim3(64 * WAVES), lds, stream, M, N, K, A, lda, B, ldb, C, ldc,
+                     mask, ldm, relu, cvec);
+  return hipGetLastError();
+}
+
+// The resident-B kernel takes tall products of at most 48 output columns
+// (the class count, 47) whose B fits in LDS. (For 256-column outputs it was
+// no faster than the staged tile: those products are bound by their C
+// stores or by the matrix cores, not by the stream of A.)
+int resident_blocks(int64_t M, int64_t N, int64_t K) {
+  if (!GCN_GEMM_RESIDENT || M < kResMinRows || N > 48 || K < 16) return 0;
+  const int nblk = 3;
+  const int64_t lds = ceil_div(K, (int64_t)16) * 16 * 16 * nblk * (int64_t)sizeof(float);
+  return lds <= kResMaxLds ? nblk : 0;
+}
+
 template <int OP>
-void launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
+hipError_t launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
                  int64_t ldb, float* C, int64_t ldc, const float* mask, int64_t ldm,
                  bool relu, hipStream_t stream) {
   const int bn = OP == kNN ? tile_n(N) : tile_n_narrow(N);
   // staged 16-byte stores need 16-byte aligned rows of C (and of the mask)
   const bool cvec = aligned16(C, ldc) && (!mask || aligned16(mask, ldm));
+  const int nblk = resident_blocks(M, N, K);
+  // ring: D slots of CPS chunks (D * CPS must divide the chunk count)
+  const int64_t nc = K / 16;
+#define GCN_BRES(D_, CPS_)                                                                 \
+  return launch_bres<OP, 3, 2, D_, CPS_, 8>(M, N, K, A, lda, B, ldb, C, ldc, mask, ldm, relu, \
+                                            cvec, stream)
+  if (nblk == 3) {
+    if (nc % 8 == 0) GCN_BRES(2, 4);
+    if (nc % 4 == 0) GCN_BRES(2, 2);
+    if (nc % 2 == 0) GCN_BRES(2, 1);
+    GCN_BRES(1, 1);
+  }
+#undef GCN_BRES
   const dim3 grid((unsigned)ceil_div(M, kTile), (unsigned)ceil_div(N, bn));
   if (bn == 48) {  // two 16-row blocks per wavefront (each B fragment feeds two MFMAs)
     const dim3 grid2((unsigned)ceil_div(M, (int64_t)kTile * 2), (unsigned)ceil_div(N, bn));
@@ -637,7 +978,9 @@ void launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, c
                          A, lda, B, ldb, C, ldc, mask, ldm, relu, cvec);
     }
   }
+  return hipGetLastError();
 }
+
 
 void launch_tn(int64_t M, int64_t N, int64_t K, int64_t split, int64_t n_chunks, const float* A,
                int64_t lda, const float* B, int64_t ldb, float* part, hipStream_t stream) {
@@ -703,9 +1046,9 @@ gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int
   const dim3 grid((unsigned)ceil_div(M, kTile), (unsigned)ceil_div(N, kTile));
   ProfScope ps(op == GCN_GEMM_NN ? "gemm_nn" : "gemm_nt", stream);
   if (vec && op == GCN_GEMM_NN)
-    launch_tall<kNN>(M, N, K, A, lda, B, ldb, C, ldc, mask, ldm, relu, stream);
+    GCN_HIP(launch_tall<kNN>(M, N, K, A, lda, B, ldb, C, ldc, mask, ldm, relu, stream));
   else if (vec)
-    launch_tall<kNT>(M, N, K, A, lda, B, ldb, C, ldc, mask, ldm, relu, stream);
+    GCN_HIP(launch_tall<kNT>(M, N, K, A, lda, B, ldb, C, ldc, mask, ldm, relu, stream));
   else if (op == GCN_GEMM_NN)
     hipLaunchKernelGGL(k_gemm_tall<kNN>, grid, dim3(kThreads), 0, stream, M, N, K, A, lda, B, ldb,
                        C, ldc);

@@ -47,6 +47,48 @@ def test_gemm_nn_nt(G, M, N, K):
     assert_close(C2, ref, S, what="NT")
 
 
+# Tall products (M >= 65536) of at most 48 output columns take the
+# resident-B kernel: K tails of 0 to 15 past the last 16-deep chunk, every
+# ring shape (chunk counts divisible by 8, 4, 2 and odd: K = 256, 516, 640;
+# 68; 47; 17, 48), several tiles per wavefront (M up to 10^6), 16-byte
+# aligned C rows (ldc a multiple of 4) and C rows of odd stride (element
+# stores). Wider outputs at the same heights check the staged tile.
+RESIDENT = [(1000003, 47, 47), (65573, 48, 516), (65536, 1, 4), (70001, 16, 17),
+            (65573, 33, 15), (65573, 40, 68), (65573, 48, 48), (65573, 512, 48),
+            (65573, 200, 4), (65573, 48, 640), (131101, 47, 256)]
+
+
+def _ld4(n):
+    return (n + 3) // 4 * 4
+
+
+@pytest.mark.parametrize("M,N,K", RESIDENT)
+def test_gemm_resident_b(G, M, N, K):
+    import torch
+    note("gemm resident-B %dx%dx%d" % (M, N, K))
+    A = synth.uniform(211, M, K, ld=_ld4(K))
+    B = synth.uniform(212, K, N, ld=_ld4(N))
+    A64 = A[:, :K].astype(np.float64)
+    B64 = B[:, :N].astype(np.float64)
+    ref = A64 @ B64
+    S = np.abs(A64) @ np.abs(B64)
+    del A64, B64
+    Ad = dev(A)[:, :K]
+    for aligned in (True, False):
+        ldc = _ld4(N) if aligned else (N | 1) + 2 * (N % 2)
+        Cfull = torch.full((M, ldc), 7.0, device="cuda:0")
+        C = G.gcn_gemm_f32(G.GCN_GEMM_NN, Ad, dev(B)[:, :N], C=Cfull[:, :N])
+        Ch = host(Cfull)
+        assert_close(Ch[:, :N], ref, S, what="NN ldc %d" % ldc)
+        assert np.all(Ch[:, N:] == 7.0)
+        del C, Cfull, Ch
+    Bt = np.zeros((N, _ld4(K)), np.float32)
+    Bt[:, :K] = B[:, :N].T
+    C2 = G.gcn_gemm_f32(G.GCN_GEMM_NT, Ad, dev(Bt)[:, :K],
+                        C=torch.empty((M, _ld4(N)), device="cuda:0")[:, :N])
+    assert_close(host(C2), ref, S, what="NT")
+
+
 @pytest.mark.parametrize("K,M,N", [(5, 3, 2), (8192, 100, 256), (20000, 256, 47),
                                    (100003, 64, 64), (33, 1, 300)])
 def test_gemm_tn_split_k(G, K, M, N):
