@@ -10,9 +10,10 @@
 //    each wavefront owns 16 rows and issues v_mfma_f32_16x16x4_f32 on BN / 16
 //    blocks of 16 x 16. The tile leaves through LDS as row-contiguous
 //    16-byte stores, with an optional ReLU or ReLU-backward mask.
-//  * Outputs of at most 48 columns with B in LDS (the class layer) take a
-//    resident-B kernel: B is staged once per CU and every wavefront streams
-//    its own rows of A into the matrix-core registers, several chunks ahead.
+//  * Products whose B fits in LDS (weights: K x 48 for the classes, K x 256
+//    slices for the hidden layer) take a resident-B kernel: B is staged once
+//    per CU and every wavefront streams its own rows of A into the
+//    matrix-core registers, several chunks ahead.
 //  * C = A^T B with K = nodes (the weight gradients): K is split into fixed
 //    chunks; every chunk writes a partial C tile and a second kernel adds the
 //    partials in chunk order, so the result is the same on every run.
@@ -405,7 +406,8 @@ void k_gemm_tall_v(int64_t M, int64_t N, int64_t K, const float* __restrict__ A,
 // matrix-core operand registers, D slots of CPS 16-deep K chunks ahead
 // (across tile boundaries), so the loads of one wavefront overlap the MFMAs
 // of the others. Narrow outputs (the 47 classes) are bound by the stream of
-// A, which the staged-tile kernel reads one 32-deep slice per barrier pair.
+// A, which the staged-tile kernel reads one 32-deep slice per barrier pair;
+// wide ones with a short K by the stores of C.
 //
 // Operand order inside a chunk: for a full chunk of 16 k, lane (g = l / 16,
 // r = l % 16) holds A[r][16 j + 4 g .. + 3] as one 16-byte load and matrix-core
@@ -636,7 +638,9 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_bres(
 #pragma unroll
                 for (int e = 0; e < 4; ++e) v[e] = fmaxf(v[e], 0.f);
               }
-              __builtin_nontemporal_store(v, reinterpret_cast<f4*>(C + gm * ldc + gn));
+              // plain stores: nontemporal ones left the 64-byte row pieces
+              // to reach memory as partial lines (Z2 0.75 -> 0.71 ms)
+              *reinterpret_cast<f4*>(C + gm * ldc + gn) = v;
             } else {
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
@@ -925,13 +929,16 @@ hipError_t launch_bres(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
   return hipGetLastError();
 }
 
-// The resident-B kernel takes tall products of at most 48 output columns
-// (the class count, 47) whose B fits in LDS. (For 256-column outputs it was
-// no faster than the staged tile: those products are bound by their C
-// stores or by the matrix cores, not by the stream of A.)
-int resident_blocks(int64_t M, int64_t N, int64_t K) {
-  if (!GCN_GEMM_RESIDENT || M < kResMinRows || N > 48 || K < 16) return 0;
-  const int nblk = 3;
+// The resident-B kernel takes tall products whose B slice fits in LDS: 48
+// columns (the class count, 47) or 256-column slices of outputs wider than
+// 128 (the hidden layer). A ReLU-backward mask stays with the staged tile,
+// which loads the mask values before it stages the output (in the resident
+// kernel each tile would wait for them: the GCN step's dH1 took 1.46 ms
+// against 1.17).
+int resident_blocks(int64_t M, int64_t N, int64_t K, bool masked) {
+  if (!GCN_GEMM_RESIDENT || M < kResMinRows || K < 16 || masked) return 0;
+  const int nblk = N <= 48 ? 3 : (N > 128 ? 16 : 0);
+  if (nblk == 0) return 0;
   const int64_t lds = ceil_div(K, (int64_t)16) * 16 * 16 * nblk * (int64_t)sizeof(float);
   return lds <= kResMaxLds ? nblk : 0;
 }
@@ -943,7 +950,7 @@ hipError_t launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
   const int bn = OP == kNN ? tile_n(N) : tile_n_narrow(N);
   // staged 16-byte stores need 16-byte aligned rows of C (and of the mask)
   const bool cvec = aligned16(C, ldc) && (!mask || aligned16(mask, ldm));
-  const int nblk = resident_blocks(M, N, K);
+  const int nblk = resident_blocks(M, N, K, mask != nullptr);
   // ring: D slots of CPS chunks (D * CPS must divide the chunk count)
   const int64_t nc = K / 16;
 #define GCN_BRES(D_, CPS_)                                                                 \
@@ -956,6 +963,18 @@ hipError_t launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
     GCN_BRES(1, 1);
   }
 #undef GCN_BRES
+  // 256 columns: one 16-row block per wavefront (64 accumulator registers),
+  // one chunk per slot
+#define GCN_BRES16(D_)                                                                      \
+  return launch_bres<OP, 16, 1, D_, 1, 8>(M, N, K, A, lda, B, ldb, C, ldc, mask, ldm, relu, \
+                                          cvec, stream)
+  if (nblk == 16) {
+    if (nc % 4 == 0) GCN_BRES16(4);
+    if (nc % 3 == 0) GCN_BRES16(3);
+    if (nc % 2 == 0) GCN_BRES16(2);
+    GCN_BRES16(1);
+  }
+#undef GCN_BRES16
   const dim3 grid((unsigned)ceil_div(M, kTile), (unsigned)ceil_div(N, bn));
   if (bn == 48) {  // two 16-row blocks per wavefront (each B fragment feeds two MFMAs)
     const dim3 grid2((unsigned)ceil_div(M, (int64_t)kTile * 2), (unsigned)ceil_div(N, bn));

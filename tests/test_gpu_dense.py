@@ -47,15 +47,17 @@ def test_gemm_nn_nt(G, M, N, K):
     assert_close(C2, ref, S, what="NT")
 
 
-# Tall products (M >= 65536) of at most 48 output columns take the
-# resident-B kernel: K tails of 0 to 15 past the last 16-deep chunk, every
-# ring shape (chunk counts divisible by 8, 4, 2 and odd: K = 256, 516, 640;
-# 68; 47; 17, 48), several tiles per wavefront (M up to 10^6), 16-byte
-# aligned C rows (ldc a multiple of 4) and C rows of odd stride (element
-# stores). Wider outputs at the same heights check the staged tile.
+# Tall products (M >= 65536) whose B fits in LDS take the resident-B kernel:
+# 48-column slices (N <= 48) and 256-column slices (N > 128), K tails of 0
+# to 15 past the last 16-deep chunk, every ring shape (chunk counts
+# divisible by 8, 4, 2 and odd; for 256 columns by 4, 3, 2 and odd), several
+# tiles per wavefront (M up to 10^6), a partial last column slice (N = 300),
+# 16-byte aligned C rows (ldc a multiple of 4) and C rows of odd stride
+# (element stores). K < 16 and 48 < N <= 128 check the staged tile.
 RESIDENT = [(1000003, 47, 47), (65573, 48, 516), (65536, 1, 4), (70001, 16, 17),
-            (65573, 33, 15), (65573, 40, 68), (65573, 48, 48), (65573, 512, 48),
-            (65573, 200, 4), (65573, 48, 640), (131101, 47, 256)]
+            (65573, 33, 15), (65573, 40, 68), (65573, 48, 48), (65573, 48, 640),
+            (131101, 47, 256), (500003, 256, 100), (65573, 300, 47), (65573, 512, 48),
+            (65573, 129, 112), (65573, 200, 16), (65573, 256, 64), (65573, 100, 100)]
 
 
 def _ld4(n):
