@@ -107,6 +107,35 @@ def test_gemm_tn_split_k(G, K, M, N):
     assert torch.equal(C.view(torch.int32), C2.view(torch.int32))
 
 
+# Weight-gradient shapes (K = nodes >= 65536, N <= 64, at most 16 output
+# tiles of 64 x 64) take the streaming A^T B kernel: dW2 (256 x 47), a
+# GraphSAGE class layer (516 x 47, two workgroups of tiles), one-column and
+# ragged tiles, K not a multiple of 4 (a partial last step), 16-byte aligned
+# rows (leading dimensions padded to a multiple of 4); dW1 (100 x 256) checks
+# the staged tile at the same depth. Also checked: identical bits on a
+# second run.
+TN_STREAM = [(1000003, 256, 47), (300007, 100, 256), (65536, 516, 47), (70001, 33, 5),
+             (65539, 1, 1), (131072, 64, 64)]
+
+
+@pytest.mark.parametrize("K,M,N", TN_STREAM)
+def test_gemm_tn_stream(G, K, M, N):
+    import torch
+    note("gemm tn stream %dx%dx%d" % (K, M, N))
+    A = synth.uniform(213, K, M, ld=_ld4(M))
+    B = synth.uniform(214, K, N, ld=_ld4(N))
+    A64 = A[:, :M].astype(np.float64)
+    B64 = B[:, :N].astype(np.float64)
+    ref = A64.T @ B64
+    S = np.abs(A64).T @ np.abs(B64)
+    del A64, B64
+    Ad, Bd = dev(A)[:, :M], dev(B)[:, :N]
+    C = G.gcn_gemm_f32(G.GCN_GEMM_TN, Ad, Bd)
+    assert_close(host(C), ref, S, what="TN stream")
+    C2 = G.gcn_gemm_f32(G.GCN_GEMM_TN, Ad, Bd)
+    assert torch.equal(C.view(torch.int32), C2.view(torch.int32))
+
+
 def test_gemm_strided_operands(G):
     import torch
     note("gemm strided")
