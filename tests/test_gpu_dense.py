@@ -53,7 +53,8 @@ def test_gemm_nn_nt(G, M, N, K):
 # divisible by 8, 4, 2 and odd; for 256 columns by 4, 3, 2 and odd), several
 # tiles per wavefront (M up to 10^6), a partial last column slice (N = 300),
 # 16-byte aligned C rows (ldc a multiple of 4) and C rows of odd stride
-# (element stores). K < 16 and 48 < N <= 128 check the staged tile.
+# (element stores); a repeated call gives identical bits. K < 16 and
+# 48 < N <= 128 check the staged tile.
 RESIDENT = [(1000003, 47, 47), (65573, 48, 516), (65536, 1, 4), (70001, 16, 17),
             (65573, 33, 15), (65573, 40, 68), (65573, 48, 48), (65573, 48, 640),
             (131101, 47, 256), (500003, 256, 100), (65573, 300, 47), (65573, 512, 48),
@@ -89,6 +90,9 @@ def test_gemm_resident_b(G, M, N, K):
     C2 = G.gcn_gemm_f32(G.GCN_GEMM_NT, Ad, dev(Bt)[:, :K],
                         C=torch.empty((M, _ld4(N)), device="cuda:0")[:, :N])
     assert_close(host(C2), ref, S, what="NT")
+    C3 = G.gcn_gemm_f32(G.GCN_GEMM_NT, Ad, dev(Bt)[:, :K],
+                        C=torch.empty((M, _ld4(N)), device="cuda:0")[:, :N])
+    assert torch.equal(C2.view(torch.int32), C3.view(torch.int32)), "NT not bit-identical"
 
 
 @pytest.mark.parametrize("K,M,N", [(5, 3, 2), (8192, 100, 256), (20000, 256, 47),
