@@ -147,22 +147,60 @@ __global__ __launch_bounds__(kBlock) void k_ln_quantize(int64_t n, int F, const 
 // 16-byte aligned storage (ldx % 4 == 0): a slot of G lanes holds a whole row
 // (NV float4 per lane), so the row is read from memory once; a wavefront
 // holds 64 / G rows per group and R groups are loaded before any arithmetic.
-// Same values as k_ln_quantize: statistics in double (only their summation
-// order differs), values rounded once to fp32, codes from IEEE fp32
-// division.
-template <int G>
-__device__ inline double slot_sum(double v) {
-#pragma unroll
-  for (int off = 1; off < G; off <<= 1) v += __shfl_xor(v, off, 64);
-  return v;
+// The values of k_ln_quantize: statistics in double (their summation order
+// and the last ulps of double in 1 / sqrt(var + eps) differ), values rounded
+// once to fp32, the codes of IEEE fp32 division.
+//
+// A slot's butterfly pairs lanes within the slot: the partner at distance 1
+// and 2 comes from a quad permutation, at 4 and 8 from the mirror of the
+// half row and of the row (after the earlier steps every lane of a quad,
+// then of a half row, holds the same value, so the mirror partner carries
+// the same operand as lane ^ 4 or lane ^ 8), further ones from a wavefront
+// shuffle. The DPP moves need no LDS round trip; the sums are those of the
+// xor butterfly, bit for bit.
+template <int CTRL>
+__device__ inline int dpp_mov(int x) {
+  return __builtin_amdgcn_mov_dpp(x, CTRL, 0xF, 0xF, false);
 }
 
-template <int G>
+template <int OFF>
+__device__ inline int slot_partner(int x) {
+  if constexpr (OFF == 1) return dpp_mov<0xB1>(x);   // quad_perm [1, 0, 3, 2]
+  if constexpr (OFF == 2) return dpp_mov<0x4E>(x);   // quad_perm [2, 3, 0, 1]
+  if constexpr (OFF == 4) return dpp_mov<0x141>(x);  // row_half_mirror
+  if constexpr (OFF == 8) return dpp_mov<0x140>(x);  // row_mirror
+  return __shfl_xor(x, OFF, 64);
+}
+
+template <int OFF>
+__device__ inline float slot_partner(float v) {
+  return __int_as_float(slot_partner<OFF>(__float_as_int(v)));
+}
+
+template <int OFF>
+__device__ inline double slot_partner(double v) {
+  const long long b = __double_as_longlong(v);
+  const int lo = slot_partner<OFF>((int)b);
+  const int hi = slot_partner<OFF>((int)(b >> 32));
+  return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+
+template <int G, int OFF = 1>
+__device__ inline double slot_sum(double v) {
+  if constexpr (OFF < G) {
+    v += slot_partner<OFF>(v);
+    return slot_sum<G, 2 * OFF>(v);
+  } else {
+    return v;
+  }
+}
+
+template <int G, int OFF = 1>
 __device__ inline void slot_minmax(float& mn, float& mx) {
-#pragma unroll
-  for (int off = 1; off < G; off <<= 1) {
-    mn = fminf(mn, __shfl_xor(mn, off, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+  if constexpr (OFF < G) {
+    mn = fminf(mn, slot_partner<OFF>(mn));
+    mx = fmaxf(mx, slot_partner<OFF>(mx));
+    slot_minmax<G, 2 * OFF>(mn, mx);
   }
 }
 
@@ -174,13 +212,38 @@ __device__ inline uint32_t code_of(float a, float s, float levels) {
 // The same code from the row's correctly rounded reciprocal rs = RN(1 / S):
 // q = RN(a rs) is within one ulp of a / S, the residual a - q S is exact in
 // an fma, and RN(q + (a - q S) rs) is the correctly rounded quotient RN(a / S)
-// (Markstein's theorem for round-to-nearest division), so the code equals
-// code_of's. Valid while the residual cannot underflow where it matters:
-// S in [2^-100, 2^100] (quotients below 1/4 round to code 0 either way).
-__device__ inline uint32_t code_of_rcp(float a, float s, float rs, float levels) {
+// (Markstein's theorem for round-to-nearest division). Valid while the
+// residual cannot underflow where it matters: S in [2^-100, 2^100] (quotients
+// below 1/4 round to code 0 either way). Adding 1.5 * 2^23 then rounds the
+// quotient to an integer, half to even (the spacing of floats there is 1),
+// and leaves it in the low mantissa bits: the returned word is 0x4B400000 +
+// code, bits 8 to 21 clear, so a byte of it, or a 2-bit field shifted into a
+// byte, is the code. Clamping the sum to [1.5 * 2^23, 1.5 * 2^23 + levels]
+// keeps the quotient's range (a in [0, max - min], so RN(a / S) is at most
+// levels up to a rounding) and maps NaN to code 0, as the division form
+// does. A row with S = 0 passes rs = 0 and gets code 0.
+__device__ inline uint32_t code_word_rcp(float a, float s, float rs, float levels) {
+  constexpr float kMagic = 0x1.8p23f;
   const float q = a * rs;
   const float e = __builtin_fmaf(-q, s, a);
-  return (uint32_t)fminf(levels, fmaxf(0.0f, __builtin_rintf(__builtin_fmaf(e, rs, q))));
+  const float w = __builtin_fmaf(e, rs, q) + kMagic;
+  return __float_as_uint(fminf(kMagic + levels, fmaxf(kMagic, w)));
+}
+
+// 1 / sqrt(x) for finite x > 0: the hardware estimate refined by two Newton
+// steps on the residual e = 1 - x r^2 (r += r e / 2; each step squares the
+// relative error), a few ulps of double from the quotient of the correctly
+// rounded square root. The normalized values are rounded to fp32 afterwards,
+// so such an ulp decides a value only when its exact product lies within
+// about 2^-50 of a rounding boundary of fp32.
+__device__ inline double inv_sqrt(double x) {
+  double r = __builtin_amdgcn_rsq(x);
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const double e = __builtin_fma(-x * r, r, 1.0);
+    r = __builtin_fma(0.5 * r, e, r);
+  }
+  return r;
 }
 
 __device__ inline bool rcp_ok(float s) { return s >= 0x1p-100f && s <= 0x1p100f; }
@@ -244,18 +307,8 @@ __global__ __launch_bounds__(kBlock) void k_ln_quantize_v(QuantArgs a) {
     }
   };
   if (it >= n_iter) return;  // whole wavefronts leave together
-  float nxt[R][NV][4];
-  load(it, nxt);
   constexpr float levels = (float)((1 << (BITS > 0 ? BITS : 1)) - 1);
-  for (; it < n_iter; it += stride) {
-    float v[R][NV][4];
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-#pragma unroll
-      for (int j = 0; j < NV; ++j)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[r][j][e] = nxt[r][j][e];
-    if (it + stride < n_iter) load(it + stride, nxt);
+  auto process = [&](int64_t it, float (&v)[R][NV][4]) {
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const int64_t i = it * (E * R) + (int64_t)r * E + lane / G;
@@ -276,7 +329,7 @@ __global__ __launch_bounds__(kBlock) void k_ln_quantize_v(QuantArgs a) {
             d[j][e] = (double)v[r][j][e] - mean;
             if (inside(4 * (sl + j * G) + e)) var = __builtin_fma(d[j][e], d[j][e], var);
           }
-        const double inv = 1.0 / sqrt(slot_sum<G>(var) / (double)F + a.eps);
+        const double inv = inv_sqrt(slot_sum<G>(var) / (double)F + a.eps);
         if (BITS == 0 && a.rstd && live && sl == 0) a.rstd[i] = (float)inv;
 #pragma unroll
         for (int j = 0; j < NV; ++j)
@@ -319,7 +372,7 @@ __global__ __launch_bounds__(kBlock) void k_ln_quantize_v(QuantArgs a) {
             }
         slot_minmax<G>(mn, mx);
         const float s = (mx - mn) / levels;
-        const float rs = 1.0f / s;
+        const float rs = s != 0.0f ? 1.0f / s : 0.0f;
         // one path per wavefront: the reciprocal form while every live row's
         // scale allows it (almost always), IEEE division otherwise
         const bool fast = __all(!live || s == 0.0f || rcp_ok(s));
@@ -329,35 +382,65 @@ __global__ __launch_bounds__(kBlock) void k_ln_quantize_v(QuantArgs a) {
           a.scale[i * a.ldp] = s;
         }
         uint8_t* qr = a.q + i * a.ldq;
+        // the path is chosen once per row group: a choice per feature costs
+        // a branch per feature
+        auto write = [&](auto code) {
 #pragma unroll
-        for (int j = 0; j < NV; ++j) {
-          const int f = 4 * (sl + j * G);
-          if (!FULL && f >= F) continue;
-          uint32_t c[4];
+          for (int j = 0; j < NV; ++j) {
+            const int f = 4 * (sl + j * G);
+            if (!FULL && f >= F) continue;
+            // code words: the code in the low bits, bits 8 to 21 clear
+            uint32_t c[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float t = v[r][j][e] - mn;
-            const uint32_t cc = fast ? code_of_rcp(t, s, rs, levels) : code_of(t, s, levels);
-            c[e] = (inside(f + e) && s != 0.0f) ? cc : 0u;
+            for (int e = 0; e < 4; ++e) {
+              const uint32_t cc = code(v[r][j][e] - mn);
+              c[e] = inside(f + e) ? cc : 0u;
+            }
+            const bool whole = FULL || f + 4 <= F;
+            if constexpr (BITS == 2) {
+              qr[f / 4] = (uint8_t)(c[0] | (c[1] << 2) | (c[2] << 4) | (c[3] << 6));
+            } else {
+              if (whole && (FULL || a.q_dword))
+                *reinterpret_cast<uint32_t*>(qr + f) = (c[0] & 0xFFu) | ((c[1] & 0xFFu) << 8) |
+                                                       ((c[2] & 0xFFu) << 16) | (c[3] << 24);
+              else
+                for (int e = 0; e < 4 && f + e < F; ++e) qr[f + e] = (uint8_t)c[e];
+            }
+            if (a.y) {
+              float* yr = a.y + i * a.ldy;
+              if (whole && (FULL || a.y_vec))
+                *reinterpret_cast<float4*>(yr + f) = make_float4(v[r][j][0], v[r][j][1], v[r][j][2], v[r][j][3]);
+              else
+                for (int e = 0; e < 4 && f + e < F; ++e) yr[f + e] = v[r][j][e];
+            }
           }
-          const bool whole = FULL || f + 4 <= F;
-          if constexpr (BITS == 2) {
-            qr[f / 4] = (uint8_t)(c[0] | (c[1] << 2) | (c[2] << 4) | (c[3] << 6));
-          } else {
-            if (whole && (FULL || a.q_dword))
-              *reinterpret_cast<uint32_t*>(qr + f) = c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24);
-            else
-              for (int e = 0; e < 4 && f + e < F; ++e) qr[f + e] = (uint8_t)c[e];
-          }
-          if (a.y) {
-            float* yr = a.y + i * a.ldy;
-            if (whole && (FULL || a.y_vec))
-              *reinterpret_cast<float4*>(yr + f) = make_float4(v[r][j][0], v[r][j][1], v[r][j][2], v[r][j][3]);
-            else
-              for (int e = 0; e < 4 && f + e < F; ++e) yr[f + e] = v[r][j][e];
-          }
-        }
+        };
+        if (fast)
+          write([&](float t) { return code_word_rcp(t, s, rs, levels); });
+        else
+          write([&](float t) { return s != 0.0f ? code_of(t, s, levels) : 0u; });
       }
+    }
+  };
+  if constexpr (!LN) {
+    // one row group per wavefront (the grid covers the rows)
+    float v[R][NV][4];
+    load(it, v);
+    process(it, v);
+  } else {
+    // the walk, unrolled by two so that the prefetched group is worked on in
+    // the registers it was loaded into
+    float va[R][NV][4], vb[R][NV][4];
+    load(it, va);
+    for (;;) {
+      if (it + stride < n_iter) load(it + stride, vb);
+      process(it, va);
+      it += stride;
+      if (it >= n_iter) break;
+      if (it + stride < n_iter) load(it + stride, va);
+      process(it, vb);
+      it += stride;
+      if (it >= n_iter) break;
     }
   }
 }
@@ -375,11 +458,12 @@ void launch_v_full(const QuantArgs& a, hipStream_t s, dim3 grid) {
 
 // With LayerNorm a wavefront works on a row group long enough that the next
 // group's loads are best issued meanwhile: the grid is capped at 32
-// workgroups per CU and every wavefront walks several groups, prefetching
-// (measured on 4M x 128 rows, LayerNorm + Int2: 0.62 ms one group per
-// wavefront, 0.60 / 0.59 / 0.56 / 0.55 ms at 4 / 8 / 16 / 32 workgroups per
-// CU). Without it the one-pass grid with two groups loaded up front is faster
-// (Int2: 0.42 against 0.46 ms).
+// workgroups per CU and every wavefront walks several groups, prefetching.
+// Without it one group per wavefront over a grid that covers the rows is
+// fastest (4M x 128 rows, Int2: 0.404 ms with one group of 8 rows per
+// wavefront, 0.417 with two, 0.441 with four; 8-bit 0.470 / 0.498 / 0.500):
+// the kernels without LayerNorm take exactly one row group per wavefront and
+// rely on this grid covering every row.
 constexpr int64_t kQuantBlocksLN = 256 * 32;
 
 template <int G, int NV, int R>
@@ -421,10 +505,8 @@ bool try_vector(const QuantArgs& a, hipStream_t s, gcn_status* st) {
     *st = launch_v<8, 1, 2>(a, s);
   else if (a.F <= 64)
     *st = launch_v<8, 2, 2>(a, s);
-  else if (a.F <= 128 && a.ln)
-    *st = launch_v<8, 4, 1>(a, s);
   else if (a.F <= 128)
-    *st = launch_v<8, 4, 2>(a, s);
+    *st = launch_v<8, 4, 1>(a, s);
   else if (a.F <= 256)
     *st = launch_v<16, 4, 1>(a, s);
   else if (a.F <= 512)
