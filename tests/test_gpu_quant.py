@@ -75,6 +75,36 @@ def test_layernorm_quantize(G, bits, F):
     assert np.array_equal(s[same].view(np.uint32), Sr[same].view(np.uint32))
 
 
+@pytest.mark.parametrize("bits", [8, 2])
+@pytest.mark.parametrize("F", [128, 100])
+def test_quantize_special_values_bit_exact(G, bits, F):
+    # NaN features get code 0 on both sides (a NaN never wins the min or max
+    # of the row, and clamping maps it to 0); a row holding an infinite
+    # feature has an infinite scale, which the kernel quantizes by division;
+    # a constant row with NaNs has S = 0. NaNs stay off the first feature,
+    # where the oracle's running min and max would start from them.
+    note("quantize special values bits=%d F=%d" % (bits, F))
+    n = 600
+    X = synth.normal(310, n, F)
+    rng = np.random.default_rng(311)
+    for i in range(0, n, 3):
+        X[i, rng.integers(1, F, 3)] = np.nan
+    X[1, 5] = np.inf
+    X[4, 7] = -np.inf
+    X[7, 2], X[7, 9] = np.inf, -np.inf
+    X[10, 1:] = np.nan
+    X[13] = 0.25
+    X[13, 3] = np.nan
+    X[16, 1:] = 3.0e38  # the range overflows to +inf
+    X[16, 0] = -3.0e38
+    Q, Z, S = oracle.quantize_rows_bits(X, bits)
+    assert np.isinf(S[[1, 4, 7, 16]]).all() and S[10] == 0 and S[13] == 0
+    q, z, s = G.gcn_layernorm_quantize(dev(X), bits=bits, layernorm=False)
+    assert np.array_equal(host(z).view(np.uint32), Z.view(np.uint32))
+    assert np.array_equal(host(s).view(np.uint32), S.view(np.uint32))
+    assert np.array_equal(host(q), Q), "codes differ on %d rows" % np.any(host(q) != Q, axis=1).sum()
+
+
 def near_half_step_rows(seed, n, F, bits, scale_exp):
     """Rows whose values sit on and around the midpoints between codes: the
     row's minimum is 0 and its maximum (2^bits - 1) * S0, the others are
