@@ -912,12 +912,41 @@ __global__ __launch_bounds__(kThreads) void k_count_kept(int64_t n, const uint8_
   if ((threadIdx.x & 63) == 0 && b) atomicAdd(cnt, (unsigned long long)__popcll(b));
 }
 
-// One wavefront per row at a time (C <= 64 classes, lane = class), 16 rows
-// per wavefront: log-softmax with the row maximum subtracted, row losses
-// lse - z[y] added in row order in double, wavefront sums added in
-// wavefront order, and dz = (softmax - onehot(y)) / m, where m is the number
-// of rows in the loss (n, or *n_kept when skip is given; skipped rows get
-// dz = 0 and add nothing).
+// Partner of a lane at distance 1, 2, 4 or 8 within its row of 16 lanes:
+// quad permutations, then the mirrors of the half row and of the row. After
+// the earlier steps of a butterfly every lane of a quad (half row) holds the
+// same value, so the mirror partner carries the operand of lane ^ 4 (^ 8).
+template <int OFF>
+__device__ inline float row16_partner(float v) {
+  const int x = __float_as_int(v);
+  constexpr int kCtrl = OFF == 1 ? 0xB1 : OFF == 2 ? 0x4E : OFF == 4 ? 0x141 : 0x140;
+  return __int_as_float(__builtin_amdgcn_mov_dpp(x, kCtrl, 0xF, 0xF, false));
+}
+
+__device__ inline float row16_max(float v) {
+  v = fmaxf(v, row16_partner<1>(v));
+  v = fmaxf(v, row16_partner<2>(v));
+  v = fmaxf(v, row16_partner<4>(v));
+  return fmaxf(v, row16_partner<8>(v));
+}
+
+__device__ inline float row16_sum(float v) {
+  v += row16_partner<1>(v);
+  v += row16_partner<2>(v);
+  v += row16_partner<4>(v);
+  return v + row16_partner<8>(v);
+}
+
+// Softmax cross-entropy over C <= 16 NS classes. A row of 16 lanes holds one
+// row of logits (lane l: classes l, l + 16, ...), so a wavefront works on 4
+// rows at a time and its 16 rows in 4 steps, with every load of the 16 rows
+// issued before any arithmetic. Per row: log-softmax with the row maximum
+// subtracted, the loss lse - z[y] (z[y] read directly), and
+// dz = (softmax - onehot(y)) / m, where m is the number of rows in the loss
+// (n, or *n_kept when skip is given; skipped rows get dz = 0 and add
+// nothing). The row losses of a wavefront are added in row order in double,
+// the wavefront sums in wavefront order.
+template <int NS>
 __global__ __launch_bounds__(kThreads) void k_softmax_xent(int64_t n, int C,
                                                            const float* __restrict__ z, int64_t ldz,
                                                            const int32_t* __restrict__ y,
@@ -925,38 +954,66 @@ __global__ __launch_bounds__(kThreads) void k_softmax_xent(int64_t n, int C,
                                                            double* __restrict__ block_loss,
                                                            const uint8_t* __restrict__ skip,
                                                            const unsigned long long* __restrict__ n_kept) {
+  constexpr int kSteps = kSoftmaxRowsPerWave / 4;
   __shared__ double wl[kThreads / 64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int grp = lane >> 4, l = lane & 15;
+  const int64_t base = ((int64_t)blockIdx.x * (kThreads / 64) + w) * kSoftmaxRowsPerWave;
+  float v[kSteps][NS], zy[kSteps];
+  int32_t yl[kSteps];
+  bool use[kSteps];
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st) {
+    const int64_t i = base + 4 * st + grp;
+    const bool live = i < n;
+    use[st] = live && !(skip && skip[i]);
+    yl[st] = live ? y[i] : 0;  // labels lie in [0, C)
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      const int c = l + 16 * k;
+      v[st][k] = live && c < C ? z[i * ldz + c] : -INFINITY;
+    }
+  }
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st)
+    zy[st] = use[st] ? z[(base + 4 * st + grp) * ldz + yl[st]] : 0.f;
+  const float m_rows = skip ? (float)*n_kept : (float)n;
+  double rl[kSteps];
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st) {
+    const int64_t i = base + 4 * st + grp;
+    float m = v[st][0];
+#pragma unroll
+    for (int k = 1; k < NS; ++k) m = fmaxf(m, v[st][k]);
+    m = row16_max(m);
+    float ex[NS], s = 0.f;
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      ex[k] = l + 16 * k < C ? expf(v[st][k] - m) : 0.f;
+      s += ex[k];
+    }
+    s = row16_sum(s);
+    rl[st] = use[st] ? (double)(m + logf(s) - zy[st]) : 0.0;
+    if (i < n) {
+#pragma unroll
+      for (int k = 0; k < NS; ++k) {
+        const int c = l + 16 * k;
+        if (c < C) dz[i * ldd + c] = use[st] ? (ex[k] / s - (c == yl[st] ? 1.f : 0.f)) / m_rows : 0.f;
+      }
+    }
+  }
+  // row 4 st + g of the wavefront sits in lane row g at step st
   double wave_loss = 0.0;
-  for (int rr = 0; rr < kSoftmaxRowsPerWave; ++rr) {
-  const int64_t i = ((int64_t)blockIdx.x * (kThreads / 64) + w) * kSoftmaxRowsPerWave + rr;
-  double row_loss = 0.0;
-  if (i < n && skip && skip[i]) {
-    if (lane < C) dz[i * ldd + lane] = 0.f;
-  } else if (i < n) {
-    const float m_rows = skip ? (float)*n_kept : (float)n;
-    const float v = lane < C ? z[i * ldz + lane] : -INFINITY;
-    float m = v;
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
-    const float ex = lane < C ? expf(v - m) : 0.f;
-    float s = ex;
+  for (int st = 0; st < kSteps; ++st)
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-    const int32_t yi = y[i];  // labels lie in [0, C)
-    const float zy = __shfl(v, yi, 64);
-    const float lse = m + logf(s);
-    row_loss = (double)(lse - zy);
-    if (lane < C) dz[i * ldd + lane] = (ex / s - (lane == yi ? 1.f : 0.f)) / m_rows;
-  }
-  wave_loss += row_loss;
-  }
+    for (int g = 0; g < 4; ++g) wave_loss += __shfl(rl[st], 16 * g, 64);
   if (lane == 0) wl[w] = wave_loss;
   __syncthreads();
   if (threadIdx.x == 0) {
-    double s = 0.0;
-    for (int k = 0; k < kThreads / 64; ++k) s += wl[k];
-    block_loss[blockIdx.x] = s;
+    double t = 0.0;
+    for (int k = 0; k < kThreads / 64; ++k) t += wl[k];
+    block_loss[blockIdx.x] = t;
   }
 }
 
@@ -1289,8 +1346,20 @@ gcn_status softmax_xent(int64_t n, int C, const float* z, int64_t ldz, const int
   }
   if (e == hipSuccess) {
     ProfScope ps("softmax_xent", stream);
-    hipLaunchKernelGGL(k_softmax_xent, dim3((unsigned)nb), dim3(kThreads), 0, stream, n, C, z, ldz,
-                       y, dz, ldd, bl, skip, (const unsigned long long*)cnt);
+    const dim3 grid((unsigned)nb);
+    const unsigned long long* kept = cnt;
+    if (C <= 16)
+      hipLaunchKernelGGL(k_softmax_xent<1>, grid, dim3(kThreads), 0, stream, n, C, z, ldz, y, dz,
+                         ldd, bl, skip, kept);
+    else if (C <= 32)
+      hipLaunchKernelGGL(k_softmax_xent<2>, grid, dim3(kThreads), 0, stream, n, C, z, ldz, y, dz,
+                         ldd, bl, skip, kept);
+    else if (C <= 48)
+      hipLaunchKernelGGL(k_softmax_xent<3>, grid, dim3(kThreads), 0, stream, n, C, z, ldz, y, dz,
+                         ldd, bl, skip, kept);
+    else
+      hipLaunchKernelGGL(k_softmax_xent<4>, grid, dim3(kThreads), 0, stream, n, C, z, ldz, y, dz,
+                         ldd, bl, skip, kept);
     e = hipGetLastError();
   }
   if (e == hipSuccess) {
