@@ -166,7 +166,11 @@ def test_relu_and_backward(G):
     assert np.array_equal(host(dHd), np.where(H > 0, dH, 0).astype(np.float32))
 
 
-@pytest.mark.parametrize("n,C", [(1, 1), (5000, 47), (333, 64), (100, 2)])
+# class counts on both sides of each 16-class step of the kernel's lane
+# layout (16 lanes per row, C / 16 rounded up classes per lane), row counts
+# that leave a wavefront's 16 rows and a workgroup's 64 rows ragged
+@pytest.mark.parametrize("n,C", [(1, 1), (5000, 47), (333, 64), (100, 2), (1000, 16), (64, 17),
+                                 (777, 32), (129, 33), (2047, 48), (70, 49)])
 def test_softmax_xent(G, n, C):
     note("softmax xent n=%d C=%d" % (n, C))
     z = synth.normal(209, n, C) * 3
