@@ -242,6 +242,45 @@ def test_golden_hand_derived(name):
     assert np.array_equal(got.astype(np.float32), want.astype(np.float32))
 
 
+@pytest.mark.parametrize("name", ["path3_ahat.txt", "star3_ahat.txt"])
+def test_golden_degrees_and_listed_normalization(name):
+    # row_degrees counts the neighbours of the hand-derived graphs (the self-
+    # loop left out), and normalize_listed, given each entry's row degree and
+    # column degree, reproduces their hand-derived A_hat entries
+    edges, entries = _read_golden(name)
+    n = 1 + max(max(e) for e in edges)
+    want_deg = np.zeros(n, np.int32)
+    for a, b in edges:
+        want_deg[a] += 1
+        want_deg[b] += 1
+    src = np.array([e[0] for e in edges], np.int32)
+    dst = np.array([e[1] for e in edges], np.int32)
+    ptr, idx = oracle.structure(n, n, src, dst, SYM | LOOPS)
+    deg = oracle.row_degrees(ptr, idx)
+    assert np.array_equal(deg, want_deg)
+    rows = np.repeat(np.arange(n), np.diff(ptr))
+    val = oracle.normalize_listed(ptr, deg, deg[idx])
+    want = {(r, c): np.float32(v) for r, c, v in entries}
+    assert len(want) == len(idx)
+    for r, c, v in zip(rows, idx, val):
+        assert v == want[(int(r), int(c))], (r, c, v)
+
+
+def test_degrees_closed_forms():
+    # star: the centre has k neighbours, every leaf one; complete graph on m
+    # nodes: m - 1 each; drawn self-loops and duplicates count no neighbour
+    k, m = 300, 40
+    ptr, idx = oracle.structure(k + 1, k + 1, np.arange(1, k + 1, dtype=np.int32),
+                                np.zeros(k, np.int32), SYM | LOOPS)
+    deg = oracle.row_degrees(ptr, idx)
+    assert deg[0] == k and np.all(deg[1:] == 1)
+    u, v = np.triu_indices(m, 1)
+    src = np.concatenate([u, u, np.arange(m)]).astype(np.int32)
+    dst = np.concatenate([v, v, np.arange(m)]).astype(np.int32)
+    ptr, idx = oracle.structure(m, m, src, dst, SYM | LOOPS)
+    assert np.all(oracle.row_degrees(ptr, idx) == m - 1)
+
+
 # ---------------------------------------------------------------------------
 # Sampled rows agree with the whole-matrix route.
 # ---------------------------------------------------------------------------
