@@ -228,11 +228,15 @@ gcn_status gcn_softmax_xent(int64_t n, int64_t C, const float* logits, int64_t l
                             void* stream);
 
 /* One training step of a 2-layer GCN on a square graph (Section 2.1: each
- * layer aggregates, then applies a linear transform), in the order
- *   Z1 = X W1, H1 = relu(A_hat Z1), Z2 = H1 W2, logits = A_hat Z2,
+ * layer aggregates, then applies a linear transform):
+ *   H1 = relu(A_hat X W1), logits = A_hat (H1 W2),
  *   loss = mean softmax cross-entropy, then the exact backward:
- *   dZ2 = A_hat^T dlogits, dW2 = H1^T dZ2, dH1 = dZ2 W2^T masked by H1 > 0,
- *   dZ1 = A_hat^T dH1, dW1 = X^T dZ1.
+ *   dZ2 = A_hat^T dlogits, dW2 = H1^T dZ2, dZ1 = dZ2 W2^T masked by H1 > 0,
+ *   dW1 = (A_hat X)^T dZ1.
+ *  Layer 1 is evaluated as relu((A_hat X) W1) with dW1 = (A_hat X)^T dZ1 when
+ *  f_in <= hidden (the aggregation gathers the narrower rows and the backward
+ *  needs none), else as relu(A_hat (X W1)) with dW1 = X^T (A_hat^T dZ1). The
+ *  two agree up to fp32 rounding.
  *  X [n x f_in] (ldx), W1 [f_in x hidden], W2 [hidden x n_classes] (dense,
  *  row-major), labels int32 [n] in [0, n_classes), n_classes <= 64.
  *  Outputs: dW1, dW2 (same shapes as W1, W2), *loss (device double).

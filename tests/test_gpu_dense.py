@@ -226,6 +226,16 @@ def test_gcn_step_small(G):
     _step_check(G, w, 100, 256, 47, 11)
 
 
+def test_gcn_step_transform_first(G):
+    # f_in > hidden: layer 1 multiplies X W1 before aggregating, and its
+    # backward aggregates the gradient (the other association of the step)
+    note("gcn step transform first")
+    n = 2000
+    src, dst = synth.rmat_edges(213, n, 10 * n, perm_seed=214)
+    w = synth.Workload("rmat2000", n, n, src, dst, synth.SYMMETRIZE | synth.ADD_SELF_LOOPS, 300)
+    _step_check(G, w, 300, 64, 10, 12)
+
+
 def test_gcn_step_product_like(G):
     import gc
     import torch
