@@ -254,7 +254,9 @@ def run_sage_step(args):
     bins = G.gcn_graph_bins(g, 0)
     rows = sum(b["rows"] for b in bins)
     ents = sum(b["entries"] for b in bins)
-    agg_bytes = 2 * sum(model_bytes(rows, ents, 0, f) for f, _ in dims)  # forward + transposed
+    # forward + transposed per layer, each gathering the narrower of the layer's
+    # input and output (the class layer aggregates Y W_neigh, 47 wide)
+    agg_bytes = 2 * sum(model_bytes(rows, ents, 0, fo if fo < f else f) for f, fo in dims)
     out_json = {
         "metric": "3-layer GraphSAGE training step (fwd + bwd, LayerNorm, masked label "
                   "propagation), product-shaped graph",

@@ -18,6 +18,14 @@
 // (f >= 128) start Z on a 128-byte boundary and every row is a multiple of
 // 128 bytes, so the gathered rows of the aggregations touch no extra cache
 // line (a 516-float stride costs 28% at f = 256).
+//
+// A layer whose output is narrower than its input (the class layer, fo < f)
+// aggregates the narrower operand instead: since D^-1 A Y W_neigh =
+// D^-1 A (Y W_neigh), it computes T = Y W_neigh, writes M = D^-1 A T into the
+// middle block (fo wide) and packs [W_self; I; b; 0], so the same product
+// adds M. Its backward aggregates the fo-wide gradient: G = (D^-1 A)^T dO,
+// dY = [dO | G] [W_self | W_neigh]^T in one product, and the weight gradients
+// come from Y^T [dO | G].
 
 #include "common.h"
 
@@ -29,12 +37,13 @@ constexpr int kThreadsS = 256;
 inline int64_t round4(int64_t v) { return (v + 3) & ~int64_t(3); }
 
 // Columns of C below K that no kernel of the layer writes: [f, zo),
-// [zo + f, oc), the ones column oc and (oc, K).
+// [zo + zw, oc) (zw: the width of the middle block's data), the ones column
+// oc and (oc, K).
 __global__ __launch_bounds__(kThreadsS) void k_concat_tail(int64_t n, int64_t f, int64_t zo,
-                                                           int64_t oc, int64_t K,
+                                                           int64_t zw, int64_t oc, int64_t K,
                                                            float* __restrict__ c, int64_t ldc) {
-  const int64_t a = zo - f, b = oc - zo - f;  // the two padding runs
-  const int64_t per_row = K - 2 * f;
+  const int64_t a = zo - f, b = oc - zo - zw;  // the two padding runs
+  const int64_t per_row = K - f - zw;
   const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
   if (t >= n * per_row) return;
   const int64_t i = t / per_row, k = t % per_row;
@@ -42,16 +51,18 @@ __global__ __launch_bounds__(kThreadsS) void k_concat_tail(int64_t n, int64_t f,
   if (k < a)
     col = f + k;
   else if (k < a + b)
-    col = zo + f + (k - a);
+    col = zo + zw + (k - a);
   else
     col = oc + (k - a - b);
   c[i * ldc + col] = (col == oc) ? 1.f : 0.f;
 }
 
-// Wp [K x fop]: rows [0, f) = W_self, [zo, zo + f) = W_neigh, row oc = b,
+// Wp [K x fop]: rows [0, f) = W_self, [zo, zo + f) = W_neigh (or, when the
+// layer aggregates Y W_neigh, [zo, zo + fo) = the identity), row oc = b,
 // every other entry 0 (fo columns used of fop).
 __global__ __launch_bounds__(kThreadsS) void k_pack_weights(int64_t f, int64_t zo, int64_t oc,
                                                             int64_t K, int64_t fo, int64_t fop,
+                                                            bool ident,
                                                             const float* __restrict__ ws,
                                                             const float* __restrict__ wn,
                                                             const float* __restrict__ b,
@@ -63,12 +74,70 @@ __global__ __launch_bounds__(kThreadsS) void k_pack_weights(int64_t f, int64_t z
   if (c < fo) {
     if (r < f)
       v = ws[r * fo + c];
-    else if (r >= zo && r < zo + f)
+    else if (ident && r >= zo && r < zo + fo)
+      v = r - zo == c ? 1.f : 0.f;
+    else if (!ident && r >= zo && r < zo + f)
       v = wn[(r - zo) * fo + c];
     else if (r == oc)
       v = b[c];
   }
   wp[t] = v;
+}
+
+// dst [rows x ldd] = src [rows x cols] (ld lds) in the first cols columns,
+// 0 in the columns [cols, ldd).
+__global__ __launch_bounds__(kThreadsS) void k_pad_cols(int64_t rows, int64_t cols,
+                                                        const float* __restrict__ src, int64_t lds,
+                                                        float* __restrict__ dst, int64_t ldd) {
+  const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
+  if (t >= rows * ldd) return;
+  const int64_t r = t / ldd, c = t % ldd;
+  dst[t] = c < cols ? src[r * lds + c] : 0.f;
+}
+
+// B [f x 2 fop] = [W_self | 0 | W_neigh | 0] (the weights of the input
+// gradient of a layer that aggregates Y W_neigh: dY = [dO | G] B^T).
+__global__ __launch_bounds__(kThreadsS) void k_pack_bcat(int64_t f, int64_t fo, int64_t fop,
+                                                         const float* __restrict__ ws,
+                                                         const float* __restrict__ wn,
+                                                         float* __restrict__ bc) {
+  const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
+  if (t >= f * 2 * fop) return;
+  const int64_t r = t / (2 * fop), c = t % (2 * fop);
+  float v = 0.f;
+  if (c < fo)
+    v = ws[r * fo + c];
+  else if (c >= fop && c < fop + fo)
+    v = wn[r * fo + c - fop];
+  bc[t] = v;
+}
+
+// Zero the padding columns [fo, fop) and [fop + fo, 2 fop) of DG [n x 2 fop]
+// (the blocks dO and G of the input-gradient product's left operand).
+__global__ __launch_bounds__(kThreadsS) void k_zero_dg_pad(int64_t n, int64_t fo, int64_t fop,
+                                                           float* __restrict__ dg) {
+  const int64_t pad = fop - fo;
+  const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
+  if (t >= n * 2 * pad) return;
+  const int64_t i = t / (2 * pad), k = t % (2 * pad);
+  const int64_t col = k < pad ? fo + k : fop + fo + (k - pad);
+  dg[i * 2 * fop + col] = 0.f;
+}
+
+// dwp [f x 2 fop] = Y^T [dO | G] -> dW_self, dW_neigh (the bias comes from
+// the column sum of dO).
+__global__ __launch_bounds__(kThreadsS) void k_unpack_grads_tf(int64_t f, int64_t fo,
+                                                               int64_t fop,
+                                                               const float* __restrict__ dwp,
+                                                               float* __restrict__ dws,
+                                                               float* __restrict__ dwn) {
+  const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
+  if (t >= 2 * f * fo) return;
+  const int64_t r = t / fo, c = t % fo;
+  if (r < f)
+    dws[r * fo + c] = dwp[r * 2 * fop + c];
+  else
+    dwn[(r - f) * fo + c] = dwp[(r - f) * 2 * fop + fop + c];
 }
 
 // The inverse of k_pack_weights for the gradient.
@@ -185,9 +254,12 @@ inline unsigned blocks(int64_t work) {
 // Buffers of one layer.
 struct Layer {
   int64_t f = 0, fp = 0, zo = 0, oc = 0, K = 0, ldc = 0, fo = 0, fop = 0;
-  float* c = nullptr;     // [n x ldc] = [Y | Z | 1 000]
+  bool tf = false;        // fo < f: the layer aggregates Y W_neigh (M) instead of Y (Z)
+  float* c = nullptr;     // [n x ldc] = [Y | Z | 1 000] or [Y | M | 1 000]
   float* rstd = nullptr;  // [n]
   float* wp = nullptr;    // [K x fop]
+  float* wn = nullptr;    // tf: W_neigh padded to [f x fop]
+  float* bc = nullptr;    // tf: [W_self | 0 | W_neigh | 0], [f x 2 fop]
   float* o = nullptr;     // [n x fop] pre-activation; after ReLU the layer output
 };
 
@@ -196,8 +268,9 @@ inline int64_t round32(int64_t v) { return (v + 31) & ~int64_t(31); }
 void set_layout(Layer& y, int64_t f, int64_t fo) {
   y.f = f;
   y.fp = round4(f);
+  y.tf = fo < f;
   y.zo = f >= 128 ? round32(f) : y.fp;
-  y.oc = y.zo + y.fp;
+  y.oc = y.zo + (y.tf ? round4(fo) : y.fp);
   y.K = y.oc + 4;
   y.ldc = round32(y.K);
   y.fo = fo;
@@ -207,7 +280,8 @@ void set_layout(Layer& y, int64_t f, int64_t fo) {
 struct Sage {
   int64_t n = 0;
   Layer L[3];
-  float* xp = nullptr;  // input with label embeddings ([n x fp of layer 1])
+  float* xp = nullptr;    // input with label embeddings ([n x fp of layer 1])
+  float* tmid = nullptr;  // Y W_neigh of the layers that aggregate it
 };
 
 gcn_status check_args(const gcn_graph* g, const float* X, int64_t ldx, int64_t f_in,
@@ -236,9 +310,13 @@ gcn_status check_args(const gcn_graph* g, const float* X, int64_t ldx, int64_t f
 }
 
 void sage_free(Sage& m, hipStream_t s) {
+  tfree(m.tmid, s);
+  m.tmid = nullptr;
   tfree(m.xp, s);
   for (int l = 2; l >= 0; --l) {
     tfree(m.L[l].o, s);
+    tfree(m.L[l].bc, s);
+    tfree(m.L[l].wn, s);
     tfree(m.L[l].wp, s);
     tfree(m.L[l].rstd, s);
     tfree(m.L[l].c, s);
@@ -264,19 +342,34 @@ gcn_status sage_forward(const gcn_graph* g, const float* X, int64_t ldx, int64_t
     if (st == GCN_OK) st = talloc(&L[l].rstd, n, s, "LayerNorm 1/std");
     if (st == GCN_OK) st = talloc(&L[l].wp, L[l].K * L[l].fop, s, "packed weights");
     if (st == GCN_OK) st = talloc(&L[l].o, n * L[l].fop, s, "layer output");
+    if (st == GCN_OK && L[l].tf) st = talloc(&L[l].wn, L[l].f * L[l].fop, s, "padded W_neigh");
+    if (st == GCN_OK && L[l].tf) st = talloc(&L[l].bc, L[l].f * 2 * L[l].fop, s, "[W_self | W_neigh]");
   }
+  int64_t t_max = 0;
+  for (int l = 0; l < 3; ++l)
+    if (L[l].tf) t_max = std::max(t_max, n * L[l].fop);
+  if (st == GCN_OK && t_max > 0) st = talloc(&m.tmid, t_max, s, "Y W_neigh");
   if (st == GCN_OK && lp_mask) st = talloc(&m.xp, n * L[0].fp, s, "input with label embeddings");
   GCN_CHECK(st);
   // packed weights and the constant columns of each C
   for (int l = 0; l < 3; ++l) {
     Layer& y = L[l];
     hipLaunchKernelGGL(k_pack_weights, dim3(blocks(y.K * y.fop)), dim3(kThreadsS), 0, s, y.f,
-                       y.zo, y.oc, y.K, y.fo, y.fop, params[3 * l], params[3 * l + 1],
+                       y.zo, y.oc, y.K, y.fo, y.fop, y.tf, params[3 * l], params[3 * l + 1],
                        params[3 * l + 2], y.wp);
     GCN_HIP(hipGetLastError());
-    hipLaunchKernelGGL(k_concat_tail, dim3(blocks(n * (y.K - 2 * y.f))), dim3(kThreadsS), 0, s, n,
-                       y.f, y.zo, y.oc, y.K, y.c, y.ldc);
+    const int64_t zw = y.tf ? y.fo : y.f;  // columns of the middle block the layer writes
+    hipLaunchKernelGGL(k_concat_tail, dim3(blocks(n * (y.K - y.f - zw))), dim3(kThreadsS), 0, s, n,
+                       y.f, y.zo, zw, y.oc, y.K, y.c, y.ldc);
     GCN_HIP(hipGetLastError());
+    if (y.tf) {
+      hipLaunchKernelGGL(k_pad_cols, dim3(blocks(y.f * y.fop)), dim3(kThreadsS), 0, s, y.f, y.fo,
+                         params[3 * l + 1], y.fo, y.wn, y.fop);
+      GCN_HIP(hipGetLastError());
+      hipLaunchKernelGGL(k_pack_bcat, dim3(blocks(y.f * 2 * y.fop)), dim3(kThreadsS), 0, s, y.f,
+                         y.fo, y.fop, params[3 * l], params[3 * l + 1], y.bc);
+      GCN_HIP(hipGetLastError());
+    }
   }
   const float* h = X;
   int64_t ldh = ldx;
@@ -287,17 +380,46 @@ gcn_status sage_forward(const gcn_graph* g, const float* X, int64_t ldx, int64_t
     h = m.xp;
     ldh = L[0].fp;
   }
-  for (int l = 0; l < 3; ++l) {
+  for (int l = 0; l < 3 && st == GCN_OK; ++l) {
     Layer& y = L[l];
-    GCN_CHECK(layernorm_fwd(n, y.f, h, ldh, eps, y.c, y.ldc, y.rstd, s));
-    GCN_CHECK(aggregate_f32(g->csr, y.c, y.ldc, y.c + y.zo, y.ldc, y.f, false, s));
+    st = layernorm_fwd(n, y.f, h, ldh, eps, y.c, y.ldc, y.rstd, s);
+    if (st == GCN_OK && !y.tf) {
+      st = aggregate_f32(g->csr, y.c, y.ldc, y.c + y.zo, y.ldc, y.f, false, s);
+    } else if (st == GCN_OK) {
+      // M = D^-1 A (Y W_neigh): the aggregation gathers fo-wide rows
+      st = gemm_f32(GCN_GEMM_NN, n, y.fo, y.f, y.c, y.ldc, y.wn, y.fop, m.tmid, y.fop, s);
+      if (st == GCN_OK)
+        st = aggregate_f32(g->csr, m.tmid, y.fop, y.c + y.zo, y.ldc, y.fo, false, s);
+    }
     // the ReLU of layers 1 and 2 is applied as the product is stored
-    GCN_CHECK(gemm_f32(GCN_GEMM_NN, n, y.fop, y.K, y.c, y.ldc, y.wp, y.fop, y.o, y.fop, s,
-                       nullptr, 0, l < 2));
+    if (st == GCN_OK)
+      st = gemm_f32(GCN_GEMM_NN, n, y.fop, y.K, y.c, y.ldc, y.wp, y.fop, y.o, y.fop, s, nullptr, 0,
+                    l < 2);
     h = y.o;
     ldh = y.fop;
   }
+  return st;
+}
+
+gcn_status copy_rows(float* dst, int64_t ldd, const float* src, int64_t lds, int64_t n,
+                     int64_t cols, hipStream_t s) {
+  if (!dst || n == 0) return GCN_OK;
+  GCN_HIP(hipMemcpy2DAsync(dst, ldd * sizeof(float), src, lds * sizeof(float),
+                           cols * sizeof(float), n, hipMemcpyDeviceToDevice, s));
   return GCN_OK;
+}
+
+// dE = M^T dXp with M the one-hot rows of the embedded rows' labels (*part
+// receives M, released by the caller).
+gcn_status embed_grad(int64_t n, int C, int64_t f_in, const uint8_t* lp_mask,
+                      const int32_t* labels, const float* dxp, int64_t ldp, float* dE,
+                      float** part, hipStream_t s) {
+  const int64_t ldo = (C + 3) & ~int64_t(3);
+  GCN_CHECK(talloc(part, n * ldo, s, "label one-hot rows"));
+  hipLaunchKernelGGL(k_onehot, dim3(blocks(n * (ldo / 4))), dim3(kThreadsS), 0, s, n, C, ldo,
+                     lp_mask, labels, *part);
+  GCN_HIP(hipGetLastError());
+  return gemm_f32(GCN_GEMM_TN, C, f_in, n, *part, ldo, dxp, ldp, dE, f_in, s);
 }
 
 // Backward pass and loss after sage_forward.
@@ -313,13 +435,21 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
   const int64_t ld_dc = std::max(std::max(L[0].ldc, L[1].ldc), L[2].ldc);
   const int64_t ld_t = std::max(L[0].fp, L[1].fp);
   int64_t w_max = 0;
-  for (int l = 0; l < 3; ++l) w_max = std::max(w_max, L[l].K * L[l].fop);
+  for (int l = 0; l < 3; ++l) {
+    w_max = std::max(w_max, L[l].K * L[l].fop);
+    if (L[l].tf) w_max = std::max(w_max, L[l].f * 2 * L[l].fop);
+  }
+  // [dO | G] of each layer that aggregates Y W_neigh: read on both streams,
+  // so one buffer per layer
+  float* dgl[3] = {nullptr, nullptr, nullptr};
   gcn_status st = talloc(&dlogits, n * L[2].fop, s, "dlogits");
   if (st == GCN_OK) st = talloc(&dc, n * ld_dc, s, "dC");
   if (st == GCN_OK) st = talloc(&t, n * ld_t, s, "transposed aggregation");
   if (st == GCN_OK) st = talloc(&dwp, w_max, s, "packed weight gradient");
   if (st == GCN_OK)
     st = talloc(&colpart, n_colsum * std::max(L[1].fop, L[2].fop), s, "bias gradient partials");
+  for (int l = 0; l < 3 && st == GCN_OK; ++l)
+    if (L[l].tf) st = talloc(&dgl[l], n * 2 * L[l].fop, s, "[dO | G]");
   if (st == GCN_OK)
     st = softmax_xent(n, C, L[2].o, L[2].fop, labels, dlogits, L[2].fop, loss, s, lp_mask);
   // The weight gradients of a layer (product, bias sums, unpacking) read only
@@ -335,6 +465,56 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
   for (int l = 2; l >= 0 && st == GCN_OK; --l) {
     Layer& y = L[l];
     const bool input_grad = l > 0 || lp_mask;
+    if (y.tf) {
+      // DG = [dO | G] with G = (D^-1 A)^T dO, fo wide; padding columns zero
+      const int64_t ldg = 2 * y.fop;
+      float* dg = dgl[l];
+      hipLaunchKernelGGL(k_zero_dg_pad, dim3(blocks(n * 2 * (y.fop - y.fo))), dim3(kThreadsS), 0,
+                         s, n, y.fo, y.fop, dg);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) {
+        st = hip_fail(e, "k_zero_dg_pad", __FILE__, __LINE__);
+        break;
+      }
+      st = copy_rows(dg, ldg, dO, ld_do, n, y.fo, s);
+      if (st == GCN_OK) st = aggregate_f32(g->csc, dO, ld_do, dg + y.fop, ldg, y.fo, false, s);
+      if (st == GCN_OK) st = side.fork();  // DG is complete on s
+      if (st != GCN_OK) break;
+      // weight gradients on the side stream: [dW_self | dW_neigh] = Y^T DG, db = colsum dO
+      st = gemm_f32(GCN_GEMM_TN, y.f, ldg, n, y.c, y.ldc, dg, ldg, dwp, ldg, s2);
+      if (st != GCN_OK) break;
+      {
+        ProfScope ps("bias_grad", s2);
+        hipLaunchKernelGGL(k_colsum_partial,
+                           dim3((unsigned)n_colsum, (unsigned)ceil_div(y.fo, kThreadsS)),
+                           dim3(kThreadsS), 0, s2, n, y.fo, (const float*)dO, ld_do, colpart);
+        hipLaunchKernelGGL(k_colsum_reduce, dim3((unsigned)y.fo), dim3(kThreadsS), 0, s2,
+                           n_colsum, y.fo, (const float*)colpart, grads[3 * l + 2]);
+      }
+      hipLaunchKernelGGL(k_unpack_grads_tf, dim3(blocks(2 * y.f * y.fo)), dim3(kThreadsS), 0, s2,
+                         y.f, y.fo, y.fop, (const float*)dwp, grads[3 * l], grads[3 * l + 1]);
+      e = hipGetLastError();
+      if (e != hipSuccess) {
+        st = hip_fail(e, "tf layer gradients", __FILE__, __LINE__);
+        break;
+      }
+      if (!input_grad) break;
+      // dY = dO W_self^T + G W_neigh^T = DG [W_self | W_neigh]^T, then the LayerNorm backward
+      st = gemm_f32(GCN_GEMM_NT, n, y.f, ldg, dg, ldg, y.bc, ldg, dc, y.ldc, s);
+      if (st != GCN_OK) break;
+      if (l > 0) {
+        Layer& below = L[l - 1];
+        st = layernorm_bwd(n, y.f, y.c, y.ldc, y.rstd, dc, y.ldc, nullptr, 0, below.o, below.fop,
+                           below.o, below.fop, s);
+        dO = below.o;
+        ld_do = below.fop;
+        continue;
+      }
+      st = layernorm_bwd(n, y.f, y.c, y.ldc, y.rstd, dc, y.ldc, nullptr, 0, nullptr, 0, m.xp, y.fp,
+                         s);
+      if (st == GCN_OK) st = embed_grad(n, C, f_in, lp_mask, labels, m.xp, y.fp, dE, &part, s);
+      break;
+    }
     // dC = dO Wp^T; the input gradient of the layer is
     // dY = dC[:, Y block] + A^T dC[:, Z block], then the LayerNorm backward
     // dC over the Y and Z blocks only (the ones and padding columns are not read)
@@ -383,22 +563,14 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
       // label propagation: dXp, then the embedding gradient
       st = layernorm_bwd(n, y.f, y.c, y.ldc, y.rstd, dc, y.ldc, t, y.fp, nullptr, 0, m.xp, y.fp,
                          s);
-      const int64_t ldo = (C + 3) & ~int64_t(3);
-      if (st == GCN_OK) st = talloc(&part, n * ldo, s, "label one-hot rows");
-      if (st == GCN_OK) {
-        hipLaunchKernelGGL(k_onehot, dim3(blocks(n * (ldo / 4))), dim3(kThreadsS), 0, s, n,
-                           (int)C, ldo, lp_mask, labels, part);
-        e = hipGetLastError();
-        if (e != hipSuccess) st = hip_fail(e, "k_onehot", __FILE__, __LINE__);
-      }
-      if (st == GCN_OK)
-        st = gemm_f32(GCN_GEMM_TN, C, f_in, n, part, ldo, m.xp, y.fp, dE, f_in, s);
+      if (st == GCN_OK) st = embed_grad(n, C, f_in, lp_mask, labels, m.xp, y.fp, dE, &part, s);
     }
   }
   // the side work ends before its buffers are released on s
   const gcn_status sj = side.join();
   if (st == GCN_OK) st = sj;
   tfree(part, s);
+  for (int l = 2; l >= 0; --l) tfree(dgl[l], s);
   tfree(colpart, s);
   tfree(dwp, s);
   tfree(t, s);
@@ -407,13 +579,6 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
   return st;
 }
 
-gcn_status copy_rows(float* dst, int64_t ldd, const float* src, int64_t lds, int64_t n,
-                     int64_t cols, hipStream_t s) {
-  if (!dst || n == 0) return GCN_OK;
-  GCN_HIP(hipMemcpy2DAsync(dst, ldd * sizeof(float), src, lds * sizeof(float),
-                           cols * sizeof(float), n, hipMemcpyDeviceToDevice, s));
-  return GCN_OK;
-}
 
 }  // namespace
 }  // namespace gcn

@@ -18,6 +18,12 @@ built from it. The softmax gradient (p - onehot) / n_rows_in_loss has scale
 (p + onehot) / n_rows_in_loss. Forward values (the hidden outputs before
 their ReLU and the logits) have the scale |Y| |W_self| + |Z| |W_neigh| + |b|.
 
+A layer whose output is narrower than its input (fo < f, the class layer)
+is evaluated by the library as Y W_self + D^-1 A (Y W_neigh) + b: its middle
+terms are D^-1[i, s] Y[s, k] W_neigh[k, c], so |Z| = |D^-1 A Y| gives way to
+D^-1 A |Y| in the scales of its output and of dW_neigh (= Y^T (D^-1 A)^T dO).
+T(dY) is the same either way (magnitudes multiply associatively).
+
 The tests compare each element with |got - want| <= 1e-5 * scale: about 170
 units of fp32 roundoff per unit of scale. Both sides use the same ReLU
 patterns (the GPU's, after every unit where they differ from float64's has
@@ -38,14 +44,21 @@ def sage_step_scales(graph, params, labels, lp_mask, E, ref):
     scales of the two hidden layers' outputs before the ReLU) for the step
     the oracle ran in `ref` (oracle.sage_step)."""
     agg_t = lambda T: oracle._agg64(graph.csc_ptr, graph.csc_idx, graph.csc_val, T)
+    agg = lambda T: oracle._agg64(graph.csr_ptr, graph.csr_idx, graph.csr_val, T)
     P = [np.abs(np.asarray(p, np.float64)) for p in params]
+    # |Z| of the layers that aggregate Y, D^-1 A |Y| of those that aggregate Y W_neigh
+    zmag = []
+    for l in range(3):
+        Yl, _, Zl, _ = ref["saved"][l]
+        f, fo = np.shape(params[3 * l])
+        zmag.append(agg(np.abs(Yl)) if fo < f else np.abs(Zl))
     y = np.asarray(labels)
     n = len(y)
     m = None if lp_mask is None else np.asarray(lp_mask).astype(bool)
     fwd_scales = []
     for l in range(3):
-        Yl, _, Zl, _ = ref["saved"][l]
-        fwd_scales.append(np.abs(Yl) @ P[3 * l] + np.abs(Zl) @ P[3 * l + 1] + P[3 * l + 2])
+        Yl = ref["saved"][l][0]
+        fwd_scales.append(np.abs(Yl) @ P[3 * l] + zmag[l] @ P[3 * l + 1] + P[3 * l + 2])
     logits = ref["logits"]
     mx = logits.max(axis=1, keepdims=True)
     p = np.exp(logits - mx)
@@ -58,9 +71,9 @@ def sage_step_scales(graph, params, labels, lp_mask, E, ref):
     scales = [None] * 9
     T_dE = None
     for l in (2, 1, 0):
-        Yl, rstd, Zl, _ = ref["saved"][l]
+        Yl, rstd, _, _ = ref["saved"][l]
         scales[3 * l] = np.abs(Yl).T @ T
-        scales[3 * l + 1] = np.abs(Zl).T @ T
+        scales[3 * l + 1] = zmag[l].T @ T
         scales[3 * l + 2] = T.sum(axis=0)
         if l == 0 and m is None:
             break
