@@ -186,16 +186,18 @@ def test_blocked_bf16_and_relu_paths(G):
         assert_close(host(G.gcn_aggregate_fwd(g, dev(X))), *og.fwd(X), what="F=%d" % F)
 
 
-def test_blocked_gcn_step(G):
-    # the 2-layer GCN step (ReLU fused into the partial-row reduction) on a
-    # column-blocked graph
+@pytest.mark.parametrize("f_in,hidden,C", [(100, 256, 47), (300, 64, 10)])
+def test_blocked_gcn_step(G, f_in, hidden, C):
+    # the 2-layer GCN step on a column-blocked graph, in both associations of
+    # layer 1: the inputs aggregated first (f_in <= hidden), and X W1
+    # aggregated with the ReLU fused into the partial-row reduction
     from test_gpu_dense import _step_check
-    note("blocked gcn step")
+    note("blocked gcn step f_in=%d hidden=%d" % (f_in, hidden))
     n = 3000
     src, dst = synth.rmat_edges(395, n, 12 * n, perm_seed=396)
-    w = synth.Workload("rmat3000", n, n, src, dst, SYM | LOOPS, 100)
+    w = synth.Workload("rmat3000", n, n, src, dst, SYM | LOOPS, f_in)
     with plan_env(GCN_BLOCK_MIN_COLS=0, GCN_COL_BLOCKS=16, GCN_SEGMENT_MIN=8):
-        _step_check(G, w, 100, 256, 47, 13)
+        _step_check(G, w, f_in, hidden, C, 13)
 
 
 @pytest.mark.parametrize("lp", [False, True])
