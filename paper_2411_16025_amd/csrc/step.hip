@@ -72,11 +72,6 @@ extern "C" gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t 
   if (st == GCN_OK) st = softmax_xent(n, (int)n_classes, lg, ldc, labels, dl, ldc, loss, s);
   // backward
   if (st == GCN_OK) st = aggregate_f32(g->csc, dl, ldc, dz2, ldc, n_classes, false, s);
-  // dH1 = dZ2 W2^T with the ReLU mask (H1 > 0) applied as it is stored: with
-  // the aggregation first this is already dZ1 (the gradient at P W1)
-  dh1 = agg_first ? dz1 : p;  // (X W1 is dead after the first aggregation)
-  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NT, n, hidden, n_classes, dz2, ldc, w2p, ldc, dh1, ldh,
-                                  s, h1, ldh);
   // dW2 = H1^T dZ2 reads only H1 and dZ2: on the side stream it overlaps the
   // rest of the backward
   SideWork side;
@@ -84,6 +79,11 @@ extern "C" gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t 
   if (st == GCN_OK) st = side.fork();
   if (st == GCN_OK) st = gemm_f32(GCN_GEMM_TN, hidden, n_classes, n, h1, ldh, dz2, ldc, dW2,
                                   n_classes, side.side);
+  // dH1 = dZ2 W2^T with the ReLU mask (H1 > 0) applied as it is stored: with
+  // the aggregation first this is already dZ1 (the gradient at P W1)
+  dh1 = agg_first ? dz1 : p;  // (X W1 is dead after the first aggregation)
+  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NT, n, hidden, n_classes, dz2, ldc, w2p, ldc, dh1, ldh,
+                                  s, h1, ldh);
   if (agg_first) {
     // dW1 = P^T dZ1
     if (st == GCN_OK) st = gemm_f32(GCN_GEMM_TN, f_in, hidden, n, p, ldp, dz1, ldh, dW1, hidden, s);
