@@ -306,7 +306,10 @@ gcn_status gcn_sage3_forward(const gcn_graph* g, const float* X, int64_t ldx, in
  * propagation (Section 6.1 step 1, Lemma 2). Layer l (l = 1, 2, 3):
  *   Y = LayerNorm(H) (as gcn_layernorm_fwd), Z = A Y with the graph's values
  *   (after gcn_normalize_mean: the neighbour mean), O = Y W_self + Z W_neigh + b,
- *   H = relu(O) for l = 1, 2; the logits are O of layer 3.
+ *   H = relu(O) for l = 1, 2; the logits are O of layer 3. A layer whose output
+ *   is narrower than its input evaluates Z W_neigh as A (Y W_neigh), so that
+ *   its aggregations (forward and backward) gather the narrower rows; the two
+ *   agree up to fp32 rounding.
  * Loss: mean softmax cross-entropy over the rows that count (all rows, or
  * those with lp_mask = 0). Label propagation: rows with lp_mask = 1 get E[label]
  * added to their input features and are left out of the loss. Dropout is not
