@@ -236,6 +236,16 @@ def test_gcn_step_transform_first(G):
     _step_check(G, w, 300, 64, 10, 12)
 
 
+def test_gcn_step_unaligned_inputs(G):
+    # f_in = 101: X rows are not 16-byte aligned, so layer 1 aggregates them
+    # on the scalar path before its product (P is stored padded to 104)
+    note("gcn step unaligned inputs")
+    n = 2000
+    src, dst = synth.rmat_edges(215, n, 10 * n, perm_seed=216)
+    w = synth.Workload("rmat2000", n, n, src, dst, synth.SYMMETRIZE | synth.ADD_SELF_LOOPS, 101)
+    _step_check(G, w, 101, 128, 10, 14)
+
+
 def test_gcn_step_product_like(G):
     import gc
     import torch
