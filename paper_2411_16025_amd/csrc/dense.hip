@@ -974,9 +974,11 @@ __global__ __launch_bounds__(kThreads) void k_softmax_xent(int64_t n, int C,
       v[st][k] = live && c < C ? z[i * ldz + c] : -INFINITY;
     }
   }
+  // z[y] of each row; the index is clamped to the row so that a label outside
+  // [0, C) (a broken precondition) gives a wrong loss, never a read outside z
 #pragma unroll
   for (int st = 0; st < kSteps; ++st)
-    zy[st] = use[st] ? z[(base + 4 * st + grp) * ldz + yl[st]] : 0.f;
+    zy[st] = use[st] ? z[(base + 4 * st + grp) * ldz + min(max(yl[st], 0), C - 1)] : 0.f;
   const float m_rows = skip ? (float)*n_kept : (float)n;
   double rl[kSteps];
 #pragma unroll
