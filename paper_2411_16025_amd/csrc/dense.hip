@@ -851,7 +851,7 @@ __global__ __launch_bounds__(kThreads) void k_sum_partials(int64_t M, int64_t N,
                                                            const float* __restrict__ part,
                                                            float* __restrict__ C, int64_t ldc) {
   __shared__ float red[kThreads / 64][64];
-  constexpr int kW = kThreads / 64, U = 4;
+  constexpr int kW = kThreads / 64, U = 16;
   const int lane = threadIdx.x & 63, g = threadIdx.x >> 6;
   const int64_t e = (int64_t)blockIdx.x * 64 + lane;
   const int64_t MN = M * N;
