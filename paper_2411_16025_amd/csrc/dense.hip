@@ -735,7 +735,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_gemm_tn_v(int64_t M, int64_t N, 
 
 // C[m][n] = sum over chunks of part[chunk][m][n] in a fixed order: a
 // workgroup takes 64 consecutive elements; its wavefront g adds chunks g,
-// g + 4, g + 8, ... in turn (4 loads in flight), and the four sums are added
+// g + 4, g + 8, ... in turn (16 loads in flight), and the four sums are added
 // in wavefront order.
 // Streaming partial C = A^T B (the weight gradients: K = nodes, C at most a
 // few hundred square) without LDS or barriers. A wavefront owns a 64 x 16 NB
