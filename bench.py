@@ -90,9 +90,12 @@ def code_bytes(F, bits=8):
 
 
 def model_bytes(rows, entries, halo_entries, F, bits=8):
-    """Minimum traffic: row pointer (8 B/row), column + value (8 B/entry),
-    gathered rows (4F B for fp32; the code bytes + 8 B for a quantized halo
-    row with its min and scale), output rows (4F B)."""
+    """Modeled bytes of one pass with no reuse of gathered rows: row pointer
+    (8 B/row), column + value (8 B/entry), every gathered row at full cost (4F B
+    for fp32; the code bytes + 8 B for a quantized halo row with its min and
+    scale), output rows (4F B). Rows gathered more than once are charged each
+    time, so this exceeds the compulsory bytes and a rate over it can exceed
+    the HBM peak; the counted fabric bytes are the physical figure."""
     local = entries - halo_entries
     return (8 * rows + 8 * entries + 4 * F * local + (code_bytes(F, bits) + 8) * halo_entries
             + 4 * F * rows)
