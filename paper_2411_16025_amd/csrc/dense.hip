@@ -24,6 +24,7 @@
 
 #include <algorithm>
 #include <mutex>
+#include <type_traits>
 
 #include "common.h"
 
@@ -733,10 +734,6 @@ __global__ __launch_bounds__(WAVES * 64) void k_gemm_tn_v(int64_t M, int64_t N, 
   }
 }
 
-// C[m][n] = sum over chunks of part[chunk][m][n] in a fixed order: a
-// workgroup takes 64 consecutive elements; its wavefront g adds chunks g,
-// g + 4, g + 8, ... in turn (16 loads in flight), and the four sums are added
-// in wavefront order.
 // Streaming partial C = A^T B (the weight gradients: K = nodes, C at most a
 // few hundred square) without LDS or barriers. A wavefront owns a 64 x 16 NB
 // tile of C and one K chunk. Lane (g = l / 16, x = l % 16) loads, for rows
@@ -847,6 +844,10 @@ __global__ __launch_bounds__(512) void k_gemm_tn_s(int64_t M, int64_t N, int64_t
       }
 }
 
+// C[m][n] = sum over chunks of part[chunk][m][n] in a fixed order: a
+// workgroup takes 64 consecutive elements; its wavefront g adds chunks g,
+// g + 4, g + 8, ... in turn (16 loads in flight), and the four sums are added
+// in wavefront order.
 __global__ __launch_bounds__(kThreads) void k_sum_partials(int64_t M, int64_t N, int64_t n_chunks,
                                                            const float* __restrict__ part,
                                                            float* __restrict__ C, int64_t ldc) {
@@ -874,6 +875,257 @@ __global__ __launch_bounds__(kThreads) void k_sum_partials(int64_t M, int64_t N,
 #pragma unroll
     for (int w = 1; w < kW; ++w) t += red[w][lane];
     C[(e / N) * ldc + (e % N)] = t;
+  }
+}
+
+// Backward of GCN layer 1 when it aggregates first (H1 = relu(P W1),
+// P = A_hat X, Z2 = H1 W2), fused over one chunk of rows:
+//   dZ1 = (dZ2 W2^T) masked by H1 > 0,   dW1 += P^T dZ1,   dW2 += H1^T dZ2.
+// dZ1 never leaves the registers: of the three separate products (dZ1 stored,
+// then read back by P^T dZ1 beside a second pass over H1 for H1^T dZ2) only
+// the operand reads remain.
+//
+// Workgroup (chunk, hidden slice of 128 columns), one wavefront per SIMD
+// (the accumulators and two groups of operands take about 280 registers);
+// wavefront w owns the two 16-column blocks hs + 32 w + 16 hb (hb = 0, 1) of
+// the hidden layer and walks the chunk in groups of 16 rows r0 ... r0 + 15.
+// Lane (g = l / 16,
+// x = l % 16), per group:
+//  * dH1 block hb = dZ2[r0 .. r0 + 15] W2^T: the A operand is a 16-byte piece
+//    dZ2[r0 + x][16 j + 4 g .. + 3] (step i of chunk j contracts over class
+//    16 j + 4 g + i), the B operand W2[col][16 j + 4 g + i] is kept in
+//    registers for the whole kernel; classes past C are zero on both sides.
+//    Result element i is dH1[r0 + 4 g + i][col], col = hs + 32 w + 16 hb + x.
+//  * dZ1 = that element where H1[r0 + 4 g + i][col] > 0, else 0.
+//  * The result layout is the B operand layout of a product contracting
+//    over the rows r0 + 4 g + i (g = 0 .. 3) at step i: dZ1 element i is the
+//    B operand of P^T dZ1 (A operand P[r0 + 4 g + i][16 b + x], one per
+//    16-row block b of dW1), and the H1 value read for the mask is the A
+//    operand of H1^T dZ2 (B operand dZ2[r0 + 4 g + i][16 c + x]).
+// The next group's operands are loaded while the current one is multiplied.
+// Columns past f_in, hidden or C read a valid column of their row and reach
+// only outputs that are not stored; rows past the chunk are zero. Chunk
+// partials go to part1 [chunks][f_in][hidden] and part2 [chunks][hidden][C],
+// summed in chunk order by k_sum_partials.
+struct Bwd1Args {
+  int64_t n, split;
+  int f_in, hidden, C;
+  const float* P;
+  int64_t ldp;
+  const float* H1;
+  int64_t ldh;
+  const float* dZ2;
+  int64_t ldc;
+  const float* W2;  // [hidden][ldw], 16-byte aligned rows
+  int64_t ldw;
+  float* part1;
+  float* part2;
+};
+
+template <int MB, int CB>
+struct Bwd1Ops {
+  f4 az[CB];      // dZ2[r0 + x][16 j + 4 g ...]
+  float h[2][4];  // H1[r0 + 4 g + i][col(hb)]
+  float p[MB][4]; // P[r0 + 4 g + i][16 b + x]
+  float z[CB][4]; // dZ2[r0 + 4 g + i][16 c + x]
+};
+
+constexpr int kBwd1Waves = 4;
+
+template <int MB, int CB>
+__global__ __launch_bounds__(64 * kBwd1Waves) void k_gcn_bwd1(Bwd1Args a) {
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int hs = (int)blockIdx.y * (32 * kBwd1Waves) + 32 * w;
+  if (hs >= a.hidden) return;
+  const int g = lane >> 4, x = lane & 15;
+  const int64_t kb = (int64_t)blockIdx.x * a.split;
+  const int64_t ke = min(a.n, kb + a.split);
+  int hcol[2];
+#pragma unroll
+  for (int hb = 0; hb < 2; ++hb) hcol[hb] = min(hs + 16 * hb + x, a.hidden - 1);
+  // W2^T operands: class 16 j + 4 g + i of hidden unit hcol[hb] (classes
+  // past C read an in-row piece and are zeroed)
+  f4 wt[2][CB];
+#pragma unroll
+  for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+    for (int j = 0; j < CB; ++j) {
+      const int k0 = 16 * j + 4 * g;
+      f4 v = *reinterpret_cast<const f4*>(a.W2 + (int64_t)hcol[hb] * a.ldw +
+                                          min(k0, (int)a.ldw - 4));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = k0 + e < a.C ? v[e] : 0.f;
+      wt[hb][j] = v;
+    }
+  int pcol[MB], zcol[CB], acol[CB];
+#pragma unroll
+  for (int b = 0; b < MB; ++b) pcol[b] = min(16 * b + x, a.f_in - 1);
+#pragma unroll
+  for (int c = 0; c < CB; ++c) zcol[c] = min(16 * c + x, a.C - 1);
+#pragma unroll
+  for (int j = 0; j < CB; ++j) acol[j] = min(16 * j + 4 * g, (int)a.ldc - 4);
+  // lane byte offsets from a group's first row r0, the same for every whole
+  // group: rows r0 + 4 g + i start at the wave-uniform row r0 + i (32-bit
+  // offsets on a wave-uniform base: one register per load)
+  uint32_t oh[2], op[MB], oz[CB], oa[CB];
+#pragma unroll
+  for (int hb = 0; hb < 2; ++hb) oh[hb] = (uint32_t)(4 * (4 * g * a.ldh + hcol[hb]));
+#pragma unroll
+  for (int b = 0; b < MB; ++b) op[b] = (uint32_t)(4 * (4 * g * a.ldp + pcol[b]));
+#pragma unroll
+  for (int c = 0; c < CB; ++c) oz[c] = (uint32_t)(4 * (4 * g * a.ldc + zcol[c]));
+#pragma unroll
+  for (int j = 0; j < CB; ++j) oa[j] = (uint32_t)(4 * (x * a.ldc + acol[j]));
+  auto at = [](const float* base, uint32_t off) __attribute__((always_inline)) {
+    return reinterpret_cast<const char*>(base) + off;
+  };
+  // operands of the 16 rows from r0; without FULL, rows at or past ke are
+  // zero (the chunk's last, partial group)
+  auto load = [&](auto full_t, int64_t r0, Bwd1Ops<MB, CB>& o) __attribute__((always_inline)) {
+    constexpr bool FULL = decltype(full_t)::value;
+    // the pieces of dZ2 are stored as loaded: their classes past C are
+    // zeroed where they are used (a select here would wait for the load)
+    if constexpr (FULL) {
+      const float* za = a.dZ2 + r0 * a.ldc;
+#pragma unroll
+      for (int j = 0; j < CB; ++j) o.az[j] = *reinterpret_cast<const f4*>(at(za, oa[j]));
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float* hr = a.H1 + (r0 + i) * a.ldh;
+        const float* pr = a.P + (r0 + i) * a.ldp;
+        const float* zr = a.dZ2 + (r0 + i) * a.ldc;
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb) o.h[hb][i] = *reinterpret_cast<const float*>(at(hr, oh[hb]));
+#pragma unroll
+        for (int b = 0; b < MB; ++b) o.p[b][i] = *reinterpret_cast<const float*>(at(pr, op[b]));
+#pragma unroll
+        for (int c = 0; c < CB; ++c) o.z[c][i] = *reinterpret_cast<const float*>(at(zr, oz[c]));
+      }
+    } else {
+      // rows past the chunk: a zero piece (whose classes are then all
+      // dropped) and zero operands
+      const int64_t ra = min(r0 + x, ke - 1);
+      const bool live_a = r0 + x < ke;
+#pragma unroll
+      for (int j = 0; j < CB; ++j) {
+        const f4 v = *reinterpret_cast<const f4*>(a.dZ2 + ra * a.ldc + acol[j]);
+        o.az[j] = live_a ? v : f4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t r = min(r0 + 4 * g + i, ke - 1);
+        const bool live = r0 + 4 * g + i < ke;
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb) {
+          const float v = a.H1[r * a.ldh + hcol[hb]];
+          o.h[hb][i] = live ? v : 0.f;
+        }
+#pragma unroll
+        for (int b = 0; b < MB; ++b) {
+          const float v = a.P[r * a.ldp + pcol[b]];
+          o.p[b][i] = live ? v : 0.f;
+        }
+#pragma unroll
+        for (int c = 0; c < CB; ++c) {
+          const float v = a.dZ2[r * a.ldc + zcol[c]];
+          o.z[c][i] = live ? v : 0.f;
+        }
+      }
+    }
+  };
+  f4 acc1[MB][2], acc2[2][CB];
+#pragma unroll
+  for (int b = 0; b < MB; ++b)
+#pragma unroll
+    for (int hb = 0; hb < 2; ++hb) acc1[b][hb] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+    for (int c = 0; c < CB; ++c) acc2[hb][c] = f4{0.f, 0.f, 0.f, 0.f};
+  auto mma = [&](const Bwd1Ops<MB, CB>& o) __attribute__((always_inline)) {
+    // classes past C are zero on both sides of dZ2 W2^T (dZ2's padding may
+    // hold anything)
+    f4 azc[CB];
+#pragma unroll
+    for (int j = 0; j < CB; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) azc[j][e] = 16 * j + 4 * g + e < a.C ? o.az[j][e] : 0.f;
+    float dz[2][4];
+#pragma unroll
+    for (int hb = 0; hb < 2; ++hb) {
+      f4 d = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < CB; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          d = __builtin_amdgcn_mfma_f32_16x16x4f32(azc[j][i], wt[hb][j][i], d, 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dz[hb][i] = o.h[hb][i] > 0.f ? d[i] : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int b = 0; b < MB; ++b)
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb)
+          acc1[b][hb] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.p[b][i], dz[hb][i], acc1[b][hb],
+                                                             0, 0, 0);
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+        for (int c = 0; c < CB; ++c)
+          acc2[hb][c] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.h[hb][i], o.z[c][i], acc2[hb][c],
+                                                             0, 0, 0);
+    }
+  };
+  using Full = std::integral_constant<bool, true>;
+  using Part = std::integral_constant<bool, false>;
+  const int64_t nf = (ke - kb) / 16;  // whole groups
+  if (nf > 0) {
+    // two operand sets in turn: while one group is multiplied the next one's
+    // operands load (the last group again where none is left: loaded, unused)
+    Bwd1Ops<MB, CB> o0, o1;
+    load(Full{}, kb, o0);
+    int64_t t = 0;
+    for (; t + 2 <= nf; t += 2) {
+      load(Full{}, kb + 16 * (t + 1), o1);
+      __builtin_amdgcn_sched_barrier(0);  // keep each load set ahead of its use
+      mma(o0);
+      __builtin_amdgcn_sched_barrier(0);
+      load(Full{}, kb + 16 * min(t + 2, nf - 1), o0);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(o1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (t < nf) mma(o0);
+  }
+  if (kb + 16 * nf < ke) {
+    Bwd1Ops<MB, CB> o;
+    load(Part{}, kb + 16 * nf, o);
+    mma(o);
+  }
+  // element i of acc1[b][hb]: dW1[16 b + 4 g + i][hs + 16 hb + x];
+  // element i of acc2[hb][c]: dW2[hs + 16 hb + 4 g + i][16 c + x]
+  float* o1 = a.part1 + (int64_t)blockIdx.x * a.f_in * a.hidden;
+  float* o2 = a.part2 + (int64_t)blockIdx.x * a.hidden * a.C;
+#pragma unroll
+  for (int hb = 0; hb < 2; ++hb) {
+    const int col = hs + 16 * hb + x;
+#pragma unroll
+    for (int b = 0; b < MB; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = 16 * b + 4 * g + i;
+        if (m < a.f_in && col < a.hidden) o1[(int64_t)m * a.hidden + col] = acc1[b][hb][i];
+      }
+#pragma unroll
+    for (int c = 0; c < CB; ++c)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = hs + 16 * hb + 4 * g + i, cls = 16 * c + x;
+        if (m < a.hidden && cls < a.C) o2[(int64_t)m * a.C + cls] = acc2[hb][c][i];
+      }
   }
 }
 
@@ -1301,6 +1553,70 @@ gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int
   GCN_HIP(hipGetLastError());
   if (mask && !vec) GCN_CHECK(relu_bwd(M, N, mask, ldm, C, ldc, stream));
   if (relu && !vec) GCN_CHECK(relu_fwd(M, N, C, ldc, stream));
+  return GCN_OK;
+}
+
+#ifndef GCN_BWD1_FUSED
+#define GCN_BWD1_FUSED 1
+#endif
+// Workgroups of the fused layer-1 backward (chunks x hidden slices): one per
+// CU (its registers fill the CU), a fixed count so that the summation order
+// does not depend on the device.
+constexpr int64_t kBwd1Blocks = 256;
+
+bool layer1_bwd_fusable(int64_t f_in, int64_t hidden, int64_t C, const float* dZ2, int64_t ldc,
+                        const float* W2, int64_t ldw) {
+  return GCN_BWD1_FUSED && f_in >= 1 && f_in <= 112 && hidden >= 1 && C >= 1 && C <= 48 &&
+         ldc >= C && ldw >= C && aligned16(dZ2, ldc) && aligned16(W2, ldw);
+}
+
+gcn_status layer1_bwd_fused(int64_t n, int64_t f_in, int64_t hidden, int64_t C, const float* P,
+                            int64_t ldp, const float* H1, int64_t ldh, const float* dZ2,
+                            int64_t ldc, const float* W2, int64_t ldw, float* dW1, float* dW2,
+                            hipStream_t stream) {
+  if (!layer1_bwd_fusable(f_in, hidden, C, dZ2, ldc, W2, ldw)) {
+    set_error("fused layer-1 backward: unsupported shape or alignment");
+    return GCN_EINVAL;
+  }
+  const int64_t slices = ceil_div(hidden, (int64_t)32 * kBwd1Waves);
+  const int64_t want = std::max<int64_t>(1, kBwd1Blocks / slices);
+  const int64_t split = std::max<int64_t>(16, ceil_div(ceil_div(n, want), (int64_t)16) * 16);
+  const int64_t chunks = ceil_div(n, split);  // 0 without rows: the sums write zeros
+  const int waves = (int)std::min<int64_t>(kBwd1Waves, ceil_div(hidden, (int64_t)32));
+  float* part = nullptr;
+  GCN_CHECK(talloc(&part, std::max<int64_t>(1, chunks) * (f_in * hidden + hidden * C), stream,
+                   "layer-1 partials"));
+  Bwd1Args a{n, split, (int)f_in, (int)hidden, (int)C, P, ldp, H1, ldh, dZ2, ldc, W2, ldw,
+             part, part + chunks * f_in * hidden};
+  {
+    ProfScope ps("gemm_layer1_bwd_fused", stream);
+    const dim3 grid((unsigned)std::max<int64_t>(1, chunks), (unsigned)slices), block(64 * waves);
+    const int mb = f_in <= 32 ? 2 : (f_in <= 64 ? 4 : 7);
+    const int cb = (int)ceil_div(C, (int64_t)16);
+#define GCN_BWD1(MB_, CB_) \
+  if (mb == MB_ && cb == CB_) hipLaunchKernelGGL((k_gcn_bwd1<MB_, CB_>), grid, block, 0, stream, a)
+    GCN_BWD1(2, 1); GCN_BWD1(2, 2); GCN_BWD1(2, 3);
+    GCN_BWD1(4, 1); GCN_BWD1(4, 2); GCN_BWD1(4, 3);
+    GCN_BWD1(7, 1); GCN_BWD1(7, 2); GCN_BWD1(7, 3);
+#undef GCN_BWD1
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) {
+      tfree(part, stream);
+      return hip_fail(e, "k_gcn_bwd1", __FILE__, __LINE__);
+    }
+  }
+  {
+    ProfScope ps("gemm_sum_partials", stream);
+    hipLaunchKernelGGL(k_sum_partials, dim3((unsigned)ceil_div(f_in * hidden, (int64_t)64)),
+                       dim3(kThreads), 0, stream, f_in, hidden, chunks, (const float*)part, dW1,
+                       hidden);
+    hipLaunchKernelGGL(k_sum_partials, dim3((unsigned)ceil_div(hidden * C, (int64_t)64)),
+                       dim3(kThreads), 0, stream, hidden, C, chunks,
+                       (const float*)(part + chunks * f_in * hidden), dW2, C);
+    hipError_t e = hipGetLastError();
+    tfree(part, stream);
+    if (e != hipSuccess) return hip_fail(e, "k_sum_partials", __FILE__, __LINE__);
+  }
   return GCN_OK;
 }
 

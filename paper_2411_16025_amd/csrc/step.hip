@@ -1,18 +1,19 @@
 // One training step of a 2-layer GCN built from the library's kernels:
 // aggregation (Section 4 of SuperGCN, arXiv 2411.16025) interleaved with the
 // dense UPDATE of each layer (Section 2.1). Everything is ordered on the
-// caller's stream without host synchronization (one product runs on the side
-// stream, forked from and joined back to it).
+// caller's stream without host synchronization (without the fused backward,
+// one product runs on the side stream, forked from and joined back to it).
 //
 // Each layer multiplies A_hat, its input and its weights; the association is
 // chosen so that the aggregation gathers the narrower operand. Layer 1
 // aggregates first when f_in <= hidden, as the paper's AGGREGATE-then-UPDATE:
 // P = A_hat X, H1 = relu(P W1). Its weight gradient is then dW1 = P^T dZ1
 // with dZ1 the gradient at P W1 (dH1 masked by H1 > 0), and no aggregation
-// runs in its backward (the input gradient is not needed). Otherwise it
-// transforms first: H1 = relu(A_hat (X W1)), dW1 = X^T (A_hat^T dZ1). Layer 2
-// transforms first (its output, the classes, is the narrower side):
-// logits = A_hat (H1 W2).
+// runs in its backward (the input gradient is not needed); for f_in <= 112
+// and at most 48 classes, dZ1, dW1 and dW2 then come from one fused pass over
+// the rows that keeps dZ1 in registers. Otherwise it transforms first:
+// H1 = relu(A_hat (X W1)), dW1 = X^T (A_hat^T dZ1). Layer 2 transforms first
+// (its output, the classes, is the narrower side): logits = A_hat (H1 W2).
 
 #include "common.h"
 
@@ -56,7 +57,6 @@ extern "C" gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t 
   if (st == GCN_OK) st = talloc(&lg, n * ldc, s, "logits");
   if (st == GCN_OK) st = talloc(&dl, n * ldc, s, "dlogits");
   if (st == GCN_OK) st = talloc(&dz2, n * ldc, s, "dZ2");
-  if (st == GCN_OK) st = talloc(&dz1, n * ldh, s, "dZ1");
   // forward
   if (agg_first) {
     if (st == GCN_OK) st = aggregate_f32(g->csr, X, ldx, p, ldp, f_in, false, s);
@@ -72,29 +72,40 @@ extern "C" gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t 
   if (st == GCN_OK) st = softmax_xent(n, (int)n_classes, lg, ldc, labels, dl, ldc, loss, s);
   // backward
   if (st == GCN_OK) st = aggregate_f32(g->csc, dl, ldc, dz2, ldc, n_classes, false, s);
-  // dW2 = H1^T dZ2 reads only H1 and dZ2: on the side stream it overlaps the
-  // rest of the backward
-  SideWork side;
-  if (st == GCN_OK) st = side.init(s);
-  if (st == GCN_OK) st = side.fork();
-  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_TN, hidden, n_classes, n, h1, ldh, dz2, ldc, dW2,
-                                  n_classes, side.side);
-  // dH1 = dZ2 W2^T with the ReLU mask (H1 > 0) applied as it is stored: with
-  // the aggregation first this is already dZ1 (the gradient at P W1)
-  dh1 = agg_first ? dz1 : p;  // (X W1 is dead after the first aggregation)
-  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NT, n, hidden, n_classes, dz2, ldc, w2p, ldc, dh1, ldh,
-                                  s, h1, ldh);
-  if (agg_first) {
-    // dW1 = P^T dZ1
-    if (st == GCN_OK) st = gemm_f32(GCN_GEMM_TN, f_in, hidden, n, p, ldp, dz1, ldh, dW1, hidden, s);
+  if (agg_first && layer1_bwd_fusable(f_in, hidden, n_classes, dz2, ldc, w2p, ldc)) {
+    // dZ1 = (dZ2 W2^T) masked by H1 > 0, dW1 = P^T dZ1 and dW2 = H1^T dZ2 in
+    // one pass over the rows, dZ1 kept in registers
+    if (st == GCN_OK)
+      st = layer1_bwd_fused(n, f_in, hidden, n_classes, p, ldp, h1, ldh, dz2, ldc, w2p, ldc, dW1,
+                            dW2, s);
   } else {
-    // dZ1 = A_hat^T dH1, dW1 = X^T dZ1
-    if (st == GCN_OK) st = aggregate_f32(g->csc, dh1, ldh, dz1, ldh, hidden, false, s);
-    if (st == GCN_OK) st = gemm_f32(GCN_GEMM_TN, f_in, hidden, n, X, ldx, dz1, ldh, dW1, hidden, s);
+    if (st == GCN_OK) st = talloc(&dz1, n * ldh, s, "dZ1");
+    // dW2 = H1^T dZ2 reads only H1 and dZ2: on the side stream it overlaps
+    // the rest of the backward
+    SideWork side;
+    if (st == GCN_OK) st = side.init(s);
+    if (st == GCN_OK) st = side.fork();
+    if (st == GCN_OK) st = gemm_f32(GCN_GEMM_TN, hidden, n_classes, n, h1, ldh, dz2, ldc, dW2,
+                                    n_classes, side.side);
+    // dH1 = dZ2 W2^T with the ReLU mask (H1 > 0) applied as it is stored:
+    // with the aggregation first this is already dZ1 (the gradient at P W1)
+    dh1 = agg_first ? dz1 : p;  // (X W1 is dead after the first aggregation)
+    if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NT, n, hidden, n_classes, dz2, ldc, w2p, ldc, dh1,
+                                    ldh, s, h1, ldh);
+    if (agg_first) {
+      // dW1 = P^T dZ1
+      if (st == GCN_OK)
+        st = gemm_f32(GCN_GEMM_TN, f_in, hidden, n, p, ldp, dz1, ldh, dW1, hidden, s);
+    } else {
+      // dZ1 = A_hat^T dH1, dW1 = X^T dZ1
+      if (st == GCN_OK) st = aggregate_f32(g->csc, dh1, ldh, dz1, ldh, hidden, false, s);
+      if (st == GCN_OK)
+        st = gemm_f32(GCN_GEMM_TN, f_in, hidden, n, X, ldx, dz1, ldh, dW1, hidden, s);
+    }
+    // the side work ends before the buffers it reads are released on s
+    const gcn_status sj = side.join();
+    if (st == GCN_OK) st = sj;
   }
-  // the side work ends before the buffers it reads are released on s
-  const gcn_status sj = side.join();
-  if (st == GCN_OK) st = sj;
   tfree(dz1, s);
   tfree(dz2, s);
   tfree(dl, s);

@@ -246,6 +246,19 @@ def test_gcn_step_unaligned_inputs(G):
     _step_check(G, w, 101, 128, 10, 14)
 
 
+@pytest.mark.parametrize("n,f_in,hidden,C", [(1203, 20, 200, 33), (777, 60, 300, 16),
+                                             (2000, 112, 128, 48), (35, 100, 256, 47)])
+def test_gcn_step_fused_backward_shapes(G, n, f_in, hidden, C):
+    # f_in <= 112 and C <= 48: layer 1's backward runs as one fused pass
+    # (dZ1 in registers); f_in of 2, 4 and 7 16-column blocks, 1-3 class
+    # blocks, hidden slices of 128 columns with partial ones, partial row
+    # groups, and chunks of one group
+    note("gcn step fused backward n=%d f_in=%d hidden=%d C=%d" % (n, f_in, hidden, C))
+    src, dst = synth.rmat_edges(217 + n, n, 8 * n, perm_seed=218)
+    w = synth.Workload("rmat%d" % n, n, n, src, dst, synth.SYMMETRIZE | synth.ADD_SELF_LOOPS, f_in)
+    _step_check(G, w, f_in, hidden, C, 15)
+
+
 def test_gcn_step_product_like(G):
     import gc
     import torch
