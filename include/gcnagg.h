@@ -236,15 +236,18 @@ gcn_status gcn_softmax_xent(int64_t n, int64_t C, const float* logits, int64_t l
  *  Layer 1 is evaluated as relu((A_hat X) W1) with dW1 = (A_hat X)^T dZ1 when
  *  f_in <= hidden (the aggregation gathers the narrower rows and the backward
  *  needs none), else as relu(A_hat (X W1)) with dW1 = X^T (A_hat^T dZ1). The
- *  two agree up to fp32 rounding.
+ *  two agree up to fp32 rounding. In the first order, with f_in <= 112 and
+ *  n_classes <= 48, dZ1, dW1 and dW2 come from one fused pass over the rows
+ *  (dZ1 is never stored); the sums are the same up to their order.
  *  X [n x f_in] (ldx), W1 [f_in x hidden], W2 [hidden x n_classes] (dense,
  *  row-major), labels int32 [n] in [0, n_classes), n_classes <= 64.
  *  Outputs: dW1, dW2 (same shapes as W1, W2), *loss (device double).
  * No bias, dropout or normalization layer. Intermediates are allocated
- * stream-ordered for the duration of the call. dW2 is computed on a second,
- * library-owned stream of the current device (non-blocking, default priority),
- * forked from `stream` by an event and joined back to it before the call
- * returns, so all outputs are ordered on `stream`. */
+ * stream-ordered for the duration of the call. Without the fused pass, dW2
+ * is computed on a second, library-owned stream of the current device
+ * (non-blocking, default priority), forked from `stream` by an event and
+ * joined back to it before the call returns, so all outputs are ordered on
+ * `stream`. */
 gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t ldx, int64_t f_in,
                          const float* W1, int64_t hidden, const float* W2, int64_t n_classes,
                          const int32_t* labels, float* dW1, float* dW2, double* loss,

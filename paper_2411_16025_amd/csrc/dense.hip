@@ -902,11 +902,15 @@ __global__ __launch_bounds__(kThreads) void k_sum_partials(int64_t M, int64_t N,
 //    B operand of P^T dZ1 (A operand P[r0 + 4 g + i][16 b + x], one per
 //    16-row block b of dW1), and the H1 value read for the mask is the A
 //    operand of H1^T dZ2 (B operand dZ2[r0 + 4 g + i][16 c + x]).
-// The next group's operands are loaded while the current one is multiplied.
+// The next group's operands are loaded while the current one is multiplied
+// (two register sets in turn).
 // Columns past f_in, hidden or C read a valid column of their row and reach
 // only outputs that are not stored; rows past the chunk are zero. Chunk
 // partials go to part1 [chunks][f_in][hidden] and part2 [chunks][hidden][C],
 // summed in chunk order by k_sum_partials.
+#ifndef GCN_BWD1_FUSED
+#define GCN_BWD1_FUSED 1
+#endif
 struct Bwd1Args {
   int64_t n, split;
   int f_in, hidden, C;
@@ -1079,6 +1083,18 @@ __global__ __launch_bounds__(64 * kBwd1Waves) void k_gcn_bwd1(Bwd1Args a) {
                                                              0, 0, 0);
     }
   };
+  // the next set's loads issued one per matrix-core operation over the
+  // first part of the current set's products (in a phase of their own before
+  // the products the step's kernel took 2.33 instead of 2.28 ms)
+  auto interleave = [&]() __attribute__((always_inline)) {
+    constexpr int kLoads = CB + 4 * (2 + MB + CB);
+#pragma unroll
+    for (int k = 0; k < kLoads; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
   using Full = std::integral_constant<bool, true>;
   using Part = std::integral_constant<bool, false>;
   const int64_t nf = (ke - kb) / 16;  // whole groups
@@ -1090,13 +1106,11 @@ __global__ __launch_bounds__(64 * kBwd1Waves) void k_gcn_bwd1(Bwd1Args a) {
     int64_t t = 0;
     for (; t + 2 <= nf; t += 2) {
       load(Full{}, kb + 16 * (t + 1), o1);
-      __builtin_amdgcn_sched_barrier(0);  // keep each load set ahead of its use
       mma(o0);
-      __builtin_amdgcn_sched_barrier(0);
+      interleave();
       load(Full{}, kb + 16 * min(t + 2, nf - 1), o0);
-      __builtin_amdgcn_sched_barrier(0);
       mma(o1);
-      __builtin_amdgcn_sched_barrier(0);
+      interleave();
     }
     if (t < nf) mma(o0);
   }
@@ -1556,9 +1570,7 @@ gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int
   return GCN_OK;
 }
 
-#ifndef GCN_BWD1_FUSED
-#define GCN_BWD1_FUSED 1
-#endif
+
 // Workgroups of the fused layer-1 backward (chunks x hidden slices): one per
 // CU (its registers fill the CU), a fixed count so that the summation order
 // does not depend on the device.
