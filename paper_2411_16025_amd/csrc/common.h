@@ -205,6 +205,16 @@ gcn_status aggregate_f32(const Mat& m, const float* X, int64_t ldx, float* Y, in
 gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
                     const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream,
                     const float* mask = nullptr, int64_t ldm = 0, bool relu = false);
+// Forward of a GCN first layer that aggregates first: H1 = relu(P W1) and
+// Z2 = H1 W2 in one pass over the rows. P [n x f_in] (ldp), H1 [n x hidden]
+// (ldh, 16-byte aligned rows), W1 [f_in x hidden] (ldw1), W2 [hidden x C]
+// (ldw2), Z2 [n x C] (ldz).
+bool layer1_fwd_fusable(int64_t f_in, int64_t hidden, int64_t C, const float* P, int64_t ldp,
+                        const float* H1, int64_t ldh);
+gcn_status layer1_fwd_fused(int64_t n, int64_t f_in, int64_t hidden, int64_t C, const float* P,
+                            int64_t ldp, const float* W1, int64_t ldw1, const float* W2,
+                            int64_t ldw2, float* H1, int64_t ldh, float* Z2, int64_t ldz,
+                            hipStream_t stream);
 // Backward of a GCN first layer that aggregates first (H1 = relu(P W1),
 // Z2 = H1 W2) in one pass over the rows: dW1 = P^T ((dZ2 W2^T) masked by
 // H1 > 0) and dW2 = H1^T dZ2, both [rows x cols] with leading dimension cols.

@@ -1143,6 +1143,135 @@ __global__ __launch_bounds__(64 * kBwd1Waves) void k_gcn_bwd1(Bwd1Args a) {
   }
 }
 
+// Forward of a GCN first layer that aggregates first, fused over groups of
+// 16 rows: H1 = relu(P W1) is stored and Z2 = H1 W2 computed from it while it
+// is still in registers (the separate Z2 product re-read H1).
+//
+// The weights sit in LDS in matrix-core operand order, filled once per
+// workgroup: W1^T as [hidden block hb][step s][lane] = W1[4 s + l / 16][16 hb +
+// l % 16] and W2 as [hb][class block c][i][lane] = W2[16 hb + 4 (l / 16) + i]
+// [16 c + l % 16], zero outside f_in, hidden and C. Every wavefront then takes
+// its own row groups r0 ... r0 + 15 (no barriers, no exchange between
+// wavefronts). Lane (g = l / 16, x = l % 16), per hidden block hb:
+//  * H1^T block = W1^T P^T over the steps s (input features 4 s + g): the B
+//    operand is P[r0 + x][4 s + g], loaded for the whole group (the next
+//    group's while this one is multiplied). Result element i is
+//    H1[r0 + x][16 hb + 4 g + i]: after the ReLU one 16-byte store of H1.
+//  * Those four elements are the A operand of H1 W2 at the steps that
+//    contract over hidden units 16 hb + 4 g + i: Z2 accumulates in registers
+//    over the hidden blocks and is stored once per group.
+// Steps s >= ceil(f_in / 4) of the fixed step count S are multiplied by zero
+// operands (their LDS reads are clamped into the table).
+struct Fwd1Args {
+  int64_t n;
+  int f_in, hidden, C;
+  const float* P;  // [n][ldp]
+  int64_t ldp;
+  const float* W1;  // [f_in][ldw1]
+  int64_t ldw1;
+  const float* W2;  // [hidden][ldw2]
+  int64_t ldw2;
+  float* H1;  // [n][ldh], 16-byte aligned rows
+  int64_t ldh;
+  float* Z2;  // [n][ldz]
+  int64_t ldz;
+};
+
+constexpr int kFwd1Waves = 16;
+
+template <int S, int CB>
+__global__ __launch_bounds__(64 * kFwd1Waves) void k_gcn_fwd1(Fwd1Args a) {
+  extern __shared__ __align__(16) float lds[];
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int g = lane >> 4, x = lane & 15;
+  const int hbn = (a.hidden + 15) / 16;  // hidden blocks
+  const int sn = (a.f_in + 3) / 4;       // steps with data (<= S)
+  float* lw1 = lds;                      // [hbn][sn][64]
+  float* lw2 = lds + hbn * sn * 64;      // [hbn][CB][4][64]
+  for (int e = threadIdx.x; e < hbn * sn * 64; e += blockDim.x) {
+    const int l = e & 63, st = (e >> 6) % sn, hb = (e >> 6) / sn;
+    const int k = 4 * st + (l >> 4), col = 16 * hb + (l & 15);
+    lw1[e] = k < a.f_in && col < a.hidden ? a.W1[(int64_t)k * a.ldw1 + col] : 0.f;
+  }
+  for (int e = threadIdx.x; e < hbn * CB * 4 * 64; e += blockDim.x) {
+    const int l = e & 63, i = (e >> 6) & 3, c = (e >> 8) % CB, hb = (e >> 8) / CB;
+    const int u = 16 * hb + 4 * (l >> 4) + i, cls = 16 * c + (l & 15);
+    lw2[e] = u < a.hidden && cls < a.C ? a.W2[(int64_t)u * a.ldw2 + cls] : 0.f;
+  }
+  __syncthreads();
+  const int64_t ng = (a.n + 15) / 16;
+  const int64_t stride = (int64_t)gridDim.x * (blockDim.x >> 6);
+  int64_t grp = (int64_t)blockIdx.x * (blockDim.x >> 6) + w;
+  if (grp >= ng) return;
+  // P operands of a group: P[r0 + x][4 s + g] (ldp >= 4 sn keeps them in the
+  // row); rows past n read the last row and reach only rows of H1 and Z2
+  // that are not stored; steps past sn read step sn - 1 and are zeroed where
+  // used, as are features past f_in (the row's padding may hold anything)
+  auto load = [&](int64_t gi, float (&pv)[S]) __attribute__((always_inline)) {
+    const float* row = a.P + min(16 * gi + x, a.n - 1) * a.ldp + g;
+#pragma unroll
+    for (int st = 0; st < S; ++st) pv[st] = row[4 * min(st, sn - 1)];
+  };
+  auto compute = [&](int64_t gi, float (&pz)[S]) __attribute__((always_inline)) {
+    const int64_t r0 = 16 * gi;
+    const bool live = r0 + x < a.n;
+#pragma unroll
+    for (int st = 0; st < S; ++st) pz[st] = 4 * st + g < a.f_in ? pz[st] : 0.f;
+    f4 z[CB];
+#pragma unroll
+    for (int c = 0; c < CB; ++c) z[c] = f4{0.f, 0.f, 0.f, 0.f};
+    const float* w1 = lw1 + lane;
+    const float* w2 = lw2 + lane;
+    for (int hb = 0; hb < hbn; ++hb) {
+      f4 h = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < S; ++st)
+        h = __builtin_amdgcn_mfma_f32_16x16x4f32(w1[64 * min(st, sn - 1)], pz[st], h, 0, 0, 0);
+      w1 += 64 * sn;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) h[i] = fmaxf(h[i], 0.f);
+      const int c0 = 16 * hb + 4 * g;
+      if (live) {
+        float* dst = a.H1 + (r0 + x) * a.ldh + c0;
+        if (c0 + 4 <= a.hidden)
+          *reinterpret_cast<f4*>(dst) = h;
+        else
+          for (int e = 0; e < 4 && c0 + e < a.hidden; ++e) dst[e] = h[e];
+      }
+#pragma unroll
+      for (int c = 0; c < CB; ++c)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          z[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(h[i], w2[64 * (4 * c + i)], z[c], 0, 0, 0);
+      w2 += 64 * 4 * CB;
+    }
+    // element i of z[c]: Z2[r0 + 4 g + i][16 c + x]
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t row = r0 + 4 * g + i;
+      if (row < a.n)
+#pragma unroll
+        for (int c = 0; c < CB; ++c)
+          if (16 * c + x < a.C) a.Z2[row * a.ldz + 16 * c + x] = z[c][i];
+    }
+  };
+  // two sets of P operands in turn; the group after the last is the last again
+  float p0[S], p1[S];
+  load(grp, p0);
+  for (;;) {
+    const int64_t g1 = grp + stride;
+    load(min(g1, ng - 1), p1);
+    compute(grp, p0);
+    if (g1 >= ng) break;
+    const int64_t g2 = g1 + stride;
+    load(min(g2, ng - 1), p0);
+    compute(g1, p1);
+    if (g2 >= ng) break;
+    grp = g2;
+  }
+}
+
 // one wavefront per row
 __global__ __launch_bounds__(kThreads) void k_relu(int64_t n, int64_t F, float* __restrict__ h,
                                                    int64_t ld) {
@@ -1629,6 +1758,59 @@ gcn_status layer1_bwd_fused(int64_t n, int64_t f_in, int64_t hidden, int64_t C, 
     tfree(part, stream);
     if (e != hipSuccess) return hip_fail(e, "k_sum_partials", __FILE__, __LINE__);
   }
+  return GCN_OK;
+}
+
+// LDS bytes of the fused forward's weight tables
+int64_t fwd1_lds(int64_t f_in, int64_t hidden, int64_t C) {
+  const int64_t hbn = ceil_div(hidden, (int64_t)16), sn = ceil_div(f_in, (int64_t)4);
+  return (hbn * sn * 64 + hbn * ceil_div(C, (int64_t)16) * 4 * 64) * (int64_t)sizeof(float);
+}
+constexpr int64_t kFwd1MaxLds = 160 * 1024;
+
+bool layer1_fwd_fusable(int64_t f_in, int64_t hidden, int64_t C, const float* P, int64_t ldp,
+                        const float* H1, int64_t ldh) {
+  (void)P;  // read element by element: any alignment
+  return GCN_BWD1_FUSED && f_in >= 1 && f_in <= 112 && hidden >= 1 && C >= 1 && C <= 48 &&
+         ldp >= 4 * ceil_div(f_in, (int64_t)4) && ldh >= hidden && aligned16(H1, ldh) &&
+         fwd1_lds(f_in, hidden, C) <= kFwd1MaxLds;
+}
+
+gcn_status layer1_fwd_fused(int64_t n, int64_t f_in, int64_t hidden, int64_t C, const float* P,
+                            int64_t ldp, const float* W1, int64_t ldw1, const float* W2,
+                            int64_t ldw2, float* H1, int64_t ldh, float* Z2, int64_t ldz,
+                            hipStream_t stream) {
+  if (!layer1_fwd_fusable(f_in, hidden, C, P, ldp, H1, ldh)) {
+    set_error("fused layer-1 forward: unsupported shape or alignment");
+    return GCN_EINVAL;
+  }
+  if (n == 0) return GCN_OK;
+  ProfScope ps("gemm_layer1_fwd_fused", stream);
+  const Fwd1Args a{n, (int)f_in, (int)hidden, (int)C, P, ldp, W1, ldw1, W2, ldw2, H1, ldh, Z2, ldz};
+  const int sn = (int)ceil_div(f_in, (int64_t)4);
+  const int smax = sn <= 8 ? 8 : (sn <= 16 ? 16 : (sn <= 25 ? 25 : 28));
+  const int cb = (int)ceil_div(C, (int64_t)16);
+  const size_t lds = (size_t)fwd1_lds(f_in, hidden, C);
+  const int64_t groups = ceil_div(n, (int64_t)16);
+  hipError_t e = hipSuccess;
+  // one workgroup per CU (the weight tables take most of its LDS), wavefronts
+  // on their own row groups
+  auto launch = [&](auto kern) {
+    e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds);
+    if (e != hipSuccess) return;
+    const int64_t wg = std::min<int64_t>(cu_count(), ceil_div(groups, (int64_t)kFwd1Waves));
+    hipLaunchKernelGGL(kern, dim3((unsigned)wg), dim3(64 * kFwd1Waves), lds, stream, a);
+    e = hipGetLastError();
+  };
+#define GCN_FWD1(S_, CB_) \
+  if (smax == S_ && cb == CB_) launch(k_gcn_fwd1<S_, CB_>)
+  GCN_FWD1(8, 1); GCN_FWD1(8, 2); GCN_FWD1(8, 3);
+  GCN_FWD1(16, 1); GCN_FWD1(16, 2); GCN_FWD1(16, 3);
+  GCN_FWD1(25, 1); GCN_FWD1(25, 2); GCN_FWD1(25, 3);
+  GCN_FWD1(28, 1); GCN_FWD1(28, 2); GCN_FWD1(28, 3);
+#undef GCN_FWD1
+  if (e != hipSuccess) return hip_fail(e, "k_gcn_fwd1", __FILE__, __LINE__);
   return GCN_OK;
 }
 

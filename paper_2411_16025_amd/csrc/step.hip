@@ -58,16 +58,24 @@ extern "C" gcn_status gcn_gcn2_step(const gcn_graph* g, const float* X, int64_t 
   if (st == GCN_OK) st = talloc(&dl, n * ldc, s, "dlogits");
   if (st == GCN_OK) st = talloc(&dz2, n * ldc, s, "dZ2");
   // forward
+  const bool fwd_fused = agg_first && layer1_fwd_fusable(f_in, hidden, n_classes, p, ldp, h1, ldh);
   if (agg_first) {
     if (st == GCN_OK) st = aggregate_f32(g->csr, X, ldx, p, ldp, f_in, false, s);
-    // H1 = relu(P W1), the ReLU applied as the product stores its tile
-    if (st == GCN_OK)
+    if (fwd_fused) {
+      // H1 = relu(P W1) and Z2 = H1 W2 in one pass (Z2 from H1 in registers)
+      if (st == GCN_OK)
+        st = layer1_fwd_fused(n, f_in, hidden, n_classes, p, ldp, W1, hidden, w2p, ldc, h1, ldh,
+                              z2, ldc, s);
+    } else if (st == GCN_OK) {
+      // H1 = relu(P W1), the ReLU applied as the product stores its tile
       st = gemm_f32(GCN_GEMM_NN, n, hidden, f_in, p, ldp, W1, hidden, h1, ldh, s, nullptr, 0, true);
+    }
   } else {
     if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NN, n, hidden, f_in, X, ldx, W1, hidden, p, ldh, s);
     if (st == GCN_OK) st = aggregate_f32(g->csr, p, ldh, h1, ldh, hidden, true, s);  // + ReLU
   }
-  if (st == GCN_OK) st = gemm_f32(GCN_GEMM_NN, n, n_classes, hidden, h1, ldh, w2p, ldc, z2, ldc, s);
+  if (st == GCN_OK && !fwd_fused)
+    st = gemm_f32(GCN_GEMM_NN, n, n_classes, hidden, h1, ldh, w2p, ldc, z2, ldc, s);
   if (st == GCN_OK) st = aggregate_f32(g->csr, z2, ldc, lg, ldc, n_classes, false, s);
   if (st == GCN_OK) st = softmax_xent(n, (int)n_classes, lg, ldc, labels, dl, ldc, loss, s);
   // backward
