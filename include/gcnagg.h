@@ -238,7 +238,8 @@ gcn_status gcn_softmax_xent(int64_t n, int64_t C, const float* logits, int64_t l
  *  needs none), else as relu(A_hat (X W1)) with dW1 = X^T (A_hat^T dZ1). The
  *  two agree up to fp32 rounding. In the first order, with f_in <= 112 and
  *  n_classes <= 48, dZ1, dW1 and dW2 come from one fused pass over the rows
- *  (dZ1 is never stored); the sums are the same up to their order.
+ *  (dZ1 is never stored), and for hidden <= 256 so do H1 and H1 W2; the sums
+ *  are the same up to their order.
  *  X [n x f_in] (ldx), W1 [f_in x hidden], W2 [hidden x n_classes] (dense,
  *  row-major), labels int32 [n] in [0, n_classes), n_classes <= 64.
  *  Outputs: dW1, dW2 (same shapes as W1, W2), *loss (device double).

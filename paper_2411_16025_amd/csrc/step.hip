@@ -11,7 +11,9 @@
 // with dZ1 the gradient at P W1 (dH1 masked by H1 > 0), and no aggregation
 // runs in its backward (the input gradient is not needed); for f_in <= 112
 // and at most 48 classes, dZ1, dW1 and dW2 then come from one fused pass over
-// the rows that keeps dZ1 in registers. Otherwise it transforms first:
+// the rows that keeps dZ1 in registers, and (hidden <= 256) H1 and Z2 = H1 W2
+// from one forward pass that keeps H1 in registers for Z2. Otherwise it
+// transforms first:
 // H1 = relu(A_hat (X W1)), dW1 = X^T (A_hat^T dZ1). Layer 2 transforms first
 // (its output, the classes, is the narrower side): logits = A_hat (H1 W2).
 
