@@ -547,49 +547,60 @@ struct LnBwdArgs {
   int64_t ldx;
 };
 
-template <int G, int NV>
+// Vector path (F a multiple of 4): G lanes per row, NV 16-byte pieces per
+// lane. Every load takes an address inside its row (pieces past F read the
+// row's first piece, rows past n the last row) and values outside the row are
+// zeroed afterwards, so all loads of a lane are issued before any arithmetic,
+// without branches. G2 and MASK say whether the second gradient and the mask
+// are given.
+template <int G, int NV, bool G2, bool MASK>
 __global__ __launch_bounds__(kBlock) void k_ln_bwd_v(LnBwdArgs a) {
   constexpr int E = 64 / G;
   const int lane = threadIdx.x & 63;
   const int sl = lane % G;
   const int64_t i = ((int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6)) * E + lane / G;
   const bool live = i < a.n;
-  float yv[NV][4], gv[NV][4], mv[NV][4];
+  const int64_t ic = live ? i : a.n - 1;
+  float4 yv[NV], gv[NV], hv[NV], mv[NV];
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
     const int f = 4 * (sl + j * G);
-    if (live && f + 4 <= a.F) {
-      const float4 t = *reinterpret_cast<const float4*>(a.y + i * a.ldy + f);
-      float4 u = *reinterpret_cast<const float4*>(a.g1 + i * a.ld1 + f);
-      if (a.g2) {
-        const float4 w = *reinterpret_cast<const float4*>(a.g2 + i * a.ld2 + f);
-        u.x += w.x;
-        u.y += w.y;
-        u.z += w.z;
-        u.w += w.w;
-      }
-      float4 m = make_float4(1.f, 1.f, 1.f, 1.f);
-      if (a.mask) m = *reinterpret_cast<const float4*>(a.mask + i * a.ldm + f);
-      yv[j][0] = t.x; yv[j][1] = t.y; yv[j][2] = t.z; yv[j][3] = t.w;
-      gv[j][0] = u.x; gv[j][1] = u.y; gv[j][2] = u.z; gv[j][3] = u.w;
-      mv[j][0] = m.x; mv[j][1] = m.y; mv[j][2] = m.z; mv[j][3] = m.w;
-    } else {
+    const int fo = f < a.F ? f : 0;
+    yv[j] = *reinterpret_cast<const float4*>(a.y + ic * a.ldy + fo);
+    gv[j] = *reinterpret_cast<const float4*>(a.g1 + ic * a.ld1 + fo);
+    if constexpr (G2) hv[j] = *reinterpret_cast<const float4*>(a.g2 + ic * a.ld2 + fo);
+    if constexpr (MASK) mv[j] = *reinterpret_cast<const float4*>(a.mask + ic * a.ldm + fo);
+  }
+  float yf[NV][4], gf[NV][4];
+  bool keep[NV][4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const bool ok = live && f + e < a.F;
-        yv[j][e] = ok ? a.y[i * a.ldy + f + e] : 0.f;
-        gv[j][e] = ok ? a.g1[i * a.ld1 + f + e] + (a.g2 ? a.g2[i * a.ld2 + f + e] : 0.f) : 0.f;
-        mv[j][e] = ok && a.mask ? a.mask[i * a.ldm + f + e] : 1.f;
-      }
+  for (int j = 0; j < NV; ++j) {
+    const int f = 4 * (sl + j * G);
+    const float yy[4] = {yv[j].x, yv[j].y, yv[j].z, yv[j].w};
+    float gg[4] = {gv[j].x, gv[j].y, gv[j].z, gv[j].w};
+    if constexpr (G2) {
+      gg[0] += hv[j].x;
+      gg[1] += hv[j].y;
+      gg[2] += hv[j].z;
+      gg[3] += hv[j].w;
+    }
+    const float mm[4] = {MASK ? mv[j].x : 1.f, MASK ? mv[j].y : 1.f, MASK ? mv[j].z : 1.f,
+                         MASK ? mv[j].w : 1.f};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bool ok = live && f < a.F;
+      yf[j][e] = ok ? yy[e] : 0.f;
+      gf[j][e] = ok ? gg[e] : 0.f;
+      keep[j][e] = mm[e] > 0.f;
     }
   }
   double s1 = 0.0, s2 = 0.0;
 #pragma unroll
   for (int j = 0; j < NV; ++j)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {  // masked entries are 0
-      s1 += (double)gv[j][e];
-      s2 += (double)gv[j][e] * (double)yv[j][e];
+    for (int e = 0; e < 4; ++e) {  // entries outside the row are 0
+      s1 += (double)gf[j][e];
+      s2 += (double)gf[j][e] * (double)yf[j][e];
     }
   const double m1 = slot_sum<G>(s1) / (double)a.F;
   const double m2 = slot_sum<G>(s2) / (double)a.F;
@@ -603,17 +614,14 @@ __global__ __launch_bounds__(kBlock) void k_ln_bwd_v(LnBwdArgs a) {
     float o[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const float d = (float)(r * ((double)gv[j][e] - m1 - (double)yv[j][e] * m2));
-      o[e] = mv[j][e] > 0.f ? d : 0.f;
+      const float d = (float)(r * ((double)gf[j][e] - m1 - (double)yf[j][e] * m2));
+      o[e] = keep[j][e] ? d : 0.f;
     }
-    if (f + 4 <= a.F)
-      *reinterpret_cast<float4*>(out + f) = make_float4(o[0], o[1], o[2], o[3]);
-    else
-      for (int e = 0; e < 4 && f + e < a.F; ++e) out[f + e] = o[e];
+    *reinterpret_cast<float4*>(out + f) = make_float4(o[0], o[1], o[2], o[3]);
   }
 }
 
-// One wavefront per row for wide rows or unaligned storage.
+// One wavefront per row for wide rows, unaligned storage or F % 4 != 0.
 __global__ __launch_bounds__(kBlock) void k_ln_bwd(LnBwdArgs a) {
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
@@ -639,9 +647,15 @@ __global__ __launch_bounds__(kBlock) void k_ln_bwd(LnBwdArgs a) {
 
 template <int G, int NV>
 void launch_bwd_v(const LnBwdArgs& a, hipStream_t s) {
-  const int64_t rows_per_block = (int64_t)(kBlock / 64) * (64 / G);
-  hipLaunchKernelGGL((k_ln_bwd_v<G, NV>), dim3((unsigned)ceil_div(a.n, rows_per_block)),
-                     dim3(kBlock), 0, s, a);
+  const dim3 grid((unsigned)ceil_div(a.n, (int64_t)(kBlock / 64) * (64 / G)));
+  if (a.g2 && a.mask)
+    hipLaunchKernelGGL((k_ln_bwd_v<G, NV, true, true>), grid, dim3(kBlock), 0, s, a);
+  else if (a.g2)
+    hipLaunchKernelGGL((k_ln_bwd_v<G, NV, true, false>), grid, dim3(kBlock), 0, s, a);
+  else if (a.mask)
+    hipLaunchKernelGGL((k_ln_bwd_v<G, NV, false, true>), grid, dim3(kBlock), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_ln_bwd_v<G, NV, false, false>), grid, dim3(kBlock), 0, s, a);
 }
 
 bool al16(const void* p, int64_t ld) { return reinterpret_cast<uintptr_t>(p) % 16 == 0 && ld % 4 == 0; }
@@ -671,7 +685,7 @@ gcn_status layernorm_bwd(int64_t n, int64_t F, const float* Y, int64_t ldy, cons
   ProfScope ps("layernorm_bwd", s);
   const LnBwdArgs a{n, (int)F, Y, ldy, rstd, G1, ld1, G2, ld2, mask, ldm, dX, lddx};
   const bool vec = al16(Y, ldy) && al16(G1, ld1) && (!G2 || al16(G2, ld2)) &&
-                   (!mask || al16(mask, ldm)) && al16(dX, lddx) && F <= 1024;
+                   (!mask || al16(mask, ldm)) && al16(dX, lddx) && F <= 1024 && F % 4 == 0;
   if (!vec)
     hipLaunchKernelGGL(k_ln_bwd, dim3((unsigned)ceil_div(n, kBlock / 64)), dim3(kBlock), 0, s, a);
   else if (F <= 32)

@@ -87,26 +87,29 @@ def test_layernorm_fwd(G, F, ld):
     assert np.allclose(rstd, r64, rtol=1e-6, atol=0)
 
 
-@pytest.mark.parametrize("F,ld", [(100, 100), (256, 256), (47, 48), (1100, 1100)])
+@pytest.mark.parametrize("F,ld", [(100, 100), (256, 256), (47, 48), (1100, 1100), (32, 32),
+                                  (64, 68), (512, 512), (100, 104)])
 def test_layernorm_bwd(G, F, ld):
     note("layernorm bwd F=%d" % F)
     n = 2003
     X = synth.normal(410 + F, n, ld)[:, :F] * 2
     Yd, rd = G.gcn_layernorm_fwd(dev(X), eps=1e-5)
-    g1 = synth.normal(411 + F, n, F)
-    g2 = synth.normal(412 + F, n, F)
-    mask = np.maximum(synth.normal(413 + F, n, F), 0).astype(np.float32)
+    # the gradients and the mask are passed as row views of ld-wide storage
+    g1p = synth.normal(411 + F, n, ld)
+    g2p = synth.normal(412 + F, n, ld)
+    maskp = np.maximum(synth.normal(413 + F, n, ld), 0).astype(np.float32)
+    g1, g2, mask = g1p[:, :F], g2p[:, :F], maskp[:, :F]
     Y, r = host(Yd).astype(np.float64), host(rd).astype(np.float64)
     g = (g1 + g2).astype(np.float64)  # the kernel adds the two in fp32
-    for use2, usem in ((False, False), (True, True)):
+    for use2, usem in ((False, False), (True, True), (True, False), (False, True)):
         gg = g if use2 else g1.astype(np.float64)
         ref = oracle.layernorm64_bwd(Y, r, gg)
         S = r[:, None] * (np.abs(gg) + np.abs(gg).mean(1, keepdims=True)
                           + np.abs(Y) * np.abs(gg * Y).mean(1, keepdims=True))
         if usem:
             ref = ref * (mask > 0)
-        out = host(G.gcn_layernorm_bwd(Yd, rd, dev(g1), dev(g2) if use2 else None,
-                                       dev(mask) if usem else None))
+        out = host(G.gcn_layernorm_bwd(Yd, rd, dev(g1p)[:, :F], dev(g2p)[:, :F] if use2 else None,
+                                       dev(maskp)[:, :F] if usem else None))
         assert np.all(np.abs(out - ref) <= 1e-5 * S + 1e-30), (use2, usem)
 
 
