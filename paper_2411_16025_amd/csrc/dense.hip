@@ -908,8 +908,8 @@ __global__ __launch_bounds__(kThreads) void k_sum_partials(int64_t M, int64_t N,
 // only outputs that are not stored; rows past the chunk are zero. Chunk
 // partials go to part1 [chunks][f_in][hidden] and part2 [chunks][hidden][C],
 // summed in chunk order by k_sum_partials.
-#ifndef GCN_BWD1_FUSED
-#define GCN_BWD1_FUSED 1
+#ifndef GCN_LAYER1_FUSED
+#define GCN_LAYER1_FUSED 1
 #endif
 struct Bwd1Args {
   int64_t n, split;
@@ -1707,7 +1707,7 @@ constexpr int64_t kBwd1Blocks = 256;
 
 bool layer1_bwd_fusable(int64_t f_in, int64_t hidden, int64_t C, const float* dZ2, int64_t ldc,
                         const float* W2, int64_t ldw) {
-  return GCN_BWD1_FUSED && f_in >= 1 && f_in <= 112 && hidden >= 1 && C >= 1 && C <= 48 &&
+  return GCN_LAYER1_FUSED && f_in >= 1 && f_in <= 112 && hidden >= 1 && C >= 1 && C <= 48 &&
          ldc >= C && ldw >= C && aligned16(dZ2, ldc) && aligned16(W2, ldw);
 }
 
@@ -1771,7 +1771,7 @@ constexpr int64_t kFwd1MaxLds = 160 * 1024;
 bool layer1_fwd_fusable(int64_t f_in, int64_t hidden, int64_t C, const float* P, int64_t ldp,
                         const float* H1, int64_t ldh) {
   (void)P;  // read element by element: any alignment
-  return GCN_BWD1_FUSED && f_in >= 1 && f_in <= 112 && hidden >= 1 && C >= 1 && C <= 48 &&
+  return GCN_LAYER1_FUSED && f_in >= 1 && f_in <= 112 && hidden >= 1 && C >= 1 && C <= 48 &&
          ldp >= 4 * ceil_div(f_in, (int64_t)4) && ldh >= hidden && aligned16(H1, ldh) &&
          fwd1_lds(f_in, hidden, C) <= kFwd1MaxLds;
 }
