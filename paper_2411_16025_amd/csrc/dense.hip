@@ -1565,20 +1565,35 @@ hipError_t launch_tall(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
 }
 
 
+// Output tiles of at most 128 rows; the wavefront count (16 rows each) is
+// chosen so that the ceil(M / 128) tiles cover M with the least padding
+// (M = 200: two tiles of 112 rows instead of 128; M = 47: one of 48).
 void launch_tn(int64_t M, int64_t N, int64_t K, int64_t split, int64_t n_chunks, const float* A,
                int64_t lda, const float* B, int64_t ldb, float* part, hipStream_t stream) {
-  constexpr int kWaves = 8, kBm = 16 * kWaves;
+  const int64_t mb = ceil_div(M, (int64_t)16);
+  const int waves = (int)ceil_div(mb, ceil_div(mb, (int64_t)8));
   const int bn = tile_n_narrow(N);
-  const dim3 grid((unsigned)ceil_div(M, kBm), (unsigned)ceil_div(N, bn), (unsigned)n_chunks);
-  if (bn == 48)
-    hipLaunchKernelGGL((k_gemm_tn_v<kWaves, 48>), grid, dim3(64 * kWaves), 0, stream, M, N, K,
-                       split, A, lda, B, ldb, part);
-  else if (bn == 64)
-    hipLaunchKernelGGL((k_gemm_tn_v<kWaves, 64>), grid, dim3(64 * kWaves), 0, stream, M, N, K,
-                       split, A, lda, B, ldb, part);
-  else
-    hipLaunchKernelGGL((k_gemm_tn_v<kWaves, 128>), grid, dim3(64 * kWaves), 0, stream, M, N, K,
-                       split, A, lda, B, ldb, part);
+  const dim3 grid((unsigned)ceil_div(M, (int64_t)16 * waves), (unsigned)ceil_div(N, bn),
+                  (unsigned)n_chunks);
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, grid, dim3(64 * waves), 0, stream, M, N, K, split, A, lda, B, ldb,
+                       part);
+  };
+#define GCN_TNV(W_)                                        \
+  case W_:                                                 \
+    if (bn == 48)                                          \
+      go(k_gemm_tn_v<W_, 48>);                             \
+    else if (bn == 64)                                     \
+      go(k_gemm_tn_v<W_, 64>);                             \
+    else                                                   \
+      go(k_gemm_tn_v<W_, 128>);                            \
+    break
+  switch (waves) {
+    GCN_TNV(1); GCN_TNV(2); GCN_TNV(3); GCN_TNV(4);
+    GCN_TNV(5); GCN_TNV(6); GCN_TNV(7);
+    default: GCN_TNV(8);
+  }
+#undef GCN_TNV
 }
 
 // The streaming A^T B kernel: C tiles of 64 x 16 NB (N <= 64), at most 16 of

@@ -95,8 +95,12 @@ def test_gemm_resident_b(G, M, N, K):
     assert torch.equal(C2.view(torch.int32), C3.view(torch.int32)), "NT not bit-identical"
 
 
+# The staged A^T B tile takes ceil(M / 16 / ceil(M / 128)) wavefronts: 1, 2,
+# 3, 7 (M = 100, 200, 516) and 8 (M = 256) are covered below.
 @pytest.mark.parametrize("K,M,N", [(5, 3, 2), (8192, 100, 256), (20000, 256, 47),
-                                   (100003, 64, 64), (33, 1, 300)])
+                                   (100003, 64, 64), (33, 1, 300), (20000, 200, 256),
+                                   (20000, 48, 100), (20011, 516, 128), (8192, 20, 96),
+                                   (8192, 16, 68)])
 def test_gemm_tn_split_k(G, K, M, N):
     import torch
     note("gemm tn %dx%dx%d" % (K, M, N))
