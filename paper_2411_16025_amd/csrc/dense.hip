@@ -1224,10 +1224,24 @@ __global__ __launch_bounds__(64 * kFwd1Waves) void k_gcn_fwd1(Fwd1Args a) {
     const float* w1 = lw1 + lane;
     const float* w2 = lw2 + lane;
     for (int hb = 0; hb < hbn; ++hb) {
+      // W1 operands from LDS: 8 reads ahead, then one read per product (read
+      // next to its product, each read's latency was exposed)
+      float wa[S];
+#pragma unroll
+      for (int st = 0; st < S; ++st) wa[st] = w1[64 * min(st, sn - 1)];
       f4 h = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int st = 0; st < S; ++st)
-        h = __builtin_amdgcn_mfma_f32_16x16x4f32(w1[64 * min(st, sn - 1)], pz[st], h, 0, 0, 0);
+        h = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[st], pz[st], h, 0, 0, 0);
+      constexpr int kAhead = S < 8 ? S : 8;
+#pragma unroll
+      for (int k = 0; k < kAhead; ++k) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+#pragma unroll
+      for (int k = 0; k < S - kAhead; ++k) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
       w1 += 64 * sn;
 #pragma unroll
       for (int i = 0; i < 4; ++i) h[i] = fmaxf(h[i], 0.f);
@@ -1239,11 +1253,16 @@ __global__ __launch_bounds__(64 * kFwd1Waves) void k_gcn_fwd1(Fwd1Args a) {
         else
           for (int e = 0; e < 4 && c0 + e < a.hidden; ++e) dst[e] = h[e];
       }
+      float wb[CB][4];
+#pragma unroll
+      for (int c = 0; c < CB; ++c)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) wb[c][i] = w2[64 * (4 * c + i)];
 #pragma unroll
       for (int c = 0; c < CB; ++c)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          z[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(h[i], w2[64 * (4 * c + i)], z[c], 0, 0, 0);
+          z[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(h[i], wb[c][i], z[c], 0, 0, 0);
       w2 += 64 * 4 * CB;
     }
     // element i of z[c]: Z2[r0 + 4 g + i][16 c + x]
