@@ -313,7 +313,9 @@ gcn_status gcn_sage3_forward(const gcn_graph* g, const float* X, int64_t ldx, in
  *   H = relu(O) for l = 1, 2; the logits are O of layer 3. A layer whose output
  *   is narrower than its input evaluates Z W_neigh as A (Y W_neigh), so that
  *   its aggregations (forward and backward) gather the narrower rows; the two
- *   agree up to fp32 rounding.
+ *   agree up to fp32 rounding. With hidden a multiple of 16 up to 256, the
+ *   input gradient of such a layer and the LayerNorm backward of its input
+ *   run as one pass (the same sums, in another order).
  * Loss: mean softmax cross-entropy over the rows that count (all rows, or
  * those with lp_mask = 0). Label propagation: rows with lp_mask = 1 get E[label]
  * added to their input features and are left out of the loss. Dropout is not

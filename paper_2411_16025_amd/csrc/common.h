@@ -205,6 +205,14 @@ gcn_status aggregate_f32(const Mat& m, const float* X, int64_t ldx, float* Y, in
 gcn_status gemm_f32(int op, int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
                     const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream,
                     const float* mask = nullptr, int64_t ldm = 0, bool relu = false);
+// Input gradient of a GraphSAGE layer whose output is narrower than its
+// input, fused with the LayerNorm backward: dY = DG B^T (DG [n x K] with
+// 16-byte aligned rows, B [F x K]), then dX = rstd (dY - mean(dY) - Y
+// mean(dY Y)) where dx > 0 on entry (the ReLU output below), else 0.
+bool sage_tf_bwd_fusable(int64_t F, int64_t K, const float* dg, int64_t ldg);
+gcn_status sage_tf_bwd_fused(int64_t n, int64_t F, int64_t K, const float* dg, int64_t ldg,
+                             const float* bw, int64_t ldb, const float* y, int64_t ldy,
+                             const float* rstd, float* dx, int64_t ldx, hipStream_t stream);
 // Forward of a GCN first layer that aggregates first: H1 = relu(P W1) and
 // Z2 = H1 W2 in one pass over the rows. P [n x f_in] (ldp), H1 [n x hidden]
 // (ldh, 16-byte aligned rows), W1 [f_in x hidden] (ldw1), W2 [hidden x C]

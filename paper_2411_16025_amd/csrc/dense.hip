@@ -1291,6 +1291,132 @@ __global__ __launch_bounds__(64 * kFwd1Waves) void k_gcn_fwd1(Fwd1Args a) {
   }
 }
 
+// Backward of a GraphSAGE layer that aggregates Y W_neigh (its output is
+// narrower than its input), fused with the LayerNorm backward of its input:
+//   dY = DG [W_self | W_neigh]^T,  DG = [dO | G]  (K = 2 fop columns),
+//   dX = rstd (dY - mean(dY) - Y mean(dY Y)) where mask > 0, else 0,
+// with mask the ReLU output of the layer below, overwritten by dX. dY never
+// leaves the registers (the separate product stored it and the LayerNorm
+// backward read it back).
+//
+// [W_self | W_neigh] sits in LDS in matrix-core operand order, [b][s][lane] =
+// B[16 b + l % 16][4 s + l / 16] for the 16-column blocks b of dY and the
+// 4-deep steps s; each wavefront stages its own 16 x K tile of DG in LDS as
+// [s][lane] = DG[r0 + l % 16][4 s + l / 16] and walks its own row groups.
+// Result element i of block b in lane (g, x) is dY[r0 + 4 g + i][16 b + x]:
+// the row sums of the LayerNorm backward add the lane's NB blocks, then the
+// 16 lanes x of the row (DPP, in double, as the separate kernel sums in
+// double).
+struct TfBwdArgs {
+  int64_t n;
+  int F, K;         // F = 16 NB, K a multiple of 4
+  const float* dg;  // [n][ldg], 16-byte aligned rows
+  int64_t ldg;
+  const float* bw;  // [F][ldb]
+  int64_t ldb;
+  const float* y;  // [n][ldy]
+  int64_t ldy;
+  const float* rstd;
+  float* dx;  // [n][ldx]: the mask on entry, dX on return
+  int64_t ldx;
+};
+
+constexpr int kTfWaves = 8;
+
+template <int OFF>
+__device__ inline double row16_partner_d(double v) {
+  constexpr int kCtrl = OFF == 1 ? 0xB1 : OFF == 2 ? 0x4E : OFF == 4 ? 0x141 : 0x140;
+  const int lo = __builtin_amdgcn_mov_dpp(__double2loint(v), kCtrl, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_mov_dpp(__double2hiint(v), kCtrl, 0xF, 0xF, false);
+  return __hiloint2double(hi, lo);
+}
+
+__device__ inline double row16_sum_d(double v) {
+  v += row16_partner_d<1>(v);
+  v += row16_partner_d<2>(v);
+  v += row16_partner_d<4>(v);
+  return v + row16_partner_d<8>(v);
+}
+
+template <int NB>
+__global__ __launch_bounds__(64 * kTfWaves) void k_sage_tf_bwd(TfBwdArgs a) {
+  extern __shared__ __align__(16) float lds[];
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int g = lane >> 4, x = lane & 15;
+  const int ks = a.K / 4;
+  float* tb = lds;                                 // [NB][ks][64]
+  float* ds = lds + (NB + w) * ks * 64;            // this wavefront's [ks][64]
+  for (int e = threadIdx.x; e < NB * ks * 64; e += blockDim.x) {
+    const int l = e & 63, st = (e >> 6) % ks, b = (e >> 6) / ks;
+    tb[e] = a.bw[(int64_t)(16 * b + (l & 15)) * a.ldb + 4 * st + (l >> 4)];
+  }
+  __syncthreads();
+  const int64_t ng = (a.n + 15) / 16;
+  const int64_t stride = (int64_t)gridDim.x * kTfWaves;
+  for (int64_t grp = (int64_t)blockIdx.x * kTfWaves + w; grp < ng; grp += stride) {
+    const int64_t r0 = 16 * grp;
+    // the DG tile: piece p (row p / ks, columns 4 (p % ks) .. + 3); rows
+    // past n are zero
+    for (int p = lane; p < 16 * ks; p += 64) {
+      const int r = p / ks, st = p % ks;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (r0 + r < a.n) v = *reinterpret_cast<const float4*>(a.dg + (r0 + r) * a.ldg + 4 * st);
+      ds[st * 64 + r] = v.x;
+      ds[st * 64 + 16 + r] = v.y;
+      ds[st * 64 + 32 + r] = v.z;
+      ds[st * 64 + 48 + r] = v.w;
+    }
+    __builtin_amdgcn_wave_barrier();
+    f4 acc[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[b] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int st = 0; st < ks; ++st) {
+      const float av = ds[st * 64 + lane];
+      float bv[NB];
+#pragma unroll
+      for (int b = 0; b < NB; ++b) bv[b] = tb[(b * ks + st) * 64 + lane];
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+        acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv[b], acc[b], 0, 0, 0);
+    }
+    // the tile's operand reads are done before the next group's writes
+    __builtin_amdgcn_wave_barrier();
+    float yv[NB][4];
+    double s1[4], s2[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t row = min(r0 + 4 * g + i, a.n - 1);
+      s1[i] = 0.0;
+      s2[i] = 0.0;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) yv[b][i] = a.y[row * a.ldy + 16 * b + x];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        s1[i] += (double)acc[b][i];
+        s2[i] += (double)acc[b][i] * (double)yv[b][i];
+      }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t row = r0 + 4 * g + i;
+      const double m1 = row16_sum_d(s1[i]) / (double)a.F;
+      const double m2 = row16_sum_d(s2[i]) / (double)a.F;
+      if (row >= a.n) continue;
+      const double r = (double)a.rstd[row];
+      float* out = a.dx + row * a.ldx;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const float mk = out[16 * b + x];
+        const float d = (float)(r * ((double)acc[b][i] - m1 - (double)yv[b][i] * m2));
+        out[16 * b + x] = mk > 0.f ? d : 0.f;
+      }
+    }
+  }
+}
+
 // one wavefront per row
 __global__ __launch_bounds__(kThreads) void k_relu(int64_t n, int64_t F, float* __restrict__ h,
                                                    int64_t ld) {
@@ -1800,14 +1926,14 @@ int64_t fwd1_lds(int64_t f_in, int64_t hidden, int64_t C) {
   const int64_t hbn = ceil_div(hidden, (int64_t)16), sn = ceil_div(f_in, (int64_t)4);
   return (hbn * sn * 64 + hbn * ceil_div(C, (int64_t)16) * 4 * 64) * (int64_t)sizeof(float);
 }
-constexpr int64_t kFwd1MaxLds = 160 * 1024;
+constexpr int64_t kMaxDynLds = 160 * 1024;
 
 bool layer1_fwd_fusable(int64_t f_in, int64_t hidden, int64_t C, const float* P, int64_t ldp,
                         const float* H1, int64_t ldh) {
   (void)P;  // read element by element: any alignment
   return GCN_LAYER1_FUSED && f_in >= 1 && f_in <= 112 && hidden >= 1 && C >= 1 && C <= 48 &&
          ldp >= 4 * ceil_div(f_in, (int64_t)4) && ldh >= hidden && aligned16(H1, ldh) &&
-         fwd1_lds(f_in, hidden, C) <= kFwd1MaxLds;
+         fwd1_lds(f_in, hidden, C) <= kMaxDynLds;
 }
 
 gcn_status layer1_fwd_fused(int64_t n, int64_t f_in, int64_t hidden, int64_t C, const float* P,
@@ -1845,6 +1971,51 @@ gcn_status layer1_fwd_fused(int64_t n, int64_t f_in, int64_t hidden, int64_t C, 
   GCN_FWD1(28, 1); GCN_FWD1(28, 2); GCN_FWD1(28, 3);
 #undef GCN_FWD1
   if (e != hipSuccess) return hip_fail(e, "k_gcn_fwd1", __FILE__, __LINE__);
+  return GCN_OK;
+}
+
+// LDS bytes of the fused GraphSAGE backward: the weight table and 8 staged
+// DG tiles
+int64_t tf_bwd_lds(int64_t F, int64_t K) {
+  return (F / 16 + kTfWaves) * (K / 4) * 64 * (int64_t)sizeof(float);
+}
+
+bool sage_tf_bwd_fusable(int64_t F, int64_t K, const float* dg, int64_t ldg) {
+  const int64_t nb = F / 16;
+  return GCN_LAYER1_FUSED && F % 16 == 0 &&
+         (nb == 1 || nb == 2 || nb == 3 || nb == 4 || nb == 8 || nb == 16) && K >= 4 &&
+         K % 4 == 0 && ldg >= K && aligned16(dg, ldg) && tf_bwd_lds(F, K) <= kMaxDynLds;
+}
+
+gcn_status sage_tf_bwd_fused(int64_t n, int64_t F, int64_t K, const float* dg, int64_t ldg,
+                             const float* bw, int64_t ldb, const float* y, int64_t ldy,
+                             const float* rstd, float* dx, int64_t ldx, hipStream_t stream) {
+  if (!sage_tf_bwd_fusable(F, K, dg, ldg)) {
+    set_error("fused GraphSAGE backward: unsupported shape or alignment");
+    return GCN_EINVAL;
+  }
+  if (n == 0) return GCN_OK;
+  ProfScope ps("gemm_sage_tf_bwd_fused", stream);
+  const TfBwdArgs a{n, (int)F, (int)K, dg, ldg, bw, ldb, y, ldy, rstd, dx, ldx};
+  const size_t lds = (size_t)tf_bwd_lds(F, K);
+  const int64_t wg = std::min<int64_t>(cu_count(), ceil_div(ceil_div(n, (int64_t)16), (int64_t)kTfWaves));
+  hipError_t e = hipSuccess;
+  auto launch = [&](auto kern) {
+    e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds);
+    if (e != hipSuccess) return;
+    hipLaunchKernelGGL(kern, dim3((unsigned)wg), dim3(64 * kTfWaves), lds, stream, a);
+    e = hipGetLastError();
+  };
+  switch (F / 16) {
+    case 1: launch(k_sage_tf_bwd<1>); break;
+    case 2: launch(k_sage_tf_bwd<2>); break;
+    case 3: launch(k_sage_tf_bwd<3>); break;
+    case 4: launch(k_sage_tf_bwd<4>); break;
+    case 8: launch(k_sage_tf_bwd<8>); break;
+    default: launch(k_sage_tf_bwd<16>); break;
+  }
+  if (e != hipSuccess) return hip_fail(e, "k_sage_tf_bwd", __FILE__, __LINE__);
   return GCN_OK;
 }
 

@@ -499,6 +499,16 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
         break;
       }
       if (!input_grad) break;
+      if (l > 0 && sage_tf_bwd_fusable(y.f, ldg, dg, ldg)) {
+        // dY in registers, straight into the LayerNorm backward and the
+        // ReLU mask of the layer below (whose output it overwrites)
+        Layer& below = L[l - 1];
+        st = sage_tf_bwd_fused(n, y.f, ldg, dg, ldg, y.bc, ldg, y.c, y.ldc, y.rstd, below.o,
+                               below.fop, s);
+        dO = below.o;
+        ld_do = below.fop;
+        continue;
+      }
       // dY = dO W_self^T + G W_neigh^T = DG [W_self | W_neigh]^T, then the LayerNorm backward
       st = gemm_f32(GCN_GEMM_NT, n, y.f, ldg, dg, ldg, y.bc, ldg, dc, y.ldc, s);
       if (st != GCN_OK) break;

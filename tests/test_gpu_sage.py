@@ -209,7 +209,11 @@ def check_step(G, n, m, f_in, hidden, C, seed, lp, flags=synth.SYMMETRIZE):
 
 
 @pytest.mark.parametrize("lp", [False, True])
-@pytest.mark.parametrize("n,f_in,hidden,C", [(3000, 100, 64, 10), (2000, 47, 33, 5)])
+# hidden 64, 128 and 48 (multiples of 16) take the fused class-layer backward
+# (its input gradient and LayerNorm backward in one kernel), hidden 33 the
+# separate product and LayerNorm backward
+@pytest.mark.parametrize("n,f_in,hidden,C", [(3000, 100, 64, 10), (2000, 47, 33, 5),
+                                             (2000, 50, 128, 47), (1500, 20, 48, 16)])
 def test_sage_step_small(G, lp, n, f_in, hidden, C):
     note("sage step n=%d f_in=%d hidden=%d C=%d lp=%s" % (n, f_in, hidden, C, lp))
     check_step(G, n, 12 * n, f_in, hidden, C, 430 + n + f_in, lp)
