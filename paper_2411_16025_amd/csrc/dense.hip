@@ -1368,6 +1368,15 @@ __global__ __launch_bounds__(64 * kTfWaves) void k_sage_tf_bwd(TfBwdArgs a) {
       ds[st * 64 + 48 + r] = v.w;
     }
     __builtin_amdgcn_wave_barrier();
+    // Y of the group's rows, loaded while the products run (rows past n read
+    // the last row and are not stored)
+    float yv[NB][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t row = min(r0 + 4 * g + i, a.n - 1);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) yv[b][i] = a.y[row * a.ldy + 16 * b + x];
+    }
     f4 acc[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) acc[b] = f4{0.f, 0.f, 0.f, 0.f};
@@ -1382,15 +1391,11 @@ __global__ __launch_bounds__(64 * kTfWaves) void k_sage_tf_bwd(TfBwdArgs a) {
     }
     // the tile's operand reads are done before the next group's writes
     __builtin_amdgcn_wave_barrier();
-    float yv[NB][4];
     double s1[4], s2[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int64_t row = min(r0 + 4 * g + i, a.n - 1);
       s1[i] = 0.0;
       s2[i] = 0.0;
-#pragma unroll
-      for (int b = 0; b < NB; ++b) yv[b][i] = a.y[row * a.ldy + 16 * b + x];
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
