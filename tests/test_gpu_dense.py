@@ -252,15 +252,17 @@ def test_gcn_step_unaligned_inputs(G):
 
 @pytest.mark.parametrize("n,f_in,hidden,C", [(1203, 20, 200, 33), (777, 60, 300, 16),
                                              (2000, 112, 128, 48), (35, 100, 256, 47),
-                                             (500, 112, 256, 48)])
+                                             (500, 112, 256, 48), (16, 100, 256, 47),
+                                             (17, 4, 32, 2)])
 def test_gcn_step_fused_backward_shapes(G, n, f_in, hidden, C):
     # f_in <= 112 and C <= 48: layer 1's backward runs as one fused pass
     # (dZ1 in registers); f_in of 2, 4 and 7 16-column blocks, 1-3 class
     # blocks, hidden slices of 128 columns with partial ones, partial row
     # groups, and chunks of one group. With hidden <= 256 the forward is
     # fused too: step counts 8, 16, 25 and 28, a hidden width of 300 that
-    # keeps the separate products, and (112, 256, 48) whose weight tables
-    # take the whole 160 KB of LDS
+    # keeps the separate products, (112, 256, 48) whose weight tables take
+    # the whole 160 KB of LDS, exactly one row group, and a one-step input
+    # with two classes
     note("gcn step fused backward n=%d f_in=%d hidden=%d C=%d" % (n, f_in, hidden, C))
     src, dst = synth.rmat_edges(217 + n, n, 8 * n, perm_seed=218)
     w = synth.Workload("rmat%d" % n, n, n, src, dst, synth.SYMMETRIZE | synth.ADD_SELF_LOOPS, f_in)
