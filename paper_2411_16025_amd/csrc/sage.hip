@@ -179,6 +179,32 @@ __global__ __launch_bounds__(kThreadsS) void k_embed_labels(int64_t n, int64_t f
   }
 }
 
+// The same with 16-byte pieces (f, ldx, ldp multiples of 4, aligned rows):
+// thread t takes piece t % q of row t / q (q = f / 4).
+__global__ __launch_bounds__(kThreadsS) void k_embed_labels_v(int64_t n, int64_t f, int C,
+                                                              const float* __restrict__ x,
+                                                              int64_t ldx,
+                                                              const uint8_t* __restrict__ mask,
+                                                              const int32_t* __restrict__ y,
+                                                              const float* __restrict__ e,
+                                                              float* __restrict__ xp, int64_t ldp) {
+  const int64_t q = f / 4;
+  const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
+  if (t >= n * q) return;
+  const int64_t i = t / q, c = 4 * (t % q);
+  const int32_t k = y[i];
+  const bool on = mask[i] && k >= 0 && k < C;
+  float4 v = *reinterpret_cast<const float4*>(x + i * ldx + c);
+  if (on) {
+    const float4 w = *reinterpret_cast<const float4*>(e + (int64_t)k * f + c);
+    v.x += w.x;
+    v.y += w.y;
+    v.z += w.z;
+    v.w += w.w;
+  }
+  *reinterpret_cast<float4*>(xp + i * ldp + c) = v;
+}
+
 // Masked label propagation, backward: Xp = X + M E with M the one-hot matrix
 // of the embedded rows' labels (row i: 1 at column y[i] if mask[i]), so
 // dE = M^T dXp, a weight-gradient product. Thread t writes the 4 entries
@@ -374,8 +400,16 @@ gcn_status sage_forward(const gcn_graph* g, const float* X, int64_t ldx, int64_t
   const float* h = X;
   int64_t ldh = ldx;
   if (lp_mask) {
-    hipLaunchKernelGGL(k_embed_labels, dim3(blocks(n * 64)), dim3(kThreadsS), 0, s, n, f_in,
-                       (int)n_classes, X, ldx, lp_mask, labels, E, m.xp, L[0].fp);
+    const bool vec = f_in % 4 == 0 && ldx % 4 == 0 && L[0].fp % 4 == 0 &&
+                     reinterpret_cast<uintptr_t>(X) % 16 == 0 &&
+                     reinterpret_cast<uintptr_t>(E) % 16 == 0 &&
+                     reinterpret_cast<uintptr_t>(m.xp) % 16 == 0;
+    if (vec)
+      hipLaunchKernelGGL(k_embed_labels_v, dim3(blocks(n * (f_in / 4))), dim3(kThreadsS), 0, s, n,
+                         f_in, (int)n_classes, X, ldx, lp_mask, labels, E, m.xp, L[0].fp);
+    else
+      hipLaunchKernelGGL(k_embed_labels, dim3(blocks(n * 64)), dim3(kThreadsS), 0, s, n, f_in,
+                         (int)n_classes, X, ldx, lp_mask, labels, E, m.xp, L[0].fp);
     GCN_HIP(hipGetLastError());
     h = m.xp;
     ldh = L[0].fp;
