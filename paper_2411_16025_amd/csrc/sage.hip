@@ -124,6 +124,31 @@ __global__ __launch_bounds__(kThreadsS) void k_zero_dg_pad(int64_t n, int64_t fo
   dg[i * 2 * fop + col] = 0.f;
 }
 
+// [dO | G] before the transposed aggregation writes G: row i of dg (2 fop
+// wide) gets dO's fo columns and zeros up to fop, and the piece of the G half
+// that holds its last columns and padding is zeroed (the aggregation then
+// writes the fo columns of G). Thread t takes 16-byte piece t % q of row
+// t / q, q = fop / 4 + (fo % 4 != 0); dO rows 16-byte aligned, ldo >= fop.
+__global__ __launch_bounds__(kThreadsS) void k_fill_dg(int64_t n, int64_t fo, int64_t fop,
+                                                       const float* __restrict__ d_o,
+                                                       int64_t ldo, float* __restrict__ dg) {
+  const int64_t q = fop / 4 + (fo % 4 != 0 ? 1 : 0);
+  const int64_t t = (int64_t)blockIdx.x * kThreadsS + threadIdx.x;
+  if (t >= n * q) return;
+  const int64_t i = t / q, p = t % q;
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  int64_t col = fop + 4 * (fo / 4);  // the extra piece: the G half's last one
+  if (p < fop / 4) {
+    col = 4 * p;
+    v = *reinterpret_cast<const float4*>(d_o + i * ldo + col);
+    if (col + 0 >= fo) v.x = 0.f;
+    if (col + 1 >= fo) v.y = 0.f;
+    if (col + 2 >= fo) v.z = 0.f;
+    if (col + 3 >= fo) v.w = 0.f;
+  }
+  *reinterpret_cast<float4*>(dg + i * 2 * fop + col) = v;
+}
+
 // dwp [f x 2 fop] = Y^T [dO | G] -> dW_self, dW_neigh (the bias comes from
 // the column sum of dO).
 __global__ __launch_bounds__(kThreadsS) void k_unpack_grads_tf(int64_t f, int64_t fo,
@@ -503,14 +528,22 @@ gcn_status sage_backward(const gcn_graph* g, int64_t f_in, int64_t n_classes,
       // DG = [dO | G] with G = (D^-1 A)^T dO, fo wide; padding columns zero
       const int64_t ldg = 2 * y.fop;
       float* dg = dgl[l];
-      hipLaunchKernelGGL(k_zero_dg_pad, dim3(blocks(n * 2 * (y.fop - y.fo))), dim3(kThreadsS), 0,
-                         s, n, y.fo, y.fop, dg);
-      hipError_t e = hipGetLastError();
+      hipError_t e = hipSuccess;
+      if (ld_do >= y.fop && ld_do % 4 == 0 && reinterpret_cast<uintptr_t>(dO) % 16 == 0) {
+        const int64_t q = y.fop / 4 + (y.fo % 4 != 0 ? 1 : 0);
+        hipLaunchKernelGGL(k_fill_dg, dim3(blocks(n * q)), dim3(kThreadsS), 0, s, n, y.fo, y.fop,
+                           (const float*)dO, ld_do, dg);
+        e = hipGetLastError();
+      } else {
+        hipLaunchKernelGGL(k_zero_dg_pad, dim3(blocks(n * 2 * (y.fop - y.fo))), dim3(kThreadsS),
+                           0, s, n, y.fo, y.fop, dg);
+        e = hipGetLastError();
+        if (e == hipSuccess) st = copy_rows(dg, ldg, dO, ld_do, n, y.fo, s);
+      }
       if (e != hipSuccess) {
-        st = hip_fail(e, "k_zero_dg_pad", __FILE__, __LINE__);
+        st = hip_fail(e, "[dO | G] fill", __FILE__, __LINE__);
         break;
       }
-      st = copy_rows(dg, ldg, dO, ld_do, n, y.fo, s);
       if (st == GCN_OK) st = aggregate_f32(g->csc, dO, ld_do, dg + y.fop, ldg, y.fo, false, s);
       if (st == GCN_OK) st = side.fork();  // DG is complete on s
       if (st != GCN_OK) break;
