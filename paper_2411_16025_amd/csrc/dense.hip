@@ -886,16 +886,15 @@ __global__ __launch_bounds__(kThreads) void k_sum_partials(int64_t M, int64_t N,
 // the operand reads remain.
 //
 // Workgroup (chunk, hidden slice of 128 columns), one wavefront per SIMD
-// (the accumulators and two groups of operands take about 280 registers);
-// wavefront w owns the two 16-column blocks hs + 32 w + 16 hb (hb = 0, 1) of
-// the hidden layer and walks the chunk in groups of 16 rows r0 ... r0 + 15.
-// Lane (g = l / 16,
-// x = l % 16), per group:
+// (the accumulators and two sets of operands take about 450 VGPRs and
+// AGPRs); wavefront w owns the two 16-column blocks hs + 16 hb (hb = 0, 1,
+// hs = 128 slice + 32 w) of the hidden layer and walks the chunk in groups of
+// 16 rows r0 ... r0 + 15. Lane (g = l / 16, x = l % 16), per group:
 //  * dH1 block hb = dZ2[r0 .. r0 + 15] W2^T: the A operand is a 16-byte piece
 //    dZ2[r0 + x][16 j + 4 g .. + 3] (step i of chunk j contracts over class
 //    16 j + 4 g + i), the B operand W2[col][16 j + 4 g + i] is kept in
 //    registers for the whole kernel; classes past C are zero on both sides.
-//    Result element i is dH1[r0 + 4 g + i][col], col = hs + 32 w + 16 hb + x.
+//    Result element i is dH1[r0 + 4 g + i][col], col = hs + 16 hb + x.
 //  * dZ1 = that element where H1[r0 + 4 g + i][col] > 0, else 0.
 //  * The result layout is the B operand layout of a product contracting
 //    over the rows r0 + 4 g + i (g = 0 .. 3) at step i: dZ1 element i is the
